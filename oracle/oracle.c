@@ -1,0 +1,315 @@
+/*
+ * oracle.c -- CPU oracle for the Auto-Precision-Scaling (APS) gradient path.
+ *
+ * TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only the test suite, the smoke
+ * check and the CPU-baseline leg of the benchmark may load this library.
+ * It shares no code with the HIP library and nothing in the product calls it.
+ *
+ * Plain, slow, scalar C99.  All rounding is done on exact real values held in
+ * double precision with frexp / ldexp / nearbyint (default rounding mode, i.e.
+ * round-half-to-even).  The only parallelism is an OpenMP loop over
+ * independent elements; the arithmetic per element is the paper's, in the
+ * paper's order.
+ *
+ * Paper: Han, Demmel, You, "Auto-Precision Scaling for Distributed Deep
+ * Learning", arXiv 1911.08907.  Cited below by section, algorithm, equation
+ * and table.
+ *
+ * Readings of the paper used here (the paper is silent or loose on these):
+ *  R1 Format layout (Algorithm 1 names only exp_bit and man_bit): IEEE-754
+ *     style -- bias 2^(e-1)-1 by default, gradual underflow (subnormals), the
+ *     all-ones exponent reserved for INF/NaN.  With it the five rows of
+ *     Table 2 come out exactly.
+ *  R2 Overflow (Sec. 3.2 says values above 2^15 overflow for (5,2)): IEEE
+ *     round-to-nearest overflow -- a value becomes INF when rounding it with
+ *     an unbounded exponent gives a magnitude above the largest finite value.
+ *  R3 Underflow (Sec. 3.2 says values below 2^-16 become 0 for (5,2)):
+ *     round-to-nearest-even onto the subnormal grid, so only magnitudes up to
+ *     half the smallest subnormal become (signed) zero.
+ *  R4 Ties when m = 0: "even" is taken as an even multiple of the quantum,
+ *     so a significand 1.1b rounds up to 10b.
+ *  R5 Signed zeros and NaN follow IEEE-754 arithmetic.
+ *  R6 All-zero (or empty) layers and layers whose max magnitude is INF/NaN,
+ *     or whose fl32(N * max) overflows, get the scale exponent 0.
+ *  R7 The SUM all-reduce runs in worker order 0..W-1 and rounds its
+ *     accumulator to the same format after every add (Sec. 5, CPD's
+ *     low-precision accumulator); the result is the sum, not the mean.
+ *  R8 The scale exponent uses emax = 2^e - 2 - bias, which is Algorithm 1's
+ *     upper_bound_exp when the bias is the default.
+ */
+#include "oracle.h"
+
+#include <limits.h>
+#include <math.h>
+#include <string.h>
+
+static float f_of_bits(uint32_t b) {
+    float f;
+    memcpy(&f, &b, sizeof f);
+    return f;
+}
+
+static uint32_t bits_of_f(float f) {
+    uint32_t b;
+    memcpy(&b, &f, sizeof b);
+    return b;
+}
+
+/* ---------------------------------------------------------------- format */
+
+int oracle_emin(oracle_format f) { return 1 - f.bias; }
+
+int oracle_emax(oracle_format f) { return (1 << f.e) - 2 - f.bias; }
+
+/* largest finite value (2 - 2^-m) * 2^emax */
+double oracle_maxfinite(oracle_format f) {
+    return ldexp(2.0 - ldexp(1.0, -f.m), oracle_emax(f));
+}
+
+/* smallest positive (subnormal) value 2^(emin - m); Table 2's lower range end */
+double oracle_minsub(oracle_format f) { return ldexp(1.0, oracle_emin(f) - f.m); }
+
+int oracle_format_ok(oracle_format f) {
+    if (f.e < 2 || f.e > 8 || f.m < 0 || f.m > 23) return 0;
+    if (oracle_emax(f) > 127) return 0;
+    if (oracle_emin(f) > oracle_emax(f)) return 0;
+    if (oracle_emin(f) - f.m < -149) return 0;
+    return 1;
+}
+
+/* ------------------------------------------------------------- rounding */
+
+/* Cast(y, exp_bit, man_bit) of Algorithm 1 with the round-to-nearest-even
+ * mode of Sec. 4 and readings R1-R5.  y is any real held exactly in a double.
+ *
+ * For a = |y| in the binade [2^E, 2^(E+1)) the format spaces its values by
+ * the quantum 2^(max(E, emin) - m); the result is the multiple of that
+ * quantum nearest to a (ties to the even multiple), or INF when that
+ * multiple exceeds the largest finite value. */
+double oracle_round(double y, oracle_format f) {
+    if (isnan(y) || isinf(y) || y == 0.0) return y;
+    const int emin = oracle_emin(f);
+    const double a = fabs(y);
+    int E;
+    (void)frexp(a, &E); /* a = r * 2^E with r in [0.5, 1) */
+    E -= 1;             /* so that a is in [2^E, 2^(E+1)) */
+    const int Eq = E > emin ? E : emin;
+    const double k = nearbyint(ldexp(a, f.m - Eq)); /* a / quantum, exact scaling */
+    double v = ldexp(k, Eq - f.m);
+    if (v > oracle_maxfinite(f)) v = INFINITY;
+    return copysign(v, y); /* an underflow to zero keeps the sign of y (R5) */
+}
+
+/* --------------------------------------------------------------- scales */
+
+int oracle_ceil_log2(double t) {
+    int E;
+    const double r = frexp(t, &E); /* t = r * 2^E, r in [0.5, 1) */
+    return (r == 0.5) ? E - 1 : E; /* exact power of two: log2 t = E - 1 */
+}
+
+/* FindMaxExp(g * N) of Algorithm 1, literally: the product is the fp32
+ * multiply of the tensor by N, zeros are skipped, and the running maximum of
+ * ceil(log2|v|) is kept.  Non-finite products are reported separately. */
+int32_t oracle_find_max_exp(const float* g, int64_t cnt, int32_t N, int32_t* nonfinite) {
+    int32_t max_exp = INT32_MIN;
+    *nonfinite = 0;
+    for (int64_t k = 0; k < cnt; ++k) {
+        const float v = (float)N * g[k];
+        if (!isfinite(v)) {
+            *nonfinite = 1;
+            continue;
+        }
+        if (v != 0.0f) {
+            const int32_t t = oracle_ceil_log2(fabs((double)v));
+            if (t > max_exp) max_exp = t;
+        }
+    }
+    return max_exp;
+}
+
+void oracle_layer_maxabs(const float* G, int32_t W, int64_t ld, int64_t n,
+                         const int64_t* offsets, int32_t L, uint32_t* maxabs_bits) {
+    (void)n;
+    for (int32_t i = 0; i < L; ++i) {
+        double best = 0.0;
+        int saw_nan = 0;
+        for (int32_t w = 0; w < W; ++w) {
+            const float* row = G + (int64_t)w * ld;
+            for (int64_t j = offsets[i]; j < offsets[i + 1]; ++j) {
+                const float x = row[j];
+                if (isnan(x))
+                    saw_nan = 1;
+                else if (fabs((double)x) > best)
+                    best = fabs((double)x);
+            }
+        }
+        maxabs_bits[i] = saw_nan ? 0x7FC00000u : bits_of_f((float)best);
+    }
+}
+
+/* Sec. 3.3.3: the scale factor is f = 2^ft with
+ *     ft = log2(p) - ceil(log2 |N * ghat|),   p = 2^emax,
+ * which is Algorithm 1's  upper_bound_exp - AllReduce_MAX(FindMaxExp(g*N))
+ * once the MAX over workers and elements is taken on ghat first (both
+ * fl32(N*x) and ceil(log2 .) are monotone in |x|). */
+int32_t oracle_scale_one(uint32_t maxabs_bits, int32_t N, oracle_format f) {
+    const float ghat = f_of_bits(maxabs_bits & 0x7FFFFFFFu);
+    if (!(ghat > 0.0f) || !isfinite(ghat)) return 0;            /* R6 */
+    const float t = (float)((double)N * (double)ghat);            /* fl32(N * ghat) */
+    if (!isfinite(t)) return 0;                                   /* R6 */
+    return oracle_emax(f) - oracle_ceil_log2((double)t);
+}
+
+void oracle_layer_scales(const uint32_t* maxabs_bits, int32_t L, int32_t N,
+                         const oracle_format* fmts, const uint8_t* fmt_idx,
+                         int32_t* scale_exp) {
+    for (int32_t i = 0; i < L; ++i) {
+        const oracle_format f = fmts[fmt_idx ? fmt_idx[i] : 0];
+        scale_exp[i] = oracle_scale_one(maxabs_bits[i], N, f);
+    }
+}
+
+/* ------------------------------------------------------- quantize/reduce */
+
+/* Algorithm 1, line "g <- g * 2^ft": the gradient is fp32, so the product is
+ * the fp32 value nearest to x * 2^ft (a single rounding, exact unless the
+ * result leaves fp32's normal range). */
+static float scale_fp32(float x, int32_t ft) { return (float)ldexp((double)x, ft); }
+
+void oracle_quantize(const float* X, int32_t W, int64_t ld, int64_t n,
+                     const int64_t* offsets, int32_t L, const int32_t* scale_exp,
+                     const oracle_format* fmts, const uint8_t* fmt_idx, float* Q) {
+    (void)n;
+    for (int32_t i = 0; i < L; ++i) {
+        const oracle_format f = fmts[fmt_idx ? fmt_idx[i] : 0];
+        const int32_t ft = scale_exp ? scale_exp[i] : 0;
+        for (int32_t w = 0; w < W; ++w) {
+            const int64_t base = (int64_t)w * ld;
+#pragma omp parallel for schedule(static)
+            for (int64_t j = offsets[i]; j < offsets[i + 1]; ++j)
+                Q[base + j] = (float)oracle_round((double)scale_fp32(X[base + j], ft), f);
+        }
+    }
+}
+
+void oracle_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n,
+                       const int64_t* offsets, int32_t L, const int32_t* scale_exp,
+                       const oracle_format* fmts, const uint8_t* fmt_idx,
+                       uint32_t flags, float* out) {
+    (void)n;
+    for (int32_t i = 0; i < L; ++i) {
+        const oracle_format f = fmts[fmt_idx ? fmt_idx[i] : 0];
+        const int32_t ft = scale_exp ? scale_exp[i] : 0;
+#pragma omp parallel for schedule(static)
+        for (int64_t j = offsets[i]; j < offsets[i + 1]; ++j) {
+            double s = 0.0;
+            for (int32_t w = 0; w < W; ++w) {
+                const float x = G[(int64_t)w * ld + j];
+                /* g <- g * 2^ft (skipped when the input is already scaled) */
+                const float y = (flags & ORACLE_INPUT_QUANTIZED) ? x : scale_fp32(x, ft);
+                /* low_g <- Cast(g, exp_bit, man_bit) */
+                const double q = oracle_round((double)y, f);
+                /* low_g <- AllReduce(low_g, SUM) with a low-precision
+                 * accumulator: each partial sum is cast to the format.  The
+                 * double add of two format values followed by one rounding
+                 * equals rounding the exact sum (53 >= 2*24 + 2). */
+                s = (w == 0) ? q : oracle_round(s + q, f);
+            }
+            /* g <- Cast(low_g, 8, 23): s is a format value, hence an fp32 value */
+            const float g = (float)s;
+            /* g <- g / 2^ft */
+            out[j] = (flags & ORACLE_OUTPUT_SCALED) ? g : (float)ldexp((double)g, -ft);
+        }
+    }
+}
+
+/* ----------------------------------------------------------------- codes */
+
+uint32_t oracle_encode(double v, oracle_format f) {
+    const uint32_t sign = signbit(v) ? 1u : 0u;
+    const uint32_t expmax = (1u << f.e) - 1u;
+    uint32_t ef, mant;
+    if (isnan(v)) {
+        ef = expmax;
+        mant = f.m > 0 ? (1u << (f.m - 1)) : 0u; /* quiet NaN; no NaN code when m = 0 */
+    } else if (isinf(v)) {
+        ef = expmax;
+        mant = 0u;
+    } else {
+        const double a = fabs(v);
+        const int emin = oracle_emin(f);
+        if (a < ldexp(1.0, emin)) { /* subnormal or zero: a = mant * 2^(emin-m) */
+            ef = 0u;
+            mant = (uint32_t)ldexp(a, f.m - emin);
+        } else { /* a = (1 + mant/2^m) * 2^E */
+            int E;
+            (void)frexp(a, &E);
+            E -= 1;
+            ef = (uint32_t)(E + f.bias);
+            mant = (uint32_t)ldexp(ldexp(a, -E) - 1.0, f.m);
+        }
+    }
+    return (sign << (f.e + f.m)) | (ef << f.m) | mant;
+}
+
+double oracle_decode(uint32_t code, oracle_format f) {
+    const uint32_t expmax = (1u << f.e) - 1u;
+    const uint32_t sign = (code >> (f.e + f.m)) & 1u;
+    const uint32_t ef = (code >> f.m) & expmax;
+    const uint32_t mant = code & ((1u << f.m) - 1u);
+    double a;
+    if (ef == expmax)
+        a = mant == 0u ? INFINITY : NAN;
+    else if (ef == 0u)
+        a = ldexp((double)mant, oracle_emin(f) - f.m);
+    else
+        a = ldexp(1.0 + ldexp((double)mant, -f.m), (int)ef - f.bias);
+    return sign ? -a : a;
+}
+
+static int code_bits(oracle_format f) { return 1 + f.e + f.m; }
+
+static void put_code(void* codes, int64_t j, uint32_t c, int bits) {
+    uint8_t* b = (uint8_t*)codes;
+    if (bits <= 4) {
+        const int shift = (int)(j & 1) * 4;
+        b[j >> 1] = (uint8_t)((b[j >> 1] & ~(0xF << shift)) | ((c & 0xF) << shift));
+    } else if (bits <= 8) {
+        b[j] = (uint8_t)c;
+    } else {
+        b[2 * j] = (uint8_t)(c & 0xFF);
+        b[2 * j + 1] = (uint8_t)(c >> 8);
+    }
+}
+
+static uint32_t get_code(const void* codes, int64_t j, int bits) {
+    const uint8_t* b = (const uint8_t*)codes;
+    if (bits <= 4) return (b[j >> 1] >> ((int)(j & 1) * 4)) & 0xFu;
+    if (bits <= 8) return b[j];
+    return (uint32_t)b[2 * j] | ((uint32_t)b[2 * j + 1] << 8);
+}
+
+void oracle_pack_codes(const float* V, int64_t n, const int64_t* offsets, int32_t L,
+                       const oracle_format* fmts, const uint8_t* fmt_idx, void* codes) {
+    (void)n;
+    for (int32_t i = 0; i < L; ++i) {
+        const oracle_format f = fmts[fmt_idx ? fmt_idx[i] : 0];
+        for (int64_t j = offsets[i]; j < offsets[i + 1]; ++j)
+            put_code(codes, j, oracle_encode((double)V[j], f), code_bits(f));
+    }
+}
+
+void oracle_dequantize(const float* Q, const void* codes, int64_t n,
+                       const int64_t* offsets, int32_t L, const int32_t* scale_exp,
+                       const oracle_format* fmts, const uint8_t* fmt_idx, float* out) {
+    (void)n;
+    for (int32_t i = 0; i < L; ++i) {
+        const oracle_format f = fmts[fmt_idx ? fmt_idx[i] : 0];
+        const int32_t ft = scale_exp ? scale_exp[i] : 0;
+        for (int64_t j = offsets[i]; j < offsets[i + 1]; ++j) {
+            const double v = Q ? (double)Q[j] : oracle_decode(get_code(codes, j, code_bits(f)), f);
+            out[j] = (float)ldexp(v, -ft); /* g <- Cast(low_g, 8, 23) / 2^ft */
+        }
+    }
+}
