@@ -1,0 +1,235 @@
+#!/usr/bin/env python3
+"""Benchmark of the APS gradient path on one MI355X.
+
+A step is one APS synchronisation of W simulated workers over a synthetic,
+HBM-resident gradient set (Algorithm 1 of arXiv 1911.08907): per-layer
+max-abs, per-layer scale exponents, and the fused scale / cast / rounded
+W-worker sum / unscale kernel.  The default workload is the ResNet-50-shaped
+set with W = 256 workers (161 tensors, 25,557,032 elements per worker,
+26.2 GB of fp32 worker gradients) in the 1-5-2 format.
+
+Prints one JSON line: whole-step throughput (worker-gradient elements per
+second), the fused kernel's HBM roofline figures measured with HIP events on
+the launch stream, and the CPU oracle's throughput on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "APS gradient elements/s (quantize+W-way sim reduce) and % of HBM peak GB/s"
+HBM_PEAK_GBPS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_1911_08907_amd", "csrc", f) for f in ("aps.hip", "aps_format.hpp")]
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="resnet50_w256")
+    ap.add_argument("--palette", default=None)
+    ap.add_argument("--mode", choices=["aps", "raw"], default="aps")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU oracle time budget")
+    ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
+                    help="only run device-to-device copies of this size (counter calibration)")
+    return ap.parse_args()
+
+
+def copy_calibration(gib: float, reps: int = 5) -> None:
+    import torch
+    nbytes = int(gib * (1 << 30))
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_per_dispatch": nbytes, "reps": reps}), flush=True)
+
+
+def traffic_from_profile(config: str, palette: str, launch_bytes: float):
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken on the current kernel source."""
+    path = os.path.join(PROFILES, f"sim_reduce_{config}_{palette}_counters.json")
+    if not os.path.exists(path):
+        return None, "no counter summary"
+    with open(path) as fh:
+        c = json.load(fh)
+    if c.get("source_digest") != source_digest():
+        return None, "kernel changed since the counters were taken"
+    fetch = c["fetch_kib_per_dispatch"] * 1024 * c["fetch_scale"]
+    write = c["write_kib_per_dispatch"] * 1024 * c["write_scale"]
+    return fetch + write, f"{os.path.basename(path)}"
+
+
+def cpu_baseline(G_t, gs, pal, budget_s: float, slice_cols: int = 65536):
+    """The CPU oracle on successive column slices (all W workers) of the same
+    gradient set until the time budget is used: max-abs, scales and the
+    rounded W-worker sum for each slice."""
+    import numpy as np
+
+    import oracle as O
+
+    opal = [O.Format(f.e, f.m, f.bias) for f in pal]
+    W, n = gs.W, gs.n
+    done = 0
+    spent = 0.0
+    start_col = 0
+    while spent < budget_s and start_col < n:
+        cols = min(slice_cols, n - start_col)
+        Gs = G_t[:, start_col:start_col + cols].cpu().numpy()
+        offs = gs.offsets
+        lo = np.searchsorted(offs, start_col, side="right") - 1
+        hi = np.searchsorted(offs, start_col + cols, side="left")
+        sub = np.clip(offs[lo:hi + 1] - start_col, 0, cols).astype(np.int64)
+        sub[0], sub[-1] = 0, cols
+        fi = None if gs.fmt_idx is None else gs.fmt_idx[lo:hi]
+        ldS = (cols + 3) // 4 * 4
+        Gp = np.zeros((W, ldS), np.float32)
+        Gp[:, :cols] = Gs
+        t0 = time.perf_counter()
+        mab = O.layer_maxabs(Gp, cols, sub)
+        se = O.layer_scales(mab, W, opal, fi)
+        O.sim_reduce(Gp, cols, sub, se, opal, fi)
+        spent += time.perf_counter() - t0
+        done += cols
+        start_col += cols
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {
+        "value": W * done / spent,
+        "unit": "elements/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"first {done} of {n} elements x all {W} workers, in {slice_cols}-element column slices "
+                  f"(max-abs + scales + rounded W-worker sum), {spent:.1f} s",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the multi-GPU path is a design, not part of this build)", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration > 0:
+        copy_calibration(args.copy_calibration)
+        return
+
+    import torch
+
+    from paper_1911_08907_amd import aps as A
+    from paper_1911_08907_amd import workloads as WL
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    A.lib()
+    dev = torch.device("cuda:0")
+    cfg = WL.CONFIGS[args.config]
+    palette = args.palette or next(iter(cfg.palettes))
+    t_gen = time.time()
+    gs = WL.generate(args.config, palette, device=dev)
+    torch.cuda.synchronize()
+    t_gen = time.time() - t_gen
+    print(f"# generated {args.config} W={gs.W} n={gs.n} ld={gs.ld} in {t_gen:.1f}s", file=sys.stderr, flush=True)
+    pal = [A.Format(p.e, p.m, p.bias) for p in gs.palette]
+    W, n, L = gs.W, gs.n, len(gs.sizes)
+    offs_t = torch.from_numpy(gs.offsets).to(dev)
+    idx_t = None if gs.fmt_idx is None else torch.from_numpy(gs.fmt_idx).to(dev)
+    mab = torch.empty(L, dtype=torch.int32, device=dev)
+    se = torch.empty(L, dtype=torch.int32, device=dev)
+    out = torch.empty(n, dtype=torch.float32, device=dev)
+    G = gs.G
+
+    ev = []
+
+    def step(record: bool):
+        if record:
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            e[0].record()
+        A.aps_layer_maxabs(G, n, offs_t, mab)
+        if record:
+            e[1].record()
+        if args.mode == "aps":
+            A.aps_layer_scales(mab, W, pal, idx_t, se)
+        if record:
+            e[2].record()
+        A.aps_sim_reduce(G, n, offs_t, se if args.mode == "aps" else None, pal, idx_t, 0, out=out)
+        if record:
+            e[3].record()
+            ev.append(e)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    k1 = sum(e[0].elapsed_time(e[1]) for e in ev) / len(ev)
+    k2 = sum(e[1].elapsed_time(e[2]) for e in ev) / len(ev)
+    k4 = sum(e[2].elapsed_time(e[3]) for e in ev) / len(ev)
+    assert bool(torch.isfinite(out).all()) or args.mode == "raw"
+
+    alg_bytes = 4.0 * W * n + 4.0 * n     # read every worker row once, write the fp32 sum
+    achieved = alg_bytes / (k4 * 1e-3) / 1e9
+    traffic, traffic_src = traffic_from_profile(args.config, palette, alg_bytes)
+    res = {
+        "metric": METRIC,
+        "value": W * n / (ms_per_step * 1e-3),
+        "unit": "elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": args.config, "W": W, "n": n, "tensors": L, "format": palette,
+                   "mode": args.mode, "layout": "[W][ld] fp32 worker-major, HBM resident"},
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": traffic,
+            "kernel": "k_sim_reduce",
+            "algorithmic_bytes_per_launch": alg_bytes,
+            "avg_launch_ms": k4,
+            "traffic_source": traffic_src,
+        },
+        "kernels_ms": {"layer_maxabs": k1, "layer_scales": k2, "sim_reduce": k4},
+        "sim_reduce_elements_per_s": W * n / (k4 * 1e-3),
+        "maxabs_GBps": 4.0 * W * n / (k1 * 1e-3) / 1e9,
+        "kernel_source": source_digest(),
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(G, gs, pal, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

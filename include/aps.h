@@ -1,0 +1,190 @@
+/*
+ * aps.h -- C ABI of the MI355X (gfx950) Auto-Precision-Scaling gradient path.
+ *
+ * Paper: Han, Demmel, You, "Auto-Precision Scaling for Distributed Deep
+ * Learning", arXiv 1911.08907.  The five compute calls are the steps of
+ * Algorithm 1 (APS) for one synchronisation of a model's gradients, with the
+ * W data-parallel workers simulated on one GPU:
+ *
+ *   aps_layer_maxabs   FindMaxExp input + AllReduce(MAX)   (Alg. 1, FindMaxExp)
+ *   aps_layer_scales   ft = upper_bound_exp - max exponent (Alg. 1; Sec. 3.3.3)
+ *   aps_quantize       g * 2^ft, Cast(g, exp_bit, man_bit) (Alg. 1; Sec. 3.3.1)
+ *   aps_sim_reduce     scale, cast, AllReduce(SUM) with a low-precision
+ *                      accumulator, cast back, unscale     (Alg. 1; Sec. 5)
+ *   aps_dequantize     Cast(low_g, 8, 23) / 2^ft           (Alg. 1)
+ *
+ * Data layout.  A model's gradients are one flat fp32 vector of n elements;
+ * layer i (one parameter tensor) owns elements [offsets[i], offsets[i+1]).
+ * W workers' gradients are stored worker-major: element j of worker w is
+ * G[w * ld + j], with row stride ld >= n.
+ *
+ * Custom float format {e, m, bias}: 1 sign bit, e exponent bits, m mantissa
+ * bits.  IEEE-754 layout: exponent field 0 holds zero and the subnormals
+ * (value mant * 2^(1-bias-m)), the all-ones field holds INF (mant 0) and NaN.
+ * Rounding is round-to-nearest-even; a magnitude at or above
+ * (2 - 2^-(m+1)) * 2^emax becomes INF, one at or below half the smallest
+ * subnormal becomes a zero of the input's sign.  With m = 0 a tie goes to
+ * the even multiple of the quantum (significand 1.1b rounds up to 10b).
+ * emin = 1 - bias, emax = 2^e - 2 - bias.  The default bias 2^(e-1)-1 gives
+ * Algorithm 1's upper_bound_exp as emax and Table 2's ranges.
+ *
+ * Memory.  Every array argument except `fmts` is DEVICE memory owned by the
+ * caller.  `fmts` is HOST memory, read during the call only.  The library
+ * allocates nothing and keeps no state between calls.
+ *
+ * Streams.  `stream` is a hipStream_t (NULL = the default stream).  A call
+ * validates its arguments on the host, enqueues its kernels on `stream` and
+ * returns without synchronising.  Calls are thread-safe.
+ *
+ * Errors.  Argument checks happen on the host before anything is enqueued and
+ * return a negative status; a failed launch returns APS_ERR_DEVICE.  The
+ * contents of device arrays are not checked: offsets must start at 0, be
+ * non-decreasing and end at n; every fmt_idx[i] must be < n_fmts.  Other
+ * contents give undefined results.
+ *
+ * Bit codes.  code = sign << (e+m) | biased exponent << m | mantissa.  A NaN
+ * is written as the all-ones exponent with the top mantissa bit set (the INF
+ * code when m = 0).  Codes of 2..4 bits are packed two per byte (element j in
+ * the low nibble of byte j/2 when j is even, the high nibble when odd); codes
+ * of 5..8 bits take one byte; codes of 9..16 bits one little-endian uint16.
+ * A call that writes or reads codes needs every format of its palette in the
+ * same one of those three classes.
+ */
+#ifndef APS_H
+#define APS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct {
+    int32_t e;    /* exponent bits, 2..8 */
+    int32_t m;    /* mantissa bits, 0..23 */
+    int32_t bias; /* exponent bias; default (1 << (e-1)) - 1 */
+} aps_format;
+
+enum {
+    APS_OK = 0,
+    APS_ERR_NULL = -1,        /* a required pointer is NULL */
+    APS_ERR_SIZE = -2,        /* W, L, n, ld, n_fmts or N out of range */
+    APS_ERR_FORMAT = -3,      /* e, m or bias outside the supported range */
+    APS_ERR_ALIGN = -4,       /* a pointer or ld breaks the alignment rules */
+    APS_ERR_UNSUPPORTED = -5, /* valid but not provided (see aps_format_supported) */
+    APS_ERR_DEVICE = -6       /* a HIP call or kernel launch failed */
+};
+
+/* sim_reduce flags */
+#define APS_INPUT_QUANTIZED 1u /* G is already scaled by 2^ft: skip that multiply (the
+                                * cast is still applied; it is exact on format values) */
+#define APS_OUTPUT_SCALED 2u   /* leave the sum scaled: skip the division by 2^ft */
+
+/* Limits checked on the host. */
+#define APS_MAX_FORMATS 8          /* palette size n_fmts is 1..8 */
+#define APS_MAX_WORKERS (1 << 24)  /* W and N: N * max|g| is an fp32 product */
+#define APS_MAX_ELEMS (1LL << 30)  /* n (elements per worker) */
+
+/*
+ * Returns APS_OK if {e, m, bias} is a format the kernels implement, else
+ * APS_ERR_FORMAT (outside e in [2,8], m in [0,23], emax <= 127,
+ * emin - m >= -149) or APS_ERR_UNSUPPORTED (e = 8 with a bias other than
+ * 127, or a format whose half-smallest-subnormal is below 2^-126).
+ * Host-only; never touches the GPU.
+ */
+int aps_format_supported(aps_format f);
+
+/*
+ * Per-layer maximum magnitude over all W workers (Algorithm 1: the input of
+ * FindMaxExp and its AllReduce(MAX); the maximum of ceil(log2|N*g|) over a
+ * layer is taken from the maximum |g|, since both maps are monotone).
+ *
+ *   G            [W][ld] fp32, 16-byte aligned, ld % 4 == 0, ld >= n
+ *   offsets      int64[L+1] layer boundaries
+ *   maxabs_bits  uint32[L] out: fp32 bit pattern of max |G[w][j]| over all
+ *                w and all j of the layer; a NaN anywhere gives a NaN
+ *                pattern (above 0x7F800000), an empty or all-zero layer 0.
+ * Sizes: 1 <= W <= APS_MAX_WORKERS, L >= 1, 0 <= n <= APS_MAX_ELEMS.
+ */
+int aps_layer_maxabs(const float* G, int32_t W, int64_t ld, int64_t n,
+                     const int64_t* offsets, int32_t L, uint32_t* maxabs_bits,
+                     void* stream);
+
+/*
+ * Per-layer power-of-two scale exponent (Sec. 3.3.3 and Algorithm 1):
+ *   scale_exp[i] = emax(fmt_i) - ceil(log2 fl32(N * ghat_i))
+ * where ghat_i is the magnitude in maxabs_bits[i] and fl32 the fp32 product.
+ * It is the largest exponent with N * ghat_i * 2^scale_exp[i] <= 2^emax.
+ * A layer with ghat 0, INF or NaN, or with fl32(N * ghat) = INF, gets 0.
+ *
+ *   maxabs_bits  uint32[L] (device), e.g. from aps_layer_maxabs
+ *   N            number of workers, 1..APS_MAX_WORKERS
+ *   fmts         host aps_format[n_fmts], 1 <= n_fmts <= APS_MAX_FORMATS
+ *   fmt_idx      uint8[L] (device) palette index per layer, or NULL (all 0)
+ *   scale_exp    int32[L] out
+ */
+int aps_layer_scales(const uint32_t* maxabs_bits, int32_t L, int32_t N,
+                     const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,
+                     int32_t* scale_exp, void* stream);
+
+/*
+ * Scale and cast every element of every worker (Algorithm 1, g <- g * 2^ft
+ * then Cast(g, exp_bit, man_bit)):
+ *   Q[w][j] = R_fmt(fl32(X[w][j] * 2^scale_exp[i]))   for j in layer i.
+ * The product is the fp32 value nearest to X * 2^ft; R_fmt is the format's
+ * round-to-nearest-even described above.
+ *
+ *   X          [W][ld] fp32 (16-byte aligned, ld % 4 == 0)
+ *   scale_exp  int32[L] or NULL (every ft = 0: casting without APS)
+ *   Q          [W][ld] fp32 out, may be X itself; or NULL
+ *   codes      [W][ld] packed codes out (row stride ld elements), 16-byte
+ *              aligned; or NULL.  At least one of Q, codes is non-NULL.
+ * Elements j in [n, ld) of each row are not written.
+ */
+int aps_quantize(const float* X, int32_t W, int64_t ld, int64_t n,
+                 const int64_t* offsets, int32_t L, const int32_t* scale_exp,
+                 const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,
+                 float* Q, void* codes, void* stream);
+
+/*
+ * The fused APS step for one simulated synchronisation (Algorithm 1 with
+ * the low-precision accumulator of Sec. 5), per element j of layer i:
+ *   q_w = R_fmt(fl32(G[w][j] * 2^ft))            w = 0..W-1
+ *   s   = q_0;  s = R_fmt(s + q_w) for w = 1..W-1   (this order, rounded
+ *                                                   after every add)
+ *   out[j] = fl32(s / 2^ft)
+ * out is the sum over workers (not the mean).  With APS_INPUT_QUANTIZED the
+ * multiply by 2^ft is skipped; with APS_OUTPUT_SCALED the division is.
+ *
+ *   G          [W][ld] fp32 (16-byte aligned, ld % 4 == 0); not aliased by out
+ *   scale_exp  int32[L] or NULL (every ft = 0)
+ *   out        fp32[n] out (16-byte aligned), or NULL
+ *   codes_out  packed codes of the scaled sum s, [n] (16-byte aligned), or NULL
+ *   At least one of out, codes_out is non-NULL.
+ */
+int aps_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n,
+                   const int64_t* offsets, int32_t L, const int32_t* scale_exp,
+                   const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,
+                   uint32_t flags, float* out, void* codes_out, void* stream);
+
+/*
+ * Cast back and unscale (Algorithm 1, Cast(low_g, 8, 23) then g / 2^ft):
+ *   out[j] = fl32(V[j] / 2^scale_exp[i])
+ * where V is Q (fp32 values) if Q is non-NULL, else the decoded codes.
+ *
+ *   Q          fp32[n] (16-byte aligned) or NULL
+ *   codes      packed codes [n] (16-byte aligned), used when Q is NULL
+ *   out        fp32[n] out (16-byte aligned), may be Q itself
+ */
+int aps_dequantize(const float* Q, const void* codes, int64_t n,
+                   const int64_t* offsets, int32_t L, const int32_t* scale_exp,
+                   const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,
+                   float* out, void* stream);
+
+/* Static text for a status code. */
+const char* aps_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* APS_H */

@@ -1,0 +1,216 @@
+"""Thin Python binding of libaps.so (argument marshalling only).
+
+The names match the C ABI declared in include/aps.h.  Arrays are torch tensors
+on the GPU (torch provides device memory and the current stream); the format
+palette is a list of ``Format``.  Every computation happens in the HIP kernels
+of libaps.so; if the library is missing, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Iterable, Sequence
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libaps.so")
+
+APS_OK = 0
+APS_ERR_NULL = -1
+APS_ERR_SIZE = -2
+APS_ERR_FORMAT = -3
+APS_ERR_ALIGN = -4
+APS_ERR_UNSUPPORTED = -5
+APS_ERR_DEVICE = -6
+
+APS_INPUT_QUANTIZED = 1
+APS_OUTPUT_SCALED = 2
+APS_MAX_FORMATS = 8
+
+EXPORTS = ("aps_format_supported", "aps_layer_maxabs", "aps_layer_scales", "aps_quantize",
+           "aps_sim_reduce", "aps_dequantize", "aps_strerror")
+
+
+class ApsError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn}: {strerror(status)} ({status})")
+        self.status = status
+
+
+class aps_format(ctypes.Structure):
+    _fields_ = [("e", ctypes.c_int32), ("m", ctypes.c_int32), ("bias", ctypes.c_int32)]
+
+
+@dataclass(frozen=True)
+class Format:
+    """Custom float: 1 sign bit, e exponent bits, m mantissa bits, bias
+    (default 2^(e-1)-1)."""
+
+    e: int
+    m: int
+    bias: int | None = None
+
+    @property
+    def b(self) -> int:
+        return (1 << (self.e - 1)) - 1 if self.bias is None else self.bias
+
+    @property
+    def bits(self) -> int:
+        return 1 + self.e + self.m
+
+    @property
+    def emax(self) -> int:
+        return (1 << self.e) - 2 - self.b
+
+    def c(self) -> aps_format:
+        return aps_format(self.e, self.m, self.b)
+
+    def __str__(self) -> str:
+        return f"1-{self.e}-{self.m}" + ("" if self.bias is None else f"/b{self.bias}")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libaps.so (built in-tree by paper_1911_08907_amd.build)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: run paper_1911_08907_amd.build.build() first")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64, u32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32
+        FP = ctypes.POINTER(aps_format)
+        sig = {
+            "aps_format_supported": (ctypes.c_int, [aps_format]),
+            "aps_layer_maxabs": (ctypes.c_int, [P, i32, i64, i64, P, i32, P, P]),
+            "aps_layer_scales": (ctypes.c_int, [P, i32, i32, FP, i32, P, P, P]),
+            "aps_quantize": (ctypes.c_int, [P, i32, i64, i64, P, i32, P, FP, i32, P, P, P, P]),
+            "aps_sim_reduce": (ctypes.c_int, [P, i32, i64, i64, P, i32, P, FP, i32, P, u32, P, P, P]),
+            "aps_dequantize": (ctypes.c_int, [P, P, i64, P, i32, P, FP, i32, P, P, P]),
+            "aps_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def strerror(status: int) -> str:
+    return lib().aps_strerror(int(status)).decode()
+
+
+def format_supported(f: Format) -> int:
+    return lib().aps_format_supported(f.c())
+
+
+# ------------------------------------------------------------ marshalling
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return ctypes.c_void_p(t)
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _palette(fmts) -> tuple:
+    if isinstance(fmts, Format):
+        fmts = [fmts]
+    fmts = list(fmts)
+    arr = (aps_format * max(1, len(fmts)))()
+    for k, f in enumerate(fmts):
+        arr[k] = f.c()
+    return arr, len(fmts)
+
+
+def _check(fn: str, st: int):
+    if st != APS_OK:
+        raise ApsError(fn, st)
+
+
+def _rows(G):
+    if G.dim() != 2:
+        raise ValueError("expected a [W][ld] tensor")
+    return G.shape[0], G.stride(0)
+
+
+# ------------------------------------------------------------ entry points
+# Each takes torch tensors on the current device; ``n`` is the gradient
+# length and ``offsets`` an int64 tensor of L+1 layer boundaries.
+
+def aps_layer_maxabs(G, n: int, offsets, maxabs_bits, stream=None) -> None:
+    W, ld = _rows(G)
+    L = offsets.numel() - 1
+    _check("aps_layer_maxabs", lib().aps_layer_maxabs(_ptr(G), W, ld, n, _ptr(offsets), L,
+                                                      _ptr(maxabs_bits), _stream(stream)))
+
+
+def aps_layer_scales(maxabs_bits, N: int, fmts, fmt_idx, scale_exp, stream=None) -> None:
+    pal, nf = _palette(fmts)
+    _check("aps_layer_scales", lib().aps_layer_scales(_ptr(maxabs_bits), maxabs_bits.numel(), int(N), pal,
+                                                      nf, _ptr(fmt_idx), _ptr(scale_exp), _stream(stream)))
+
+
+def aps_quantize(X, n: int, offsets, scale_exp, fmts, fmt_idx, Q=None, codes=None, stream=None) -> None:
+    W, ld = _rows(X)
+    pal, nf = _palette(fmts)
+    L = offsets.numel() - 1
+    _check("aps_quantize", lib().aps_quantize(_ptr(X), W, ld, n, _ptr(offsets), L, _ptr(scale_exp), pal, nf,
+                                              _ptr(fmt_idx), _ptr(Q), _ptr(codes), _stream(stream)))
+
+
+def aps_sim_reduce(G, n: int, offsets, scale_exp, fmts, fmt_idx, flags: int = 0, out=None,
+                   codes_out=None, stream=None) -> None:
+    W, ld = _rows(G)
+    pal, nf = _palette(fmts)
+    L = offsets.numel() - 1
+    _check("aps_sim_reduce", lib().aps_sim_reduce(_ptr(G), W, ld, n, _ptr(offsets), L, _ptr(scale_exp), pal,
+                                                  nf, _ptr(fmt_idx), int(flags), _ptr(out), _ptr(codes_out),
+                                                  _stream(stream)))
+
+
+def aps_dequantize(Q, codes, n: int, offsets, scale_exp, fmts, fmt_idx, out, stream=None) -> None:
+    pal, nf = _palette(fmts)
+    L = offsets.numel() - 1
+    _check("aps_dequantize", lib().aps_dequantize(_ptr(Q), _ptr(codes), n, _ptr(offsets), L, _ptr(scale_exp),
+                                                  pal, nf, _ptr(fmt_idx), _ptr(out), _stream(stream)))
+
+
+def code_bytes(count: int, bits: int) -> int:
+    """Bytes of a packed code array of ``count`` elements."""
+    if bits <= 4:
+        return (count + 1) // 2
+    if bits <= 8:
+        return count
+    return 2 * count
+
+
+# ------------------------------------------------------------ convenience
+
+def aps_step(G, n: int, offsets, fmts, fmt_idx=None, N: int | None = None, flags: int = 0, stream=None):
+    """One full APS synchronisation of W simulated workers (Algorithm 1):
+    max-abs, scales, fused scale/cast/rounded-sum/unscale.  Returns
+    (out, scale_exp, maxabs_bits) as new device tensors."""
+    import torch
+    W, _ = _rows(G)
+    L = offsets.numel() - 1
+    dev = G.device
+    maxabs = torch.empty(L, dtype=torch.int32, device=dev)
+    scale = torch.empty(L, dtype=torch.int32, device=dev)
+    out = torch.empty(max(n, 1), dtype=torch.float32, device=dev)[:n]
+    aps_layer_maxabs(G, n, offsets, maxabs, stream)
+    aps_layer_scales(maxabs, W if N is None else N, fmts, fmt_idx, scale, stream)
+    aps_sim_reduce(G, n, offsets, scale, fmts, fmt_idx, flags, out, None, stream)
+    return out, scale, maxabs

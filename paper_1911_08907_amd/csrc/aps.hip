@@ -1,0 +1,959 @@
+// aps.hip -- HIP kernels (gfx950) and the C ABI of the APS gradient path.
+//
+// Algorithm 1 of arXiv 1911.08907 for W data-parallel workers simulated on
+// one GPU: per-layer max magnitude (FindMaxExp input + AllReduce MAX),
+// power-of-two scale exponents (Sec. 3.3.3), scale + cast to a custom float
+// (Sec. 3.3.1, Sec. 4), the SUM all-reduce with a low-precision accumulator
+// rounded after every add in worker order (Sec. 5), cast back and unscale.
+//
+// Work decomposition.  The flat n-element gradient is cut into chunks of
+// CH = 1024 elements; each thread owns 4 consecutive elements (one 16-byte
+// load per worker row).  A launch has about 8 blocks per CU and each block
+// walks a contiguous range of chunks, so the layer of a chunk is found by a
+// forward scan from the previous one (scalar loads of the offsets table).
+// A chunk may cover several layers; as long as they share one palette entry
+// the fast kernels handle it with a per-element scale exponent.  Chunks that
+// mix palette entries (only possible with several formats) go to a small
+// generic kernel, one block per such chunk.
+//
+// Nothing here allocates memory; every kernel is enqueued on the caller's
+// stream.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "aps.h"
+#include "aps_format.hpp"
+
+namespace aps {
+
+constexpr int BLOCK = 256;
+constexpr int VEC = 4;
+constexpr int64_t CH = BLOCK * VEC;
+constexpr int UNROLL = 4;  // worker rows per register set (two sets in flight)
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+struct Pal {
+    FmtK f[APS_MAX_FORMATS];
+};
+
+struct Layers {
+    const int64_t* __restrict__ offsets;
+    const uint8_t* __restrict__ fmt_idx;
+    const int32_t* __restrict__ scale_exp;
+    int64_t n;
+    int32_t L;
+    int32_t n_fmts;
+};
+
+// Copy of the palette in LDS, for kernels that index it per lane.
+__device__ __forceinline__ void pal_to_lds(const Pal& pal, FmtK* spal) {
+    if (threadIdx.x < APS_MAX_FORMATS) spal[threadIdx.x] = pal.f[threadIdx.x];
+    __syncthreads();
+}
+
+__device__ __forceinline__ float u2f(uint32_t u) { return __uint_as_float(u); }
+__device__ __forceinline__ uint32_t f2u(float f) { return __float_as_uint(f); }
+
+__device__ __forceinline__ int clamp_exp(int32_t ft) {
+    // |ft| beyond 400 takes every fp32 value to 0 or INF exactly as 400 does
+    return ft < -400 ? -400 : (ft > 400 ? 400 : ft);
+}
+
+// ------------------------------------------------------------ rounding
+
+template <int V>
+struct VT {
+    static constexpr int cls = V <= V_INT_M0 ? CLS_INT : (V <= V_TOP_M0 ? CLS_TOP : CLS_LOW);
+    static constexpr int acc = V == V_INT_EXACT ? ACC_EXACT
+                               : ((V == V_INT_F64 || V == V_TOP_F64 || V == V_LOW_F64) ? ACC_F64 : ACC_F32);
+    static constexpr bool m0 = (V == V_INT_M0 || V == V_TOP_M0 || V == V_LOW_M0);
+};
+
+// Working-domain format value of fl32(x * 2^F) (F already includes the
+// domain shift k).  Sets `bad` when the input is NaN (m = 0 formats have no
+// NaN pattern that survives the rounding, so NaN is tracked on the side).
+template <int V>
+__device__ __forceinline__ float quant(float x, int F, const FmtK& f, bool& bad) {
+    using T = VT<V>;
+    const float y = __builtin_amdgcn_ldexpf(x, F);
+    if constexpr (T::m0) bad |= (x != x);
+    if constexpr (T::acc == ACC_EXACT) {
+        return y;
+    } else if constexpr (T::cls == CLS_INT) {
+        const uint32_t b = f2u(y);
+        uint32_t r;
+        if constexpr (T::m0) {
+            // tie bit: 1 for normal fp32 (round half up), 0 on fp32's subnormal grid
+            r = b + ((1u << 22) - 1u) + min(__builtin_amdgcn_ubfe(b, 23, 8), 1u);
+        } else {
+            r = b + f.half + __builtin_amdgcn_ubfe(b, f.sh, T::acc == ACC_F32 ? 1u : f.lsbw);
+            r = (y != y) ? b : r;  // a NaN keeps its quiet payload
+        }
+        return u2f(r & f.mask);
+    } else {
+        const uint32_t b = f2u(y);
+        uint32_t rn;
+        if constexpr (T::m0)
+            rn = b + f.half;
+        else
+            rn = b + f.half + __builtin_amdgcn_ubfe(b, f.sh, T::acc == ACC_F32 ? 1u : f.lsbw);
+        float ys = y;
+        if constexpr (T::cls == CLS_LOW) ys = __builtin_amdgcn_ldexpf(y, -f.j);
+        float rs = (__builtin_fabsf(ys) + f.c0) - f.c0;
+        if constexpr (T::cls == CLS_LOW) rs = __builtin_amdgcn_ldexpf(rs, f.j);
+        const uint32_t rsb = (b & 0x80000000u) | f2u(rs);
+        // NaN fails the compare and takes the subnormal path, which keeps it NaN
+        const uint32_t r = (__builtin_fabsf(y) >= f.thr) ? rn : rsb;
+        return u2f(r & f.mask);
+    }
+}
+
+// R_fmt(s + q) for two working-domain format values.
+template <int V>
+__device__ __forceinline__ float accum(float s, float q, const FmtK& f, bool& bad) {
+    using T = VT<V>;
+    if constexpr (T::acc == ACC_EXACT) {
+        return s + q;
+    } else if constexpr (T::acc == ACC_F32) {
+        const float t = s + q;
+        if constexpr (T::m0) bad |= (t != t);
+        const uint32_t b = f2u(t);
+        uint32_t r;
+        if constexpr (T::m0)
+            r = b + f.half;
+        else
+            r = b + f.half + __builtin_amdgcn_ubfe(b, f.sh, 1u);
+        return u2f(r & f.mask);
+    } else {
+        const double t = (double)s + (double)q;
+        const uint64_t b = (uint64_t)__double_as_longlong(t);
+        const uint64_t r = (b + f.half64 + ((b >> f.sh64) & 1ull)) & f.mask64;
+        return (float)__longlong_as_double((long long)r);
+    }
+}
+
+template <int V>
+__device__ __forceinline__ float finish(float s, bool bad) {
+    if constexpr (VT<V>::m0) return bad ? __builtin_nanf("") : s;
+    return s;
+}
+
+// ---------------------------------------------------------------- codes
+
+// code of a native-domain format value v
+__device__ __forceinline__ uint32_t encode(float v, const FmtK& f) {
+    const uint32_t b = f2u(v);
+    const uint32_t sign = (b >> 31) << (f.e + f.m);
+    const uint32_t a = b & 0x7FFFFFFFu;
+    uint32_t c;
+    if (a > 0x7F800000u)
+        c = (uint32_t)f.emax_code | (f.m > 0 ? (1u << (f.m - 1)) : 0u);
+    else if (a == 0x7F800000u)
+        c = (uint32_t)f.emax_code;
+    else if (a < (uint32_t)(f.emin + 127) << 23)  // below 2^emin: subnormal or zero
+        c = (uint32_t)__builtin_amdgcn_ldexpf(u2f(a), f.m - f.emin);
+    else
+        c = (a >> (23 - f.m)) - ((uint32_t)(127 - f.bias) << f.m);
+    return sign | c;
+}
+
+__device__ __forceinline__ float decode(uint32_t code, const FmtK& f) {
+    const uint32_t ef = (code >> f.m) & ((1u << f.e) - 1u);
+    const uint32_t mant = code & ((1u << f.m) - 1u);
+    float a;
+    if (ef == (1u << f.e) - 1u)
+        a = mant ? __builtin_nanf("") : __builtin_inff();
+    else if (ef == 0)
+        a = __builtin_amdgcn_ldexpf((float)mant, f.emin - f.m);
+    else
+        a = u2f(((ef + 127u - (uint32_t)f.bias) << 23) | (mant << (23 - f.m)));
+    return ((code >> (f.e + f.m)) & 1u) ? -a : a;
+}
+
+__device__ __forceinline__ int64_t code_byte(int64_t j, int cls) {
+    return cls == 0 ? (j >> 1) : (cls == 1 ? j : 2 * j);
+}
+
+// Store the codes of elements j..j+3 (j % 4 == 0) of a row; only those < lim.
+__device__ __forceinline__ void store_codes4(uint8_t* row, int64_t j, const uint32_t c[4], int cls, int64_t lim) {
+    if (j + 4 <= lim) {
+        if (cls == 0) {
+            const uint16_t v = (uint16_t)((c[0] & 15u) | ((c[1] & 15u) << 4) | ((c[2] & 15u) << 8) | ((c[3] & 15u) << 12));
+            *(uint16_t*)(row + (j >> 1)) = v;
+        } else if (cls == 1) {
+            *(uint32_t*)(row + j) = (c[0] & 255u) | ((c[1] & 255u) << 8) | ((c[2] & 255u) << 16) | (c[3] << 24);
+        } else {
+            uint2 v;
+            v.x = (c[0] & 0xFFFFu) | (c[1] << 16);
+            v.y = (c[2] & 0xFFFFu) | (c[3] << 16);
+            *(uint2*)(row + 2 * j) = v;
+        }
+        return;
+    }
+    for (int e = 0; e < 4; ++e) {
+        const int64_t jj = j + e;
+        if (jj >= lim) break;
+        if (cls == 0) {
+            uint8_t* p = row + (jj >> 1);
+            const int sh = (int)(jj & 1) * 4;
+            *p = (uint8_t)((*p & ~(15u << sh)) | ((c[e] & 15u) << sh));
+        } else if (cls == 1) {
+            row[jj] = (uint8_t)c[e];
+        } else {
+            *(uint16_t*)(row + 2 * jj) = (uint16_t)c[e];
+        }
+    }
+}
+
+__device__ __forceinline__ uint32_t load_code(const uint8_t* row, int64_t j, int cls) {
+    if (cls == 0) return (row[j >> 1] >> ((j & 1) * 4)) & 15u;
+    if (cls == 1) return row[j];
+    return *(const uint16_t*)(row + 2 * j);
+}
+
+// --------------------------------------------------------- chunk walking
+
+// Largest i in [0, L-1] with offsets[i] <= pos (pos < n), searching from a hint.
+__device__ __forceinline__ int find_layer(const int64_t* __restrict__ off, int L, int64_t pos, int hint) {
+    int i = hint;
+    if (off[i] > pos) {
+        int lo = 0, hi = i;
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (off[mid] <= pos) lo = mid; else hi = mid;
+        }
+        return lo;
+    }
+    for (int s = 0; s < 4; ++s) {
+        if (i + 1 >= L || off[i + 1] > pos) return i;
+        ++i;
+    }
+    int lo = i, hi = L;  // off[lo] <= pos; off[L] = n > pos
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (off[mid] <= pos) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+// Layers of chunk [start, end): first i0, last i1 (uniform); whether they all
+// use one palette entry, and which.
+struct ChunkInfo {
+    int i0, i1, pidx;
+    bool mixed;
+};
+
+__device__ __forceinline__ ChunkInfo chunk_layers(const Layers& ly, int64_t start, int64_t end, int hint) {
+    ChunkInfo ci;
+    ci.i0 = find_layer(ly.offsets, ly.L, start, hint);
+    int i = ci.i0;
+    while (ly.offsets[i + 1] < end) ++i;  // offsets[L] = n >= end
+    ci.i1 = i;
+    ci.pidx = ly.fmt_idx ? ly.fmt_idx[ci.i0] : 0;
+    ci.mixed = false;
+    if (ly.fmt_idx && ci.i1 > ci.i0) {
+        for (int t = ci.i0 + 1; t <= ci.i1; ++t) {
+            if (ly.offsets[t] == ly.offsets[t + 1]) continue;  // empty layer
+            if (ly.fmt_idx[t] != ci.pidx) ci.mixed = true;
+        }
+    }
+    return ci;
+}
+
+// Per-element scale exponent for elements j..j+3 of a chunk spanning layers i0..i1.
+__device__ __forceinline__ void elem_scales(const Layers& ly, const ChunkInfo& ci, int64_t j, int32_t ft[4]) {
+    int li = ci.i0;
+    for (int e = 0; e < 4; ++e) {
+        const int64_t jj = j + e;
+        while (li < ci.i1 && ly.offsets[li + 1] <= jj) ++li;
+        ft[e] = ly.scale_exp ? clamp_exp(ly.scale_exp[li]) : 0;
+    }
+}
+
+__device__ __forceinline__ void block_range(int64_t nitems, int64_t& b, int64_t& e) {
+    const int64_t G = gridDim.x;
+    b = nitems * (int64_t)blockIdx.x / G;
+    e = nitems * ((int64_t)blockIdx.x + 1) / G;
+}
+
+__device__ __forceinline__ f4 ld4(const float* p) { return __builtin_nontemporal_load((const f4*)p); }
+
+// ============================================================ K0: fill
+
+__global__ void k_fill_u32(uint32_t* __restrict__ p, int64_t cnt, uint32_t v) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < cnt) p[i] = v;
+}
+
+// ======================================================== K1: max-abs
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+    for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, 64));
+    return v;
+}
+
+__global__ __launch_bounds__(BLOCK) void k_maxabs(const float* __restrict__ G, int32_t W, int64_t ld,
+                                                 Layers ly, uint32_t* __restrict__ maxabs) {
+    __shared__ uint32_t red[BLOCK / 64];
+    const int64_t nchunks = (ly.n + CH - 1) / CH;
+    int64_t cb, ce;
+    block_range(nchunks, cb, ce);
+    int hint = 0;
+    uint32_t run = 0;      // running max for layer run_layer (uniform layer runs only)
+    int run_layer = -1;
+    for (int64_t c = cb; c < ce; ++c) {
+        const int64_t start = c * CH;
+        const int64_t end = min(start + CH, ly.n);
+        const ChunkInfo ci = chunk_layers(ly, start, end, hint);
+        hint = ci.i0;
+        const int64_t j = start + (int64_t)threadIdx.x * VEC;
+        uint32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
+        if (j < end) {
+            const float* p = G + j;
+            for (int w = 0; w < W; ++w) {
+                const f4 x = ld4(p);
+                p += ld;
+                m0 = max(m0, f2u(x.x) & 0x7FFFFFFFu);
+                m1 = max(m1, f2u(x.y) & 0x7FFFFFFFu);
+                m2 = max(m2, f2u(x.z) & 0x7FFFFFFFu);
+                m3 = max(m3, f2u(x.w) & 0x7FFFFFFFu);
+            }
+            // elements past the end of the gradient (row padding) do not count
+            if (j + 1 >= end) m1 = 0;
+            if (j + 2 >= end) m2 = 0;
+            if (j + 3 >= end) m3 = 0;
+        }
+        if (ci.i0 == ci.i1) {
+            uint32_t v = max(max(m0, m1), max(m2, m3));
+            if (ci.i0 != run_layer) {
+                if (run_layer >= 0) {
+                    // flush the previous run (block-wide max, one atomic)
+                    uint32_t r = wave_max_u32(run);
+                    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = r;
+                    __syncthreads();
+                    if (threadIdx.x == 0) {
+                        uint32_t t = red[0];
+                        for (int k = 1; k < BLOCK / 64; ++k) t = max(t, red[k]);
+                        if (t) atomicMax(maxabs + run_layer, t);
+                    }
+                    __syncthreads();
+                }
+                run_layer = ci.i0;
+                run = 0;
+            }
+            run = max(run, v);
+        } else if (j < end) {
+            // chunk crosses layer boundaries: one atomic per element
+            const uint32_t mv[4] = {m0, m1, m2, m3};
+            int li = ci.i0;
+            for (int e = 0; e < 4; ++e) {
+                const int64_t jj = j + e;
+                if (jj >= end) break;
+                while (li < ci.i1 && ly.offsets[li + 1] <= jj) ++li;
+                if (mv[e]) atomicMax(maxabs + li, mv[e]);
+            }
+        }
+    }
+    if (run_layer >= 0) {
+        uint32_t r = wave_max_u32(run);
+        if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = r;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint32_t t = red[0];
+            for (int k = 1; k < BLOCK / 64; ++k) t = max(t, red[k]);
+            if (t) atomicMax(maxabs + run_layer, t);
+        }
+    }
+}
+
+// ========================================================= K2: scales
+
+__device__ __forceinline__ int ceil_log2_bits(uint32_t t) {
+    // t: bits of a finite positive fp32
+    const uint32_t ef = t >> 23, frac = t & 0x7FFFFFu;
+    if (ef == 0) {  // subnormal: t = frac * 2^-149
+        const int fl = 31 - __builtin_clz(frac);
+        return fl - 149 + ((frac & (frac - 1u)) ? 1 : 0);
+    }
+    return (int)ef - 127 + (frac ? 1 : 0);
+}
+
+__global__ void k_scales(const uint32_t* __restrict__ maxabs, int32_t L, int32_t N, Pal pal,
+                         const uint8_t* __restrict__ fmt_idx, int32_t* __restrict__ scale_exp) {
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    pal_to_lds(pal, spal);
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= L) return;
+    const FmtK& f = spal[fmt_idx ? fmt_idx[i] : 0];
+    const uint32_t gb = maxabs[i] & 0x7FFFFFFFu;
+    int32_t r = 0;
+    if (gb != 0 && gb < 0x7F800000u) {
+        const float t = (float)N * u2f(gb);  // fl32(N * ghat), N <= 2^24 is exact in fp32
+        const uint32_t tb = f2u(t);
+        if (tb < 0x7F800000u) r = f.emax - ceil_log2_bits(tb);
+    }
+    scale_exp[i] = r;
+}
+
+// ===================================================== K4: sim reduce
+
+struct ReduceArgs {
+    const float* __restrict__ G;
+    float* __restrict__ out;
+    uint8_t* __restrict__ codes;
+    int64_t ld;
+    int32_t W;
+    uint32_t flags;
+    int32_t code_cls;
+};
+
+template <int V>
+__device__ __forceinline__ void reduce_vec(const ReduceArgs& a, const FmtK& f, int64_t j, int64_t lim,
+                                           const int32_t ft[4]) {
+    const bool inq = a.flags & APS_INPUT_QUANTIZED;
+    const bool outs = a.flags & APS_OUTPUT_SCALED;
+    int F[4], Fo[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        F[e] = (inq ? 0 : ft[e]) + f.k;
+        Fo[e] = -((outs ? 0 : ft[e]) + f.k);
+    }
+    bool bad0 = false, bad1 = false, bad2 = false, bad3 = false;
+    const float* p = a.G + j;
+    const int64_t ld = a.ld;
+    const int W = a.W;
+    // Two register sets of UNROLL rows each: while one set is consumed, the
+    // loads of the next UNROLL rows (into the other set) are already in
+    // flight; the scheduling barrier keeps those loads ahead of the math.
+    // Loads past the last row are clamped to row W-1 and their values are
+    // replaced by -0 when consumed (s + -0 == s, signs of zero included), so
+    // every path consumes the same loads and the compiler waits for exactly
+    // the row it is about to use.
+    f4 A[UNROLL], B[UNROLL];
+    const f4 neg0 = {-0.0f, -0.0f, -0.0f, -0.0f};
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) A[u] = ld4(p + (int64_t)min(u, W - 1) * ld);
+#define APS_CONSUME(v)                                                   \
+    do {                                                                 \
+        s0 = accum<V>(s0, quant<V>((v).x, F[0], f, bad0), f, bad0);      \
+        s1 = accum<V>(s1, quant<V>((v).y, F[1], f, bad1), f, bad1);      \
+        s2 = accum<V>(s2, quant<V>((v).z, F[2], f, bad2), f, bad2);      \
+        s3 = accum<V>(s3, quant<V>((v).w, F[3], f, bad3), f, bad3);      \
+    } while (0)
+#define APS_LOAD(NXT)                                                    \
+    _Pragma("unroll") for (int u = 0; u < UNROLL; ++u)                   \
+        NXT[u] = ld4(p + (int64_t)min(w + UNROLL + u, W - 1) * ld);      \
+    __builtin_amdgcn_sched_barrier(0);
+#define APS_LAST(CUR)                                                    \
+    _Pragma("unroll") for (int u = 0; u < UNROLL; ++u) {                 \
+        const f4 v = (w + u < W) ? CUR[u] : neg0;                        \
+        APS_CONSUME(v);                                                  \
+    }
+#define APS_STEP(CUR, NXT)                                               \
+    if (w + UNROLL < W) {                                                \
+        APS_LOAD(NXT)                                                    \
+        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u)               \
+            APS_CONSUME(CUR[u]);                                         \
+        w += UNROLL;                                                     \
+    } else {                                                             \
+        APS_LAST(CUR)                                                    \
+        break;                                                           \
+    }
+    int w = 0;
+    const bool more = UNROLL < W;
+    if (more) {
+        APS_LOAD(B)
+    }
+    // row 0 starts the sums; rows 1..UNROLL-1 of the first group follow
+    float s0 = quant<V>(A[0].x, F[0], f, bad0);
+    float s1 = quant<V>(A[0].y, F[1], f, bad1);
+    float s2 = quant<V>(A[0].z, F[2], f, bad2);
+    float s3 = quant<V>(A[0].w, F[3], f, bad3);
+    if (more) {
+#pragma unroll
+        for (int u = 1; u < UNROLL; ++u) APS_CONSUME(A[u]);
+        w = UNROLL;
+        for (;;) {
+            APS_STEP(B, A)
+            APS_STEP(A, B)
+        }
+    } else {
+#pragma unroll
+        for (int u = 1; u < UNROLL; ++u) {
+            const f4 v = (u < W) ? A[u] : neg0;
+            APS_CONSUME(v);
+        }
+    }
+#undef APS_STEP
+#undef APS_LAST
+#undef APS_LOAD
+#undef APS_CONSUME
+    s0 = finish<V>(s0, bad0);
+    s1 = finish<V>(s1, bad1);
+    s2 = finish<V>(s2, bad2);
+    s3 = finish<V>(s3, bad3);
+    if (a.out) {
+        f4 o;
+        o.x = __builtin_amdgcn_ldexpf(s0, Fo[0]);
+        o.y = __builtin_amdgcn_ldexpf(s1, Fo[1]);
+        o.z = __builtin_amdgcn_ldexpf(s2, Fo[2]);
+        o.w = __builtin_amdgcn_ldexpf(s3, Fo[3]);
+        if (j + 4 <= lim) {
+            __builtin_nontemporal_store(o, (f4*)(a.out + j));
+        } else {
+            if (j < lim) a.out[j] = o.x;
+            if (j + 1 < lim) a.out[j + 1] = o.y;
+            if (j + 2 < lim) a.out[j + 2] = o.z;
+        }
+    }
+    if (a.codes) {
+        uint32_t c[4];
+        c[0] = encode(__builtin_amdgcn_ldexpf(s0, -f.k), f);
+        c[1] = encode(__builtin_amdgcn_ldexpf(s1, -f.k), f);
+        c[2] = encode(__builtin_amdgcn_ldexpf(s2, -f.k), f);
+        c[3] = encode(__builtin_amdgcn_ldexpf(s3, -f.k), f);
+        store_codes4(a.codes, j, c, a.code_cls, lim);
+    }
+}
+
+template <int V>
+__global__ __launch_bounds__(BLOCK) void k_sim_reduce(ReduceArgs a, Layers ly, Pal pal) {
+    const int64_t nchunks = (ly.n + CH - 1) / CH;
+    int64_t cb, ce;
+    block_range(nchunks, cb, ce);
+    int hint = 0;
+    for (int64_t c = cb; c < ce; ++c) {
+        const int64_t start = c * CH;
+        const int64_t end = min(start + CH, ly.n);
+        const ChunkInfo ci = chunk_layers(ly, start, end, hint);
+        hint = ci.i0;
+        if (ci.mixed) continue;  // handled by k_sim_reduce_mixed
+        const FmtK& f = pal.f[ci.pidx];
+        if (f.variant != V) continue;  // another launch owns this format
+        const int64_t j = start + (int64_t)threadIdx.x * VEC;
+        if (j >= end) continue;
+        int32_t ft[4];
+        if (ci.i0 == ci.i1) {
+            const int32_t t = ly.scale_exp ? clamp_exp(ly.scale_exp[ci.i0]) : 0;
+            ft[0] = ft[1] = ft[2] = ft[3] = t;
+        } else {
+            elem_scales(ly, ci, j, ft);
+        }
+        reduce_vec<V>(a, f, j, end, ft);
+    }
+}
+
+// One element through the whole W-worker loop, any variant (per-lane format).
+template <int V>
+__device__ float reduce_elem(const ReduceArgs& a, const FmtK& f, int64_t j, int F) {
+    bool bad = false;
+    float s = quant<V>(a.G[j], F, f, bad);
+    for (int w = 1; w < a.W; ++w) s = accum<V>(s, quant<V>(a.G[(int64_t)w * a.ld + j], F, f, bad), f, bad);
+    return finish<V>(s, bad);
+}
+
+__device__ float reduce_elem_any(const ReduceArgs& a, const FmtK& f, int64_t j, int F) {
+    switch (f.variant) {
+        case V_INT_F32: return reduce_elem<V_INT_F32>(a, f, j, F);
+        case V_INT_F64: return reduce_elem<V_INT_F64>(a, f, j, F);
+        case V_INT_EXACT: return reduce_elem<V_INT_EXACT>(a, f, j, F);
+        case V_INT_M0: return reduce_elem<V_INT_M0>(a, f, j, F);
+        case V_TOP_F32: return reduce_elem<V_TOP_F32>(a, f, j, F);
+        case V_TOP_F64: return reduce_elem<V_TOP_F64>(a, f, j, F);
+        case V_TOP_M0: return reduce_elem<V_TOP_M0>(a, f, j, F);
+        case V_LOW_F32: return reduce_elem<V_LOW_F32>(a, f, j, F);
+        case V_LOW_F64: return reduce_elem<V_LOW_F64>(a, f, j, F);
+        default: return reduce_elem<V_LOW_M0>(a, f, j, F);
+    }
+}
+
+// Chunks whose layers use different palette entries.  One block per layer
+// boundary; the block owning the first boundary strictly inside a chunk
+// processes that chunk element by element.
+__device__ __forceinline__ bool mixed_chunk_of_boundary(const Layers& ly, int b, int64_t& start, int64_t& end) {
+    if (b < 1 || b >= ly.L) return false;
+    const int64_t p = ly.offsets[b];
+    if (p <= 0 || p >= ly.n || p % CH == 0) return false;
+    const int64_t c = p / CH;
+    start = c * CH;
+    end = min(start + CH, ly.n);
+    if (ly.offsets[b - 1] > start) return false;  // an earlier boundary owns it
+    const ChunkInfo ci = chunk_layers(ly, start, end, 0);
+    return ci.mixed;
+}
+
+__device__ __forceinline__ void put_code(uint8_t* row, int64_t j, uint32_t c, int cls) {
+    if (cls == 1)
+        row[j] = (uint8_t)c;
+    else
+        *(uint16_t*)(row + 2 * j) = (uint16_t)c;
+}
+
+// Each thread owns an element pair (2t, 2t+1) of the chunk, so a byte of
+// nibble codes is written by one thread only.
+__global__ __launch_bounds__(BLOCK) void k_sim_reduce_mixed(ReduceArgs a, Layers ly, Pal pal) {
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    pal_to_lds(pal, spal);
+    int64_t start, end;
+    if (!mixed_chunk_of_boundary(ly, blockIdx.x, start, end)) return;
+    for (int64_t j0 = start + 2 * (int64_t)threadIdx.x; j0 < end; j0 += 2 * BLOCK) {
+        uint32_t c[2] = {0, 0};
+        for (int e = 0; e < 2; ++e) {
+            const int64_t j = j0 + e;
+            if (j >= end) break;
+            const int li = find_layer(ly.offsets, ly.L, j, 0);
+            const FmtK& f = spal[ly.fmt_idx[li]];
+            const int32_t ft = ly.scale_exp ? clamp_exp(ly.scale_exp[li]) : 0;
+            const int F = ((a.flags & APS_INPUT_QUANTIZED) ? 0 : ft) + f.k;
+            const int Fo = -(((a.flags & APS_OUTPUT_SCALED) ? 0 : ft) + f.k);
+            const float s = reduce_elem_any(a, f, j, F);
+            if (a.out) a.out[j] = __builtin_amdgcn_ldexpf(s, Fo);
+            c[e] = encode(__builtin_amdgcn_ldexpf(s, -f.k), f);
+            if (a.codes && a.code_cls != 0) put_code(a.codes, j, c[e], a.code_cls);
+        }
+        if (a.codes && a.code_cls == 0) {
+            uint8_t* pb = a.codes + (j0 >> 1);
+            *pb = (j0 + 1 < end) ? (uint8_t)((c[0] & 15u) | ((c[1] & 15u) << 4))
+                                 : (uint8_t)((*pb & 0xF0u) | (c[0] & 15u));
+        }
+    }
+}
+
+// ======================================================= K3: quantize
+
+struct QuantArgs {
+    const float* __restrict__ X;
+    float* Q;  // may alias X
+    uint8_t* __restrict__ codes;
+    int64_t ld;
+    int32_t W;
+    int32_t code_cls;
+};
+
+template <int V>
+__global__ __launch_bounds__(BLOCK) void k_quantize(QuantArgs a, Layers ly, Pal pal) {
+    const int64_t nchunks = (ly.n + CH - 1) / CH;
+    int64_t tb, te;
+    block_range(nchunks * a.W, tb, te);
+    int hint = 0;
+    for (int64_t t = tb; t < te; ++t) {
+        const int64_t w = t / nchunks;
+        const int64_t c = t - w * nchunks;
+        const int64_t start = c * CH;
+        const int64_t end = min(start + CH, ly.n);
+        const ChunkInfo ci = chunk_layers(ly, start, end, hint);
+        hint = ci.i0;
+        if (ci.mixed) continue;
+        const FmtK& f = pal.f[ci.pidx];
+        if (f.variant != V) continue;
+        const int64_t j = start + (int64_t)threadIdx.x * VEC;
+        if (j >= end) continue;
+        int32_t ft[4];
+        if (ci.i0 == ci.i1) {
+            const int32_t s = ly.scale_exp ? clamp_exp(ly.scale_exp[ci.i0]) : 0;
+            ft[0] = ft[1] = ft[2] = ft[3] = s;
+        } else {
+            elem_scales(ly, ci, j, ft);
+        }
+        const int64_t off = w * a.ld + j;
+        const f4 x = *(const f4*)(a.X + off);
+        bool bad = false;
+        float q[4];
+        q[0] = quant<V>(x.x, ft[0] + f.k, f, bad);
+        q[1] = quant<V>(x.y, ft[1] + f.k, f, bad);
+        q[2] = quant<V>(x.z, ft[2] + f.k, f, bad);
+        q[3] = quant<V>(x.w, ft[3] + f.k, f, bad);
+        const float xs[4] = {x.x, x.y, x.z, x.w};
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            v[e] = __builtin_amdgcn_ldexpf(q[e], -f.k);                   // native scaled value
+            if constexpr (VT<V>::m0) v[e] = (xs[e] != xs[e]) ? xs[e] : v[e];  // NaN stays NaN
+        }
+        if (a.Q) {
+            if (j + 4 <= end) {
+                f4 o;
+                o.x = v[0];
+                o.y = v[1];
+                o.z = v[2];
+                o.w = v[3];
+                *(f4*)(a.Q + off) = o;
+            } else {
+                for (int e = 0; e < 4 && j + e < end; ++e) a.Q[off + e] = v[e];
+            }
+        }
+        if (a.codes) {
+            uint32_t cc[4];
+            for (int e = 0; e < 4; ++e) cc[e] = encode(v[e], f);
+            store_codes4(a.codes + code_byte(w * a.ld, a.code_cls), j, cc, a.code_cls, end);
+        }
+    }
+}
+
+template <int V>
+__device__ float quant_one(float x, int F, const FmtK& f) {
+    bool bad = false;
+    const float q = __builtin_amdgcn_ldexpf(quant<V>(x, F, f, bad), -f.k);
+    return bad ? x : q;
+}
+
+__device__ float quant_any(float x, int F, const FmtK& f) {
+    switch (f.variant) {
+        case V_INT_F32: return quant_one<V_INT_F32>(x, F, f);
+        case V_INT_F64: return quant_one<V_INT_F64>(x, F, f);
+        case V_INT_EXACT: return quant_one<V_INT_EXACT>(x, F, f);
+        case V_INT_M0: return quant_one<V_INT_M0>(x, F, f);
+        case V_TOP_F32: return quant_one<V_TOP_F32>(x, F, f);
+        case V_TOP_F64: return quant_one<V_TOP_F64>(x, F, f);
+        case V_TOP_M0: return quant_one<V_TOP_M0>(x, F, f);
+        case V_LOW_F32: return quant_one<V_LOW_F32>(x, F, f);
+        case V_LOW_F64: return quant_one<V_LOW_F64>(x, F, f);
+        default: return quant_one<V_LOW_M0>(x, F, f);
+    }
+}
+
+// Mixed-format chunks, all W rows; grid (boundary, worker); element pairs
+// per thread as in k_sim_reduce_mixed.
+__global__ __launch_bounds__(BLOCK) void k_quantize_mixed(QuantArgs a, Layers ly, Pal pal) {
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    pal_to_lds(pal, spal);
+    int64_t start, end;
+    if (!mixed_chunk_of_boundary(ly, blockIdx.x, start, end)) return;
+    const int64_t w = blockIdx.y;
+    uint8_t* row = a.codes ? a.codes + code_byte(w * a.ld, a.code_cls) : nullptr;
+    for (int64_t j0 = start + 2 * (int64_t)threadIdx.x; j0 < end; j0 += 2 * BLOCK) {
+        uint32_t c[2] = {0, 0};
+        for (int e = 0; e < 2; ++e) {
+            const int64_t j = j0 + e;
+            if (j >= end) break;
+            const int li = find_layer(ly.offsets, ly.L, j, 0);
+            const FmtK& f = spal[ly.fmt_idx[li]];
+            const int32_t ft = ly.scale_exp ? clamp_exp(ly.scale_exp[li]) : 0;
+            const int64_t off = w * a.ld + j;
+            const float v = quant_any(a.X[off], ft + f.k, f);  // Q may alias X: same element
+            if (a.Q) a.Q[off] = v;
+            c[e] = encode(v, f);
+            if (row && a.code_cls != 0) put_code(row, j, c[e], a.code_cls);
+        }
+        if (row && a.code_cls == 0) {
+            uint8_t* pb = row + (j0 >> 1);
+            *pb = (j0 + 1 < end) ? (uint8_t)((c[0] & 15u) | ((c[1] & 15u) << 4))
+                                 : (uint8_t)((*pb & 0xF0u) | (c[0] & 15u));
+        }
+    }
+}
+
+// ===================================================== K5: dequantize
+
+struct DeqArgs {
+    const float* Q;  // may alias out
+    const uint8_t* __restrict__ codes;
+    float* out;
+    int32_t code_cls;
+};
+
+__global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal pal) {
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    pal_to_lds(pal, spal);
+    const int64_t nchunks = (ly.n + CH - 1) / CH;
+    int64_t cb, ce;
+    block_range(nchunks, cb, ce);
+    int hint = 0;
+    for (int64_t c = cb; c < ce; ++c) {
+        const int64_t start = c * CH;
+        const int64_t end = min(start + CH, ly.n);
+        const int i0 = find_layer(ly.offsets, ly.L, start, hint);
+        hint = i0;
+        const int64_t j = start + (int64_t)threadIdx.x * VEC;
+        if (j >= end) continue;
+        int li = i0;
+        for (int e = 0; e < 4; ++e) {
+            const int64_t jj = j + e;
+            if (jj >= end) break;
+            while (ly.offsets[li + 1] <= jj) ++li;
+            const FmtK& f = spal[ly.fmt_idx ? ly.fmt_idx[li] : 0];
+            const int32_t ft = ly.scale_exp ? clamp_exp(ly.scale_exp[li]) : 0;
+            const float v = a.Q ? a.Q[jj] : decode(load_code(a.codes, jj, a.code_cls), f);
+            a.out[jj] = __builtin_amdgcn_ldexpf(v, -ft);
+        }
+    }
+}
+
+// ================================================================ host
+
+static int device_cus() {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    return cus;
+}
+
+static int64_t grid_for(int64_t items, int per_cu) {
+    const int cus = device_cus();
+    int64_t g = (int64_t)(cus > 0 ? cus : 256) * per_cu;
+    if (g > items) g = items;
+    return g < 1 ? 1 : g;
+}
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+static int check_palette(const aps_format* fmts, int32_t n_fmts, Pal& pal, int* ccls) {
+    if (!fmts) return APS_ERR_NULL;
+    if (n_fmts < 1 || n_fmts > APS_MAX_FORMATS) return APS_ERR_SIZE;
+    int cls = -1;
+    bool mixed_cls = false;
+    for (int i = 0; i < n_fmts; ++i) {
+        const int st = fmt_status(fmts[i]);
+        if (st != APS_OK) return st;
+        pal.f[i] = make_fmtk(fmts[i]);
+        const int c = code_class(pal.f[i].code_bits);
+        if (cls >= 0 && c != cls) mixed_cls = true;
+        cls = c;
+    }
+    for (int i = n_fmts; i < APS_MAX_FORMATS; ++i) pal.f[i] = pal.f[0];
+    if (ccls) *ccls = mixed_cls ? -1 : cls;
+    return APS_OK;
+}
+
+static int check_rows(const void* G, int32_t W, int64_t ld, int64_t n, const int64_t* offsets, int32_t L) {
+    if (!G || !offsets) return APS_ERR_NULL;
+    if (W < 1 || W > APS_MAX_WORKERS || L < 1 || n < 0 || n > APS_MAX_ELEMS || ld < n) return APS_ERR_SIZE;
+    if (!aligned16(G) || (ld & 3)) return APS_ERR_ALIGN;
+    return APS_OK;
+}
+
+static int launched() { return hipGetLastError() == hipSuccess ? APS_OK : APS_ERR_DEVICE; }
+
+// which variants occur in the palette
+static unsigned variant_mask(const Pal& pal, int32_t n_fmts) {
+    unsigned m = 0;
+    for (int i = 0; i < n_fmts; ++i) m |= 1u << pal.f[i].variant;
+    return m;
+}
+
+}  // namespace aps
+
+using namespace aps;
+
+// The kernels are templates over the variant; dispatch table per entry point.
+#define APS_FOR_VARIANTS(X) X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9)
+
+extern "C" int aps_format_supported(aps_format f) { return fmt_status(f); }
+
+extern "C" const char* aps_strerror(int s) {
+    switch (s) {
+        case APS_OK: return "ok";
+        case APS_ERR_NULL: return "required pointer is NULL";
+        case APS_ERR_SIZE: return "size argument out of range";
+        case APS_ERR_FORMAT: return "format {e, m, bias} out of range";
+        case APS_ERR_ALIGN: return "pointer or row stride misaligned";
+        case APS_ERR_UNSUPPORTED: return "valid but unsupported combination";
+        case APS_ERR_DEVICE: return "HIP launch or device error";
+        default: return "unknown status";
+    }
+}
+
+extern "C" int aps_layer_maxabs(const float* G, int32_t W, int64_t ld, int64_t n, const int64_t* offsets,
+                                int32_t L, uint32_t* maxabs_bits, void* stream) {
+    int st = check_rows(G, W, ld, n, offsets, L);
+    if (st != APS_OK) return st;
+    if (!maxabs_bits) return APS_ERR_NULL;
+    hipStream_t s = (hipStream_t)stream;
+    hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)((L + 255) / 256)), dim3(256), 0, s, maxabs_bits, (int64_t)L, 0u);
+    if (n == 0) return launched();
+    Layers ly{offsets, nullptr, nullptr, n, L, 1};
+    const int64_t nchunks = (n + CH - 1) / CH;
+    hipLaunchKernelGGL(k_maxabs, dim3((unsigned)grid_for(nchunks, 8)), dim3(BLOCK), 0, s, G, W, ld, ly, maxabs_bits);
+    return launched();
+}
+
+extern "C" int aps_layer_scales(const uint32_t* maxabs_bits, int32_t L, int32_t N, const aps_format* fmts,
+                                int32_t n_fmts, const uint8_t* fmt_idx, int32_t* scale_exp, void* stream) {
+    if (!maxabs_bits || !scale_exp) return APS_ERR_NULL;
+    if (L < 1 || N < 1 || N > APS_MAX_WORKERS) return APS_ERR_SIZE;
+    Pal pal;
+    int st = check_palette(fmts, n_fmts, pal, nullptr);
+    if (st != APS_OK) return st;
+    hipLaunchKernelGGL(k_scales, dim3((unsigned)((L + 255) / 256)), dim3(256), 0, (hipStream_t)stream, maxabs_bits,
+                       L, N, pal, fmt_idx, scale_exp);
+    return launched();
+}
+
+extern "C" int aps_quantize(const float* X, int32_t W, int64_t ld, int64_t n, const int64_t* offsets, int32_t L,
+                            const int32_t* scale_exp, const aps_format* fmts, int32_t n_fmts,
+                            const uint8_t* fmt_idx, float* Q, void* codes, void* stream) {
+    int st = check_rows(X, W, ld, n, offsets, L);
+    if (st != APS_OK) return st;
+    if (!Q && !codes && n > 0) return APS_ERR_NULL;
+    if ((Q && !aligned16(Q)) || (codes && !aligned16(codes))) return APS_ERR_ALIGN;
+    Pal pal;
+    int ccls = 0;
+    st = check_palette(fmts, n_fmts, pal, &ccls);
+    if (st != APS_OK) return st;
+    if (codes && (ccls < 0 || ccls > 2)) return APS_ERR_UNSUPPORTED;
+    if (n == 0) return APS_OK;
+    hipStream_t s = (hipStream_t)stream;
+    Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
+    QuantArgs a{X, Q, (uint8_t*)codes, ld, W, ccls};
+    const int64_t nchunks = (n + CH - 1) / CH;
+    const dim3 grid((unsigned)grid_for(nchunks * W, 8));
+    const unsigned vm = variant_mask(pal, n_fmts);
+#define APS_LAUNCH_Q(v) \
+    if (vm & (1u << (v))) hipLaunchKernelGGL(k_quantize<v>, grid, dim3(BLOCK), 0, s, a, ly, pal);
+    APS_FOR_VARIANTS(APS_LAUNCH_Q)
+#undef APS_LAUNCH_Q
+    if (fmt_idx && n_fmts > 1 && L > 1)
+        hipLaunchKernelGGL(k_quantize_mixed, dim3((unsigned)L, (unsigned)W), dim3(BLOCK), 0, s, a, ly, pal);
+    return launched();
+}
+
+extern "C" int aps_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n, const int64_t* offsets,
+                              int32_t L, const int32_t* scale_exp, const aps_format* fmts, int32_t n_fmts,
+                              const uint8_t* fmt_idx, uint32_t flags, float* out, void* codes_out,
+                              void* stream) {
+    int st = check_rows(G, W, ld, n, offsets, L);
+    if (st != APS_OK) return st;
+    if (!out && !codes_out && n > 0) return APS_ERR_NULL;
+    if ((out && !aligned16(out)) || (codes_out && !aligned16(codes_out))) return APS_ERR_ALIGN;
+    if (flags & ~(APS_INPUT_QUANTIZED | APS_OUTPUT_SCALED)) return APS_ERR_UNSUPPORTED;
+    Pal pal;
+    int ccls = 0;
+    st = check_palette(fmts, n_fmts, pal, &ccls);
+    if (st != APS_OK) return st;
+    if (codes_out && (ccls < 0 || ccls > 2)) return APS_ERR_UNSUPPORTED;
+    if (n == 0) return APS_OK;
+    hipStream_t s = (hipStream_t)stream;
+    Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
+    ReduceArgs a{G, out, (uint8_t*)codes_out, ld, W, flags, ccls};
+    const int64_t nchunks = (n + CH - 1) / CH;
+    const dim3 grid((unsigned)grid_for(nchunks, 8));
+    const unsigned vm = variant_mask(pal, n_fmts);
+#define APS_LAUNCH_R(v) \
+    if (vm & (1u << (v))) hipLaunchKernelGGL(k_sim_reduce<v>, grid, dim3(BLOCK), 0, s, a, ly, pal);
+    APS_FOR_VARIANTS(APS_LAUNCH_R)
+#undef APS_LAUNCH_R
+    if (fmt_idx && n_fmts > 1 && L > 1)
+        hipLaunchKernelGGL(k_sim_reduce_mixed, dim3((unsigned)L), dim3(BLOCK), 0, s, a, ly, pal);
+    return launched();
+}
+
+extern "C" int aps_dequantize(const float* Q, const void* codes, int64_t n, const int64_t* offsets, int32_t L,
+                              const int32_t* scale_exp, const aps_format* fmts, int32_t n_fmts,
+                              const uint8_t* fmt_idx, float* out, void* stream) {
+    if (!offsets || ((!out || (!Q && !codes)) && n > 0)) return APS_ERR_NULL;
+    if (L < 1 || n < 0 || n > APS_MAX_ELEMS) return APS_ERR_SIZE;
+    if ((Q && !aligned16(Q)) || (codes && !aligned16(codes)) || !aligned16(out)) return APS_ERR_ALIGN;
+    Pal pal;
+    int ccls = 0;
+    int st = check_palette(fmts, n_fmts, pal, &ccls);
+    if (st != APS_OK) return st;
+    if (!Q && (ccls < 0 || ccls > 2)) return APS_ERR_UNSUPPORTED;
+    if (n == 0) return APS_OK;
+    Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
+    DeqArgs a{Q, (const uint8_t*)codes, out, ccls};
+    const int64_t nchunks = (n + CH - 1) / CH;
+    hipLaunchKernelGGL(k_dequantize, dim3((unsigned)grid_for(nchunks, 8)), dim3(BLOCK), 0, (hipStream_t)stream, a,
+                       ly, pal);
+    return launched();
+}

@@ -1,0 +1,160 @@
+// aps_format.hpp -- custom-float constants and device rounding for gfx950.
+//
+// Cast(g, exp_bit, man_bit) of Algorithm 1 (arXiv 1911.08907), with the
+// round-to-nearest-even mode of Sec. 4, the format layout that reproduces
+// Table 2, and the low-precision accumulator of Sec. 5.
+//
+// Working domain.  Every kernel rounds in a shifted copy of the format: a
+// native value v is carried as v * 2^k with k = 127 - emax, so that the
+// format's overflow threshold coincides with fp32's.  Power-of-two scaling is
+// exact (Sec. 3.3.1), so rounding in the shifted domain and shifting back
+// gives the same result as rounding natively, as long as nothing below the
+// format's half-smallest-subnormal is decided by fp32's own underflow; the
+// host only accepts formats for which that holds (or e = 8, bias 127, where
+// k = 0).  In that domain:
+//   * a value with |y| >= 2^emin (format normal range) is rounded on its
+//     fp32 bit pattern: add half an ulp of the m-bit mantissa (plus the
+//     lowest kept bit, for ties to even) and clear the dropped bits.  A carry
+//     out of the mantissa bumps the exponent; at the top it produces the
+//     bit pattern of INF, which is the format's overflow;
+//   * a value below 2^emin (format subnormal range) is rounded onto the fixed
+//     subnormal grid with one fp32 add/subtract of c0 = 2^(emin - m + 23)
+//     ("magic" constant): fp32's own round-to-nearest-even does the work.
+//     When c0 would not be an fp32 value (small e), the subtraction happens
+//     in a domain shifted down by j more bits (class LOW);
+//   * for e = 8 with bias 127 the format's subnormal grid is a coarsening of
+//     fp32's, so the bit-pattern rounding covers every magnitude (class INT).
+// A sum of two format values whose magnitude is below 2^emin is a multiple
+// of the smallest subnormal and so exact, and for m <= 10 an fp32 add
+// followed by one rounding equals rounding the exact sum (24 >= 2(m+1) + 2,
+// the double-rounding bound of Figueroa); wider mantissas add in fp64.
+#pragma once
+
+#include <stdint.h>
+
+#include "aps.h"
+
+namespace aps {
+
+enum Cls : int32_t { CLS_INT = 0, CLS_TOP = 1, CLS_LOW = 2 };
+enum Acc : int32_t { ACC_F32 = 0, ACC_F64 = 1, ACC_EXACT = 2 };
+
+// Kernel variants: one instantiation per (class, accumulator, m == 0).
+enum Variant : int32_t {
+    V_INT_F32 = 0,
+    V_INT_F64 = 1,
+    V_INT_EXACT = 2,
+    V_INT_M0 = 3,
+    V_TOP_F32 = 4,
+    V_TOP_F64 = 5,
+    V_TOP_M0 = 6,
+    V_LOW_F32 = 7,
+    V_LOW_F64 = 8,
+    V_LOW_M0 = 9,
+    N_VARIANTS = 10
+};
+
+// Everything a kernel needs about one palette entry; built on the host.
+struct FmtK {
+    int32_t e, m, bias, emin, emax;
+    int32_t k;        // working value = native value * 2^k
+    int32_t j;        // LOW: subnormal rounding happens at working * 2^-j
+    int32_t variant;  // Variant
+    uint32_t sh;      // 23 - m: dropped fp32 mantissa bits
+    uint32_t lsbw;    // width (0/1) of the tie bit read at position sh
+    uint32_t half;    // increment added before the tie bit
+    uint32_t mask;    // clears the dropped bits
+    float thr;        // 2^emin in the working domain
+    float c0;         // magic constant of the subnormal path (shifted by -j)
+    uint32_t sh64;    // 52 - m  (fp64 accumulator)
+    uint32_t pad0;
+    uint64_t half64;  // 2^(sh64-1) - 1
+    uint64_t mask64;  // clears the dropped fp64 bits
+    int32_t code_bits;
+    int32_t emax_code;  // all-ones exponent field << m
+};
+
+// ------------------------------------------------------------------ host
+
+inline int fmt_status(const aps_format& f) {
+    if (f.e < 2 || f.e > 8 || f.m < 0 || f.m > 23) return APS_ERR_FORMAT;
+    const int emin = 1 - f.bias;
+    const int emax = (1 << f.e) - 2 - f.bias;
+    if (emax > 127 || emin > emax || emin - f.m < -149) return APS_ERR_FORMAT;
+    if (f.e == 8) return f.bias == 127 ? APS_OK : APS_ERR_UNSUPPORTED;
+    // below half the smallest subnormal fp32's own underflow must not matter
+    if (emin - f.m - 1 < -126) return APS_ERR_UNSUPPORTED;
+    return APS_OK;
+}
+
+inline float pow2f_host(int p) {  // exact 2^p for -126 <= p <= 127
+    union {
+        uint32_t u;
+        float f;
+    } v;
+    v.u = (uint32_t)(p + 127) << 23;
+    return v.f;
+}
+
+inline FmtK make_fmtk(const aps_format& f) {
+    FmtK o{};
+    o.e = f.e;
+    o.m = f.m;
+    o.bias = f.bias;
+    o.emin = 1 - f.bias;
+    o.emax = (1 << f.e) - 2 - f.bias;
+    const bool is_int = (f.e == 8 && f.bias == 127);
+    o.k = is_int ? 0 : 127 - o.emax;
+    const int emin_w = o.emin + o.k;
+    o.sh = 23u - (uint32_t)f.m;
+    if (f.m == 0) {  // ties of a 1-bit significand go to the even multiple: up
+        o.half = 1u << 22;
+        o.lsbw = 0;
+    } else if (f.m == 23) {
+        o.half = 0;
+        o.lsbw = 0;
+    } else {
+        o.half = (1u << (o.sh - 1)) - 1u;
+        o.lsbw = 1;
+    }
+    o.mask = ~((1u << o.sh) - 1u);
+    o.thr = pow2f_host(emin_w < -126 ? -126 : emin_w);
+    int cls;
+    if (is_int) {
+        cls = CLS_INT;
+        o.j = 0;
+        o.c0 = 0.f;
+    } else if (emin_w - f.m + 23 <= 127) {
+        cls = CLS_TOP;
+        o.j = 0;
+        o.c0 = pow2f_host(emin_w - f.m + 23);
+    } else {
+        cls = CLS_LOW;
+        o.j = emin_w - f.m + 23 - 127;
+        o.c0 = pow2f_host(127);
+    }
+    int acc;
+    if (is_int && f.m == 23)
+        acc = ACC_EXACT;
+    else if (f.m <= 10)
+        acc = ACC_F32;
+    else
+        acc = ACC_F64;
+    o.sh64 = 52u - (uint32_t)f.m;
+    o.half64 = (1ull << (o.sh64 - 1)) - 1ull;
+    o.mask64 = ~((1ull << o.sh64) - 1ull);
+    if (cls == CLS_INT)
+        o.variant = f.m == 0 ? V_INT_M0 : (acc == ACC_EXACT ? V_INT_EXACT : (acc == ACC_F64 ? V_INT_F64 : V_INT_F32));
+    else if (cls == CLS_TOP)
+        o.variant = f.m == 0 ? V_TOP_M0 : (acc == ACC_F64 ? V_TOP_F64 : V_TOP_F32);
+    else
+        o.variant = f.m == 0 ? V_LOW_M0 : (acc == ACC_F64 ? V_LOW_F64 : V_LOW_F32);
+    o.code_bits = 1 + f.e + f.m;
+    o.emax_code = (int32_t)(((1u << f.e) - 1u) << f.m);
+    return o;
+}
+
+// code container class: 0 nibble, 1 byte, 2 uint16, 3 none
+inline int code_class(int bits) { return bits <= 4 ? 0 : (bits <= 8 ? 1 : (bits <= 16 ? 2 : 3)); }
+
+}  // namespace aps

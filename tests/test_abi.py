@@ -1,0 +1,156 @@
+"""Host-side checks of the C ABI: the library loads, exports what the header
+declares, and rejects bad arguments before anything is enqueued.
+
+Every call below carries at least one invalid argument, so none of them ever
+reaches a kernel launch (these tests run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1911_08907_amd import aps as A
+from paper_1911_08907_amd import build as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "aps.h")
+
+
+def _gpu_visible() -> bool:
+    try:
+        import torch
+        return torch.cuda.device_count() > 0
+    except Exception:
+        return False
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(A.LIB_PATH):
+        B.build()
+    return A.lib()
+
+
+def _declared():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(aps_[a-z_]+)\s*\(", txt)))
+
+
+def test_header_declares_the_five_calls():
+    d = _declared()
+    for name in ("aps_layer_maxabs", "aps_layer_scales", "aps_quantize", "aps_sim_reduce", "aps_dequantize"):
+        assert name in d
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in _declared():
+        assert hasattr(lib, name), name
+    assert set(_declared()) == set(A.EXPORTS)
+
+
+def test_strerror(lib):
+    for st in (0, -1, -2, -3, -4, -5, -6):
+        assert A.strerror(st) and A.strerror(st) != "unknown status"
+    assert A.strerror(12345) == "unknown status"
+
+
+@pytest.mark.parametrize("f,ok", [
+    (A.Format(5, 2), A.APS_OK), (A.Format(4, 3), A.APS_OK), (A.Format(3, 0), A.APS_OK),
+    (A.Format(2, 0), A.APS_OK), (A.Format(8, 23), A.APS_OK), (A.Format(8, 7), A.APS_OK),
+    (A.Format(8, 0), A.APS_OK), (A.Format(5, 10), A.APS_OK), (A.Format(6, 9), A.APS_OK),
+    (A.Format(7, 23), A.APS_OK), (A.Format(4, 3, 5), A.APS_OK), (A.Format(5, 2, 20), A.APS_OK),
+    (A.Format(1, 2), A.APS_ERR_FORMAT), (A.Format(9, 2), A.APS_ERR_FORMAT),
+    (A.Format(5, 24), A.APS_ERR_FORMAT), (A.Format(5, -1), A.APS_ERR_FORMAT),
+    (A.Format(8, 7, 126), A.APS_ERR_FORMAT),      # emax 128
+    (A.Format(8, 7, 128), A.APS_ERR_UNSUPPORTED),  # e = 8 needs bias 127
+    (A.Format(7, 20, 127), A.APS_ERR_UNSUPPORTED),  # subnormals below 2^-126
+    (A.Format(5, 2, 200), A.APS_ERR_FORMAT),       # smallest subnormal below 2^-149
+])
+def test_format_supported(lib, f, ok):
+    assert A.format_supported(f) == ok
+
+
+def _pal(*fs):
+    arr = (A.aps_format * max(1, len(fs)))()
+    for i, f in enumerate(fs):
+        arr[i] = f.c()
+    return arr
+
+
+# The calls below pass fake device pointers; each also carries an invalid
+# argument so validation rejects it first.  They are skipped where a GPU is
+# visible, so that a wrong expectation can never turn into a launch.
+no_gpu = pytest.mark.skipif(_gpu_visible(), reason="host-validation tests use fake pointers")
+
+P = ctypes.c_void_p
+GOOD = P(4096)      # an aligned non-NULL value; never dereferenced by these calls
+MIS = P(4100)       # misaligned
+
+
+@no_gpu
+def test_maxabs_validation(lib):
+    f = lib.aps_layer_maxabs
+    assert f(None, 2, 64, 64, GOOD, 1, GOOD, None) == A.APS_ERR_NULL
+    assert f(GOOD, 2, 64, 64, None, 1, GOOD, None) == A.APS_ERR_NULL
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, None) == A.APS_ERR_NULL
+    assert f(GOOD, 0, 64, 64, GOOD, 1, GOOD, None) == A.APS_ERR_SIZE
+    assert f(GOOD, (1 << 24) + 1, 64, 64, GOOD, 1, GOOD, None) == A.APS_ERR_SIZE
+    assert f(GOOD, 2, 64, 64, GOOD, 0, GOOD, None) == A.APS_ERR_SIZE
+    assert f(GOOD, 2, 60, 64, GOOD, 1, GOOD, None) == A.APS_ERR_SIZE     # ld < n
+    assert f(GOOD, 2, 64, -1, GOOD, 1, GOOD, None) == A.APS_ERR_SIZE
+    assert f(GOOD, 2, 66, 64, GOOD, 1, GOOD, None) == A.APS_ERR_ALIGN    # ld % 4
+    assert f(MIS, 2, 64, 64, GOOD, 1, GOOD, None) == A.APS_ERR_ALIGN
+
+
+@no_gpu
+def test_scales_validation(lib):
+    f = lib.aps_layer_scales
+    pal = _pal(A.Format(5, 2))
+    assert f(None, 4, 8, pal, 1, None, GOOD, None) == A.APS_ERR_NULL
+    assert f(GOOD, 4, 8, pal, 1, None, None, None) == A.APS_ERR_NULL
+    assert f(GOOD, 4, 8, None, 1, None, GOOD, None) == A.APS_ERR_NULL
+    assert f(GOOD, 0, 8, pal, 1, None, GOOD, None) == A.APS_ERR_SIZE
+    assert f(GOOD, 4, 0, pal, 1, None, GOOD, None) == A.APS_ERR_SIZE
+    assert f(GOOD, 4, 8, pal, 0, None, GOOD, None) == A.APS_ERR_SIZE
+    assert f(GOOD, 4, 8, _pal(*[A.Format(5, 2)] * 9), 9, None, GOOD, None) == A.APS_ERR_SIZE
+    assert f(GOOD, 4, 8, _pal(A.Format(9, 2)), 1, None, GOOD, None) == A.APS_ERR_FORMAT
+    assert f(GOOD, 4, 8, _pal(A.Format(5, 2), A.Format(8, 3, 100)), 2, None, GOOD, None) == A.APS_ERR_FORMAT
+
+
+@no_gpu
+def test_quantize_validation(lib):
+    f = lib.aps_quantize
+    pal = _pal(A.Format(5, 2))
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, pal, 1, None, None, None, None) == A.APS_ERR_NULL
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, pal, 1, None, MIS, None, None) == A.APS_ERR_ALIGN
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, pal, 1, None, None, MIS, None) == A.APS_ERR_ALIGN
+    # codes need one container class across the palette, and at most 16 bits
+    two = _pal(A.Format(5, 2), A.Format(5, 10))
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, two, 2, None, None, GOOD, None) == A.APS_ERR_UNSUPPORTED
+    wide = _pal(A.Format(8, 23))
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, wide, 1, None, None, GOOD, None) == A.APS_ERR_UNSUPPORTED
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, _pal(A.Format(5, 30)), 1, None, GOOD, None, None) == A.APS_ERR_FORMAT
+
+
+@no_gpu
+def test_sim_reduce_validation(lib):
+    f = lib.aps_sim_reduce
+    pal = _pal(A.Format(5, 2))
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, pal, 1, None, 0, None, None, None) == A.APS_ERR_NULL
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, pal, 1, None, 0, MIS, None, None) == A.APS_ERR_ALIGN
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, pal, 1, None, 4, GOOD, None, None) == A.APS_ERR_UNSUPPORTED
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, _pal(A.Format(7, 20, 127)), 1, None, 0, GOOD, None,
+             None) == A.APS_ERR_UNSUPPORTED
+    assert f(None, 2, 64, 64, GOOD, 1, None, pal, 1, None, 0, GOOD, None, None) == A.APS_ERR_NULL
+
+
+@no_gpu
+def test_dequantize_validation(lib):
+    f = lib.aps_dequantize
+    pal = _pal(A.Format(5, 2))
+    assert f(None, None, 64, GOOD, 1, None, pal, 1, None, GOOD, None) == A.APS_ERR_NULL
+    assert f(GOOD, None, 64, GOOD, 1, None, pal, 1, None, None, None) == A.APS_ERR_NULL
+    assert f(GOOD, None, 64, GOOD, 0, None, pal, 1, None, GOOD, None) == A.APS_ERR_SIZE
+    assert f(GOOD, None, 64, GOOD, 1, None, pal, 1, None, MIS, None) == A.APS_ERR_ALIGN
+    assert f(None, GOOD, 64, GOOD, 1, None, _pal(A.Format(8, 23)), 1, None, GOOD, None) == A.APS_ERR_UNSUPPORTED

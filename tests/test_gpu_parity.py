@@ -1,0 +1,369 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bit-exact comparison on every output (fp32 values bitwise, NaN as a class;
+codes byte for byte), on seeded synthetic inputs: edge layouts, every code of
+the small formats, the paper-shaped configurations (full where the oracle
+finishes in seconds, sampled outputs otherwise)."""
+import math
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_1911_08907_amd import aps as A
+from paper_1911_08907_amd import workloads as WL
+from tests import exact_ref as X
+from tests._util import first_diff, log, ofmt, same_f32, same_maxabs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    A.lib()  # the HIP library must be there: no fallback
+    return torch.device("cuda:0")
+
+
+def _code_cls(bits):
+    return 0 if bits <= 4 else (1 if bits <= 8 else 2)
+
+
+def _codes_equal(g: np.ndarray, o: np.ndarray, n: int, bits: int) -> bool:
+    """Compare packed code arrays over the first n elements only."""
+    cls = _code_cls(bits)
+    if cls == 0:
+        full = n // 2
+        if not np.array_equal(g[:full], o[:full]):
+            return False
+        if n % 2:
+            return (g[full] & 15) == (o[full] & 15)
+        return True
+    nb = n if cls == 1 else 2 * n
+    return np.array_equal(g[:nb], o[:nb])
+
+
+def _row_code_bytes(ld, bits):
+    cls = _code_cls(bits)
+    return ld // 2 if cls == 0 else (ld if cls == 1 else 2 * ld)
+
+
+def run_case(dev, G: np.ndarray, n: int, offs: np.ndarray, pal, fmt_idx=None, mode="aps", N=None,
+             scale_exp=None, codes=True, tag=""):
+    """Run every entry point on the GPU and the oracle on the same bytes."""
+    W, ld = G.shape
+    L = offs.size - 1
+    opal = [ofmt(f) for f in pal]
+    G_t = torch.from_numpy(G).to(dev)
+    offs_t = torch.from_numpy(offs).to(dev)
+    idx_t = None if fmt_idx is None else torch.from_numpy(fmt_idx).to(dev)
+    bits = {f.bits for f in pal}
+    classes = {_code_cls(b) for b in bits}
+    with_codes = codes and len(classes) == 1 and max(bits) <= 16
+    cbits = max(bits)
+
+    # max-abs (always) and scales (APS mode)
+    mab = torch.zeros(L, dtype=torch.int32, device=dev)
+    A.aps_layer_maxabs(G_t, n, offs_t, mab)
+    o_mab = O.layer_maxabs(G, n, offs)
+    torch.cuda.synchronize()
+    assert same_maxabs(mab.cpu().numpy(), o_mab), f"{tag} maxabs"
+    if mode == "aps":
+        Nw = W if N is None else N
+        se_t = torch.zeros(L, dtype=torch.int32, device=dev)
+        A.aps_layer_scales(mab, Nw, pal, idx_t, se_t)
+        o_se = O.layer_scales(o_mab, Nw, opal, fmt_idx)
+        assert np.array_equal(se_t.cpu().numpy(), o_se), f"{tag} scales"
+    elif mode == "raw":
+        se_t, o_se = None, None
+    else:  # explicit exponents
+        o_se = np.asarray(scale_exp, np.int32)
+        se_t = torch.from_numpy(o_se).to(dev)
+
+    # quantize
+    Q_t = torch.zeros_like(G_t)
+    qc_t = torch.zeros(max(1, W * _row_code_bytes(ld, cbits)), dtype=torch.uint8, device=dev) if with_codes else None
+    A.aps_quantize(G_t, n, offs_t, se_t, pal, idx_t, Q=Q_t, codes=qc_t)
+    o_Q = O.quantize(G, n, offs, o_se, opal, fmt_idx)
+    Qg = Q_t.cpu().numpy()
+    ok = same_f32(Qg[:, :n], o_Q[:, :n])
+    assert ok, f"{tag} quantize {first_diff(Qg[:, :n], o_Q[:, :n])}"
+    if with_codes:
+        qc = qc_t.cpu().numpy()
+        rb = _row_code_bytes(ld, cbits)
+        for w in range(W):
+            oc = O.pack_codes(o_Q[w, :n], offs, opal, fmt_idx)
+            assert _codes_equal(qc[w * rb:(w + 1) * rb], oc, n, cbits), f"{tag} quantize codes row {w}"
+
+    # fused reduce, plain and scaled output, with codes
+    out_t = torch.zeros(max(n, 1), dtype=torch.float32, device=dev)
+    rc_t = torch.zeros(max(16, A.code_bytes(n, cbits)), dtype=torch.uint8, device=dev) if with_codes else None
+    A.aps_sim_reduce(G_t, n, offs_t, se_t, pal, idx_t, 0, out=out_t, codes_out=rc_t)
+    o_out = O.sim_reduce(G, n, offs, o_se, opal, fmt_idx)
+    og = out_t.cpu().numpy()[:n]
+    assert same_f32(og, o_out), f"{tag} sim_reduce {first_diff(og, o_out)}"
+    o_sc = O.sim_reduce(G, n, offs, o_se, opal, fmt_idx, flags=O.OUTPUT_SCALED)
+    if with_codes:
+        oc = O.pack_codes(o_sc, offs, opal, fmt_idx)
+        assert _codes_equal(rc_t.cpu().numpy(), oc, n, cbits), f"{tag} sim_reduce codes"
+
+    # composition: reduce of the quantized input, scaled output, then dequantize
+    sc_t = torch.zeros(max(n, 1), dtype=torch.float32, device=dev)
+    A.aps_sim_reduce(Q_t, n, offs_t, se_t, pal, idx_t, A.APS_INPUT_QUANTIZED | A.APS_OUTPUT_SCALED, out=sc_t)
+    sg = sc_t.cpu().numpy()[:n]
+    o_sc2 = O.sim_reduce(o_Q, n, offs, o_se, opal, fmt_idx, flags=O.INPUT_QUANTIZED | O.OUTPUT_SCALED)
+    assert same_f32(sg, o_sc2), f"{tag} reduce(IN_Q|OUT_SCALED) {first_diff(sg, o_sc2)}"
+    assert same_f32(o_sc2, o_sc), f"{tag} oracle composition"
+    dq_t = torch.zeros(max(n, 1), dtype=torch.float32, device=dev)
+    A.aps_dequantize(sc_t, None, n, offs_t, se_t, pal, idx_t, dq_t)
+    dg = dq_t.cpu().numpy()[:n]
+    assert same_f32(dg, o_out), f"{tag} dequantize(Q) {first_diff(dg, o_out)}"
+    if with_codes:
+        dq2_t = torch.zeros(max(n, 1), dtype=torch.float32, device=dev)
+        A.aps_dequantize(None, rc_t, n, offs_t, se_t, pal, idx_t, dq2_t)
+        d2 = dq2_t.cpu().numpy()[:n]
+        o_d2 = O.dequantize(None, O.pack_codes(o_sc, offs, opal, fmt_idx), n, offs, o_se, opal, fmt_idx)
+        assert same_f32(d2, o_d2), f"{tag} dequantize(codes) {first_diff(d2, o_d2)}"
+    return og
+
+
+# ----------------------------------------------------------- edge layouts
+
+F = A.Format
+ALL_FORMATS = [F(5, 2), F(4, 3), F(3, 0), F(2, 0), F(2, 1), F(3, 2), F(5, 10), F(6, 9), F(8, 7), F(8, 23),
+               F(8, 0), F(8, 15), F(5, 12), F(7, 23), F(4, 3, 5), F(5, 2, 20), F(6, 1), F(7, 5), F(2, 23)]
+
+SIZES = [0, 1, 3, 5, 7, 1023, 1024, 1025, 2049, 0, 64, 13, 4095, 2, 3000]
+
+
+def _layout(sizes, pad_to=64):
+    offs = np.zeros(len(sizes) + 1, np.int64)
+    offs[1:] = np.cumsum(sizes)
+    n = int(offs[-1])
+    ld = max(4, (n + pad_to - 1) // pad_to * pad_to)
+    return offs, n, ld
+
+
+def _values(rng, W, ld, offs, kind):
+    L = offs.size - 1
+    G = np.zeros((W, ld), np.float32)
+    for i in range(L):
+        a, b = offs[i], offs[i + 1]
+        if b == a:
+            continue
+        s = 2.0 ** rng.uniform(-40, 10) if kind != "tiny" else 2.0 ** rng.uniform(-149, -100)
+        G[:, a:b] = (rng.standard_normal((W, b - a)) * s).astype(np.float32)
+        r = rng.random((W, b - a))
+        G[:, a:b][r < 0.05] = 0.0
+        G[:, a:b][(r >= 0.05) & (r < 0.07)] = -0.0
+    if kind == "special":
+        flat = G[:, :offs[-1]]
+        k = flat.size
+        for val, cnt in ((np.nan, 3), (np.inf, 3), (-np.inf, 3), (3e38, 5), (1e-45, 5), (-1e-40, 5)):
+            idx = rng.integers(0, k, cnt)
+            flat.reshape(-1)[idx] = val
+    # padding past n holds garbage that must not matter
+    G[:, offs[-1]:] = np.nan
+    return G
+
+
+@pytest.mark.parametrize("f", ALL_FORMATS, ids=str)
+@pytest.mark.parametrize("kind", ["normal", "special", "tiny"])
+def test_edge_layouts_single_format(dev, f, kind):
+    rng = np.random.default_rng(hash((str(f), kind)) & 0xFFFF)
+    offs, n, ld = _layout(SIZES)
+    for W in (1, 2, 3, 8, 13):
+        G = _values(rng, W, ld, offs, kind)
+        tag = f"{f} {kind} W={W}"
+        log("case", tag)
+        run_case(dev, G, n, offs, [f], mode="aps", tag=tag + " aps")
+        run_case(dev, G, n, offs, [f], mode="raw", tag=tag + " raw")
+        se = rng.integers(-300, 300, offs.size - 1).astype(np.int32)
+        run_case(dev, G, n, offs, [f], mode="exp", scale_exp=se, tag=tag + " exp")
+    # N different from W (non power of two)
+    G = _values(rng, 5, ld, offs, kind)
+    run_case(dev, G, n, offs, [f], mode="aps", N=7, tag=f"{f} {kind} W=5 N=7")
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_edge_layouts_mixed_palette(dev, seed):
+    rng = np.random.default_rng(100 + seed)
+    pal_choices = [[F(5, 2), F(4, 3), F(3, 0), F(2, 1)],        # 4-8 bit codes mix classes
+                   [F(5, 2), F(4, 3), F(6, 1), F(3, 4)],         # all byte codes
+                   [F(5, 10), F(5, 2), F(8, 7)],
+                   [F(8, 23), F(5, 12), F(3, 0), F(8, 0), F(4, 3, 5)]]
+    pal = pal_choices[seed % len(pal_choices)]
+    sizes = [int(v) for v in rng.choice([0, 1, 2, 3, 5, 17, 255, 1000, 1023, 1024, 1500, 4096], 40)]
+    offs, n, ld = _layout(sizes)
+    fmt_idx = rng.integers(0, len(pal), len(sizes)).astype(np.uint8)
+    for W in (1, 4, 9):
+        G = _values(rng, W, ld, offs, "special" if seed % 2 else "normal")
+        tag = f"mixed seed={seed} W={W}"
+        log("case", tag)
+        run_case(dev, G, n, offs, pal, fmt_idx=fmt_idx, mode="aps", tag=tag + " aps")
+        run_case(dev, G, n, offs, pal, fmt_idx=fmt_idx, mode="raw", tag=tag + " raw")
+
+
+def test_empty_gradient(dev):
+    offs = np.zeros(4, np.int64)
+    G = np.zeros((3, 4), np.float32)
+    G_t = torch.from_numpy(G).to(dev)
+    offs_t = torch.from_numpy(offs).to(dev)
+    mab = torch.full((3,), 7, dtype=torch.int32, device=dev)
+    A.aps_layer_maxabs(G_t, 0, offs_t, mab)
+    assert mab.cpu().tolist() == [0, 0, 0]
+    A.aps_sim_reduce(G_t, 0, offs_t, None, [F(5, 2)], None, 0, out=None)
+    torch.cuda.synchronize()
+
+
+# ------------------------------------------------ exhaustive small formats
+
+SMALL = [F(5, 2), F(4, 3), F(3, 0), F(2, 0), F(2, 1), F(3, 2), F(6, 1), F(3, 4), F(4, 3, 5)]
+
+
+@pytest.mark.parametrize("f", SMALL, ids=str)
+def test_every_code_and_midpoint(dev, f):
+    vals = [float(v) for v in X.values(f.e, f.m, f.b)]
+    ext = vals + [2.0 ** (f.emax + 1)]
+    pts = list(vals)
+    for lo, hi in zip(ext[:-1], ext[1:]):
+        mid = np.float32((lo + hi) / 2)
+        pts += [float(mid), float(np.nextafter(mid, np.float32(0))), float(np.nextafter(mid, np.float32(np.inf)))]
+    pts = np.array(pts + [-p for p in pts] + [np.inf, -np.inf, np.nan], np.float32)
+    n = pts.size
+    ld = (n + 63) // 64 * 64
+    G = np.full((1, ld), np.nan, np.float32)
+    G[0, :n] = pts
+    offs = np.array([0, n], np.int64)
+    run_case(dev, G, n, offs, [f], mode="raw", tag=f"{f} all codes/midpoints")
+
+
+@pytest.mark.parametrize("f", [F(5, 2), F(4, 3), F(3, 0), F(2, 1), F(3, 2)], ids=str)
+def test_every_code_pair_sum(dev, f):
+    vals = [float(v) for v in X.values(f.e, f.m, f.b)]
+    vals = np.array(vals + [-v for v in vals[1:]] + [np.inf, -np.inf], np.float32)
+    a, b = np.meshgrid(vals, vals, indexing="ij")
+    n = a.size
+    ld = (n + 63) // 64 * 64
+    G = np.zeros((2, ld), np.float32)
+    G[0, :n] = a.ravel()
+    G[1, :n] = b.ravel()
+    offs = np.array([0, n], np.int64)
+    G_t = torch.from_numpy(G).to(dev)
+    offs_t = torch.from_numpy(offs).to(dev)
+    out = torch.zeros(n, dtype=torch.float32, device=dev)
+    flags = A.APS_INPUT_QUANTIZED | A.APS_OUTPUT_SCALED
+    A.aps_sim_reduce(G_t, n, offs_t, None, [f], None, flags, out=out)
+    o = O.sim_reduce(G, n, offs, None, ofmt(f), flags=O.INPUT_QUANTIZED | O.OUTPUT_SCALED)
+    g = out.cpu().numpy()
+    assert same_f32(g, o), first_diff(g, o)
+
+
+# ----------------------------------------------------- paper-shaped sets
+
+def _small_config(dev, name, palette):
+    gs = WL.generate(name, palette, device="cpu")
+    G = gs.G.numpy()
+    pal = [A.Format(p.e, p.m, p.bias) for p in gs.palette]
+    return G, gs, pal
+
+
+@pytest.mark.parametrize("name,palette", [("mlp", "1-4-3"), ("resnet20", "1-5-2"), ("resnet20", "1-4-3"),
+                                          ("resnet20", "1-3-0")])
+def test_config_full_parity(dev, name, palette):
+    G, gs, pal = _small_config(dev, name, palette)
+    log("config", name, palette, G.shape)
+    run_case(dev, G, gs.n, gs.offsets, pal, fmt_idx=gs.fmt_idx, mode="aps", tag=f"{name} {palette} aps")
+    run_case(dev, G, gs.n, gs.offsets, pal, fmt_idx=gs.fmt_idx, mode="raw", tag=f"{name} {palette} raw")
+
+
+def _sample_idx(rng, offs, n, per=20000):
+    """Sorted unique sample of element indices: layer edges, chunk edges, random."""
+    picks = [rng.integers(0, n, per)]
+    for o in offs[1:-1]:
+        picks.append(np.arange(max(0, o - 5), min(n, o + 5)))
+    picks.append(np.arange(0, min(n, 2048)))
+    picks.append(np.arange(max(0, n - 2048), n))
+    picks.append((np.arange(0, n, 1024 * 997))[:200])
+    idx = np.unique(np.concatenate(picks))
+    return idx[(idx >= 0) & (idx < n)]
+
+
+def _sampled_oracle(G_t, gs, pal, idx, o_se, fmt_idx, W):
+    """Oracle on the sampled columns: same bytes, same per-layer exponents."""
+    idx_t = torch.from_numpy(idx).to(G_t.device)
+    Gs = G_t[:, idx_t].cpu().numpy()                       # [W][S]
+    layer = np.searchsorted(gs.offsets, idx, side="right") - 1
+    uniq, starts = np.unique(layer, return_index=True)
+    sub_offs = np.append(starts, idx.size).astype(np.int64)
+    se = None if o_se is None else o_se[uniq]
+    fi = None if fmt_idx is None else fmt_idx[uniq]
+    S = idx.size
+    ldS = (S + 3) // 4 * 4
+    Gp = np.zeros((W, ldS), np.float32)
+    Gp[:, :S] = Gs
+    return O.sim_reduce(Gp, S, sub_offs, se, [ofmt(f) for f in pal], fi)
+
+
+def _oracle_maxabs_streamed(G_t, gs, rows=8):
+    """Oracle max-abs of a large set, a few worker rows at a time."""
+    W = G_t.shape[0]
+    acc = np.zeros(gs.offsets.size - 1, np.uint32)
+    for w0 in range(0, W, rows):
+        part = G_t[w0:w0 + rows].cpu().numpy()
+        m = O.layer_maxabs(part, gs.n, gs.offsets).view(np.uint32)
+        acc = np.maximum(acc, m)
+    return acc
+
+
+@pytest.mark.parametrize("name,palette", [("resnet50_w8", "1-5-2"), ("resnet50_w256", "1-5-2"),
+                                          ("resnet50_w256", "1-4-3"), ("bert_large", "hybrid")])
+def test_config_large_parity(dev, name, palette):
+    t0 = time.time()
+    gs = WL.generate(name, palette, device=dev)
+    G_t = gs.G
+    W, n = gs.W, gs.n
+    pal = [A.Format(p.e, p.m, p.bias) for p in gs.palette]
+    opal = [ofmt(f) for f in pal]
+    offs_t = torch.from_numpy(gs.offsets).to(dev)
+    idx_t = None if gs.fmt_idx is None else torch.from_numpy(gs.fmt_idx).to(dev)
+    log(name, palette, "generated", tuple(G_t.shape), f"{time.time() - t0:.1f}s")
+    out, se_t, mab = A.aps_step(G_t, n, offs_t, pal, idx_t)
+    torch.cuda.synchronize()
+    log("gpu step done", f"{time.time() - t0:.1f}s")
+    o_mab = _oracle_maxabs_streamed(G_t, gs)
+    assert same_maxabs(mab.cpu().numpy(), o_mab), "maxabs"
+    o_se = O.layer_scales(o_mab, W, opal, gs.fmt_idx)
+    assert np.array_equal(se_t.cpu().numpy(), o_se), "scales"
+    log("maxabs/scales match", f"{time.time() - t0:.1f}s")
+    rng = np.random.default_rng(7)
+    if name == "resnet50_w8":
+        G = G_t.cpu().numpy()
+        o_out = O.sim_reduce(G, n, gs.offsets, o_se, opal, gs.fmt_idx)
+        g = out.cpu().numpy()
+        assert same_f32(g, o_out), first_diff(g, o_out)
+        assert np.all(np.isfinite(g))
+        log("full reduce parity", f"{time.time() - t0:.1f}s")
+    else:
+        idx = _sample_idx(rng, gs.offsets, n)
+        o_s = _sampled_oracle(G_t, gs, pal, idx, o_se, gs.fmt_idx, W)
+        g = out[torch.from_numpy(idx).to(dev)].cpu().numpy()
+        assert same_f32(g, o_s), first_diff(g, o_s)
+        log("sampled reduce parity on", idx.size, f"{time.time() - t0:.1f}s")
+    # APS mode never overflows on finite gradients
+    assert bool(torch.isfinite(out).all())
+    del G_t, gs
+    torch.cuda.empty_cache()
+
+
+def test_run_to_run_determinism(dev):
+    gs = WL.generate("resnet20", "1-5-2", device=dev)
+    offs_t = torch.from_numpy(gs.offsets).to(dev)
+    pal = [A.Format(5, 2)]
+    a, _, _ = A.aps_step(gs.G, gs.n, offs_t, pal)
+    b, _, _ = A.aps_step(gs.G, gs.n, offs_t, pal)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
