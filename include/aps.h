@@ -44,9 +44,10 @@
  *
  * Bit codes.  code = sign << (e+m) | biased exponent << m | mantissa.  A NaN
  * is written as the all-ones exponent with the top mantissa bit set (the INF
- * code when m = 0).  Codes of 2..4 bits are packed two per byte (element j in
- * the low nibble of byte j/2 when j is even, the high nibble when odd); codes
- * of 5..8 bits take one byte; codes of 9..16 bits one little-endian uint16.
+ * code when m = 0); the sign bit of a NaN's code is unspecified.  Codes of
+ * 2..4 bits are packed two per byte (element j in the low nibble of byte j/2
+ * when j is even, the high nibble when odd); codes of 5..8 bits take one
+ * byte; codes of 9..16 bits one little-endian uint16.
  * A call that writes or reads codes needs every format of its palette in the
  * same one of those three classes.
  */
