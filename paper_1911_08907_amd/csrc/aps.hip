@@ -26,10 +26,26 @@
 
 namespace aps {
 
+#ifndef APS_UNROLL
+#define APS_UNROLL 4
+#endif
+#ifndef APS_BLOCKS_PER_CU
+#define APS_BLOCKS_PER_CU 16
+#endif
+#ifndef APS_MAXABS_BLOCKS_PER_CU
+#define APS_MAXABS_BLOCKS_PER_CU 4
+#endif
+#ifndef APS_MAXABS_UNROLL
+#define APS_MAXABS_UNROLL 8
+#endif
+
 constexpr int BLOCK = 256;
 constexpr int VEC = 4;
 constexpr int64_t CH = BLOCK * VEC;
-constexpr int UNROLL = 4;  // worker rows per register set (two sets in flight)
+constexpr int UNROLL = APS_UNROLL;                // worker rows per register set (two sets in flight)
+constexpr int BLOCKS_PER_CU = APS_BLOCKS_PER_CU;  // launch width of the streaming kernels
+constexpr int MAXABS_BLOCKS_PER_CU = APS_MAXABS_BLOCKS_PER_CU;
+constexpr int MAXABS_UNROLL = APS_MAXABS_UNROLL;  // worker rows per load batch in k_maxabs
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
@@ -50,6 +66,21 @@ struct Layers {
 __device__ __forceinline__ void pal_to_lds(const Pal& pal, FmtK* spal) {
     if (threadIdx.x < APS_MAX_FORMATS) spal[threadIdx.x] = pal.f[threadIdx.x];
     __syncthreads();
+}
+
+// Read-only tables (offsets, palette indices, scale exponents) are read
+// through the constant address space: uniform reads then become scalar loads,
+// which do not wait for the kernel's own outstanding vector stores.
+template <class T>
+__device__ __forceinline__ T cld(const T* p, int64_t i) {
+    return ((const __attribute__((address_space(4))) T*)p)[i];
+}
+
+// A palette index (one byte) through a scalar load of its aligned 32-bit word.
+__device__ __forceinline__ int cld_idx(const uint8_t* p, int64_t i) {
+    const uintptr_t a = (uintptr_t)(p + i);
+    const uint32_t w = *(const __attribute__((address_space(4))) uint32_t*)(a & ~(uintptr_t)3);
+    return (int)((w >> ((a & 3u) * 8u)) & 0xFFu);
 }
 
 __device__ __forceinline__ float u2f(uint32_t u) { return __uint_as_float(u); }
@@ -217,22 +248,22 @@ __device__ __forceinline__ uint32_t load_code(const uint8_t* row, int64_t j, int
 // Largest i in [0, L-1] with offsets[i] <= pos (pos < n), searching from a hint.
 __device__ __forceinline__ int find_layer(const int64_t* __restrict__ off, int L, int64_t pos, int hint) {
     int i = hint;
-    if (off[i] > pos) {
+    if (cld(off, i) > pos) {
         int lo = 0, hi = i;
         while (hi - lo > 1) {
             const int mid = (lo + hi) >> 1;
-            if (off[mid] <= pos) lo = mid; else hi = mid;
+            if (cld(off, mid) <= pos) lo = mid; else hi = mid;
         }
         return lo;
     }
     for (int s = 0; s < 4; ++s) {
-        if (i + 1 >= L || off[i + 1] > pos) return i;
+        if (i + 1 >= L || cld(off, i + 1) > pos) return i;
         ++i;
     }
     int lo = i, hi = L;  // off[lo] <= pos; off[L] = n > pos
     while (hi - lo > 1) {
         const int mid = (lo + hi) >> 1;
-        if (off[mid] <= pos) lo = mid; else hi = mid;
+        if (cld(off, mid) <= pos) lo = mid; else hi = mid;
     }
     return lo;
 }
@@ -248,14 +279,14 @@ __device__ __forceinline__ ChunkInfo chunk_layers(const Layers& ly, int64_t star
     ChunkInfo ci;
     ci.i0 = find_layer(ly.offsets, ly.L, start, hint);
     int i = ci.i0;
-    while (ly.offsets[i + 1] < end) ++i;  // offsets[L] = n >= end
+    while (cld(ly.offsets, i + 1) < end) ++i;  // offsets[L] = n >= end
     ci.i1 = i;
-    ci.pidx = ly.fmt_idx ? ly.fmt_idx[ci.i0] : 0;
+    ci.pidx = ly.fmt_idx ? cld_idx(ly.fmt_idx, ci.i0) : 0;
     ci.mixed = false;
     if (ly.fmt_idx && ci.i1 > ci.i0) {
         for (int t = ci.i0 + 1; t <= ci.i1; ++t) {
-            if (ly.offsets[t] == ly.offsets[t + 1]) continue;  // empty layer
-            if (ly.fmt_idx[t] != ci.pidx) ci.mixed = true;
+            if (cld(ly.offsets, t) == cld(ly.offsets, t + 1)) continue;  // empty layer
+            if (cld_idx(ly.fmt_idx, t) != ci.pidx) ci.mixed = true;
         }
     }
     return ci;
@@ -293,6 +324,19 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
     return v;
 }
 
+// Block-wide max of v (all threads call it), then one atomicMax if nonzero.
+__device__ __forceinline__ void block_max_atomic(uint32_t v, uint32_t* dst, uint32_t* red) {
+    v = wave_max_u32(v);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t t = red[0];
+        for (int k = 1; k < BLOCK / 64; ++k) t = max(t, red[k]);
+        if (t) atomicMax(dst, t);
+    }
+    __syncthreads();
+}
+
 __global__ __launch_bounds__(BLOCK) void k_maxabs(const float* __restrict__ G, int32_t W, int64_t ld,
                                                  Layers ly, uint32_t* __restrict__ maxabs) {
     __shared__ uint32_t red[BLOCK / 64];
@@ -311,13 +355,19 @@ __global__ __launch_bounds__(BLOCK) void k_maxabs(const float* __restrict__ G, i
         uint32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
         if (j < end) {
             const float* p = G + j;
-            for (int w = 0; w < W; ++w) {
-                const f4 x = ld4(p);
-                p += ld;
-                m0 = max(m0, f2u(x.x) & 0x7FFFFFFFu);
-                m1 = max(m1, f2u(x.y) & 0x7FFFFFFFu);
-                m2 = max(m2, f2u(x.z) & 0x7FFFFFFFu);
-                m3 = max(m3, f2u(x.w) & 0x7FFFFFFFu);
+            // batches of MAXABS_UNROLL rows; rows past W-1 re-read row W-1,
+            // which leaves a maximum unchanged
+            for (int w = 0; w < W; w += MAXABS_UNROLL) {
+                f4 x[MAXABS_UNROLL];
+#pragma unroll
+                for (int u = 0; u < MAXABS_UNROLL; ++u) x[u] = ld4(p + (int64_t)min(w + u, W - 1) * ld);
+#pragma unroll
+                for (int u = 0; u < MAXABS_UNROLL; ++u) {
+                    m0 = max(m0, f2u(x[u].x) & 0x7FFFFFFFu);
+                    m1 = max(m1, f2u(x[u].y) & 0x7FFFFFFFu);
+                    m2 = max(m2, f2u(x[u].z) & 0x7FFFFFFFu);
+                    m3 = max(m3, f2u(x[u].w) & 0x7FFFFFFFu);
+                }
             }
             // elements past the end of the gradient (row padding) do not count
             if (j + 1 >= end) m1 = 0;
@@ -327,44 +377,25 @@ __global__ __launch_bounds__(BLOCK) void k_maxabs(const float* __restrict__ G, i
         if (ci.i0 == ci.i1) {
             uint32_t v = max(max(m0, m1), max(m2, m3));
             if (ci.i0 != run_layer) {
-                if (run_layer >= 0) {
-                    // flush the previous run (block-wide max, one atomic)
-                    uint32_t r = wave_max_u32(run);
-                    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = r;
-                    __syncthreads();
-                    if (threadIdx.x == 0) {
-                        uint32_t t = red[0];
-                        for (int k = 1; k < BLOCK / 64; ++k) t = max(t, red[k]);
-                        if (t) atomicMax(maxabs + run_layer, t);
-                    }
-                    __syncthreads();
-                }
+                if (run_layer >= 0) block_max_atomic(run, maxabs + run_layer, red);
                 run_layer = ci.i0;
                 run = 0;
             }
             run = max(run, v);
-        } else if (j < end) {
-            // chunk crosses layer boundaries: one atomic per element
+        } else {
+            // chunk crosses layer boundaries: one block-wide max per layer
             const uint32_t mv[4] = {m0, m1, m2, m3};
-            int li = ci.i0;
-            for (int e = 0; e < 4; ++e) {
-                const int64_t jj = j + e;
-                if (jj >= end) break;
-                while (li < ci.i1 && ly.offsets[li + 1] <= jj) ++li;
-                if (mv[e]) atomicMax(maxabs + li, mv[e]);
+            for (int li = ci.i0; li <= ci.i1; ++li) {
+                const int64_t lo = cld(ly.offsets, li), hi = cld(ly.offsets, li + 1);
+                uint32_t v = 0;
+                if (j < end)
+                    for (int e = 0; e < 4; ++e)
+                        if (j + e >= lo && j + e < hi) v = max(v, mv[e]);
+                block_max_atomic(v, maxabs + li, red);
             }
         }
     }
-    if (run_layer >= 0) {
-        uint32_t r = wave_max_u32(run);
-        if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = r;
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            uint32_t t = red[0];
-            for (int k = 1; k < BLOCK / 64; ++k) t = max(t, red[k]);
-            if (t) atomicMax(maxabs + run_layer, t);
-        }
-    }
+    if (run_layer >= 0) block_max_atomic(run, maxabs + run_layer, red);
 }
 
 // ========================================================= K2: scales
@@ -408,9 +439,36 @@ struct ReduceArgs {
     int32_t code_cls;
 };
 
+// A thread's finished outputs (4 elements), kept in registers until the next
+// chunk's first loads have been issued.  Loads and stores share one in-order
+// completion counter, so a store issued before those loads would make the
+// first wait for them also wait for the store's write acknowledgement.
+struct PendingOut {
+    f4 o;
+    uint32_t c[4];
+    int64_t j, lim;  // first element; elements >= lim are not written
+    bool valid;
+};
+
+__device__ __forceinline__ void flush_out(const ReduceArgs& a, PendingOut& pd) {
+    if (!pd.valid) return;
+    pd.valid = false;
+    if (a.out) {
+        const int64_t j = pd.j, lim = pd.lim;
+        if (j + 4 <= lim) {
+            __builtin_nontemporal_store(pd.o, (f4*)(a.out + j));
+        } else {
+            if (j < lim) a.out[j] = pd.o.x;
+            if (j + 1 < lim) a.out[j + 1] = pd.o.y;
+            if (j + 2 < lim) a.out[j + 2] = pd.o.z;
+        }
+    }
+    if (a.codes) store_codes4(a.codes, pd.j, pd.c, a.code_cls, pd.lim);
+}
+
 template <int V>
 __device__ __forceinline__ void reduce_vec(const ReduceArgs& a, const FmtK& f, int64_t j, int64_t lim,
-                                           const int32_t ft[4]) {
+                                           const int32_t ft[4], PendingOut& pd) {
     const bool inq = a.flags & APS_INPUT_QUANTIZED;
     const bool outs = a.flags & APS_OUTPUT_SCALED;
     int F[4], Fo[4];
@@ -447,6 +505,9 @@ __device__ __forceinline__ void reduce_vec(const ReduceArgs& a, const FmtK& f, i
     __builtin_amdgcn_sched_barrier(0);
 #define APS_LAST(CUR)                                                    \
     _Pragma("unroll") for (int u = 0; u < UNROLL; ++u) {                 \
+        /* an empty asm that reads the row makes the compiler wait for   \
+           its load here, also for rows the select below discards */     \
+        asm volatile("" ::"v"(CUR[u].x), "v"(CUR[u].y), "v"(CUR[u].z), "v"(CUR[u].w)); \
         const f4 v = (w + u < W) ? CUR[u] : neg0;                        \
         APS_CONSUME(v);                                                  \
     }
@@ -461,16 +522,14 @@ __device__ __forceinline__ void reduce_vec(const ReduceArgs& a, const FmtK& f, i
         break;                                                           \
     }
     int w = 0;
-    const bool more = UNROLL < W;
-    if (more) {
-        APS_LOAD(B)
-    }
+    APS_LOAD(B)  // rows UNROLL..2*UNROLL-1, clamped: loaded whatever W is
+    flush_out(a, pd);  // the previous chunk's outputs, now behind this chunk's loads
     // row 0 starts the sums; rows 1..UNROLL-1 of the first group follow
     float s0 = quant<V>(A[0].x, F[0], f, bad0);
     float s1 = quant<V>(A[0].y, F[1], f, bad1);
     float s2 = quant<V>(A[0].z, F[2], f, bad2);
     float s3 = quant<V>(A[0].w, F[3], f, bad3);
-    if (more) {
+    if (UNROLL < W) {
 #pragma unroll
         for (int u = 1; u < UNROLL; ++u) APS_CONSUME(A[u]);
         w = UNROLL;
@@ -479,11 +538,14 @@ __device__ __forceinline__ void reduce_vec(const ReduceArgs& a, const FmtK& f, i
             APS_STEP(A, B)
         }
     } else {
+        // W <= UNROLL: the B rows are all past the end; consume them as -0 too
 #pragma unroll
         for (int u = 1; u < UNROLL; ++u) {
             const f4 v = (u < W) ? A[u] : neg0;
             APS_CONSUME(v);
         }
+        w = UNROLL;
+        APS_LAST(B)
     }
 #undef APS_STEP
 #undef APS_LAST
@@ -493,28 +555,19 @@ __device__ __forceinline__ void reduce_vec(const ReduceArgs& a, const FmtK& f, i
     s1 = finish<V>(s1, bad1);
     s2 = finish<V>(s2, bad2);
     s3 = finish<V>(s3, bad3);
-    if (a.out) {
-        f4 o;
-        o.x = __builtin_amdgcn_ldexpf(s0, Fo[0]);
-        o.y = __builtin_amdgcn_ldexpf(s1, Fo[1]);
-        o.z = __builtin_amdgcn_ldexpf(s2, Fo[2]);
-        o.w = __builtin_amdgcn_ldexpf(s3, Fo[3]);
-        if (j + 4 <= lim) {
-            __builtin_nontemporal_store(o, (f4*)(a.out + j));
-        } else {
-            if (j < lim) a.out[j] = o.x;
-            if (j + 1 < lim) a.out[j + 1] = o.y;
-            if (j + 2 < lim) a.out[j + 2] = o.z;
-        }
-    }
+    pd.o.x = __builtin_amdgcn_ldexpf(s0, Fo[0]);
+    pd.o.y = __builtin_amdgcn_ldexpf(s1, Fo[1]);
+    pd.o.z = __builtin_amdgcn_ldexpf(s2, Fo[2]);
+    pd.o.w = __builtin_amdgcn_ldexpf(s3, Fo[3]);
     if (a.codes) {
-        uint32_t c[4];
-        c[0] = encode(__builtin_amdgcn_ldexpf(s0, -f.k), f);
-        c[1] = encode(__builtin_amdgcn_ldexpf(s1, -f.k), f);
-        c[2] = encode(__builtin_amdgcn_ldexpf(s2, -f.k), f);
-        c[3] = encode(__builtin_amdgcn_ldexpf(s3, -f.k), f);
-        store_codes4(a.codes, j, c, a.code_cls, lim);
+        pd.c[0] = encode(__builtin_amdgcn_ldexpf(s0, -f.k), f);
+        pd.c[1] = encode(__builtin_amdgcn_ldexpf(s1, -f.k), f);
+        pd.c[2] = encode(__builtin_amdgcn_ldexpf(s2, -f.k), f);
+        pd.c[3] = encode(__builtin_amdgcn_ldexpf(s3, -f.k), f);
     }
+    pd.j = j;
+    pd.lim = lim;
+    pd.valid = true;
 }
 
 template <int V>
@@ -523,6 +576,8 @@ __global__ __launch_bounds__(BLOCK) void k_sim_reduce(ReduceArgs a, Layers ly, P
     int64_t cb, ce;
     block_range(nchunks, cb, ce);
     int hint = 0;
+    PendingOut pd;
+    pd.valid = false;
     for (int64_t c = cb; c < ce; ++c) {
         const int64_t start = c * CH;
         const int64_t end = min(start + CH, ly.n);
@@ -535,13 +590,14 @@ __global__ __launch_bounds__(BLOCK) void k_sim_reduce(ReduceArgs a, Layers ly, P
         if (j >= end) continue;
         int32_t ft[4];
         if (ci.i0 == ci.i1) {
-            const int32_t t = ly.scale_exp ? clamp_exp(ly.scale_exp[ci.i0]) : 0;
+            const int32_t t = ly.scale_exp ? clamp_exp(cld(ly.scale_exp, ci.i0)) : 0;
             ft[0] = ft[1] = ft[2] = ft[3] = t;
         } else {
             elem_scales(ly, ci, j, ft);
         }
-        reduce_vec<V>(a, f, j, end, ft);
+        reduce_vec<V>(a, f, j, end, ft, pd);
     }
+    flush_out(a, pd);
 }
 
 // One element through the whole W-worker loop, any variant (per-lane format).
@@ -573,12 +629,12 @@ __device__ float reduce_elem_any(const ReduceArgs& a, const FmtK& f, int64_t j, 
 // processes that chunk element by element.
 __device__ __forceinline__ bool mixed_chunk_of_boundary(const Layers& ly, int b, int64_t& start, int64_t& end) {
     if (b < 1 || b >= ly.L) return false;
-    const int64_t p = ly.offsets[b];
+    const int64_t p = cld(ly.offsets, b);
     if (p <= 0 || p >= ly.n || p % CH == 0) return false;
     const int64_t c = p / CH;
     start = c * CH;
     end = min(start + CH, ly.n);
-    if (ly.offsets[b - 1] > start) return false;  // an earlier boundary owns it
+    if (cld(ly.offsets, b - 1) > start) return false;  // an earlier boundary owns it
     const ChunkInfo ci = chunk_layers(ly, start, end, 0);
     return ci.mixed;
 }
@@ -651,7 +707,7 @@ __global__ __launch_bounds__(BLOCK) void k_quantize(QuantArgs a, Layers ly, Pal 
         if (j >= end) continue;
         int32_t ft[4];
         if (ci.i0 == ci.i1) {
-            const int32_t s = ly.scale_exp ? clamp_exp(ly.scale_exp[ci.i0]) : 0;
+            const int32_t s = ly.scale_exp ? clamp_exp(cld(ly.scale_exp, ci.i0)) : 0;
             ft[0] = ft[1] = ft[2] = ft[3] = s;
         } else {
             elem_scales(ly, ci, j, ft);
@@ -864,7 +920,7 @@ extern "C" int aps_layer_maxabs(const float* G, int32_t W, int64_t ld, int64_t n
     if (n == 0) return launched();
     Layers ly{offsets, nullptr, nullptr, n, L, 1};
     const int64_t nchunks = (n + CH - 1) / CH;
-    hipLaunchKernelGGL(k_maxabs, dim3((unsigned)grid_for(nchunks, 8)), dim3(BLOCK), 0, s, G, W, ld, ly, maxabs_bits);
+    hipLaunchKernelGGL(k_maxabs, dim3((unsigned)grid_for(nchunks, MAXABS_BLOCKS_PER_CU)), dim3(BLOCK), 0, s, G, W, ld, ly, maxabs_bits);
     return launched();
 }
 
@@ -897,7 +953,7 @@ extern "C" int aps_quantize(const float* X, int32_t W, int64_t ld, int64_t n, co
     Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
     QuantArgs a{X, Q, (uint8_t*)codes, ld, W, ccls};
     const int64_t nchunks = (n + CH - 1) / CH;
-    const dim3 grid((unsigned)grid_for(nchunks * W, 8));
+    const dim3 grid((unsigned)grid_for(nchunks * W, BLOCKS_PER_CU));
     const unsigned vm = variant_mask(pal, n_fmts);
 #define APS_LAUNCH_Q(v) \
     if (vm & (1u << (v))) hipLaunchKernelGGL(k_quantize<v>, grid, dim3(BLOCK), 0, s, a, ly, pal);
@@ -927,7 +983,7 @@ extern "C" int aps_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n, 
     Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
     ReduceArgs a{G, out, (uint8_t*)codes_out, ld, W, flags, ccls};
     const int64_t nchunks = (n + CH - 1) / CH;
-    const dim3 grid((unsigned)grid_for(nchunks, 8));
+    const dim3 grid((unsigned)grid_for(nchunks, BLOCKS_PER_CU));
     const unsigned vm = variant_mask(pal, n_fmts);
 #define APS_LAUNCH_R(v) \
     if (vm & (1u << (v))) hipLaunchKernelGGL(k_sim_reduce<v>, grid, dim3(BLOCK), 0, s, a, ly, pal);
@@ -953,7 +1009,7 @@ extern "C" int aps_dequantize(const float* Q, const void* codes, int64_t n, cons
     Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
     DeqArgs a{Q, (const uint8_t*)codes, out, ccls};
     const int64_t nchunks = (n + CH - 1) / CH;
-    hipLaunchKernelGGL(k_dequantize, dim3((unsigned)grid_for(nchunks, 8)), dim3(BLOCK), 0, (hipStream_t)stream, a,
+    hipLaunchKernelGGL(k_dequantize, dim3((unsigned)grid_for(nchunks, BLOCKS_PER_CU)), dim3(BLOCK), 0, (hipStream_t)stream, a,
                        ly, pal);
     return launched();
 }
