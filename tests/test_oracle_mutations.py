@@ -1,0 +1,53 @@
+"""The pins are strong enough: each plausible mistake planted in a copy of the
+oracle makes the pin suite fail.
+
+Every mutant is built from oracle/oracle.c with one textual change, loaded by
+a separate pytest process (APS_ORACLE_LIB) that runs tests/test_oracle_pins.py
+and must fail.  CPU only; the real oracle is untouched."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "oracle.c")
+
+MUTANTS = {
+    "no_subnormals": ("const int Eq = E > emin ? E : emin;", "const int Eq = E;"),
+    "ties_away": ("const double k = nearbyint(", "const double k = round("),
+    "no_overflow": ("if (v > oracle_maxfinite(f)) v = INFINITY;", ""),
+    "emax_off_by_one": ("int oracle_emax(oracle_format f) { return (1 << f.e) - 2 - f.bias; }",
+                        "int oracle_emax(oracle_format f) { return (1 << f.e) - 1 - f.bias; }"),
+    "sign_dropped": ("return copysign(v, y);", "return v;"),
+    "unrounded_accumulator": ("s = (w == 0) ? q : oracle_round(s + q, f);", "s = (w == 0) ? q : s + q;"),
+    "scale_off_by_one": ("return oracle_emax(f) - oracle_ceil_log2((double)t);",
+                         "return oracle_emax(f) - oracle_ceil_log2((double)t) + 1;"),
+    "floor_not_ceil_on_powers_of_two": ("return (r == 0.5) ? E - 1 : E;", "return E;"),
+    "reversed_worker_order": ("const float x = G[(int64_t)w * ld + j];",
+                              "const float x = G[(int64_t)(W - 1 - w) * ld + j];"),
+    "unscale_wrong_direction": ("out[j] = (flags & ORACLE_OUTPUT_SCALED) ? g : (float)ldexp((double)g, -ft);",
+                                "out[j] = (flags & ORACLE_OUTPUT_SCALED) ? g : (float)ldexp((double)g, ft);"),
+    "nan_ignored_in_maxabs": ("if (isnan(x))\n                    saw_nan = 1;", "if (0)\n                    saw_nan = 1;"),
+    "scale_before_rounding_skipped": ("const float y = (flags & ORACLE_INPUT_QUANTIZED) ? x : scale_fp32(x, ft);",
+                                      "const float y = x;"),
+    "mantissa_bits_off_by_one": ("const double k = nearbyint(ldexp(a, f.m - Eq));",
+                                 "const double k = nearbyint(ldexp(a, f.m + 1 - Eq));"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(tmp_path, name):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not found exactly once"
+    mutated = tmp_path / "oracle_mut.c"
+    mutated.write_text(src.replace(old, new))
+    lib = O.build(force=True, src=str(mutated), out=str(tmp_path / "liboracle_mut.so"))
+    env = dict(os.environ, APS_ORACLE_LIB=lib)
+    res = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                          os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                         cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert res.returncode != 0, f"mutant {name} survived the pins:\n{res.stdout[-2000:]}"
