@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--palette", default=None)
     ap.add_argument("--mode", choices=["aps", "raw"], default="aps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-calls", action="store_true",
+                    help="skip timing aps_quantize / aps_dequantize outside the step")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU oracle time budget")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only run device-to-device copies of this size (counter calibration)")
@@ -78,6 +80,48 @@ def traffic_from_profile(config: str, palette: str, launch_bytes: float):
     fetch = c["fetch_kib_per_dispatch"] * 1024 * c["fetch_scale"]
     write = c["write_kib_per_dispatch"] * 1024 * c["write_scale"]
     return fetch + write, f"{os.path.basename(path)}"
+
+
+def other_calls(A, G, gs, pal, idx_t, offs_t, se, out, reps: int = 5):
+    """Event-timed aps_quantize (codes out) and aps_dequantize (codes in) on
+    the same set, outside the timed step; GB/s from their algorithmic bytes."""
+    import torch
+
+    bits = max(f.bits for f in pal)
+    if len({A.code_bytes(8, f.bits) for f in pal}) != 1 or bits > 16:
+        return {}
+    W, n, ld = gs.W, gs.n, gs.ld
+    row_bytes = A.code_bytes(ld, bits)
+    codes = torch.empty(W * row_bytes, dtype=torch.uint8, device=G.device)
+    rcodes = codes[:A.code_bytes(n, bits) + 16]
+    res = {}
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return sorted(ts)[len(ts) // 2]
+
+    cb = A.code_bytes(W * n, bits)
+    t = timed(lambda: A.aps_quantize(G, n, offs_t, se, pal, idx_t, Q=None, codes=codes))
+    res["quantize_to_codes"] = {"ms": t, "GBps": (4.0 * W * n + cb) / (t * 1e-3) / 1e9}
+    if row_bytes % 16 == 0:
+        # the W-worker sum over the codes themselves (the exchanged form)
+        t = timed(lambda: A.aps_sim_reduce_codes(codes, W, ld, n, offs_t, se, pal, idx_t, 0, out=out))
+        res["sim_reduce_codes"] = {"ms": t, "GBps": (A.code_bytes(n, bits) * W + 4.0 * n) / (t * 1e-3) / 1e9,
+                                   "elements_per_s": W * n / (t * 1e-3)}
+    A.aps_sim_reduce(G, n, offs_t, se, pal, idx_t, A.APS_OUTPUT_SCALED, out=None, codes_out=rcodes)
+    t = timed(lambda: A.aps_dequantize(None, rcodes, n, offs_t, se, pal, idx_t, out))
+    res["dequantize_from_codes"] = {"ms": t, "GBps": (A.code_bytes(n, bits) + 4.0 * n) / (t * 1e-3) / 1e9}
+    del codes
+    return res
 
 
 def cpu_baseline(G_t, gs, pal, budget_s: float, slice_cols: int = 65536):
@@ -191,6 +235,8 @@ def main():
     k4 = sum(e[2].elapsed_time(e[3]) for e in ev) / len(ev)
     assert bool(torch.isfinite(out).all()) or args.mode == "raw"
 
+    other = {} if args.no_other_calls else other_calls(A, G, gs, pal, idx_t, offs_t, se, out)
+
     alg_bytes = 4.0 * W * n + 4.0 * n     # read every worker row once, write the fp32 sum
     achieved = alg_bytes / (k4 * 1e-3) / 1e9
     traffic, traffic_src = traffic_from_profile(args.config, palette, alg_bytes)
@@ -222,6 +268,7 @@ def main():
             "traffic_source": traffic_src,
         },
         "kernels_ms": {"layer_maxabs": k1, "layer_scales": k2, "sim_reduce": k4},
+        "other_calls": other,
         "sim_reduce_elements_per_s": W * n / (k4 * 1e-3),
         "maxabs_GBps": 4.0 * W * n / (k1 * 1e-3) / 1e9,
         "kernel_source": source_digest(),

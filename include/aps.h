@@ -169,6 +169,30 @@ int aps_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n,
                    uint32_t flags, float* out, void* codes_out, void* stream);
 
 /*
+ * The SUM all-reduce of Algorithm 1 on low_g in the form the workers would
+ * exchange it: W rows of packed codes of already scaled and cast values (as
+ * written by aps_quantize), summed in worker order with the accumulator
+ * rounded to the format after every add (Sec. 5), then cast back and
+ * unscaled:
+ *   s = decode(c_0[j]);  s = R_fmt(s + decode(c_w[j])) for w = 1..W-1
+ *   out[j] = fl32(s / 2^ft)            (s itself with APS_OUTPUT_SCALED)
+ * It is the kernel each owner of a slice would run in a multi-GPU
+ * reduce-scatter of codes; for 5..8-bit formats it reads one byte per
+ * element-worker instead of four.
+ *
+ *   codes      W rows of packed codes, 16-byte aligned; the row stride is the
+ *              code bytes of ld elements (ld/2, ld or 2*ld), which must be a
+ *              multiple of 16 bytes
+ *   flags      0 or APS_OUTPUT_SCALED
+ *   out        fp32[n] out (16-byte aligned), or NULL
+ *   codes_out  packed codes of the scaled sum s, [n] (16-byte aligned), or NULL
+ */
+int aps_sim_reduce_codes(const void* codes, int32_t W, int64_t ld, int64_t n,
+                         const int64_t* offsets, int32_t L, const int32_t* scale_exp,
+                         const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,
+                         uint32_t flags, float* out, void* codes_out, void* stream);
+
+/*
  * Cast back and unscale (Algorithm 1, Cast(low_g, 8, 23) then g / 2^ft):
  *   out[j] = fl32(V[j] / 2^scale_exp[i])
  * where V is Q (fp32 values) if Q is non-NULL, else the decoded codes.

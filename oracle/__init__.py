@@ -95,6 +95,7 @@ def lib():
             "oracle_encode": (u32, [f64, _Fmt]),
             "oracle_decode": (f64, [u32, _Fmt]),
             "oracle_pack_codes": (None, [P, i64, P, i32, P, P, P]),
+            "oracle_sim_reduce_codes": (None, [P, i32, i64, i64, P, i32, P, P, P, u32, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -257,4 +258,16 @@ def dequantize(Q, codes, n: int, offsets, scale_exp, fmts, fmt_idx=None) -> np.n
     out = np.zeros(n, dtype=np.float32)
     lib().oracle_dequantize(_ptr(q), _ptr(c), n, _ptr(offs), offs.size - 1, _ptr(se),
                             _fmts(fmts), _ptr(_idx(fmt_idx)), _ptr(out))
+    return out
+
+
+def sim_reduce_codes(codes: np.ndarray, W: int, ld: int, n: int, offsets, scale_exp, fmts, fmt_idx=None,
+                     flags: int = 0) -> np.ndarray:
+    """codes: uint8 array of W rows of packed codes, row stride ld elements."""
+    c = _c(codes, np.uint8)
+    offs = _c(offsets, np.int64)
+    se = None if scale_exp is None else _c(scale_exp, np.int32)
+    out = np.zeros(n, dtype=np.float32)
+    lib().oracle_sim_reduce_codes(_ptr(c), int(W), int(ld), int(n), _ptr(offs), offs.size - 1, _ptr(se),
+                                  _fmts(fmts), _ptr(_idx(fmt_idx)), int(flags), _ptr(out))
     return out

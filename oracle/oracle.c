@@ -172,7 +172,7 @@ void oracle_layer_scales(const uint32_t* maxabs_bits, int32_t L, int32_t N,
 
 /* ------------------------------------------------------- quantize/reduce */
 
-/* Algorithm 1, line "g <- g * 2^ft": the gradient is fp32, so the product is
+/* Algorithm 1 scales the gradient, g <- g * 2^ft; g is fp32, so the product is
  * the fp32 value nearest to x * 2^ft (a single rounding, exact unless the
  * result leaves fp32's normal range). */
 static float scale_fp32(float x, int32_t ft) { return (float)ldexp((double)x, ft); }
@@ -310,6 +310,35 @@ void oracle_dequantize(const float* Q, const void* codes, int64_t n,
         for (int64_t j = offsets[i]; j < offsets[i + 1]; ++j) {
             const double v = Q ? (double)Q[j] : oracle_decode(get_code(codes, j, code_bits(f)), f);
             out[j] = (float)ldexp(v, -ft); /* g <- Cast(low_g, 8, 23) / 2^ft */
+        }
+    }
+}
+
+/* byte offset of element j's code in a row, and the row stride in bytes */
+static int64_t code_row_bytes(int64_t ld, int bits) {
+    return bits <= 4 ? ld / 2 : (bits <= 8 ? ld : 2 * ld);
+}
+
+void oracle_sim_reduce_codes(const void* codes, int32_t W, int64_t ld, int64_t n,
+                             const int64_t* offsets, int32_t L, const int32_t* scale_exp,
+                             const oracle_format* fmts, const uint8_t* fmt_idx,
+                             uint32_t flags, float* out) {
+    (void)n;
+    const uint8_t* base = (const uint8_t*)codes;
+    for (int32_t i = 0; i < L; ++i) {
+        const oracle_format f = fmts[fmt_idx ? fmt_idx[i] : 0];
+        const int bits = code_bits(f);
+        const int64_t stride = code_row_bytes(ld, bits);
+        const int32_t ft = scale_exp ? scale_exp[i] : 0;
+#pragma omp parallel for schedule(static)
+        for (int64_t j = offsets[i]; j < offsets[i + 1]; ++j) {
+            double s = 0.0;
+            for (int32_t w = 0; w < W; ++w) {
+                const double q = oracle_decode(get_code(base + w * stride, j, bits), f);
+                s = (w == 0) ? q : oracle_round(s + q, f); /* low-precision accumulator */
+            }
+            const float g = (float)s;
+            out[j] = (flags & ORACLE_OUTPUT_SCALED) ? g : (float)ldexp((double)g, -ft);
         }
     }
 }

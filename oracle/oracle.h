@@ -100,6 +100,16 @@ double oracle_decode(uint32_t code, oracle_format f);
 void oracle_pack_codes(const float* V, int64_t n, const int64_t* offsets, int32_t L,
                        const oracle_format* fmts, const uint8_t* fmt_idx, void* codes);
 
+/* The SUM all-reduce of Algorithm 1 applied to low_g as exchanged between
+ * workers: W rows of packed codes (row stride ld elements, code layout as in
+ * oracle_pack_codes), already scaled and cast.  Per element:
+ * s = decode(c_0); s = Cast(s + decode(c_w)) for w = 1..W-1; out = s / 2^ft
+ * (or s with ORACLE_OUTPUT_SCALED). */
+void oracle_sim_reduce_codes(const void* codes, int32_t W, int64_t ld, int64_t n,
+                             const int64_t* offsets, int32_t L, const int32_t* scale_exp,
+                             const oracle_format* fmts, const uint8_t* fmt_idx,
+                             uint32_t flags, float* out);
+
 #ifdef __cplusplus
 }
 #endif

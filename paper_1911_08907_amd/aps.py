@@ -28,7 +28,7 @@ APS_OUTPUT_SCALED = 2
 APS_MAX_FORMATS = 8
 
 EXPORTS = ("aps_format_supported", "aps_layer_maxabs", "aps_layer_scales", "aps_quantize",
-           "aps_sim_reduce", "aps_dequantize", "aps_strerror")
+           "aps_sim_reduce", "aps_sim_reduce_codes", "aps_dequantize", "aps_strerror")
 
 
 class ApsError(RuntimeError):
@@ -87,6 +87,7 @@ def lib() -> ctypes.CDLL:
             "aps_layer_scales": (ctypes.c_int, [P, i32, i32, FP, i32, P, P, P]),
             "aps_quantize": (ctypes.c_int, [P, i32, i64, i64, P, i32, P, FP, i32, P, P, P, P]),
             "aps_sim_reduce": (ctypes.c_int, [P, i32, i64, i64, P, i32, P, FP, i32, P, u32, P, P, P]),
+            "aps_sim_reduce_codes": (ctypes.c_int, [P, i32, i64, i64, P, i32, P, FP, i32, P, u32, P, P, P]),
             "aps_dequantize": (ctypes.c_int, [P, P, i64, P, i32, P, FP, i32, P, P, P]),
             "aps_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         }
@@ -179,6 +180,17 @@ def aps_sim_reduce(G, n: int, offsets, scale_exp, fmts, fmt_idx, flags: int = 0,
     _check("aps_sim_reduce", lib().aps_sim_reduce(_ptr(G), W, ld, n, _ptr(offsets), L, _ptr(scale_exp), pal,
                                                   nf, _ptr(fmt_idx), int(flags), _ptr(out), _ptr(codes_out),
                                                   _stream(stream)))
+
+
+def aps_sim_reduce_codes(codes, W: int, ld: int, n: int, offsets, scale_exp, fmts, fmt_idx, flags: int = 0,
+                         out=None, codes_out=None, stream=None) -> None:
+    """codes: a uint8 tensor holding W rows of packed codes (row stride: the
+    code bytes of ld elements)."""
+    pal, nf = _palette(fmts)
+    L = offsets.numel() - 1
+    _check("aps_sim_reduce_codes", lib().aps_sim_reduce_codes(_ptr(codes), int(W), int(ld), n, _ptr(offsets), L,
+                                                              _ptr(scale_exp), pal, nf, _ptr(fmt_idx), int(flags),
+                                                              _ptr(out), _ptr(codes_out), _stream(stream)))
 
 
 def aps_dequantize(Q, codes, n: int, offsets, scale_exp, fmts, fmt_idx, out, stream=None) -> None:

@@ -202,7 +202,7 @@ __device__ __forceinline__ float decode(uint32_t code, const FmtK& f) {
     return ((code >> (f.e + f.m)) & 1u) ? -a : a;
 }
 
-__device__ __forceinline__ int64_t code_byte(int64_t j, int cls) {
+__host__ __device__ __forceinline__ int64_t code_byte(int64_t j, int cls) {
     return cls == 0 ? (j >> 1) : (cls == 1 ? j : 2 * j);
 }
 
@@ -235,6 +235,13 @@ __device__ __forceinline__ void store_codes4(uint8_t* row, int64_t j, const uint
             *(uint16_t*)(row + 2 * jj) = (uint16_t)c[e];
         }
     }
+}
+
+__device__ __forceinline__ void put_code(uint8_t* row, int64_t j, uint32_t c, int cls) {
+    if (cls == 1)
+        row[j] = (uint8_t)c;
+    else
+        *(uint16_t*)(row + 2 * j) = (uint16_t)c;
 }
 
 __device__ __forceinline__ uint32_t load_code(const uint8_t* row, int64_t j, int cls) {
@@ -427,6 +434,67 @@ __global__ void k_scales(const uint32_t* __restrict__ maxabs, int32_t L, int32_t
     scale_exp[i] = r;
 }
 
+// ========================================================= row streaming
+
+// Makes the compiler wait for the load that produced v here, without an
+// instruction: an empty asm that reads its registers.
+__device__ __forceinline__ void touch(const f4& v) { asm volatile("" ::"v"(v.x), "v"(v.y), "v"(v.z), "v"(v.w)); }
+
+// Streams W rows of one thread's 16-byte column slice through the callbacks:
+// first(row 0), then step(row w, valid) for w = 1, 2, ... in order.  Two
+// register sets of UNROLL rows are in flight: while one set is consumed, the
+// loads of the next UNROLL rows are outstanding; the scheduling barrier keeps
+// those loads ahead of the math.  Rows past W-1 are loaded from row W-1 and
+// handed to step() with valid = false, so every path issues the same loads
+// and the compiler waits for exactly the row it is about to use.
+// after_issue() runs once, right after the first 2*UNROLL loads are issued.
+template <class Load, class AfterIssue, class First, class Step>
+__device__ __forceinline__ void stream_rows(int W, Load load, AfterIssue after_issue, First first, Step step) {
+    f4 A[UNROLL], B[UNROLL];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) A[u] = load(min(u, W - 1));
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) B[u] = load(min(UNROLL + u, W - 1));
+    __builtin_amdgcn_sched_barrier(0);
+    after_issue();
+    first(A[0]);
+#define APS_STEP(CUR, NXT)                                                        \
+    if (w + UNROLL < W) {                                                         \
+        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u)                        \
+            NXT[u] = load(min(w + UNROLL + u, W - 1));                            \
+        __builtin_amdgcn_sched_barrier(0);                                        \
+        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u) step(CUR[u], true);    \
+        w += UNROLL;                                                              \
+    } else {                                                                      \
+        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u) {                      \
+            touch(CUR[u]);                                                        \
+            step(CUR[u], w + u < W);                                              \
+        }                                                                         \
+        break;                                                                    \
+    }
+    if (UNROLL < W) {
+#pragma unroll
+        for (int u = 1; u < UNROLL; ++u) step(A[u], true);
+        int w = UNROLL;
+        for (;;) {
+            APS_STEP(B, A)
+            APS_STEP(A, B)
+        }
+    } else {
+#pragma unroll
+        for (int u = 1; u < UNROLL; ++u) {
+            touch(A[u]);
+            step(A[u], u < W);
+        }
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+            touch(B[u]);
+            step(B[u], false);
+        }
+    }
+#undef APS_STEP
+}
+
 // ===================================================== K4: sim reduce
 
 struct ReduceArgs {
@@ -480,77 +548,26 @@ __device__ __forceinline__ void reduce_vec(const ReduceArgs& a, const FmtK& f, i
     bool bad0 = false, bad1 = false, bad2 = false, bad3 = false;
     const float* p = a.G + j;
     const int64_t ld = a.ld;
-    const int W = a.W;
-    // Two register sets of UNROLL rows each: while one set is consumed, the
-    // loads of the next UNROLL rows (into the other set) are already in
-    // flight; the scheduling barrier keeps those loads ahead of the math.
-    // Loads past the last row are clamped to row W-1 and their values are
-    // replaced by -0 when consumed (s + -0 == s, signs of zero included), so
-    // every path consumes the same loads and the compiler waits for exactly
-    // the row it is about to use.
-    f4 A[UNROLL], B[UNROLL];
+    float s0, s1, s2, s3;
+    // a row past the last one counts as -0, which leaves every sum unchanged
+    // (s + -0 == s, signs of zero included)
     const f4 neg0 = {-0.0f, -0.0f, -0.0f, -0.0f};
-#pragma unroll
-    for (int u = 0; u < UNROLL; ++u) A[u] = ld4(p + (int64_t)min(u, W - 1) * ld);
-#define APS_CONSUME(v)                                                   \
-    do {                                                                 \
-        s0 = accum<V>(s0, quant<V>((v).x, F[0], f, bad0), f, bad0);      \
-        s1 = accum<V>(s1, quant<V>((v).y, F[1], f, bad1), f, bad1);      \
-        s2 = accum<V>(s2, quant<V>((v).z, F[2], f, bad2), f, bad2);      \
-        s3 = accum<V>(s3, quant<V>((v).w, F[3], f, bad3), f, bad3);      \
-    } while (0)
-#define APS_LOAD(NXT)                                                    \
-    _Pragma("unroll") for (int u = 0; u < UNROLL; ++u)                   \
-        NXT[u] = ld4(p + (int64_t)min(w + UNROLL + u, W - 1) * ld);      \
-    __builtin_amdgcn_sched_barrier(0);
-#define APS_LAST(CUR)                                                    \
-    _Pragma("unroll") for (int u = 0; u < UNROLL; ++u) {                 \
-        /* an empty asm that reads the row makes the compiler wait for   \
-           its load here, also for rows the select below discards */     \
-        asm volatile("" ::"v"(CUR[u].x), "v"(CUR[u].y), "v"(CUR[u].z), "v"(CUR[u].w)); \
-        const f4 v = (w + u < W) ? CUR[u] : neg0;                        \
-        APS_CONSUME(v);                                                  \
-    }
-#define APS_STEP(CUR, NXT)                                               \
-    if (w + UNROLL < W) {                                                \
-        APS_LOAD(NXT)                                                    \
-        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u)               \
-            APS_CONSUME(CUR[u]);                                         \
-        w += UNROLL;                                                     \
-    } else {                                                             \
-        APS_LAST(CUR)                                                    \
-        break;                                                           \
-    }
-    int w = 0;
-    APS_LOAD(B)  // rows UNROLL..2*UNROLL-1, clamped: loaded whatever W is
-    flush_out(a, pd);  // the previous chunk's outputs, now behind this chunk's loads
-    // row 0 starts the sums; rows 1..UNROLL-1 of the first group follow
-    float s0 = quant<V>(A[0].x, F[0], f, bad0);
-    float s1 = quant<V>(A[0].y, F[1], f, bad1);
-    float s2 = quant<V>(A[0].z, F[2], f, bad2);
-    float s3 = quant<V>(A[0].w, F[3], f, bad3);
-    if (UNROLL < W) {
-#pragma unroll
-        for (int u = 1; u < UNROLL; ++u) APS_CONSUME(A[u]);
-        w = UNROLL;
-        for (;;) {
-            APS_STEP(B, A)
-            APS_STEP(A, B)
-        }
-    } else {
-        // W <= UNROLL: the B rows are all past the end; consume them as -0 too
-#pragma unroll
-        for (int u = 1; u < UNROLL; ++u) {
-            const f4 v = (u < W) ? A[u] : neg0;
-            APS_CONSUME(v);
-        }
-        w = UNROLL;
-        APS_LAST(B)
-    }
-#undef APS_STEP
-#undef APS_LAST
-#undef APS_LOAD
-#undef APS_CONSUME
+    stream_rows(
+        a.W, [&](int r) { return ld4(p + (int64_t)r * ld); },
+        [&]() { flush_out(a, pd); },  // the previous chunk's outputs, behind this chunk's loads
+        [&](const f4& x) {
+            s0 = quant<V>(x.x, F[0], f, bad0);
+            s1 = quant<V>(x.y, F[1], f, bad1);
+            s2 = quant<V>(x.z, F[2], f, bad2);
+            s3 = quant<V>(x.w, F[3], f, bad3);
+        },
+        [&](const f4& r, bool valid) {
+            const f4 v = valid ? r : neg0;
+            s0 = accum<V>(s0, quant<V>(v.x, F[0], f, bad0), f, bad0);
+            s1 = accum<V>(s1, quant<V>(v.y, F[1], f, bad1), f, bad1);
+            s2 = accum<V>(s2, quant<V>(v.z, F[2], f, bad2), f, bad2);
+            s3 = accum<V>(s3, quant<V>(v.w, F[3], f, bad3), f, bad3);
+        });
     s0 = finish<V>(s0, bad0);
     s1 = finish<V>(s1, bad1);
     s2 = finish<V>(s2, bad2);
@@ -600,6 +617,229 @@ __global__ __launch_bounds__(BLOCK) void k_sim_reduce(ReduceArgs a, Layers ly, P
     flush_out(a, pd);
 }
 
+// ================================================ K4c: reduce of packed codes
+
+struct CodesArgs {
+    const uint8_t* __restrict__ codes;  // W rows of packed codes
+    float* __restrict__ out;
+    uint8_t* __restrict__ codes_out;
+    int64_t row_bytes;  // bytes per code row (a multiple of 16)
+    int32_t W;
+    uint32_t flags;
+};
+
+// Per-element scale exponents for N consecutive elements from j.
+template <int N>
+__device__ __forceinline__ void elem_scales_n(const Layers& ly, const ChunkInfo& ci, int64_t j, int32_t* ft) {
+    int li = ci.i0;
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+        while (li < ci.i1 && ly.offsets[li + 1] <= j + e) ++li;
+        ft[e] = ly.scale_exp ? clamp_exp(ly.scale_exp[li]) : 0;
+    }
+}
+
+// Code e (0..EPT-1) of a thread's 16-byte slice.
+template <int CC>
+__device__ __forceinline__ uint32_t slice_code(const f4& v, int e) {
+    const uint32_t w[4] = {f2u(v.x), f2u(v.y), f2u(v.z), f2u(v.w)};
+    if constexpr (CC == 0) return (w[e >> 3] >> ((e & 7) * 4)) & 15u;
+    else if constexpr (CC == 1) return (w[e >> 2] >> ((e & 3) * 8)) & 255u;
+    else return (w[e >> 1] >> ((e & 1) * 16)) & 0xFFFFu;
+}
+
+// The W-worker rounded sum of already scaled and cast gradients given as
+// packed codes (the low-precision values the workers exchange).  A thread
+// owns the codes in 16 bytes of each row: 32 nibble, 16 byte or 8 uint16
+// codes.  Codes of up to 8 bits decode through a table of working-domain
+// values in LDS; 16-bit codes decode arithmetically.
+template <int V, int CC>
+__global__ __launch_bounds__(BLOCK) void k_sim_reduce_codes(CodesArgs a, Layers ly, Pal pal) {
+    constexpr int EPT = CC == 0 ? 32 : (CC == 1 ? 16 : 8);
+    constexpr int64_t CHC = (int64_t)BLOCK * EPT;
+    __shared__ float lut[256];
+    int lut_pidx = -1;
+    const int64_t nchunks = (ly.n + CHC - 1) / CHC;
+    int64_t cb, ce;
+    block_range(nchunks, cb, ce);
+    int hint = 0;
+    for (int64_t c = cb; c < ce; ++c) {
+        const int64_t start = c * CHC;
+        const int64_t end = min(start + CHC, ly.n);
+        const ChunkInfo ci = chunk_layers(ly, start, end, hint);
+        hint = ci.i0;
+        if (ci.mixed) continue;
+        const FmtK& f = pal.f[ci.pidx];
+        if (f.variant != V) continue;
+        if constexpr (CC < 2) {
+            if (ci.pidx != lut_pidx) {  // uniform
+                __syncthreads();
+                for (int t = threadIdx.x; t < (CC == 0 ? 16 : 256); t += BLOCK)
+                    lut[t] = __builtin_amdgcn_ldexpf(decode((uint32_t)t, f), f.k);
+                __syncthreads();
+                lut_pidx = ci.pidx;
+            }
+        }
+        const int64_t j = start + (int64_t)threadIdx.x * EPT;
+        if (j >= end) continue;
+        const uint8_t* p = a.codes + code_byte(j, CC);
+        const int64_t rb = a.row_bytes;
+        float s[EPT];
+        uint32_t bad = 0;
+        auto dec = [&](uint32_t code) -> float {
+            if constexpr (CC < 2) return lut[code];
+            else return __builtin_amdgcn_ldexpf(decode(code, f), f.k);
+        };
+        stream_rows(
+            a.W, [&](int r) { return ld4((const float*)(p + (int64_t)r * rb)); }, [&]() {},
+            [&](const f4& v) {
+#pragma unroll
+                for (int e = 0; e < EPT; ++e) s[e] = dec(slice_code<CC>(v, e));
+            },
+            [&](const f4& v, bool valid) {
+                if (valid) {
+#pragma unroll
+                    for (int e = 0; e < EPT; ++e) {
+                        bool b = false;
+                        s[e] = accum<V>(s[e], dec(slice_code<CC>(v, e)), f, b);
+                        if constexpr (VT<V>::m0) bad |= (uint32_t)b << e;
+                    }
+                }
+            });
+        // output exponents, per element when the chunk crosses layers
+        const int32_t fdom = ((a.flags & APS_OUTPUT_SCALED) ? 0 : 1);
+        int32_t ft[EPT];
+        if (ci.i0 == ci.i1) {
+            const int32_t t = ly.scale_exp ? clamp_exp(cld(ly.scale_exp, ci.i0)) : 0;
+#pragma unroll
+            for (int e = 0; e < EPT; ++e) ft[e] = t;
+        } else {
+            elem_scales_n<EPT>(ly, ci, j, ft);
+        }
+        float o[EPT];
+        uint32_t cw[4] = {0, 0, 0, 0};
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+            const float se = VT<V>::m0 ? (((bad >> e) & 1u) ? __builtin_nanf("") : s[e]) : s[e];
+            o[e] = __builtin_amdgcn_ldexpf(se, -(fdom * ft[e] + f.k));
+            if (a.codes_out) {
+                const uint32_t cd = encode(__builtin_amdgcn_ldexpf(se, -f.k), f);
+                if constexpr (CC == 0) cw[e >> 3] |= (cd & 15u) << ((e & 7) * 4);
+                else if constexpr (CC == 1) cw[e >> 2] |= (cd & 255u) << ((e & 3) * 8);
+                else cw[e >> 1] |= (cd & 0xFFFFu) << ((e & 1) * 16);
+            }
+        }
+        if (j + EPT <= end) {
+            if (a.out) {
+#pragma unroll
+                for (int q = 0; q < EPT / 4; ++q) {
+                    const f4 v = {o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]};
+                    __builtin_nontemporal_store(v, (f4*)(a.out + j + 4 * q));
+                }
+            }
+            if (a.codes_out) {
+                uint4 v;
+                v.x = cw[0];
+                v.y = cw[1];
+                v.z = cw[2];
+                v.w = cw[3];
+                *(uint4*)(a.codes_out + code_byte(j, CC)) = v;
+            }
+        } else {
+            // ragged end of the gradient: element by element
+            for (int e = 0; e < EPT && j + e < end; ++e) {
+                if (a.out) a.out[j + e] = o[e];
+                if (a.codes_out) {
+                    const int64_t jj = j + e;
+                    if constexpr (CC == 0) {
+                        const uint32_t cd = (cw[e >> 3] >> ((e & 7) * 4)) & 15u;
+                        uint8_t* pb = a.codes_out + (jj >> 1);
+                        const int sh = (int)(jj & 1) * 4;
+                        *pb = (uint8_t)((*pb & ~(15u << sh)) | (cd << sh));
+                    } else if constexpr (CC == 1) {
+                        a.codes_out[jj] = (uint8_t)(cw[e >> 2] >> ((e & 3) * 8));
+                    } else {
+                        *(uint16_t*)(a.codes_out + 2 * jj) = (uint16_t)(cw[e >> 1] >> ((e & 1) * 16));
+                    }
+                }
+            }
+        }
+    }
+}
+
+// Mixed-format chunks of the codes reduce: element pairs per thread, any variant.
+template <int V>
+__device__ float reduce_codes_elem(const CodesArgs& a, const FmtK& f, int cc, int64_t j) {
+    bool bad = false;
+    const int64_t cb = code_byte(j, cc);
+    auto get = [&](int w) -> float {
+        const uint8_t* row = a.codes + (int64_t)w * a.row_bytes;
+        uint32_t code;
+        if (cc == 0)
+            code = (row[cb] >> ((j & 1) * 4)) & 15u;
+        else if (cc == 1)
+            code = row[cb];
+        else
+            code = *(const uint16_t*)(row + cb);
+        return __builtin_amdgcn_ldexpf(decode(code, f), f.k);
+    };
+    float s = get(0);
+    for (int w = 1; w < a.W; ++w) s = accum<V>(s, get(w), f, bad);
+    return finish<V>(s, bad);
+}
+
+__device__ float reduce_codes_any(const CodesArgs& a, const FmtK& f, int cc, int64_t j) {
+    switch (f.variant) {
+        case V_INT_F32: return reduce_codes_elem<V_INT_F32>(a, f, cc, j);
+        case V_INT_F64: return reduce_codes_elem<V_INT_F64>(a, f, cc, j);
+        case V_INT_EXACT: return reduce_codes_elem<V_INT_EXACT>(a, f, cc, j);
+        case V_INT_M0: return reduce_codes_elem<V_INT_M0>(a, f, cc, j);
+        case V_TOP_F32: return reduce_codes_elem<V_TOP_F32>(a, f, cc, j);
+        case V_TOP_F64: return reduce_codes_elem<V_TOP_F64>(a, f, cc, j);
+        case V_TOP_M0: return reduce_codes_elem<V_TOP_M0>(a, f, cc, j);
+        case V_LOW_F32: return reduce_codes_elem<V_LOW_F32>(a, f, cc, j);
+        case V_LOW_F64: return reduce_codes_elem<V_LOW_F64>(a, f, cc, j);
+        default: return reduce_codes_elem<V_LOW_M0>(a, f, cc, j);
+    }
+}
+
+// One block per layer boundary; the chunk (of the codes reduce's chunk size)
+// owning the first boundary strictly inside it, when it mixes palette entries.
+template <int CC>
+__global__ __launch_bounds__(BLOCK) void k_sim_reduce_codes_mixed(CodesArgs a, Layers ly, Pal pal) {
+    constexpr int64_t CHC = (int64_t)BLOCK * (CC == 0 ? 32 : (CC == 1 ? 16 : 8));
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    pal_to_lds(pal, spal);
+    const int b = blockIdx.x;
+    if (b < 1 || b >= ly.L) return;
+    const int64_t pb = cld(ly.offsets, b);
+    if (pb <= 0 || pb >= ly.n || pb % CHC == 0) return;
+    const int64_t start = pb / CHC * CHC;
+    const int64_t end = min(start + CHC, ly.n);
+    if (cld(ly.offsets, b - 1) > start) return;
+    if (!chunk_layers(ly, start, end, 0).mixed) return;
+    for (int64_t j0 = start + 2 * (int64_t)threadIdx.x; j0 < end; j0 += 2 * BLOCK) {
+        uint32_t cd[2] = {0, 0};
+        for (int e = 0; e < 2; ++e) {
+            const int64_t j = j0 + e;
+            if (j >= end) break;
+            const int li = find_layer(ly.offsets, ly.L, j, 0);
+            const FmtK& f = spal[ly.fmt_idx[li]];
+            const int32_t ft = ly.scale_exp ? clamp_exp(ly.scale_exp[li]) : 0;
+            const float sv = reduce_codes_any(a, f, CC, j);
+            const int fd = (a.flags & APS_OUTPUT_SCALED) ? 0 : ft;
+            if (a.out) a.out[j] = __builtin_amdgcn_ldexpf(sv, -(fd + f.k));
+            cd[e] = encode(__builtin_amdgcn_ldexpf(sv, -f.k), f);
+            if (a.codes_out && CC != 0) put_code(a.codes_out, j, cd[e], CC);
+        }
+        if (a.codes_out && CC == 0) {
+            uint8_t* q = a.codes_out + (j0 >> 1);
+            *q = (j0 + 1 < end) ? (uint8_t)((cd[0] & 15u) | ((cd[1] & 15u) << 4))
+                                : (uint8_t)((*q & 0xF0u) | (cd[0] & 15u));
+        }
+    }
+}
+
 // One element through the whole W-worker loop, any variant (per-lane format).
 template <int V>
 __device__ float reduce_elem(const ReduceArgs& a, const FmtK& f, int64_t j, int F) {
@@ -637,13 +877,6 @@ __device__ __forceinline__ bool mixed_chunk_of_boundary(const Layers& ly, int b,
     if (cld(ly.offsets, b - 1) > start) return false;  // an earlier boundary owns it
     const ChunkInfo ci = chunk_layers(ly, start, end, 0);
     return ci.mixed;
-}
-
-__device__ __forceinline__ void put_code(uint8_t* row, int64_t j, uint32_t c, int cls) {
-    if (cls == 1)
-        row[j] = (uint8_t)c;
-    else
-        *(uint16_t*)(row + 2 * j) = (uint16_t)c;
 }
 
 // Each thread owns an element pair (2t, 2t+1) of the chunk, so a byte of
@@ -991,6 +1224,46 @@ extern "C" int aps_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n, 
 #undef APS_LAUNCH_R
     if (fmt_idx && n_fmts > 1 && L > 1)
         hipLaunchKernelGGL(k_sim_reduce_mixed, dim3((unsigned)L), dim3(BLOCK), 0, s, a, ly, pal);
+    return launched();
+}
+
+extern "C" int aps_sim_reduce_codes(const void* codes, int32_t W, int64_t ld, int64_t n, const int64_t* offsets,
+                                    int32_t L, const int32_t* scale_exp, const aps_format* fmts, int32_t n_fmts,
+                                    const uint8_t* fmt_idx, uint32_t flags, float* out, void* codes_out,
+                                    void* stream) {
+    if (!codes || !offsets) return APS_ERR_NULL;
+    if (W < 1 || W > APS_MAX_WORKERS || L < 1 || n < 0 || n > APS_MAX_ELEMS || ld < n) return APS_ERR_SIZE;
+    if (!out && !codes_out && n > 0) return APS_ERR_NULL;
+    if (flags & ~APS_OUTPUT_SCALED) return APS_ERR_UNSUPPORTED;
+    Pal pal;
+    int ccls = 0;
+    int st = check_palette(fmts, n_fmts, pal, &ccls);
+    if (st != APS_OK) return st;
+    if (ccls < 0 || ccls > 2) return APS_ERR_UNSUPPORTED;
+    const int64_t row_bytes = code_byte(ld, ccls);
+    if (!aligned16(codes) || (row_bytes & 15) || (out && !aligned16(out)) || (codes_out && !aligned16(codes_out)))
+        return APS_ERR_ALIGN;
+    if (n == 0) return APS_OK;
+    hipStream_t s = (hipStream_t)stream;
+    Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
+    CodesArgs a{(const uint8_t*)codes, out, (uint8_t*)codes_out, row_bytes, W, flags};
+    const int64_t ept = ccls == 0 ? 32 : (ccls == 1 ? 16 : 8);
+    const int64_t nchunks = (n + BLOCK * ept - 1) / (BLOCK * ept);
+    const dim3 grid((unsigned)grid_for(nchunks, BLOCKS_PER_CU));
+    const unsigned vm = variant_mask(pal, n_fmts);
+#define APS_LAUNCH_C(v)                                                                                      \
+    if (vm & (1u << (v))) {                                                                                  \
+        if (ccls == 0) hipLaunchKernelGGL((k_sim_reduce_codes<v, 0>), grid, dim3(BLOCK), 0, s, a, ly, pal);  \
+        if (ccls == 1) hipLaunchKernelGGL((k_sim_reduce_codes<v, 1>), grid, dim3(BLOCK), 0, s, a, ly, pal);  \
+        if (ccls == 2) hipLaunchKernelGGL((k_sim_reduce_codes<v, 2>), grid, dim3(BLOCK), 0, s, a, ly, pal);  \
+    }
+    APS_FOR_VARIANTS(APS_LAUNCH_C)
+#undef APS_LAUNCH_C
+    if (fmt_idx && n_fmts > 1 && L > 1) {
+        if (ccls == 0) hipLaunchKernelGGL(k_sim_reduce_codes_mixed<0>, dim3((unsigned)L), dim3(BLOCK), 0, s, a, ly, pal);
+        if (ccls == 1) hipLaunchKernelGGL(k_sim_reduce_codes_mixed<1>, dim3((unsigned)L), dim3(BLOCK), 0, s, a, ly, pal);
+        if (ccls == 2) hipLaunchKernelGGL(k_sim_reduce_codes_mixed<2>, dim3((unsigned)L), dim3(BLOCK), 0, s, a, ly, pal);
+    }
     return launched();
 }
 

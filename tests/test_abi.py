@@ -39,7 +39,8 @@ def _declared():
 
 def test_header_declares_the_five_calls():
     d = _declared()
-    for name in ("aps_layer_maxabs", "aps_layer_scales", "aps_quantize", "aps_sim_reduce", "aps_dequantize"):
+    for name in ("aps_layer_maxabs", "aps_layer_scales", "aps_quantize", "aps_sim_reduce", "aps_dequantize",
+                 "aps_sim_reduce_codes"):
         assert name in d
 
 
@@ -154,3 +155,17 @@ def test_dequantize_validation(lib):
     assert f(GOOD, None, 64, GOOD, 0, None, pal, 1, None, GOOD, None) == A.APS_ERR_SIZE
     assert f(GOOD, None, 64, GOOD, 1, None, pal, 1, None, MIS, None) == A.APS_ERR_ALIGN
     assert f(None, GOOD, 64, GOOD, 1, None, _pal(A.Format(8, 23)), 1, None, GOOD, None) == A.APS_ERR_UNSUPPORTED
+
+
+@no_gpu
+def test_sim_reduce_codes_validation(lib):
+    f = lib.aps_sim_reduce_codes
+    pal = _pal(A.Format(5, 2))
+    assert f(None, 2, 64, 64, GOOD, 1, None, pal, 1, None, 0, GOOD, None, None) == A.APS_ERR_NULL
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, pal, 1, None, 0, None, None, None) == A.APS_ERR_NULL
+    assert f(GOOD, 0, 64, 64, GOOD, 1, None, pal, 1, None, 0, GOOD, None, None) == A.APS_ERR_SIZE
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, pal, 1, None, 1, GOOD, None, None) == A.APS_ERR_UNSUPPORTED
+    assert f(MIS, 2, 64, 64, GOOD, 1, None, pal, 1, None, 0, GOOD, None, None) == A.APS_ERR_ALIGN
+    assert f(GOOD, 2, 68, 64, GOOD, 1, None, pal, 1, None, 0, GOOD, None, None) == A.APS_ERR_ALIGN   # 68-byte rows
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, _pal(A.Format(8, 23)), 1, None, 0, GOOD, None,
+             None) == A.APS_ERR_UNSUPPORTED

@@ -116,6 +116,18 @@ def run_case(dev, G: np.ndarray, n: int, offs: np.ndarray, pal, fmt_idx=None, mo
             assert _codes_equal(qc[w * rb:(w + 1) * rb], oc, n, cbits, np.isnan(o_Q[w, :n])), \
                 f"{tag} quantize codes row {w}"
 
+    # reduce of the quantized codes (the exchanged form), when rows are 16-byte aligned
+    if with_codes and _row_code_bytes(ld, cbits) % 16 == 0 and n > 0:
+        rc2 = torch.zeros(max(16, A.code_bytes(n, cbits)), dtype=torch.uint8, device=dev)
+        o2 = torch.zeros(max(n, 1), dtype=torch.float32, device=dev)
+        A.aps_sim_reduce_codes(qc_t, W, ld, n, offs_t, se_t, pal, idx_t, 0, out=o2, codes_out=rc2)
+        oq = O.sim_reduce_codes(qc.reshape(W, -1), W, ld, n, offs, o_se, opal, fmt_idx)
+        g2 = o2.cpu().numpy()[:n]
+        assert same_f32(g2, oq), f"{tag} sim_reduce_codes {first_diff(g2, oq)}"
+        oq_s = O.sim_reduce_codes(qc.reshape(W, -1), W, ld, n, offs, o_se, opal, fmt_idx, flags=O.OUTPUT_SCALED)
+        assert _codes_equal(rc2.cpu().numpy(), O.pack_codes(oq_s, offs, opal, fmt_idx), n, cbits,
+                            np.isnan(oq_s)), f"{tag} sim_reduce_codes codes"
+
     # fused reduce, plain and scaled output, with codes
     out_t = torch.zeros(max(n, 1), dtype=torch.float32, device=dev)
     rc_t = torch.zeros(max(16, A.code_bytes(n, cbits)), dtype=torch.uint8, device=dev) if with_codes else None
@@ -386,3 +398,33 @@ def test_run_to_run_determinism(dev):
     b, _, _ = A.aps_step(gs.G, gs.n, offs_t, pal)
     torch.cuda.synchronize()
     assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+@pytest.mark.parametrize("f", [F(5, 2), F(4, 3), F(3, 0), F(2, 1), F(5, 10), F(8, 7), F(3, 4), F(4, 3, 5)], ids=str)
+def test_sim_reduce_codes_random_codes(dev, f):
+    """Every code value (INF and NaN codes included) as input to the codes reduce."""
+    rng = np.random.default_rng(40 + f.e * 3 + f.m)
+    cls = _code_cls(f.bits)
+    sizes = [0, 5, 4096, 31, 1, 8191, 3, 600]
+    offs = np.zeros(len(sizes) + 1, np.int64)
+    offs[1:] = np.cumsum(sizes)
+    n = int(offs[-1])
+    ld = (n + 63) // 64 * 64
+    for W in (1, 2, 7, 16):
+        codes = rng.integers(0, 1 << f.bits, (W, ld))
+        if cls == 0:
+            rows = np.zeros((W, ld // 2), np.uint8)
+            rows[:] = (codes[:, 0::2] & 15) | ((codes[:, 1::2] & 15) << 4)
+        elif cls == 1:
+            rows = codes.astype(np.uint8)
+        else:
+            rows = codes.astype("<u2").view(np.uint8).reshape(W, -1)
+        se = rng.integers(-20, 20, len(sizes)).astype(np.int32)
+        c_t = torch.from_numpy(np.ascontiguousarray(rows).reshape(-1)).to(dev)
+        offs_t = torch.from_numpy(offs).to(dev)
+        se_t = torch.from_numpy(se).to(dev)
+        out = torch.zeros(n, dtype=torch.float32, device=dev)
+        A.aps_sim_reduce_codes(c_t, W, ld, n, offs_t, se_t, [f], None, 0, out=out)
+        o = O.sim_reduce_codes(rows, W, ld, n, offs, se, ofmt(f))
+        g = out.cpu().numpy()
+        assert same_f32(g, o), (f, W, first_diff(g, o))

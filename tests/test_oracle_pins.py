@@ -412,3 +412,42 @@ def test_raw_mode_overflow_and_nan():
     assert np.isnan(out[1])          # -INF + INF
     assert np.isnan(out[2])          # NaN propagates
     assert out[3] == np.inf          # 49152 + 49152 = 98304 > 61440 -> INF
+
+
+# --------------------------------------------------- reduce of packed codes
+
+def _pack(codes_rows, bits):
+    """Pack W rows of integer codes (independent of the oracle's packer)."""
+    W, n = codes_rows.shape
+    if bits <= 4:
+        rb = (n + 1) // 2
+        out = np.zeros((W, rb), np.uint8)
+        for w in range(W):
+            for j in range(n):
+                out[w, j // 2] |= (int(codes_rows[w, j]) & 15) << (4 * (j % 2))
+    elif bits <= 8:
+        out = codes_rows.astype(np.uint8)
+    else:
+        out = codes_rows.astype("<u2").view(np.uint8).reshape(W, -1)
+    return out
+
+
+@pytest.mark.parametrize("f", [F(3, 0), F(4, 3), F(5, 2), F(2, 1), F(5, 10)], ids=str)
+def test_sim_reduce_codes_brute_force(f):
+    rng = np.random.default_rng(30 + f.e + f.m)
+    vals = X.values(f.e, f.m, f.b)
+    nfin = len(vals)
+    for trial in range(5):
+        W = int(rng.integers(1, 9))
+        n = int(rng.integers(2, 41)) // 2 * 2
+        # finite codes only (INF/NaN arithmetic is covered elsewhere)
+        mags = rng.integers(0, nfin, (W, n))
+        signs = rng.integers(0, 2, (W, n))
+        codes = mags | (signs << (f.e + f.m))
+        packed = _pack(codes, f.bits)
+        offs = np.array([0, n // 2, n], np.int64)
+        got = O.sim_reduce_codes(packed, W, n, n, offs, None, f, flags=O.OUTPUT_SCALED)
+        for j in range(n):
+            qs = [(-1 if signs[w, j] else 1) * vals[mags[w, j]] for w in range(W)]
+            ref = X.sum_exact(qs, f.e, f.m, f.b)
+            assert got[j] == float(ref), (f, trial, j)
