@@ -920,63 +920,64 @@ struct QuantArgs {
     int32_t code_cls;
 };
 
+// One block walks a range of chunks; for each chunk its threads stream all W
+// rows (two register sets of rows in flight), cast each row and store it.
 template <int V>
 __global__ __launch_bounds__(BLOCK) void k_quantize(QuantArgs a, Layers ly, Pal pal) {
     const int64_t nchunks = (ly.n + CH - 1) / CH;
-    int64_t tb, te;
-    block_range(nchunks * a.W, tb, te);
+    int64_t cb, ce;
+    block_range(nchunks, cb, ce);
     int hint = 0;
-    for (int64_t t = tb; t < te; ++t) {
-        const int64_t w = t / nchunks;
-        const int64_t c = t - w * nchunks;
+    for (int64_t c = cb; c < ce; ++c) {
         const int64_t start = c * CH;
         const int64_t end = min(start + CH, ly.n);
         const ChunkInfo ci = chunk_layers(ly, start, end, hint);
         hint = ci.i0;
-        if (ci.mixed) continue;
+        if (ci.mixed) continue;  // handled by k_quantize_mixed
         const FmtK& f = pal.f[ci.pidx];
         if (f.variant != V) continue;
         const int64_t j = start + (int64_t)threadIdx.x * VEC;
         if (j >= end) continue;
         int32_t ft[4];
         if (ci.i0 == ci.i1) {
-            const int32_t s = ly.scale_exp ? clamp_exp(cld(ly.scale_exp, ci.i0)) : 0;
-            ft[0] = ft[1] = ft[2] = ft[3] = s;
+            const int32_t t = ly.scale_exp ? clamp_exp(cld(ly.scale_exp, ci.i0)) : 0;
+            ft[0] = ft[1] = ft[2] = ft[3] = t;
         } else {
             elem_scales(ly, ci, j, ft);
         }
-        const int64_t off = w * a.ld + j;
-        const f4 x = *(const f4*)(a.X + off);
-        bool bad = false;
-        float q[4];
-        q[0] = quant<V>(x.x, ft[0] + f.k, f, bad);
-        q[1] = quant<V>(x.y, ft[1] + f.k, f, bad);
-        q[2] = quant<V>(x.z, ft[2] + f.k, f, bad);
-        q[3] = quant<V>(x.w, ft[3] + f.k, f, bad);
-        const float xs[4] = {x.x, x.y, x.z, x.w};
-        float v[4];
+        const float* p = a.X + j;
+        const int64_t ld = a.ld;
+        int64_t r = 0;  // row of the next callback
+        auto row = [&](const f4& x, bool valid) {
+            if (valid) {
+                bool bad = false;
+                const float xs[4] = {x.x, x.y, x.z, x.w};
+                float v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            v[e] = __builtin_amdgcn_ldexpf(q[e], -f.k);                   // native scaled value
-            if constexpr (VT<V>::m0) v[e] = (xs[e] != xs[e]) ? xs[e] : v[e];  // NaN stays NaN
-        }
-        if (a.Q) {
-            if (j + 4 <= end) {
-                f4 o;
-                o.x = v[0];
-                o.y = v[1];
-                o.z = v[2];
-                o.w = v[3];
-                *(f4*)(a.Q + off) = o;
-            } else {
-                for (int e = 0; e < 4 && j + e < end; ++e) a.Q[off + e] = v[e];
+                for (int e = 0; e < 4; ++e) {
+                    v[e] = __builtin_amdgcn_ldexpf(quant<V>(xs[e], ft[e] + f.k, f, bad), -f.k);  // native scaled value
+                    if constexpr (VT<V>::m0) v[e] = (xs[e] != xs[e]) ? xs[e] : v[e];       // NaN stays NaN
+                }
+                const int64_t off = r * ld + j;
+                if (a.Q) {
+                    if (j + 4 <= end) {
+                        const f4 o = {v[0], v[1], v[2], v[3]};
+                        *(f4*)(a.Q + off) = o;
+                    } else {
+                        for (int e = 0; e < 4 && j + e < end; ++e) a.Q[off + e] = v[e];
+                    }
+                }
+                if (a.codes) {
+                    uint32_t cc[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) cc[e] = encode(v[e], f);
+                    store_codes4(a.codes + code_byte(r * ld, a.code_cls), j, cc, a.code_cls, end);
+                }
             }
-        }
-        if (a.codes) {
-            uint32_t cc[4];
-            for (int e = 0; e < 4; ++e) cc[e] = encode(v[e], f);
-            store_codes4(a.codes + code_byte(w * a.ld, a.code_cls), j, cc, a.code_cls, end);
-        }
+            ++r;
+        };
+        stream_rows(
+            a.W, [&](int rr) { return ld4(p + (int64_t)rr * ld); }, [&]() {}, [&](const f4& x) { row(x, true); }, row);
     }
 }
 
@@ -1052,11 +1053,29 @@ __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal 
     for (int64_t c = cb; c < ce; ++c) {
         const int64_t start = c * CH;
         const int64_t end = min(start + CH, ly.n);
-        const int i0 = find_layer(ly.offsets, ly.L, start, hint);
-        hint = i0;
+        const ChunkInfo ci = chunk_layers(ly, start, end, hint);
+        hint = ci.i0;
         const int64_t j = start + (int64_t)threadIdx.x * VEC;
         if (j >= end) continue;
-        int li = i0;
+        if (ci.i0 == ci.i1 && j + 4 <= end) {
+            // one layer: uniform format and exponent, 16-byte accesses
+            const FmtK& f = pal.f[ci.pidx];
+            const int32_t ft = ly.scale_exp ? clamp_exp(cld(ly.scale_exp, ci.i0)) : 0;
+            f4 v;
+            if (a.Q) {
+                v = *(const f4*)(a.Q + j);
+            } else {
+                v.x = decode(load_code(a.codes, j, a.code_cls), f);
+                v.y = decode(load_code(a.codes, j + 1, a.code_cls), f);
+                v.z = decode(load_code(a.codes, j + 2, a.code_cls), f);
+                v.w = decode(load_code(a.codes, j + 3, a.code_cls), f);
+            }
+            const f4 o = {__builtin_amdgcn_ldexpf(v.x, -ft), __builtin_amdgcn_ldexpf(v.y, -ft),
+                          __builtin_amdgcn_ldexpf(v.z, -ft), __builtin_amdgcn_ldexpf(v.w, -ft)};
+            *(f4*)(a.out + j) = o;  // out may alias Q: same elements
+            continue;
+        }
+        int li = ci.i0;
         for (int e = 0; e < 4; ++e) {
             const int64_t jj = j + e;
             if (jj >= end) break;
@@ -1186,7 +1205,7 @@ extern "C" int aps_quantize(const float* X, int32_t W, int64_t ld, int64_t n, co
     Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
     QuantArgs a{X, Q, (uint8_t*)codes, ld, W, ccls};
     const int64_t nchunks = (n + CH - 1) / CH;
-    const dim3 grid((unsigned)grid_for(nchunks * W, BLOCKS_PER_CU));
+    const dim3 grid((unsigned)grid_for(nchunks, BLOCKS_PER_CU));
     const unsigned vm = variant_mask(pal, n_fmts);
 #define APS_LAUNCH_Q(v) \
     if (vm & (1u << (v))) hipLaunchKernelGGL(k_quantize<v>, grid, dim3(BLOCK), 0, s, a, ly, pal);
