@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--no-other-calls", action="store_true",
                     help="skip timing aps_quantize / aps_dequantize outside the step")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU oracle time budget")
+    ap.add_argument("--roundoff", action="store_true",
+                    help="only run the group-size round-off study (Eq. 5) and print it")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only run device-to-device copies of this size (counter calibration)")
     return ap.parse_args()
@@ -117,11 +119,62 @@ def other_calls(A, G, gs, pal, idx_t, offs_t, se, out, reps: int = 5):
         t = timed(lambda: A.aps_sim_reduce_codes(codes, W, ld, n, offs_t, se, pal, idx_t, 0, out=out))
         res["sim_reduce_codes"] = {"ms": t, "GBps": (A.code_bytes(n, bits) * W + 4.0 * n) / (t * 1e-3) / 1e9,
                                    "elements_per_s": W * n / (t * 1e-3)}
+    # summation orders of the hierarchical all-reduce and the Kahan accumulator (fp32 input)
+    for name, k, acc in (("sim_reduce_ex_group16", 16, A.APS_ACC_SEQUENTIAL), ("sim_reduce_ex_ring", 1, A.APS_ACC_SEQUENTIAL),
+                         ("sim_reduce_ex_kahan", None, A.APS_ACC_KAHAN)):
+        if k is not None and W % k:
+            continue
+        t = timed(lambda: A.aps_sim_reduce_ex(G, n, offs_t, se, pal, idx_t, 0, group=k, accumulator=acc, out=out))
+        res[name] = {"ms": t, "GBps": (4.0 * W * n + 4.0 * n) / (t * 1e-3) / 1e9, "elements_per_s": W * n / (t * 1e-3)}
     A.aps_sim_reduce(G, n, offs_t, se, pal, idx_t, A.APS_OUTPUT_SCALED, out=None, codes_out=rcodes)
     t = timed(lambda: A.aps_dequantize(None, rcodes, n, offs_t, se, pal, idx_t, out))
     res["dequantize_from_codes"] = {"ms": t, "GBps": (A.code_bytes(n, bits) + 4.0 * n) / (t * 1e-3) / 1e9}
     del codes
     return res
+
+
+def roundoff_study(groups=(4, 8, 16, 32, 64, 1)):
+    """Sec. 4.2's round-off study on synthetic data: Eq. (5) for the first
+    convolution's gradient (64x3x7x7) with W = 256 workers in 1-5-2 with APS
+    scales, for hierarchical all-reduces of several group sizes (1 is the
+    ring over all workers), against the fp32 all-reduce.  Two draws: the
+    configs' recipe (workers independent, so their sum largely cancels) and
+    correlated workers (a shared gradient plus per-worker noise of the same
+    size, which is how data-parallel gradients relate)."""
+    import numpy as np
+    import torch
+
+    from paper_1911_08907_amd import aps as A
+    from paper_1911_08907_amd import workloads as WL
+
+    dev = torch.device("cuda:0")
+    W, n = 256, 64 * 3 * 7 * 7
+    ld = (n + 63) // 64 * 64
+    offs_t = torch.tensor([0, n], dtype=torch.int64, device=dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(WL.BASE_SEED)
+    s = 1e-3
+    draws = {
+        "independent": torch.randn(W, ld, generator=g, device=dev) * s,
+        "correlated": (torch.randn(1, ld, generator=g, device=dev) + torch.randn(W, ld, generator=g, device=dev)) * s,
+    }
+    result = {}
+    for name, G in draws.items():
+        G[:, n:] = 0
+        hi = torch.empty(n, dtype=torch.float32, device=dev)
+        A.aps_sim_reduce(G, n, offs_t, None, [A.Format(8, 23)], None, 0, out=hi)
+        _, se, _ = A.aps_step(G, n, offs_t, [A.Format(5, 2)])
+        h = hi.double().cpu().numpy()
+        nz = h != 0
+        lo = torch.empty(n, dtype=torch.float32, device=dev)
+        rows = {}
+        for k in groups:
+            A.aps_sim_reduce_ex(G, n, offs_t, se, [A.Format(5, 2)], None, 0, group=k, out=lo)
+            l = lo.double().cpu().numpy()
+            rows["ring_256" if k == 1 else f"group_{k}"] = float(np.mean(np.abs((h[nz] - l[nz]) / h[nz])))
+        result[name] = rows
+    print(json.dumps({"study": "Eq.5 round-off error vs all-reduce group size, 64x3x7x7 gradient, W=256, "
+                               "1-5-2 with APS scales, synthetic", "error": result}), flush=True)
 
 
 def cpu_baseline(G_t, gs, pal, budget_s: float, slice_cols: int = 65536):
@@ -175,6 +228,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration > 0:
         copy_calibration(args.copy_calibration)
+        return
+    if args.roundoff:
+        roundoff_study()
         return
 
     import torch

@@ -168,6 +168,37 @@ int aps_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n,
                    const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,
                    uint32_t flags, float* out, void* codes_out, void* stream);
 
+/* Summation order and accumulator of aps_sim_reduce_ex. */
+enum { APS_ACC_SEQUENTIAL = 0, APS_ACC_KAHAN = 1 };
+typedef struct {
+    int32_t group;       /* group size k of the hierarchical all-reduce: a power of
+                            two dividing W.  k = W: one group, worker order 0..W-1;
+                            k = 1: a ring all-reduce over all W workers */
+    int32_t accumulator; /* APS_ACC_SEQUENTIAL: s = R(s + x); APS_ACC_KAHAN:
+                            Kahan's compensated summation, every operation
+                            rounded to the format */
+} aps_reduce_opts;
+
+/*
+ * aps_sim_reduce with the summation order of the hierarchical all-reduce of
+ * Sec. 4.2 and an accumulation strategy of CPD (Sec. 5):
+ *   - the W workers form W/k groups of k consecutive workers; each group's
+ *     master (its first worker) sums the group in worker order;
+ *   - the masters then run a ring all-reduce on the group sums: element j
+ *     lies in ring segment s = floor(j * (W/k) / n), and segment s adds the
+ *     group sums in master order s, s+1, ..., s + W/k - 1 (mod W/k);
+ *   - every add of both chains is rounded to the format (or is one step of
+ *     Kahan's compensated summation with every operation rounded).
+ * opts == NULL is {k = W, APS_ACC_SEQUENTIAL}, i.e. aps_sim_reduce.
+ * A k that is not a power of two dividing W returns APS_ERR_SIZE; an unknown
+ * accumulator APS_ERR_UNSUPPORTED.  Other arguments as for aps_sim_reduce.
+ */
+int aps_sim_reduce_ex(const float* G, int32_t W, int64_t ld, int64_t n,
+                      const int64_t* offsets, int32_t L, const int32_t* scale_exp,
+                      const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,
+                      uint32_t flags, const aps_reduce_opts* opts, float* out, void* codes_out,
+                      void* stream);
+
 /*
  * The SUM all-reduce of Algorithm 1 on low_g in the form the workers would
  * exchange it: W rows of packed codes of already scaled and cast values (as

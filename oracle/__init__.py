@@ -23,6 +23,8 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 
 INPUT_QUANTIZED = 1
 OUTPUT_SCALED = 2
+ACC_SEQUENTIAL = 0
+ACC_KAHAN = 1
 
 
 GCC_FLAGS = ["-std=c99", "-O2", "-fPIC", "-shared", "-fopenmp", "-fno-fast-math", "-ffp-contract=off",
@@ -96,6 +98,8 @@ def lib():
             "oracle_decode": (f64, [u32, _Fmt]),
             "oracle_pack_codes": (None, [P, i64, P, i32, P, P, P]),
             "oracle_sim_reduce_codes": (None, [P, i32, i64, i64, P, i32, P, P, P, u32, P]),
+            "oracle_sim_reduce_ex": (None, [P, i32, i64, i64, P, i32, P, P, P, u32, i32, i32, P]),
+            "oracle_round_off_error": (f64, [P, P, i64]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -271,3 +275,22 @@ def sim_reduce_codes(codes: np.ndarray, W: int, ld: int, n: int, offsets, scale_
     lib().oracle_sim_reduce_codes(_ptr(c), int(W), int(ld), int(n), _ptr(offs), offs.size - 1, _ptr(se),
                                   _fmts(fmts), _ptr(_idx(fmt_idx)), int(flags), _ptr(out))
     return out
+
+
+def sim_reduce_ex(G: np.ndarray, n: int, offsets, scale_exp, fmts, fmt_idx=None, flags: int = 0,
+                  group: int | None = None, accumulator: int = ACC_SEQUENTIAL) -> np.ndarray:
+    G = _c(G, np.float32)
+    offs = _c(offsets, np.int64)
+    se = None if scale_exp is None else _c(scale_exp, np.int32)
+    W, ld = G.shape
+    k = W if group is None else int(group)
+    out = np.zeros(n, dtype=np.float32)
+    lib().oracle_sim_reduce_ex(_ptr(G), W, ld, n, _ptr(offs), offs.size - 1, _ptr(se), _fmts(fmts),
+                               _ptr(_idx(fmt_idx)), int(flags), k, int(accumulator), _ptr(out))
+    return out
+
+
+def round_off_error(grad_h: np.ndarray, grad_l: np.ndarray) -> float:
+    h = _c(grad_h, np.float32)
+    l = _c(grad_l, np.float32)
+    return lib().oracle_round_off_error(_ptr(h), _ptr(l), h.size)

@@ -342,3 +342,66 @@ void oracle_sim_reduce_codes(const void* codes, int32_t W, int64_t ld, int64_t n
         }
     }
 }
+
+/* ---------------------------------------------- summation order, Kahan */
+
+/* One add of a chain: plain (s = Cast(s + x)) or Kahan, where every
+ * intermediate is cast to the format as a low-precision accumulator would
+ * hold it (Sec. 5). */
+static void chain_add(double* s, double* c, double x, oracle_format f, int32_t accumulator) {
+    if (accumulator == ORACLE_ACC_KAHAN) {
+        const double y = oracle_round(x - *c, f);
+        const double t = oracle_round(*s + y, f);
+        *c = oracle_round(oracle_round(t - *s, f) - y, f);
+        *s = t;
+    } else {
+        *s = oracle_round(*s + x, f);
+    }
+}
+
+void oracle_sim_reduce_ex(const float* G, int32_t W, int64_t ld, int64_t n,
+                          const int64_t* offsets, int32_t L, const int32_t* scale_exp,
+                          const oracle_format* fmts, const uint8_t* fmt_idx,
+                          uint32_t flags, int32_t group, int32_t accumulator, float* out) {
+    const int32_t k = group;
+    const int32_t ng = W / k; /* number of groups (masters) */
+    for (int32_t i = 0; i < L; ++i) {
+        const oracle_format f = fmts[fmt_idx ? fmt_idx[i] : 0];
+        const int32_t ft = scale_exp ? scale_exp[i] : 0;
+#pragma omp parallel for schedule(static)
+        for (int64_t j = offsets[i]; j < offsets[i + 1]; ++j) {
+            const int64_t seg = j * ng / n; /* ring segment of this element */
+            double T = 0.0, cT = 0.0;
+            for (int32_t gi = 0; gi < ng; ++gi) {
+                const int32_t g = (int32_t)((seg + gi) % ng);
+                double S = 0.0, cS = 0.0;
+                for (int32_t m = 0; m < k; ++m) {
+                    const float x = G[(int64_t)(g * k + m) * ld + j];
+                    const float y = (flags & ORACLE_INPUT_QUANTIZED) ? x : scale_fp32(x, ft);
+                    const double q = oracle_round((double)y, f);
+                    if (m == 0)
+                        S = q; /* the master's own gradient */
+                    else
+                        chain_add(&S, &cS, q, f, accumulator);
+                }
+                if (gi == 0)
+                    T = S; /* the ring starts at master seg */
+                else
+                    chain_add(&T, &cT, S, f, accumulator);
+            }
+            const float gv = (float)T;
+            out[j] = (flags & ORACLE_OUTPUT_SCALED) ? gv : (float)ldexp((double)gv, -ft);
+        }
+    }
+}
+
+double oracle_round_off_error(const float* grad_h, const float* grad_l, int64_t n) {
+    double sum = 0.0;
+    int64_t cnt = 0;
+    for (int64_t j = 0; j < n; ++j) {
+        if (grad_h[j] == 0.0f) continue;
+        sum += fabs(((double)grad_h[j] - (double)grad_l[j]) / (double)grad_h[j]);
+        ++cnt;
+    }
+    return cnt ? sum / (double)cnt : 0.0;
+}

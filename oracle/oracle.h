@@ -110,6 +110,26 @@ void oracle_sim_reduce_codes(const void* codes, int32_t W, int64_t ld, int64_t n
                              const oracle_format* fmts, const uint8_t* fmt_idx,
                              uint32_t flags, float* out);
 
+/* Accumulation strategies of Sec. 5 (CPD) for a chain of adds. */
+#define ORACLE_ACC_SEQUENTIAL 0 /* s = Cast(s + x) */
+#define ORACLE_ACC_KAHAN 1      /* Kahan's compensated summation, every op cast */
+
+/* The SUM all-reduce with the summation order of Sec. 4.2's hierarchical
+ * all-reduce and a chosen accumulation strategy.  The W workers form W/k
+ * groups of k consecutive workers; a group's master (its first worker) sums
+ * the group in worker order; the masters then run a ring reduce-scatter, so
+ * segment s of the gradient (element j belongs to s = floor(j * (W/k) / n))
+ * accumulates the group sums in master order s, s+1, ..., s+W/k-1 (mod W/k).
+ * k = W is the plain worker order 0..W-1, k = 1 a ring over all workers. */
+void oracle_sim_reduce_ex(const float* G, int32_t W, int64_t ld, int64_t n,
+                          const int64_t* offsets, int32_t L, const int32_t* scale_exp,
+                          const oracle_format* fmts, const uint8_t* fmt_idx,
+                          uint32_t flags, int32_t group, int32_t accumulator, float* out);
+
+/* Eq. (5) of Sec. 4.2: the mean over the elements with grad_h != 0 of
+ * |(grad_h - grad_l) / grad_h|; elements with grad_h == 0 are left out. */
+double oracle_round_off_error(const float* grad_h, const float* grad_l, int64_t n);
+
 #ifdef __cplusplus
 }
 #endif

@@ -28,7 +28,10 @@ APS_OUTPUT_SCALED = 2
 APS_MAX_FORMATS = 8
 
 EXPORTS = ("aps_format_supported", "aps_layer_maxabs", "aps_layer_scales", "aps_quantize",
-           "aps_sim_reduce", "aps_sim_reduce_codes", "aps_dequantize", "aps_strerror")
+           "aps_sim_reduce", "aps_sim_reduce_ex", "aps_sim_reduce_codes", "aps_dequantize", "aps_strerror")
+
+APS_ACC_SEQUENTIAL = 0
+APS_ACC_KAHAN = 1
 
 
 class ApsError(RuntimeError):
@@ -39,6 +42,10 @@ class ApsError(RuntimeError):
 
 class aps_format(ctypes.Structure):
     _fields_ = [("e", ctypes.c_int32), ("m", ctypes.c_int32), ("bias", ctypes.c_int32)]
+
+
+class aps_reduce_opts(ctypes.Structure):
+    _fields_ = [("group", ctypes.c_int32), ("accumulator", ctypes.c_int32)]
 
 
 @dataclass(frozen=True)
@@ -88,6 +95,8 @@ def lib() -> ctypes.CDLL:
             "aps_quantize": (ctypes.c_int, [P, i32, i64, i64, P, i32, P, FP, i32, P, P, P, P]),
             "aps_sim_reduce": (ctypes.c_int, [P, i32, i64, i64, P, i32, P, FP, i32, P, u32, P, P, P]),
             "aps_sim_reduce_codes": (ctypes.c_int, [P, i32, i64, i64, P, i32, P, FP, i32, P, u32, P, P, P]),
+            "aps_sim_reduce_ex": (ctypes.c_int, [P, i32, i64, i64, P, i32, P, FP, i32, P, u32,
+                                                 ctypes.POINTER(aps_reduce_opts), P, P, P]),
             "aps_dequantize": (ctypes.c_int, [P, P, i64, P, i32, P, FP, i32, P, P, P]),
             "aps_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         }
@@ -180,6 +189,19 @@ def aps_sim_reduce(G, n: int, offsets, scale_exp, fmts, fmt_idx, flags: int = 0,
     _check("aps_sim_reduce", lib().aps_sim_reduce(_ptr(G), W, ld, n, _ptr(offsets), L, _ptr(scale_exp), pal,
                                                   nf, _ptr(fmt_idx), int(flags), _ptr(out), _ptr(codes_out),
                                                   _stream(stream)))
+
+
+def aps_sim_reduce_ex(G, n: int, offsets, scale_exp, fmts, fmt_idx, flags: int = 0, group: int | None = None,
+                      accumulator: int = APS_ACC_SEQUENTIAL, out=None, codes_out=None, stream=None) -> None:
+    """aps_sim_reduce with the hierarchical-all-reduce order (group size k)
+    and a plain or Kahan low-precision accumulator."""
+    W, ld = _rows(G)
+    pal, nf = _palette(fmts)
+    L = offsets.numel() - 1
+    opts = aps_reduce_opts(W if group is None else int(group), int(accumulator))
+    _check("aps_sim_reduce_ex", lib().aps_sim_reduce_ex(_ptr(G), W, ld, n, _ptr(offsets), L, _ptr(scale_exp), pal,
+                                                        nf, _ptr(fmt_idx), int(flags), ctypes.byref(opts),
+                                                        _ptr(out), _ptr(codes_out), _stream(stream)))
 
 
 def aps_sim_reduce_codes(codes, W: int, ld: int, n: int, offsets, scale_exp, fmts, fmt_idx, flags: int = 0,

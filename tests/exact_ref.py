@@ -105,3 +105,28 @@ def ceil_log2_exact(t: Fraction) -> int:
     while Fraction(2) ** (c - 1) >= t:
         c -= 1
     return c
+
+
+def chain_exact(xs, e, m, bias=None, kahan=False):
+    """A chain of adds with every intermediate rounded: plain or Kahan."""
+    s = xs[0]
+    c = Fraction(0)
+    for x in xs[1:]:
+        if kahan:
+            y = round_exact(x - c, e, m, bias)
+            t = round_exact(s + y, e, m, bias)
+            c = round_exact(round_exact(t - s, e, m, bias) - y, e, m, bias)
+            s = t
+        else:
+            s = round_exact(s + x, e, m, bias)
+    return s
+
+
+def hierarchical_exact(qs, k, seg, e, m, bias=None, kahan=False):
+    """Groups of k consecutive workers summed at their master, then the
+    masters' ring starting at master `seg`."""
+    W = len(qs)
+    ng = W // k
+    sums = [chain_exact(qs[g * k:(g + 1) * k], e, m, bias, kahan) for g in range(ng)]
+    order = [sums[(seg + i) % ng] for i in range(ng)]
+    return chain_exact(order, e, m, bias, kahan)

@@ -40,7 +40,7 @@ def _declared():
 def test_header_declares_the_five_calls():
     d = _declared()
     for name in ("aps_layer_maxabs", "aps_layer_scales", "aps_quantize", "aps_sim_reduce", "aps_dequantize",
-                 "aps_sim_reduce_codes"):
+                 "aps_sim_reduce_codes", "aps_sim_reduce_ex"):
         assert name in d
 
 
@@ -169,3 +169,17 @@ def test_sim_reduce_codes_validation(lib):
     assert f(GOOD, 2, 68, 64, GOOD, 1, None, pal, 1, None, 0, GOOD, None, None) == A.APS_ERR_ALIGN   # 68-byte rows
     assert f(GOOD, 2, 64, 64, GOOD, 1, None, _pal(A.Format(8, 23)), 1, None, 0, GOOD, None,
              None) == A.APS_ERR_UNSUPPORTED
+
+
+@no_gpu
+def test_sim_reduce_ex_validation(lib):
+    f = lib.aps_sim_reduce_ex
+    pal = _pal(A.Format(5, 2))
+    o = lambda k, acc: ctypes.byref(A.aps_reduce_opts(k, acc))
+    assert f(GOOD, 8, 64, 64, GOOD, 1, None, pal, 1, None, 0, o(3, 0), GOOD, None, None) == A.APS_ERR_SIZE
+    assert f(GOOD, 8, 64, 64, GOOD, 1, None, pal, 1, None, 0, o(16, 0), GOOD, None, None) == A.APS_ERR_SIZE
+    assert f(GOOD, 8, 64, 64, GOOD, 1, None, pal, 1, None, 0, o(0, 0), GOOD, None, None) == A.APS_ERR_SIZE
+    assert f(GOOD, 8, 64, 64, GOOD, 1, None, pal, 1, None, 0, o(2, 7), GOOD, None, None) == A.APS_ERR_UNSUPPORTED
+    assert f(None, 8, 64, 64, GOOD, 1, None, pal, 1, None, 0, o(2, 1), GOOD, None, None) == A.APS_ERR_NULL
+    assert f(GOOD, 8, 64, 64, GOOD, 1, None, pal, 1, None, 0, o(2, 1), None, None, None) == A.APS_ERR_NULL
+    assert f(GOOD, 8, 64, 64, GOOD, 1, None, pal, 1, None, 0, o(2, 1), MIS, None, None) == A.APS_ERR_ALIGN

@@ -428,3 +428,77 @@ def test_sim_reduce_codes_random_codes(dev, f):
         o = O.sim_reduce_codes(rows, W, ld, n, offs, se, ofmt(f))
         g = out.cpu().numpy()
         assert same_f32(g, o), (f, W, first_diff(g, o))
+
+
+
+# ------------------------------------------- summation orders and Kahan
+
+def _run_ex(dev, G, n, offs, pal, fmt_idx, se, k, acc, tag):
+    W, ld = G.shape
+    G_t = torch.from_numpy(G).to(dev)
+    offs_t = torch.from_numpy(offs).to(dev)
+    idx_t = None if fmt_idx is None else torch.from_numpy(fmt_idx).to(dev)
+    se_t = None if se is None else torch.from_numpy(se).to(dev)
+    out = torch.zeros(max(n, 1), dtype=torch.float32, device=dev)
+    A.aps_sim_reduce_ex(G_t, n, offs_t, se_t, pal, idx_t, 0, group=k, accumulator=acc, out=out)
+    o = O.sim_reduce_ex(G, n, offs, se, [ofmt(f) for f in pal], fmt_idx, group=k, accumulator=acc)
+    g = out.cpu().numpy()[:n]
+    assert same_f32(g, o), f"{tag} {first_diff(g, o)}"
+
+
+@pytest.mark.parametrize("acc", [A.APS_ACC_SEQUENTIAL, A.APS_ACC_KAHAN])
+@pytest.mark.parametrize("f", [F(5, 2), F(4, 3), F(3, 0), F(5, 10), F(8, 7), F(5, 12), F(8, 23)], ids=str)
+def test_ordered_reduce_edge_layouts(dev, f, acc):
+    rng = np.random.default_rng(60 + f.e * 5 + f.m + 100 * acc)
+    offs, n, ld = _layout(SIZES)
+    for W, k in ((8, 1), (8, 2), (8, 8), (16, 4), (12, 4), (5, 1), (1, 1)):
+        G = _values(rng, W, ld, offs, "special" if W % 2 else "normal")
+        mab = O.layer_maxabs(G, n, offs)
+        se = O.layer_scales(mab, W, ofmt(f))
+        log("case", f, W, k, acc)
+        _run_ex(dev, G, n, offs, [f], None, se, k, acc, f"{f} W={W} k={k} acc={acc}")
+
+
+@pytest.mark.parametrize("acc", [A.APS_ACC_SEQUENTIAL, A.APS_ACC_KAHAN])
+def test_ordered_reduce_mixed_palette(dev, acc):
+    rng = np.random.default_rng(70 + acc)
+    pal = [F(5, 2), F(4, 3), F(5, 10)]
+    sizes = [int(v) for v in rng.choice([0, 1, 3, 17, 1000, 1023, 1024, 3000], 30)]
+    offs, n, ld = _layout(sizes)
+    fmt_idx = rng.integers(0, len(pal), len(sizes)).astype(np.uint8)
+    G = _values(rng, 16, ld, offs, "normal")
+    _run_ex(dev, G, n, offs, pal, fmt_idx, None, 2, acc, "mixed k=2")
+    _run_ex(dev, G, n, offs, pal, fmt_idx, None, 1, acc, "mixed ring")
+
+
+@pytest.mark.parametrize("k,acc", [(1, 0), (2, 0), (4, 1), (8, 1)])
+def test_ordered_reduce_resnet50_w8_full(dev, k, acc):
+    gs = WL.generate("resnet50_w8", "1-5-2", device=dev)
+    G_t = gs.G
+    offs_t = torch.from_numpy(gs.offsets).to(dev)
+    pal = [F(5, 2)]
+    _, se_t, _ = A.aps_step(G_t, gs.n, offs_t, pal)
+    out = torch.empty(gs.n, dtype=torch.float32, device=dev)
+    A.aps_sim_reduce_ex(G_t, gs.n, offs_t, se_t, pal, None, 0, group=k, accumulator=acc, out=out)
+    G = G_t.cpu().numpy()
+    o = O.sim_reduce_ex(G, gs.n, gs.offsets, se_t.cpu().numpy(), ofmt(pal[0]), group=k, accumulator=acc)
+    g = out.cpu().numpy()
+    assert same_f32(g, o), first_diff(g, o)
+    assert np.all(np.isfinite(g))
+
+
+def test_ordered_reduce_w256_groups(dev):
+    """W = 256 with the paper's group sizes on a 1.1 M-element ResNet-like slice."""
+    rng = np.random.default_rng(80)
+    sizes = [9408, 64, 64, 4096, 64, 64, 36864, 64, 64, 16384, 256, 256, 16384, 256, 256, 1000000, 1000]
+    offs, n, ld = _layout(sizes)
+    W = 256
+    G = np.zeros((W, ld), np.float32)
+    for i, sz in enumerate(sizes):
+        a, b = offs[i], offs[i + 1]
+        G[:, a:b] = (rng.standard_normal((W, sz)) * 10.0 ** rng.uniform(-7, -1)).astype(np.float32)
+    mab = O.layer_maxabs(G, n, offs)
+    se = O.layer_scales(mab, W, O.Format(5, 2))
+    for k in (1, 16, 64):
+        log("W=256 k", k)
+        _run_ex(dev, G, n, offs, [F(5, 2)], None, se, k, A.APS_ACC_SEQUENTIAL, f"W=256 k={k}")

@@ -1,7 +1,8 @@
 """The pins are strong enough: each plausible mistake planted in a copy of the
 oracle makes the pin suite fail.
 
-Every mutant is built from oracle/oracle.c with one textual change, loaded by
+Every mutant is built from oracle/oracle.c with one textual change (applied
+at every place the mutated text occurs), loaded by
 a separate pytest process (APS_ORACLE_LIB) that runs tests/test_oracle_pins.py
 and must fail.  CPU only; the real oracle is untouched."""
 import os
@@ -31,8 +32,15 @@ MUTANTS = {
     "unscale_wrong_direction": ("out[j] = (flags & ORACLE_OUTPUT_SCALED) ? g : (float)ldexp((double)g, -ft);",
                                 "out[j] = (flags & ORACLE_OUTPUT_SCALED) ? g : (float)ldexp((double)g, ft);"),
     "nan_ignored_in_maxabs": ("if (isnan(x))\n                    saw_nan = 1;", "if (0)\n                    saw_nan = 1;"),
-    "scale_before_rounding_skipped": ("const float y = (flags & ORACLE_INPUT_QUANTIZED) ? x : scale_fp32(x, ft);",
-                                      "const float y = x;"),
+    "scale_before_rounding_skipped": (
+        "(skipped when the input is already scaled) */\n"
+        "                const float y = (flags & ORACLE_INPUT_QUANTIZED) ? x : scale_fp32(x, ft);",
+        "(skipped when the input is already scaled) */\n"
+        "                const float y = x;"),
+    "kahan_compensation_sign": ("const double y = oracle_round(x - *c, f);",
+                                "const double y = oracle_round(x + *c, f);"),
+    "ring_starts_one_master_late": ("const int32_t g = (int32_t)((seg + gi) % ng);",
+                                    "const int32_t g = (int32_t)((seg + gi + 1) % ng);"),
     "mantissa_bits_off_by_one": ("const double k = nearbyint(ldexp(a, f.m - Eq));",
                                  "const double k = nearbyint(ldexp(a, f.m + 1 - Eq));"),
 }
@@ -42,7 +50,7 @@ MUTANTS = {
 def test_pins_catch_mutant(tmp_path, name):
     old, new = MUTANTS[name]
     src = open(SRC).read()
-    assert src.count(old) == 1, f"mutation site for {name} not found exactly once"
+    assert src.count(old) >= 1, f"mutation site for {name} not found"
     mutated = tmp_path / "oracle_mut.c"
     mutated.write_text(src.replace(old, new))
     lib = O.build(force=True, src=str(mutated), out=str(tmp_path / "liboracle_mut.so"))

@@ -451,3 +451,76 @@ def test_sim_reduce_codes_brute_force(f):
             qs = [(-1 if signs[w, j] else 1) * vals[mags[w, j]] for w in range(W)]
             ref = X.sum_exact(qs, f.e, f.m, f.b)
             assert got[j] == float(ref), (f, trial, j)
+
+
+# ----------------------------------------- summation orders and Kahan (Sec. 4.2, 5)
+
+@pytest.mark.parametrize("f", [F(5, 2), F(4, 3), F(3, 0)], ids=str)
+@pytest.mark.parametrize("acc", [O.ACC_SEQUENTIAL, O.ACC_KAHAN])
+def test_ordered_reduce_brute_force(f, acc):
+    rng = np.random.default_rng(50 + f.e + 7 * acc)
+    for W, k in ((4, 1), (4, 2), (8, 2), (8, 4), (8, 8), (6, 3), (3, 1)):
+        n = 24
+        G = (rng.standard_normal((W, n)) * 2.0 ** rng.uniform(-4, 2, (W, 1))).astype(np.float32)
+        offs = np.array([0, n], np.int64)
+        got = O.sim_reduce_ex(G, n, offs, None, f, group=k, accumulator=acc)
+        ng = W // k
+        for j in range(n):
+            qs = [X.round_exact(Fraction(float(G[w, j])), f.e, f.m, f.b) for w in range(W)]
+            if any(isinstance(q, float) for q in qs):
+                continue
+            ref = X.hierarchical_exact(qs, k, j * ng // n, f.e, f.m, f.b, kahan=(acc == O.ACC_KAHAN))
+            if isinstance(ref, float):
+                assert got[j] == ref, (f, W, k, j)
+            else:
+                assert got[j] == float(ref), (f, W, k, acc, j, got[j], float(ref))
+
+
+def test_kahan_recovers_what_plain_loses():
+    # 1-5-10: 1 + 2^-11 is a tie that rounds back to 1, so a plain low-precision
+    # accumulator never moves; the exact sum of 1 and 2048 * 2^-11 is 2
+    W, n = 2049, 1
+    G = np.full((W, 4), 2.0 ** -11, np.float32)
+    G[0, :] = 1.0
+    offs = np.array([0, n], np.int64)
+    plain = O.sim_reduce_ex(G, n, offs, None, F(5, 10), accumulator=O.ACC_SEQUENTIAL)
+    kahan = O.sim_reduce_ex(G, n, offs, None, F(5, 10), accumulator=O.ACC_KAHAN)
+    assert plain[0] == 1.0
+    assert kahan[0] == 2.0
+
+
+def test_kahan_error_bound_fp32():
+    # Kahan's bound for the fp32 format: |sum - exact| <= (2u + O(W u^2)) * sum |x|
+    rng = np.random.default_rng(51)
+    W, n = 1000, 64
+    G = (rng.standard_normal((W, n)) * 10.0 ** rng.uniform(-3, 3, (W, n))).astype(np.float32)
+    offs = np.array([0, n], np.int64)
+    got = O.sim_reduce_ex(G, n, offs, None, F(8, 23), accumulator=O.ACC_KAHAN)
+    u = 2.0 ** -24
+    for j in range(n):
+        exact = sum(Fraction(float(v)) for v in G[:, j])
+        absum = sum(abs(Fraction(float(v))) for v in G[:, j])
+        err = abs(Fraction(float(got[j])) - exact)
+        assert err <= (2 * u + 4 * W * u * u) * absum + Fraction(abs(float(exact))) * u
+
+
+def test_order_special_cases():
+    rng = np.random.default_rng(52)
+    W, n = 8, 50
+    G = rng.standard_normal((W, n)).astype(np.float32)
+    offs = np.array([0, 20, n], np.int64)
+    f = F(5, 2)
+    se = np.array([3, -2], np.int32)
+    # one group of W workers is the plain worker order
+    assert np.array_equal(O.sim_reduce_ex(G, n, offs, se, f, group=W), O.sim_reduce(G, n, offs, se, f))
+    # any order of the fp32 format with exact adds: integers sum exactly
+    Gi = rng.integers(-1000, 1000, (W, n)).astype(np.float32)
+    ring = O.sim_reduce_ex(Gi, n, offs, None, F(8, 23), group=1)
+    assert np.array_equal(ring, Gi.sum(0))
+
+
+def test_round_off_error_eq5():
+    h = np.array([1.0, 2.0, 0.0, 4.0], np.float32)
+    l = np.array([1.5, 2.0, 7.0, 3.0], np.float32)
+    # (0.5 + 0 + 0.25) / 3, the zero entry of grad_h left out
+    assert O.round_off_error(h, l) == pytest.approx(0.25, abs=0)
