@@ -48,6 +48,8 @@ constexpr int MAXABS_BLOCKS_PER_CU = APS_MAXABS_BLOCKS_PER_CU;
 constexpr int MAXABS_UNROLL = APS_MAXABS_UNROLL;  // worker rows per load batch in k_maxabs
 
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 
 struct Pal {
     FmtK f[APS_MAX_FORMATS];
@@ -172,20 +174,21 @@ __device__ __forceinline__ float finish(float s, bool bad) {
 
 // ---------------------------------------------------------------- codes
 
-// code of a native-domain format value v
+// code of a native-domain format value v.  Every case is computed and one is
+// selected, so the wave never splits on the value's class.
 __device__ __forceinline__ uint32_t encode(float v, const FmtK& f) {
     const uint32_t b = f2u(v);
     const uint32_t sign = (b >> 31) << (f.e + f.m);
     const uint32_t a = b & 0x7FFFFFFFu;
-    uint32_t c;
-    if (a > 0x7F800000u)
-        c = (uint32_t)f.emax_code | (f.m > 0 ? (1u << (f.m - 1)) : 0u);
-    else if (a == 0x7F800000u)
-        c = (uint32_t)f.emax_code;
-    else if (a < (uint32_t)(f.emin + 127) << 23)  // below 2^emin: subnormal or zero
-        c = (uint32_t)__builtin_amdgcn_ldexpf(u2f(a), f.m - f.emin);
-    else
-        c = (a >> (23 - f.m)) - ((uint32_t)(127 - f.bias) << f.m);
+    const uint32_t lo = (uint32_t)(f.emin + 127) << 23;  // bits of 2^emin
+    // below 2^emin: the subnormal code counts multiples of 2^(emin-m); the
+    // clamp keeps the conversion's input finite when another case is taken
+    const uint32_t c_sub = (uint32_t)__builtin_amdgcn_ldexpf(u2f(min(a, lo)), f.m - f.emin);
+    const uint32_t c_norm = (a >> (23 - f.m)) - ((uint32_t)(127 - f.bias) << f.m);
+    const uint32_t c_nan = (uint32_t)f.emax_code | (f.m > 0 ? (1u << (f.m - 1)) : 0u);
+    uint32_t c = a < lo ? c_sub : c_norm;
+    c = a == 0x7F800000u ? (uint32_t)f.emax_code : c;
+    c = a > 0x7F800000u ? c_nan : c;
     return sign | c;
 }
 
@@ -206,20 +209,25 @@ __host__ __device__ __forceinline__ int64_t code_byte(int64_t j, int cls) {
     return cls == 0 ? (j >> 1) : (cls == 1 ? j : 2 * j);
 }
 
+// Store the codes of elements j..j+3 (j % 4 == 0) of a row, all four present.
+__device__ __forceinline__ void store_codes4_full(uint8_t* row, int64_t j, const uint32_t c[4], int cls) {
+    // streaming (non-temporal) stores: the codes are not read back by this launch
+    if (cls == 0) {
+        const uint16_t v = (uint16_t)((c[0] & 15u) | ((c[1] & 15u) << 4) | ((c[2] & 15u) << 8) | ((c[3] & 15u) << 12));
+        __builtin_nontemporal_store(v, (uint16_t*)(row + (j >> 1)));
+    } else if (cls == 1) {
+        const uint32_t v = (c[0] & 255u) | ((c[1] & 255u) << 8) | ((c[2] & 255u) << 16) | (c[3] << 24);
+        __builtin_nontemporal_store(v, (uint32_t*)(row + j));
+    } else {
+        const u2v v = {(c[0] & 0xFFFFu) | (c[1] << 16), (c[2] & 0xFFFFu) | (c[3] << 16)};
+        __builtin_nontemporal_store(v, (u2v*)(row + 2 * j));
+    }
+}
+
 // Store the codes of elements j..j+3 (j % 4 == 0) of a row; only those < lim.
 __device__ __forceinline__ void store_codes4(uint8_t* row, int64_t j, const uint32_t c[4], int cls, int64_t lim) {
     if (j + 4 <= lim) {
-        if (cls == 0) {
-            const uint16_t v = (uint16_t)((c[0] & 15u) | ((c[1] & 15u) << 4) | ((c[2] & 15u) << 8) | ((c[3] & 15u) << 12));
-            *(uint16_t*)(row + (j >> 1)) = v;
-        } else if (cls == 1) {
-            *(uint32_t*)(row + j) = (c[0] & 255u) | ((c[1] & 255u) << 8) | ((c[2] & 255u) << 16) | (c[3] << 24);
-        } else {
-            uint2 v;
-            v.x = (c[0] & 0xFFFFu) | (c[1] << 16);
-            v.y = (c[2] & 0xFFFFu) | (c[3] << 16);
-            *(uint2*)(row + 2 * j) = v;
-        }
+        store_codes4_full(row, j, c, cls);
         return;
     }
     for (int e = 0; e < 4; ++e) {
@@ -448,6 +456,14 @@ __device__ __forceinline__ void touch(const f4& v) { asm volatile("" ::"v"(v.x),
 // handed to step() with valid = false, so every path issues the same loads
 // and the compiler waits for exactly the row it is about to use.
 // after_issue() runs once, right after the first 2*UNROLL loads are issued.
+//
+// The sets of UNROLL rows are numbered 0 .. nsets-1.  Set 0 and set 1 are
+// loaded up front; a full step consumes set s (all rows valid) after issuing
+// the loads of set s+1, for s = 1 .. nsets-2; the last set is consumed with
+// per-row validity.  The full steps run as a counted loop of pairs with no
+// exit in its body: an exit in the middle of the body is merged by the
+// compiler's control-flow structurizer into the back edge, and the loads it
+// would leave outstanding then force waits at the top of every iteration.
 template <class Load, class AfterIssue, class First, class Step>
 __device__ __forceinline__ void stream_rows(int W, Load load, AfterIssue after_issue, First first, Step step) {
     f4 A[UNROLL], B[UNROLL];
@@ -458,29 +474,8 @@ __device__ __forceinline__ void stream_rows(int W, Load load, AfterIssue after_i
     __builtin_amdgcn_sched_barrier(0);
     after_issue();
     first(A[0]);
-#define APS_STEP(CUR, NXT)                                                        \
-    if (w + UNROLL < W) {                                                         \
-        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u)                        \
-            NXT[u] = load(min(w + UNROLL + u, W - 1));                            \
-        __builtin_amdgcn_sched_barrier(0);                                        \
-        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u) step(CUR[u], true);    \
-        w += UNROLL;                                                              \
-    } else {                                                                      \
-        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u) {                      \
-            touch(CUR[u]);                                                        \
-            step(CUR[u], w + u < W);                                              \
-        }                                                                         \
-        break;                                                                    \
-    }
-    if (UNROLL < W) {
-#pragma unroll
-        for (int u = 1; u < UNROLL; ++u) step(A[u], true);
-        int w = UNROLL;
-        for (;;) {
-            APS_STEP(B, A)
-            APS_STEP(A, B)
-        }
-    } else {
+    const int nsets = (W + UNROLL - 1) / UNROLL;
+    if (nsets == 1) {
 #pragma unroll
         for (int u = 1; u < UNROLL; ++u) {
             touch(A[u]);
@@ -491,8 +486,40 @@ __device__ __forceinline__ void stream_rows(int W, Load load, AfterIssue after_i
             touch(B[u]);
             step(B[u], false);
         }
+        return;
     }
-#undef APS_STEP
+#pragma unroll
+    for (int u = 1; u < UNROLL; ++u) step(A[u], true);
+    int w = UNROLL;  // first row of the set being consumed
+#define APS_FULL(CUR, NXT)                                                     \
+    {                                                                          \
+        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u)                     \
+            NXT[u] = load(min(w + UNROLL + u, W - 1));                         \
+        __builtin_amdgcn_sched_barrier(0);                                     \
+        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u) step(CUR[u], true); \
+        w += UNROLL;                                                           \
+    }
+#define APS_LAST(CUR)                                                          \
+    {                                                                          \
+        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u) {                   \
+            touch(CUR[u]);                                                     \
+            step(CUR[u], w + u < W);                                           \
+        }                                                                      \
+    }
+    const int nfull = nsets - 2;
+#pragma unroll 1
+    for (int it = 0; it < nfull / 2; ++it) {
+        APS_FULL(B, A)
+        APS_FULL(A, B)
+    }
+    if (nfull & 1) {
+        APS_FULL(B, A)
+        APS_LAST(A)
+    } else {
+        APS_LAST(B)
+    }
+#undef APS_FULL
+#undef APS_LAST
 }
 
 // ===================================================== K4: sim reduce
@@ -944,12 +971,8 @@ __global__ __launch_bounds__(BLOCK) void k_sim_reduce_codes(CodesArgs a, Layers 
                 }
             }
             if (a.codes_out) {
-                uint4 v;
-                v.x = cw[0];
-                v.y = cw[1];
-                v.z = cw[2];
-                v.w = cw[3];
-                *(uint4*)(a.codes_out + code_byte(j, CC)) = v;
+                const u4v v = {cw[0], cw[1], cw[2], cw[3]};
+                __builtin_nontemporal_store(v, (u4v*)(a.codes_out + code_byte(j, CC)));
             }
         } else {
             // ragged end of the gradient: element by element
@@ -1118,18 +1141,61 @@ __global__ __launch_bounds__(BLOCK) void k_sim_reduce_mixed(ReduceArgs a, Layers
 // ======================================================= K3: quantize
 
 struct QuantArgs {
-    const float* __restrict__ X;
-    float* Q;  // may alias X
+    const float* X;
+    float* Q;  // may alias X: each element is read before its own store
     uint8_t* __restrict__ codes;
     int64_t ld;
     int32_t W;
     int32_t code_cls;
 };
 
+// Native-domain value of x cast to the format (scale exponent F includes k);
+// an m = 0 format keeps a NaN input NaN.
+template <int V>
+__device__ __forceinline__ float quant_native(float x, int F, const FmtK& f) {
+    bool bad = false;
+    const float v = __builtin_amdgcn_ldexpf(quant<V>(x, F, f, bad), -f.k);
+    if constexpr (VT<V>::m0) return (x != x) ? x : v;
+    return v;
+}
+
+// The ragged end of the gradient (fewer than 4 elements left for a thread):
+// every row, element by element.
+template <int V>
+__device__ __forceinline__ void quantize_tail(const QuantArgs& a, const FmtK& f, int64_t j, int64_t end,
+                                           const int32_t ft[4]) {
+#pragma unroll 1
+    for (int64_t r = 0; r < a.W; ++r) {
+        const int64_t off = r * a.ld + j;
+        uint32_t cc[4] = {0, 0, 0, 0};
+        for (int e = 0; e < 4 && j + e < end; ++e) {
+            const float v = quant_native<V>(a.X[off + e], ft[e] + f.k, f);
+            if (a.Q) a.Q[off + e] = v;
+            cc[e] = encode(v, f);
+        }
+        if (a.codes) store_codes4(a.codes + code_byte(r * a.ld, a.code_cls), j, cc, a.code_cls, end);
+    }
+}
+
+// The cast alone does not depend on the accumulator width, so the F32 and F64
+// variants of a class cast alike; the F64 form reads the tie-bit width from the
+// format (1 whenever the F32 form applies).
+__host__ __device__ constexpr int cast_variant(int v) {
+    return v == V_INT_F32 ? V_INT_F64 : (v == V_TOP_F32 ? V_TOP_F64 : (v == V_LOW_F32 ? V_LOW_F64 : v));
+}
+
+// What one k_quantize launch writes per row.
+enum QuantOut { QO_Q = 0, QO_CODES4 = 1, QO_CODES8 = 2, QO_CODES16 = 3, QO_BOTH = 4 };
+
 // One block walks a range of chunks; for each chunk its threads stream all W
 // rows (two register sets of rows in flight), cast each row and store it.
-template <int V>
+// The stores of a row are fixed at compile time (OUT): a store that is
+// conditional inside the streamed loop makes the compiler's load-counter
+// waits at the loop's joins far more conservative.
+template <int V, int OUT>
 __global__ __launch_bounds__(BLOCK) void k_quantize(QuantArgs a, Layers ly, Pal pal) {
+    constexpr bool HQ = OUT == QO_Q || OUT == QO_BOTH;
+    constexpr bool HC = OUT != QO_Q;
     const int64_t nchunks = (ly.n + CH - 1) / CH;
     int64_t cb, ce;
     block_range(nchunks, cb, ce);
@@ -1141,7 +1207,7 @@ __global__ __launch_bounds__(BLOCK) void k_quantize(QuantArgs a, Layers ly, Pal 
         hint = ci.i0;
         if (ci.mixed) continue;  // handled by k_quantize_mixed
         const FmtK& f = pal.f[ci.pidx];
-        if (f.variant != V) continue;
+        if (cast_variant(f.variant) != V) continue;
         const int64_t j = start + (int64_t)threadIdx.x * VEC;
         if (j >= end) continue;
         int32_t ft[4];
@@ -1151,33 +1217,22 @@ __global__ __launch_bounds__(BLOCK) void k_quantize(QuantArgs a, Layers ly, Pal 
         } else {
             elem_scales(ly, ci, j, ft);
         }
+        if (j + 4 > end) {
+            quantize_tail<V>(a, f, j, end, ft);
+            continue;
+        }
         const float* p = a.X + j;
         const int64_t ld = a.ld;
+        const int cls = OUT == QO_CODES4 ? 0 : (OUT == QO_CODES8 ? 1 : (OUT == QO_CODES16 ? 2 : a.code_cls));
         int64_t r = 0;  // row of the next callback
         auto row = [&](const f4& x, bool valid) {
             if (valid) {
-                bool bad = false;
-                const float xs[4] = {x.x, x.y, x.z, x.w};
-                float v[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    v[e] = __builtin_amdgcn_ldexpf(quant<V>(xs[e], ft[e] + f.k, f, bad), -f.k);  // native scaled value
-                    if constexpr (VT<V>::m0) v[e] = (xs[e] != xs[e]) ? xs[e] : v[e];       // NaN stays NaN
-                }
-                const int64_t off = r * ld + j;
-                if (a.Q) {
-                    if (j + 4 <= end) {
-                        const f4 o = {v[0], v[1], v[2], v[3]};
-                        *(f4*)(a.Q + off) = o;
-                    } else {
-                        for (int e = 0; e < 4 && j + e < end; ++e) a.Q[off + e] = v[e];
-                    }
-                }
-                if (a.codes) {
-                    uint32_t cc[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) cc[e] = encode(v[e], f);
-                    store_codes4(a.codes + code_byte(r * ld, a.code_cls), j, cc, a.code_cls, end);
+                const f4 v = {quant_native<V>(x.x, ft[0] + f.k, f), quant_native<V>(x.y, ft[1] + f.k, f),
+                              quant_native<V>(x.z, ft[2] + f.k, f), quant_native<V>(x.w, ft[3] + f.k, f)};
+                if constexpr (HQ) __builtin_nontemporal_store(v, (f4*)(a.Q + j + r * ld));
+                if constexpr (HC) {
+                    const uint32_t cc[4] = {encode(v.x, f), encode(v.y, f), encode(v.z, f), encode(v.w, f)};
+                    store_codes4_full(a.codes + code_byte(r * ld, cls), j, cc, cls);
                 }
             }
             ++r;
@@ -1187,25 +1242,18 @@ __global__ __launch_bounds__(BLOCK) void k_quantize(QuantArgs a, Layers ly, Pal 
     }
 }
 
-template <int V>
-__device__ float quant_one(float x, int F, const FmtK& f) {
-    bool bad = false;
-    const float q = __builtin_amdgcn_ldexpf(quant<V>(x, F, f, bad), -f.k);
-    return bad ? x : q;
-}
-
 __device__ float quant_any(float x, int F, const FmtK& f) {
     switch (f.variant) {
-        case V_INT_F32: return quant_one<V_INT_F32>(x, F, f);
-        case V_INT_F64: return quant_one<V_INT_F64>(x, F, f);
-        case V_INT_EXACT: return quant_one<V_INT_EXACT>(x, F, f);
-        case V_INT_M0: return quant_one<V_INT_M0>(x, F, f);
-        case V_TOP_F32: return quant_one<V_TOP_F32>(x, F, f);
-        case V_TOP_F64: return quant_one<V_TOP_F64>(x, F, f);
-        case V_TOP_M0: return quant_one<V_TOP_M0>(x, F, f);
-        case V_LOW_F32: return quant_one<V_LOW_F32>(x, F, f);
-        case V_LOW_F64: return quant_one<V_LOW_F64>(x, F, f);
-        default: return quant_one<V_LOW_M0>(x, F, f);
+        case V_INT_F32: return quant_native<V_INT_F32>(x, F, f);
+        case V_INT_F64: return quant_native<V_INT_F64>(x, F, f);
+        case V_INT_EXACT: return quant_native<V_INT_EXACT>(x, F, f);
+        case V_INT_M0: return quant_native<V_INT_M0>(x, F, f);
+        case V_TOP_F32: return quant_native<V_TOP_F32>(x, F, f);
+        case V_TOP_F64: return quant_native<V_TOP_F64>(x, F, f);
+        case V_TOP_M0: return quant_native<V_TOP_M0>(x, F, f);
+        case V_LOW_F32: return quant_native<V_LOW_F32>(x, F, f);
+        case V_LOW_F64: return quant_native<V_LOW_F64>(x, F, f);
+        default: return quant_native<V_LOW_M0>(x, F, f);
     }
 }
 
@@ -1278,7 +1326,7 @@ __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal 
             }
             const f4 o = {__builtin_amdgcn_ldexpf(v.x, -ft), __builtin_amdgcn_ldexpf(v.y, -ft),
                           __builtin_amdgcn_ldexpf(v.z, -ft), __builtin_amdgcn_ldexpf(v.w, -ft)};
-            *(f4*)(a.out + j) = o;  // out may alias Q: same elements
+            __builtin_nontemporal_store(o, (f4*)(a.out + j));  // out may alias Q: same elements
             continue;
         }
         int li = ci.i0;
@@ -1412,10 +1460,21 @@ extern "C" int aps_quantize(const float* X, int32_t W, int64_t ld, int64_t n, co
     QuantArgs a{X, Q, (uint8_t*)codes, ld, W, ccls};
     const int64_t nchunks = (n + CH - 1) / CH;
     const dim3 grid((unsigned)grid_for(nchunks, BLOCKS_PER_CU));
-    const unsigned vm = variant_mask(pal, n_fmts);
-#define APS_LAUNCH_Q(v) \
-    if (vm & (1u << (v))) hipLaunchKernelGGL(k_quantize<v>, grid, dim3(BLOCK), 0, s, a, ly, pal);
-    APS_FOR_VARIANTS(APS_LAUNCH_Q)
+    unsigned cm = 0;  // cast variants present
+    for (int i = 0; i < n_fmts; ++i) cm |= 1u << cast_variant(pal.f[i].variant);
+    const int out = !codes ? QO_Q : (Q ? QO_BOTH : QO_CODES4 + ccls);
+#define APS_LAUNCH_Q(v)                                                                                    \
+    if (cm & (1u << (v))) {                                                                                \
+        switch (out) {                                                                                     \
+            case QO_Q: hipLaunchKernelGGL((k_quantize<v, QO_Q>), grid, dim3(BLOCK), 0, s, a, ly, pal); break; \
+            case QO_CODES4: hipLaunchKernelGGL((k_quantize<v, QO_CODES4>), grid, dim3(BLOCK), 0, s, a, ly, pal); break; \
+            case QO_CODES8: hipLaunchKernelGGL((k_quantize<v, QO_CODES8>), grid, dim3(BLOCK), 0, s, a, ly, pal); break; \
+            case QO_CODES16: hipLaunchKernelGGL((k_quantize<v, QO_CODES16>), grid, dim3(BLOCK), 0, s, a, ly, pal); break; \
+            default: hipLaunchKernelGGL((k_quantize<v, QO_BOTH>), grid, dim3(BLOCK), 0, s, a, ly, pal); break; \
+        }                                                                                                  \
+    }
+    APS_LAUNCH_Q(V_INT_F64) APS_LAUNCH_Q(V_INT_EXACT) APS_LAUNCH_Q(V_INT_M0) APS_LAUNCH_Q(V_TOP_F64)
+    APS_LAUNCH_Q(V_TOP_M0) APS_LAUNCH_Q(V_LOW_F64) APS_LAUNCH_Q(V_LOW_M0)
 #undef APS_LAUNCH_Q
     if (fmt_idx && n_fmts > 1 && L > 1)
         hipLaunchKernelGGL(k_quantize_mixed, dim3((unsigned)L, (unsigned)W), dim3(BLOCK), 0, s, a, ly, pal);
