@@ -931,10 +931,16 @@ __global__ __launch_bounds__(BLOCK) void k_sim_reduce_codes(CodesArgs a, Layers 
             },
             [&](const f4& v, bool valid) {
                 if (valid) {
+                    // all of the row's table reads first, so their latencies
+                    // overlap instead of each add waiting for its own read
+                    float d[EPT];
+#pragma unroll
+                    for (int e = 0; e < EPT; ++e) d[e] = dec(slice_code<CC>(v, e));
+                    if constexpr (CC < 2) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                     for (int e = 0; e < EPT; ++e) {
                         bool b = false;
-                        s[e] = accum<V>(s[e], dec(slice_code<CC>(v, e)), f, b);
+                        s[e] = accum<V>(s[e], d[e], f, b);
                         if constexpr (VT<V>::m0) bad |= (uint32_t)b << e;
                     }
                 }
