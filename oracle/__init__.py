@@ -100,6 +100,7 @@ def lib():
             "oracle_sim_reduce_codes": (None, [P, i32, i64, i64, P, i32, P, P, P, u32, P]),
             "oracle_sim_reduce_ex": (None, [P, i32, i64, i64, P, i32, P, P, P, u32, i32, i32, P]),
             "oracle_round_off_error": (f64, [P, P, i64]),
+            "oracle_lp_gemm": (None, [P, i64, P, i64, P, i64, i32, i32, i32, _Fmt, _Fmt, i32]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -294,3 +295,16 @@ def round_off_error(grad_h: np.ndarray, grad_l: np.ndarray) -> float:
     h = _c(grad_h, np.float32)
     l = _c(grad_l, np.float32)
     return lib().oracle_round_off_error(_ptr(h), _ptr(l), h.size)
+
+
+def lp_gemm(A: np.ndarray, B: np.ndarray, fin: Format, facc: Format, accumulator: int = ACC_SEQUENTIAL) -> np.ndarray:
+    """C = A @ B on a low-precision multiply-accumulate unit (A: [M][K], B: [K][N])."""
+    A = _c(A, np.float32)
+    B = _c(B, np.float32)
+    M, K = A.shape
+    K2, N = B.shape
+    assert K == K2
+    C = np.zeros((M, N), dtype=np.float32)
+    lib().oracle_lp_gemm(_ptr(A), max(K, 1), _ptr(B), max(N, 1), _ptr(C), max(N, 1), M, N, K,
+                         fin.c(), facc.c(), int(accumulator))
+    return C

@@ -395,6 +395,36 @@ void oracle_sim_reduce_ex(const float* G, int32_t W, int64_t ld, int64_t n,
     }
 }
 
+/* ------------------------------------ low-precision-accumulator GEMM */
+
+/* Sec. 5 (CPD): a matrix product whose multiply-accumulate unit works in a
+ * low-precision format.  Each input element is cast to `in` (x -> Cast_in(x)),
+ * each product of two cast inputs is cast to the accumulator format `acc`,
+ * and the products of one output are accumulated in k order 0..K-1 by a
+ * chain of adds in `acc` (plain or Kahan, every intermediate cast).  The
+ * product of two values of at most 24 significant bits is exact in double,
+ * so each cast below rounds an exact real value once.  K = 0 gives +0. */
+void oracle_lp_gemm(const float* A, int64_t lda, const float* B, int64_t ldb, float* C, int64_t ldc,
+                    int32_t M, int32_t N, int32_t K, oracle_format in, oracle_format acc,
+                    int32_t accumulator) {
+#pragma omp parallel for schedule(static)
+    for (int32_t i = 0; i < M; ++i) {
+        for (int32_t j = 0; j < N; ++j) {
+            double s = 0.0, c = 0.0;
+            for (int32_t k = 0; k < K; ++k) {
+                const double a = oracle_round((double)A[(int64_t)i * lda + k], in);
+                const double b = oracle_round((double)B[(int64_t)k * ldb + j], in);
+                const double p = oracle_round(a * b, acc); /* the product, held in acc */
+                if (k == 0)
+                    s = p;
+                else
+                    chain_add(&s, &c, p, acc, accumulator);
+            }
+            C[(int64_t)i * ldc + j] = (float)s;
+        }
+    }
+}
+
 double oracle_round_off_error(const float* grad_h, const float* grad_l, int64_t n) {
     double sum = 0.0;
     int64_t cnt = 0;

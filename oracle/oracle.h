@@ -126,6 +126,16 @@ void oracle_sim_reduce_ex(const float* G, int32_t W, int64_t ld, int64_t n,
                           const oracle_format* fmts, const uint8_t* fmt_idx,
                           uint32_t flags, int32_t group, int32_t accumulator, float* out);
 
+/* Sec. 5 (CPD): C[M][N] = A[M][K] * B[K][N] (row-major, leading dimensions
+ * lda, ldb, ldc) on a low-precision multiply-accumulate unit: inputs cast to
+ * `in`, every product cast to `acc`, the K products of an output summed in k
+ * order by a chain of adds in `acc` (ORACLE_ACC_SEQUENTIAL or
+ * ORACLE_ACC_KAHAN), every intermediate cast.  C holds the format values;
+ * K = 0 gives +0. */
+void oracle_lp_gemm(const float* A, int64_t lda, const float* B, int64_t ldb, float* C, int64_t ldc,
+                    int32_t M, int32_t N, int32_t K, oracle_format in, oracle_format acc,
+                    int32_t accumulator);
+
 /* Eq. (5) of Sec. 4.2: the mean over the elements with grad_h != 0 of
  * |(grad_h - grad_l) / grad_h|; elements with grad_h == 0 are left out. */
 double oracle_round_off_error(const float* grad_h, const float* grad_l, int64_t n);

@@ -43,6 +43,11 @@ MUTANTS = {
                                     "const int32_t g = (int32_t)((seg + gi + 1) % ng);"),
     "mantissa_bits_off_by_one": ("const double k = nearbyint(ldexp(a, f.m - Eq));",
                                  "const double k = nearbyint(ldexp(a, f.m + 1 - Eq));"),
+    "gemm_product_not_cast": ("const double p = oracle_round(a * b, acc);", "const double p = a * b;"),
+    "gemm_inputs_not_cast": ("const double a = oracle_round((double)A[(int64_t)i * lda + k], in);",
+                             "const double a = (double)A[(int64_t)i * lda + k];"),
+    "gemm_accumulates_in_input_format": ("chain_add(&s, &c, p, acc, accumulator);",
+                                         "chain_add(&s, &c, p, in, accumulator);"),
 }
 
 

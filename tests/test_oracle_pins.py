@@ -524,3 +524,123 @@ def test_round_off_error_eq5():
     l = np.array([1.5, 2.0, 7.0, 3.0], np.float32)
     # (0.5 + 0 + 0.25) / 3, the zero entry of grad_h left out
     assert O.round_off_error(h, l) == pytest.approx(0.25, abs=0)
+
+
+# ------------------------------- low-precision-accumulator GEMM (Sec. 5, CPD)
+
+def _gemm_exact(A, B, fin, facc, kahan):
+    """Exact-rational reference: inputs cast to fin, each product cast to facc,
+    the products of an output chained in k order in facc.  INF and NaN pass
+    through Python float arithmetic (IEEE)."""
+    M, K = A.shape
+    N = B.shape[1]
+    out = np.zeros((M, N))
+    for i in range(M):
+        for j in range(N):
+            ps = []
+            for k in range(K):
+                a = X.round_exact(Fraction(float(A[i, k])), fin.e, fin.m, fin.b)
+                b = X.round_exact(Fraction(float(B[k, j])), fin.e, fin.m, fin.b)
+                ps.append(X.round_exact(a * b, facc.e, facc.m, facc.b))
+            out[i, j] = float(X.chain_exact(ps, facc.e, facc.m, facc.b, kahan=kahan))
+    return out
+
+
+@pytest.mark.parametrize("fin,facc", [(F(5, 2), F(5, 2)), (F(4, 3), F(5, 2)), (F(5, 2), F(4, 3)),
+                                      (F(2, 1), F(3, 0)), (F(2, 0), F(2, 0)), (F(3, 2), F(4, 3, 5))],
+                         ids=lambda f: str(f))
+@pytest.mark.parametrize("acc", [O.ACC_SEQUENTIAL, O.ACC_KAHAN])
+def test_lp_gemm_brute_force(fin, facc, acc):
+    rng = np.random.default_rng(60 + fin.e + 3 * facc.m + 11 * acc)
+    # magnitudes over the input format's range, from below its smallest
+    # subnormal to about the square root of its largest value
+    lo, hi = O.emin(fin) - fin.m - 1, max(O.emax(fin) // 2, 1)
+    finite = 0
+    for M, N, K in ((3, 4, 7), (2, 2, 1), (1, 3, 12), (4, 2, 5)):
+        A = (rng.standard_normal((M, K)) * 2.0 ** rng.uniform(lo, hi, (M, K))).astype(np.float32)
+        B = (rng.standard_normal((K, N)) * 2.0 ** rng.uniform(lo, hi, (K, N))).astype(np.float32)
+        got = O.lp_gemm(A, B, fin, facc, acc)
+        ref = _gemm_exact(A, B, fin, facc, acc == O.ACC_KAHAN)
+        same = (got == ref) | (np.isnan(got) & np.isnan(ref))
+        assert same.all(), (fin, facc, acc, M, N, K, got, ref)
+        finite += int(np.isfinite(ref).sum())
+    assert finite >= 10
+
+
+def test_lp_gemm_fp32_accumulator_is_a_float32_dot_product():
+    # products of fp16 values are exact in fp32, so with the fp32 format as the
+    # accumulator each output is numpy's float32 dot product taken in k order
+    rng = np.random.default_rng(61)
+    M, N, K = 5, 6, 40
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    B = (rng.standard_normal((K, N)) * 100).astype(np.float32)
+    got = O.lp_gemm(A, B, F(5, 10), F(8, 23))
+    a = A.astype(np.float16).astype(np.float32)
+    b = B.astype(np.float16).astype(np.float32)
+    for i in range(M):
+        for j in range(N):
+            s = np.float32(a[i, 0] * b[0, j])
+            for k in range(1, K):
+                s = np.float32(s + np.float32(a[i, k] * b[k, j]))
+            assert got[i, j] == s
+
+
+def test_lp_gemm_fp16_equals_numpy_float16_arithmetic():
+    # numpy float16 multiplies and adds round their exact result to float16
+    # (through float32, which is innocuous: 24 >= 2 * 11 + 2)
+    rng = np.random.default_rng(62)
+    M, N, K = 4, 5, 64
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    B = (rng.standard_normal((K, N)) * 8).astype(np.float32)
+    got = O.lp_gemm(A, B, F(5, 10), F(5, 10))
+    a = A.astype(np.float16)
+    b = B.astype(np.float16)
+    for i in range(M):
+        for j in range(N):
+            s = a[i, 0] * b[0, j]
+            for k in range(1, K):
+                s = np.float16(s + a[i, k] * b[k, j])
+            assert got[i, j] == np.float32(s)
+
+
+def test_lp_gemm_bf16_equals_torch_bfloat16_arithmetic():
+    rng = np.random.default_rng(63)
+    M, N, K = 6, 7, 50
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    B = (rng.standard_normal((K, N)) * 3).astype(np.float32)
+    got = O.lp_gemm(A, B, F(8, 7), F(8, 7))
+    a = torch.from_numpy(A).to(torch.bfloat16)
+    b = torch.from_numpy(B).to(torch.bfloat16)
+    s = a[:, 0:1] * b[0:1, :]
+    for k in range(1, K):
+        s = s + a[:, k:k + 1] * b[k:k + 1, :]
+    assert np.array_equal(got, s.to(torch.float32).numpy())
+
+
+@pytest.mark.parametrize("f", [F(5, 2), F(4, 3), F(5, 10), F(3, 1)], ids=str)
+def test_lp_gemm_swamping_closed_form(f):
+    # a sum of ones in a p-bit significand grows to 2^p and stops there: 2^p + 1
+    # is a tie between 2^p (even) and 2^p + 2 -- the loss Sec. 5 describes
+    p = f.m + 1
+    for K in (1, 2, 2 ** p - 1, 2 ** p, 2 ** p + 1, 2 ** p + 7, 3 * 2 ** p):
+        if K > O.maxfinite(f):
+            continue
+        got = O.lp_gemm(np.ones((1, K), np.float32), np.ones((K, 1), np.float32), f, f)
+        assert got[0, 0] == min(K, 2 ** p), (f, K)
+        # Kahan keeps the running sum within one quantum of K
+        kah = O.lp_gemm(np.ones((1, K), np.float32), np.ones((K, 1), np.float32), f, f, O.ACC_KAHAN)
+        quantum = 2.0 ** (max(math.floor(math.log2(K)), 0) - f.m)
+        assert abs(kah[0, 0] - K) <= quantum, (f, K, kah[0, 0])
+
+
+def test_lp_gemm_transpose_and_edge_shapes():
+    rng = np.random.default_rng(64)
+    A = rng.standard_normal((5, 9)).astype(np.float32)
+    B = rng.standard_normal((9, 3)).astype(np.float32)
+    for acc in (O.ACC_SEQUENTIAL, O.ACC_KAHAN):
+        C = O.lp_gemm(A, B, F(4, 3), F(5, 2), acc)
+        Ct = O.lp_gemm(np.ascontiguousarray(B.T), np.ascontiguousarray(A.T), F(4, 3), F(5, 2), acc)
+        assert np.array_equal(C, Ct.T)
+    # K = 0: the empty sum is +0
+    Z = O.lp_gemm(np.zeros((2, 0), np.float32), np.zeros((0, 3), np.float32), F(5, 2), F(5, 2))
+    assert np.array_equal(Z, np.zeros((2, 3))) and not np.signbit(Z).any()
