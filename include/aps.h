@@ -13,6 +13,10 @@
  *                      accumulator, cast back, unscale     (Alg. 1; Sec. 5)
  *   aps_dequantize     Cast(low_g, 8, 23) / 2^ft           (Alg. 1)
  *
+ * Beside them, CPD's accumulation experiments (Sec. 5): aps_sim_reduce_ex
+ * (summation orders, Kahan), aps_sim_reduce_codes (the sum over packed
+ * codes) and aps_lp_gemm (a GEMM with a low-precision accumulator).
+ *
  * Data layout.  A model's gradients are one flat fp32 vector of n elements;
  * layer i (one parameter tensor) owns elements [offsets[i], offsets[i+1]).
  * W workers' gradients are stored worker-major: element j of worker w is
@@ -236,6 +240,33 @@ int aps_dequantize(const float* Q, const void* codes, int64_t n,
                    const int64_t* offsets, int32_t L, const int32_t* scale_exp,
                    const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,
                    float* out, void* stream);
+
+/*
+ * A matrix product on a multiply-accumulate unit of a chosen low precision,
+ * CPD's low-precision-accumulator GEMM (Sec. 5): C = A * B with
+ *   a = R_in(A[i][k]), b = R_in(B[k][j])       (inputs cast to in_fmt)
+ *   p_k = R_acc(a * b)                          (each product cast to acc_fmt)
+ *   s = p_0;  s = R_acc(s + p_k) for k = 1..K-1 (sequential, k order), or
+ *   Kahan's compensated summation with every operation rounded to acc_fmt
+ *   C[i][j] = s                                 (K = 0 gives +0)
+ * R_* round to nearest even as described above (overflow to INF, gradual
+ * underflow).  Row-major device arrays: A[M][lda], B[K][ldb], C[M][ldc];
+ * C must not overlap A or B.
+ *
+ *   accumulator  APS_ACC_SEQUENTIAL or APS_ACC_KAHAN
+ *
+ * The product of two in_fmt values is formed exactly in fp32 and then
+ * rounded, which needs in_fmt.m <= 11, and either every product of two
+ * in_fmt values a multiple of 2^-149 (2 * (emin_in - m_in) >= -149) or
+ * every product too small for that rounding to zero in acc_fmt
+ * (2 * (m_in + 1) <= emin_acc - m_acc + 149); other pairs return
+ * APS_ERR_UNSUPPORTED.  M, N, K in [0, 2^22]; lda >= K, ldb >= N,
+ * ldc >= N; A and B may be NULL when K = 0 or M * N = 0.
+ */
+#define APS_MAX_GEMM_DIM (1 << 22)
+int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t ldb, float* C, int64_t ldc,
+                int32_t M, int32_t N, int32_t K, aps_format in_fmt, aps_format acc_fmt,
+                int32_t accumulator, void* stream);
 
 /* Static text for a status code. */
 const char* aps_strerror(int status);

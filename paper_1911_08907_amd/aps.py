@@ -28,7 +28,8 @@ APS_OUTPUT_SCALED = 2
 APS_MAX_FORMATS = 8
 
 EXPORTS = ("aps_format_supported", "aps_layer_maxabs", "aps_layer_scales", "aps_quantize",
-           "aps_sim_reduce", "aps_sim_reduce_ex", "aps_sim_reduce_codes", "aps_dequantize", "aps_strerror")
+           "aps_sim_reduce", "aps_sim_reduce_ex", "aps_sim_reduce_codes", "aps_dequantize", "aps_lp_gemm",
+           "aps_strerror")
 
 APS_ACC_SEQUENTIAL = 0
 APS_ACC_KAHAN = 1
@@ -98,6 +99,7 @@ def lib() -> ctypes.CDLL:
             "aps_sim_reduce_ex": (ctypes.c_int, [P, i32, i64, i64, P, i32, P, FP, i32, P, u32,
                                                  ctypes.POINTER(aps_reduce_opts), P, P, P]),
             "aps_dequantize": (ctypes.c_int, [P, P, i64, P, i32, P, FP, i32, P, P, P]),
+            "aps_lp_gemm": (ctypes.c_int, [P, i64, P, i64, P, i64, i32, i32, i32, aps_format, aps_format, i32, P]),
             "aps_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         }
         for name, (res, args) in sig.items():
@@ -220,6 +222,32 @@ def aps_dequantize(Q, codes, n: int, offsets, scale_exp, fmts, fmt_idx, out, str
     L = offsets.numel() - 1
     _check("aps_dequantize", lib().aps_dequantize(_ptr(Q), _ptr(codes), n, _ptr(offsets), L, _ptr(scale_exp),
                                                   pal, nf, _ptr(fmt_idx), _ptr(out), _stream(stream)))
+
+
+def aps_lp_gemm(A, B, fin: Format, facc: Format, accumulator: int = APS_ACC_SEQUENTIAL, C=None,
+                stream=None):
+    """C = A @ B on a low-precision multiply-accumulate unit: A [M][K] and
+    B [K][N] row-major fp32 device tensors (row strides from the tensors),
+    inputs cast to ``fin``, products and partial sums rounded to ``facc``."""
+    import torch
+
+    M, K = A.shape
+    K2, N = B.shape
+    if K != K2:
+        raise ValueError(f"inner dimensions differ: {K} vs {K2}")
+    def ld(t, rows, cols):  # row stride; an empty or one-row tensor may report anything
+        if rows <= 1 or cols == 0:
+            return max(cols, 1)
+        if cols > 1 and t.stride(1) != 1:
+            raise ValueError("A, B and C need unit column stride")
+        return t.stride(0)
+
+    if C is None:
+        C = torch.empty((M, N), dtype=torch.float32, device=A.device)
+    lda, ldb, ldc = ld(A, M, K), ld(B, K, N), ld(C, M, N)
+    _check("aps_lp_gemm", lib().aps_lp_gemm(_ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, M, N, K, fin.c(),
+                                            facc.c(), int(accumulator), _stream(stream)))
+    return C
 
 
 def code_bytes(count: int, bits: int) -> int:

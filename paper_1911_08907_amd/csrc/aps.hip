@@ -646,14 +646,30 @@ __global__ __launch_bounds__(BLOCK) void k_sim_reduce(ReduceArgs a, Layers ly, P
 
 // ======================================= K4x: summation orders, Kahan
 
+// R_fmt(a + b) with a NaN sum kept as NaN in the value itself (the rounding
+// of an m = 0 format does not keep NaN bit patterns; accum() flags them).
+template <int V>
+__device__ __forceinline__ float accum_nan(float a, float b, const FmtK& f) {
+    bool unused = false;
+    const float r = accum<V>(a, b, f, unused);
+    if constexpr (VT<V>::m0) {
+        const float t = a + b;
+        return (t != t) ? t : r;
+    }
+    return r;
+}
+
 // One add of a chain, plain (s = R(s + x)) or Kahan's compensated summation
-// with every intermediate rounded to the format.
+// with every intermediate rounded to the format.  In the plain chain a NaN
+// partial sum stays NaN to the end, so one flag per chain is exact; in Kahan's
+// the compensation can turn NaN (INF - INF) while the sum does not, so there
+// NaN travels in the values.  `bad` still marks NaN inputs of m = 0 formats.
 template <int V, bool KAHAN>
 __device__ __forceinline__ void chain_step(float& s, float& c, float x, const FmtK& f, bool& bad) {
     if constexpr (KAHAN) {
-        const float y = accum<V>(x, -c, f, bad);
-        const float t = accum<V>(s, y, f, bad);
-        c = accum<V>(accum<V>(t, -s, f, bad), -y, f, bad);
+        const float y = accum_nan<V>(x, -c, f);
+        const float t = accum_nan<V>(s, y, f);
+        c = accum_nan<V>(accum_nan<V>(t, -s, f), -y, f);
         s = t;
     } else {
         s = accum<V>(s, x, f, bad);
@@ -1348,6 +1364,106 @@ __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal 
     }
 }
 
+// ================================================== K6: low-precision GEMM
+
+struct GemmArgs {
+    const float* __restrict__ A;
+    const float* __restrict__ B;
+    float* __restrict__ C;
+    int64_t lda, ldb, ldc;
+    int32_t M, N, K;
+};
+
+constexpr int GT = 64;  // output tile GT x GT per block, 4 x 4 per thread
+constexpr int GK = 16;  // k-tile staged in LDS
+
+// One block computes a GT x GT tile of C.  Each k-tile of A and B is cast to
+// the input format while it is staged into LDS (A transposed, so a thread's
+// four rows are one 16-byte read); each thread then runs 16 independent
+// chains, one per output, adding its products in k order.  The work is the
+// VALU's: a product, its rounding and the rounded add per multiply-accumulate.
+template <int V, bool KAHAN>
+__global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa) {
+    __shared__ __align__(16) float As[GK][GT + 4];  // As[k][m]; the pad spreads the staging writes over banks
+    __shared__ __align__(16) float Bs[GK][GT + 4];  // Bs[k][n]
+    const int t = threadIdx.x;
+    const int tx = t & 15, ty = t >> 4;
+    const int64_t m0 = (int64_t)blockIdx.y * GT, n0 = (int64_t)blockIdx.x * GT;
+    float s[4][4], c[4][4];
+    bool bad[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            s[i][j] = 0.0f;
+            c[i][j] = 0.0f;
+            bad[i][j] = false;
+        }
+    float ra[4], rb[4];
+    // global -> registers, cast to the input format; outside A and B: 0
+    auto fetch = [&](int64_t k0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int idx = t + BLOCK * r;
+            const int64_t am = m0 + (idx >> 4), ak = k0 + (idx & 15);
+            ra[r] = (am < g.M && ak < g.K) ? quant_any(g.A[am * g.lda + ak], fi.k, fi) : 0.0f;
+            const int64_t bk = k0 + (idx >> 6), bn = n0 + (idx & 63);
+            rb[r] = (bk < g.K && bn < g.N) ? quant_any(g.B[bk * g.ldb + bn], fi.k, fi) : 0.0f;
+        }
+    };
+    auto mac = [&](int kk, bool first) {
+        const f4 av = *(const f4*)&As[kk][ty * 4];
+        const f4 bv = *(const f4*)&Bs[kk][tx * 4];
+        const float a[4] = {av.x, av.y, av.z, av.w};
+        const float b[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                // exact fp32 product of two input-format values, cast to the accumulator
+                const float p = quant<V>(a[i] * b[j], fa.k, fa, bad[i][j]);
+                if (first)
+                    s[i][j] = p;
+                else
+                    chain_step<V, KAHAN>(s[i][j], c[i][j], p, fa, bad[i][j]);
+            }
+    };
+    if (g.K > 0) fetch(0);
+    for (int64_t k0 = 0; k0 < g.K; k0 += GK) {
+        __syncthreads();  // the previous k-tile is consumed
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int idx = t + BLOCK * r;
+            As[idx & 15][idx >> 4] = ra[r];
+            Bs[idx >> 6][idx & 63] = rb[r];
+        }
+        __syncthreads();
+        if (k0 + GK < g.K) fetch(k0 + GK);  // the next k-tile's loads overlap this tile's math
+        const int kend = (int)min((int64_t)GK, g.K - k0);
+        int kk = 0;
+        if (k0 == 0) {
+            mac(0, true);  // an output's chain starts with its first product
+            kk = 1;
+        }
+        if (kend == GK) {
+            for (; kk < GK; ++kk) mac(kk, false);
+        } else {
+#pragma unroll 1
+            for (; kk < kend; ++kk) mac(kk, false);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t m = m0 + ty * 4 + i;
+        if (m >= g.M) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t n = n0 + tx * 4 + j;
+            if (n < g.N) g.C[m * g.ldc + n] = __builtin_amdgcn_ldexpf(finish<V>(s[i][j], bad[i][j]), -fa.k);
+        }
+    }
+}
+
 // ================================================================ host
 
 static int device_cus() {
@@ -1623,5 +1739,40 @@ extern "C" int aps_dequantize(const float* Q, const void* codes, int64_t n, cons
     const int64_t nchunks = (n + CH - 1) / CH;
     hipLaunchKernelGGL(k_dequantize, dim3((unsigned)grid_for(nchunks, BLOCKS_PER_CU)), dim3(BLOCK), 0, (hipStream_t)stream, a,
                        ly, pal);
+    return launched();
+}
+
+extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t ldb, float* C, int64_t ldc,
+                           int32_t M, int32_t N, int32_t K, aps_format in_fmt, aps_format acc_fmt,
+                           int32_t accumulator, void* stream) {
+    if (M < 0 || N < 0 || K < 0 || M > APS_MAX_GEMM_DIM || N > APS_MAX_GEMM_DIM || K > APS_MAX_GEMM_DIM)
+        return APS_ERR_SIZE;
+    const bool has_out = (int64_t)M * N > 0;
+    if (has_out && (!C || (K > 0 && (!A || !B)))) return APS_ERR_NULL;
+    if (has_out && (ldc < N || (K > 0 && (lda < K || ldb < N)))) return APS_ERR_SIZE;
+    int st = fmt_status(in_fmt);
+    if (st != APS_OK) return st;
+    st = fmt_status(acc_fmt);
+    if (st != APS_OK) return st;
+    if (accumulator != APS_ACC_SEQUENTIAL && accumulator != APS_ACC_KAHAN) return APS_ERR_UNSUPPORTED;
+    // the product of two input values must be exact in fp32, or round to zero anyway
+    const int emin_in = 1 - in_fmt.bias, emin_acc = 1 - acc_fmt.bias;
+    if (in_fmt.m > 11) return APS_ERR_UNSUPPORTED;
+    if (2 * (emin_in - in_fmt.m) < -149 && 2 * (in_fmt.m + 1) > emin_acc - acc_fmt.m + 149) return APS_ERR_UNSUPPORTED;
+    if (!has_out) return APS_OK;
+    const FmtK fi = make_fmtk(in_fmt), fa = make_fmtk(acc_fmt);
+    GemmArgs g{A, B, C, lda, ldb, ldc, M, N, K};
+    const dim3 grid((unsigned)((N + GT - 1) / GT), (unsigned)((M + GT - 1) / GT));
+    hipStream_t s = (hipStream_t)stream;
+    const bool kahan = accumulator == APS_ACC_KAHAN;
+#define APS_LAUNCH_G(v)                                                                          \
+    if (fa.variant == (v)) {                                                                     \
+        if (kahan)                                                                               \
+            hipLaunchKernelGGL((k_lp_gemm<v, true>), grid, dim3(BLOCK), 0, s, g, fi, fa);         \
+        else                                                                                     \
+            hipLaunchKernelGGL((k_lp_gemm<v, false>), grid, dim3(BLOCK), 0, s, g, fi, fa);        \
+    }
+    APS_FOR_VARIANTS(APS_LAUNCH_G)
+#undef APS_LAUNCH_G
     return launched();
 }

@@ -183,3 +183,27 @@ def test_sim_reduce_ex_validation(lib):
     assert f(None, 8, 64, 64, GOOD, 1, None, pal, 1, None, 0, o(2, 1), GOOD, None, None) == A.APS_ERR_NULL
     assert f(GOOD, 8, 64, 64, GOOD, 1, None, pal, 1, None, 0, o(2, 1), None, None, None) == A.APS_ERR_NULL
     assert f(GOOD, 8, 64, 64, GOOD, 1, None, pal, 1, None, 0, o(2, 1), MIS, None, None) == A.APS_ERR_ALIGN
+
+
+@no_gpu
+def test_lp_gemm_validation(lib):
+    f = lib.aps_lp_gemm
+    F5, F8 = A.Format(5, 2).c(), A.Format(8, 23).c()
+    g = lambda M=8, N=8, K=8, lda=8, ldb=8, ldc=8, a=GOOD, b=GOOD, c=GOOD, fin=F5, facc=F5, acc=0: \
+        f(a, lda, b, ldb, c, ldc, M, N, K, fin, facc, acc, None)
+    assert g(M=-1) == A.APS_ERR_SIZE
+    assert g(K=(1 << 22) + 1, lda=1 << 23) == A.APS_ERR_SIZE
+    assert g(c=None) == A.APS_ERR_NULL
+    assert g(a=None) == A.APS_ERR_NULL
+    assert g(lda=7) == A.APS_ERR_SIZE
+    assert g(ldb=7) == A.APS_ERR_SIZE
+    assert g(ldc=7) == A.APS_ERR_SIZE
+    assert g(fin=A.aps_format(9, 2, 255)) == A.APS_ERR_FORMAT
+    assert g(acc=5) == A.APS_ERR_UNSUPPORTED
+    # products of two 13-bit significands are not exact in fp32
+    assert g(fin=A.Format(5, 12).c()) == A.APS_ERR_UNSUPPORTED
+    # bf16-range inputs with 12-bit significands: tiny products would need
+    # fp32's subnormal rounding, which the fp32 accumulator format can see
+    assert g(fin=A.Format(8, 11).c(), facc=F8) == A.APS_ERR_UNSUPPORTED
+    # empty output: nothing to do (and nothing checked beyond the sizes)
+    assert g(M=0, a=None, b=None, c=None) == A.APS_OK

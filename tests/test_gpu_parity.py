@@ -502,3 +502,112 @@ def test_ordered_reduce_w256_groups(dev):
     for k in (1, 16, 64):
         log("W=256 k", k)
         _run_ex(dev, G, n, offs, [F(5, 2)], None, se, k, A.APS_ACC_SEQUENTIAL, f"W=256 k={k}")
+
+
+# ------------------------------- low-precision-accumulator GEMM (Sec. 5, CPD)
+
+# (input format, accumulator format): every accumulator variant of the kernel
+GEMM_PAIRS = [
+    (F(5, 2), F(5, 2)),     # TOP class, fp32 adds
+    (F(4, 3), F(4, 3)),     # LOW class
+    (F(4, 3), F(5, 2)),
+    (F(5, 10), F(5, 10)),   # fp16
+    (F(8, 7), F(8, 7)),     # bf16: INT class, products below fp32's normal range
+    (F(5, 10), F(8, 23)),   # fp32 accumulator
+    (F(5, 2), F(6, 12)),    # TOP class, fp64 adds
+    (F(3, 2), F(3, 12)),    # LOW class, fp64 adds
+    (F(5, 10), F(8, 15)),   # INT class, fp64 adds
+    (F(4, 3), F(5, 0)),     # m = 0, TOP class
+    (F(2, 1), F(2, 0)),     # m = 0, LOW class: the 3-bit accumulator
+    (F(8, 3), F(8, 0)),     # m = 0, INT class
+]
+GEMM_SHAPES = [(1, 1, 1), (70, 130, 37), (64, 64, 16), (5, 200, 0), (128, 96, 300), (3, 65, 17)]
+
+
+def _gemm_inputs(rng, M, N, K, fin, specials=True):
+    lo, hi = O.emin(ofmt(fin)) - fin.m - 1, max(O.emax(ofmt(fin)) // 2, 1)
+    Am = (rng.standard_normal((M, K)) * 2.0 ** rng.uniform(lo, hi, (M, K))).astype(np.float32)
+    Bm = (rng.standard_normal((K, N)) * 2.0 ** rng.uniform(lo, hi, (K, N))).astype(np.float32)
+    if specials and M * K > 8 and K * N > 8:
+        for arr in (Am, Bm):
+            flat = arr.reshape(-1)
+            idx = rng.choice(flat.size, 6, replace=False)
+            flat[idx] = [0.0, -0.0, np.inf, -np.inf, np.nan, 3.0e38]
+    return Am, Bm
+
+
+@pytest.mark.parametrize("acc", [A.APS_ACC_SEQUENTIAL, A.APS_ACC_KAHAN])
+@pytest.mark.parametrize("fin,facc", GEMM_PAIRS, ids=lambda f: str(f))
+def test_lp_gemm_parity(dev, fin, facc, acc):
+    rng = np.random.default_rng(900 + 7 * fin.e + facc.m + 31 * acc)
+    for M, N, K in GEMM_SHAPES:
+        for specials in (False, True):
+            Am, Bm = _gemm_inputs(rng, M, N, K, fin, specials)
+            log(f"lp_gemm {fin}->{facc} acc={acc} M={M} N={N} K={K} specials={specials}")
+            got = A.aps_lp_gemm(torch.from_numpy(Am).to(dev), torch.from_numpy(Bm).to(dev), fin, facc, acc)
+            torch.cuda.synchronize()
+            ref = O.lp_gemm(Am, Bm, ofmt(fin), ofmt(facc), acc)
+            g = got.cpu().numpy()
+            assert same_f32(g, ref), (fin, facc, acc, M, N, K, specials, first_diff(g, ref))
+
+
+def test_lp_gemm_strided_views(dev):
+    # row strides from the tensors (leading dimensions larger than the width)
+    rng = np.random.default_rng(950)
+    fin, facc = F(4, 3), F(5, 2)
+    Abig = rng.standard_normal((40, 100)).astype(np.float32)
+    Bbig = rng.standard_normal((77, 90)).astype(np.float32)
+    At = torch.from_numpy(Abig).to(dev)[:, 3:80]
+    Bt = torch.from_numpy(Bbig).to(dev)[:, 5:70]
+    C = torch.full((40, 80), 7.0, device=dev)
+    A.aps_lp_gemm(At, Bt, fin, facc, C=C[:, :65])
+    torch.cuda.synchronize()
+    ref = O.lp_gemm(Abig[:, 3:80], Bbig[:, 5:70], ofmt(fin), ofmt(facc))
+    c = C.cpu().numpy()
+    assert same_f32(c[:, :65], ref)
+    assert (c[:, 65:] == 7.0).all()  # nothing written past N
+
+
+@pytest.mark.parametrize("acc", [A.APS_ACC_SEQUENTIAL, A.APS_ACC_KAHAN])
+def test_lp_gemm_bert_ffn_sampled(dev, acc):
+    # BERT-large's first FFN product at 8 sequences of 512 tokens:
+    # [4096 tokens x 1024] x [1024 x 4096], 1-5-2 inputs, 1-5-10 accumulator;
+    # sampled rows and columns against the oracle
+    rng = np.random.default_rng(960 + acc)
+    M, K, N = 4096, 1024, 4096
+    fin, facc = F(5, 2), F(5, 10)
+    Am = rng.standard_normal((M, K)).astype(np.float32)
+    Bm = (rng.standard_normal((K, N)) * 0.02).astype(np.float32)
+    log(f"lp_gemm BERT FFN M={M} K={K} N={N} acc={acc}")
+    got = A.aps_lp_gemm(torch.from_numpy(Am).to(dev), torch.from_numpy(Bm).to(dev), fin, facc, acc)
+    torch.cuda.synchronize()
+    g = got.cpu().numpy()
+    rows = np.sort(rng.choice(M, 6, replace=False))
+    cols = np.sort(rng.choice(N, 6, replace=False))
+    ref_r = O.lp_gemm(Am[rows], Bm, ofmt(fin), ofmt(facc), acc)
+    assert same_f32(g[rows], ref_r), first_diff(g[rows], ref_r)
+    ref_c = O.lp_gemm(Am, np.ascontiguousarray(Bm[:, cols]), ofmt(fin), ofmt(facc), acc)
+    assert same_f32(g[:, cols], ref_c), first_diff(g[:, cols], ref_c)
+
+
+@pytest.mark.parametrize("f", [F(3, 0), F(5, 0), F(8, 0), F(5, 2)], ids=str)
+def test_kahan_compensation_nan_does_not_reach_the_sum(dev, f):
+    # s = INF, then x = 1: t = INF, but the compensation R(R(t - s) - y) is
+    # NaN; the sum itself stays INF (m = 0 formats included)
+    G = np.array([[np.inf] * 8, [1.0] * 8], np.float32)
+    offs = np.array([0, 8], np.int64)
+    ref = O.sim_reduce_ex(G, 8, offs, None, ofmt(f), accumulator=O.ACC_KAHAN)
+    assert np.isinf(ref).all()
+    out = torch.empty(8, device=dev)
+    A.aps_sim_reduce_ex(torch.from_numpy(G).to(dev), 8, torch.from_numpy(offs).to(dev), None, [f], None, 0,
+                        accumulator=A.APS_ACC_KAHAN, out=out)
+    torch.cuda.synchronize()
+    assert same_f32(out.cpu().numpy(), ref)
+    # the same chain as a dot product: products INF * 1 and 1 * 1
+    Am = np.array([[np.inf, 1.0]], np.float32)
+    Bm = np.array([[1.0], [1.0]], np.float32)
+    fin = F(5, 2) if f.e < 8 else F(8, 3)
+    refg = O.lp_gemm(Am, Bm, ofmt(fin), ofmt(f), O.ACC_KAHAN)
+    got = A.aps_lp_gemm(torch.from_numpy(Am).to(dev), torch.from_numpy(Bm).to(dev), fin, f, A.APS_ACC_KAHAN)
+    torch.cuda.synchronize()
+    assert np.isinf(refg).all() and same_f32(got.cpu().numpy(), refg)
