@@ -47,6 +47,7 @@ def parse():
     ap.add_argument("--config", default="resnet50_w256")
     ap.add_argument("--palette", default=None)
     ap.add_argument("--mode", choices=["aps", "raw"], default="aps")
+    ap.add_argument("--gemm", action="store_true", help="time only aps_lp_gemm (BERT-large FFN shape)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-other-calls", action="store_true",
                     help="skip timing aps_quantize / aps_dequantize outside the step")
@@ -220,6 +221,59 @@ def cpu_baseline(G_t, gs, pal, budget_s: float, slice_cols: int = 65536):
     }
 
 
+# VALU peak: 256 CUs x 128 lanes/clk x 2.4 GHz = 78.6 T lane-instructions/s,
+# the published 157.3 TFLOP/s fp32 vector rate counted one lane-instruction
+# per FMA.  Two-operand (VOP2/VOPC) adds, multiplies and logic ops issue at
+# that rate; three-operand or modifier-carrying (VOP3) instructions such as
+# v_add3_u32, v_bfe_u32, v_ldexp_f32 or v_fma_f32 at half of it (measured:
+# about 54-71 against 87-112 lanes/clk/CU).
+VALU_PEAK_T = 256 * 128 * 2.4e9 / 1e12
+# k_lp_gemm's k-loop for 1-5-2 inputs and a 1-5-10 accumulator (products fit
+# the accumulator's significand), counted in the kernel's ISA per
+# multiply-accumulate: VALU instructions, and issue slots with a VOP3
+# instruction taking two.
+GEMM_VALU_PER_MAC = {"sequential": (11.125, 14.125), "kahan": (24.125, 33.125)}
+GEMM_SHAPE = (4096, 1024, 4096)  # BERT-large FFN up-projection at 8 x 512 tokens: M, K, N
+
+
+def lp_gemm_calls(A, dev, reps: int = 5):
+    """Event-timed aps_lp_gemm on the BERT-large FFN shape, 1-5-2 inputs and
+    a 1-5-10 accumulator, plain and Kahan; an ALU roofline from the VALU
+    instructions the kernel issues per multiply-accumulate."""
+    import torch
+
+    M, K, N = GEMM_SHAPE
+    g = torch.Generator(device=dev).manual_seed(1911)
+    Am = torch.randn((M, K), generator=g, device=dev)
+    Bm = torch.randn((K, N), generator=g, device=dev) * 0.02
+    C = torch.empty((M, N), device=dev)
+    fin, facc = A.Format(5, 2), A.Format(5, 10)
+    res = {"workload": f"bert_large_ffn M={M} K={K} N={N}", "in": str(fin), "acc": str(facc)}
+    for name, acc in (("sequential", A.APS_ACC_SEQUENTIAL), ("kahan", A.APS_ACC_KAHAN)):
+        A.aps_lp_gemm(Am, Bm, fin, facc, acc, C=C)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            A.aps_lp_gemm(Am, Bm, fin, facc, acc, C=C)
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        t = sorted(ts)[len(ts) // 2]
+        macs = float(M) * N * K
+        instr, slots = GEMM_VALU_PER_MAC[name]
+        achieved = macs * instr / (t * 1e-3) / 1e12
+        ceiling = VALU_PEAK_T * 1e12 / slots  # MAC/s if every issue slot were used
+        res[name] = {"ms": t, "MAC_per_s": macs / (t * 1e-3),
+                     "roofline": {"bound": "alu", "achieved": achieved, "peak": VALU_PEAK_T,
+                                  "unit": "T VALU lane-instructions/s", "frac": achieved / VALU_PEAK_T,
+                                  "valu_per_mac": instr, "issue_slots_per_mac": slots,
+                                  "mix_ceiling_MAC_per_s": ceiling,
+                                  "frac_of_mix_ceiling": macs / (t * 1e-3) / ceiling}}
+    return res
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -231,6 +285,13 @@ def main():
         return
     if args.roundoff:
         roundoff_study()
+        return
+    if args.gemm:
+        import torch
+
+        from paper_1911_08907_amd import aps as A
+        A.lib()
+        print(json.dumps(lp_gemm_calls(A, torch.device("cuda:0"))), flush=True)
         return
 
     import torch
@@ -292,6 +353,8 @@ def main():
     assert bool(torch.isfinite(out).all()) or args.mode == "raw"
 
     other = {} if args.no_other_calls else other_calls(A, G, gs, pal, idx_t, offs_t, se, out)
+    if not args.no_other_calls:
+        other["lp_gemm"] = lp_gemm_calls(A, dev)
 
     alg_bytes = 4.0 * W * n + 4.0 * n     # read every worker row once, write the fp32 sum
     achieved = alg_bytes / (k4 * 1e-3) / 1e9

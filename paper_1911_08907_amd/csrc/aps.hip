@@ -103,14 +103,13 @@ struct VT {
     static constexpr bool m0 = (V == V_INT_M0 || V == V_TOP_M0 || V == V_LOW_M0);
 };
 
-// Working-domain format value of fl32(x * 2^F) (F already includes the
-// domain shift k).  Sets `bad` when the input is NaN (m = 0 formats have no
-// NaN pattern that survives the rounding, so NaN is tracked on the side).
+// Working-domain format value of y, a value already in the working domain
+// (fl32 of the scaled input).  Sets `bad` when y is NaN (m = 0 formats have
+// no NaN pattern that survives the rounding, so NaN is tracked on the side).
 template <int V>
-__device__ __forceinline__ float quant(float x, int F, const FmtK& f, bool& bad) {
+__device__ __forceinline__ float quant_w(float y, const FmtK& f, bool& bad) {
     using T = VT<V>;
-    const float y = __builtin_amdgcn_ldexpf(x, F);
-    if constexpr (T::m0) bad |= (x != x);
+    if constexpr (T::m0) bad |= (y != y);
     if constexpr (T::acc == ACC_EXACT) {
         return y;
     } else if constexpr (T::cls == CLS_INT) {
@@ -140,6 +139,30 @@ __device__ __forceinline__ float quant(float x, int F, const FmtK& f, bool& bad)
         const uint32_t r = (__builtin_fabsf(y) >= f.thr) ? rn : rsb;
         return u2f(r & f.mask);
     }
+}
+
+// Working-domain format value of fl32(x * 2^F) (F already includes the
+// domain shift k).
+template <int V>
+__device__ __forceinline__ float quant(float x, int F, const FmtK& f, bool& bad) {
+    return quant_w<V>(__builtin_amdgcn_ldexpf(x, F), f, bad);
+}
+
+// quant_w for a y whose significand already fits the format's (at most m+1
+// significant bits) and whose overflow is already INF: only the subnormal
+// range rounds.  TOP and LOW classes, m >= 1.
+template <int V>
+__device__ __forceinline__ float quant_fit(float y, const FmtK& f) {
+    static_assert(VT<V>::cls != CLS_INT && !VT<V>::m0, "TOP or LOW class, m >= 1");
+    const uint32_t b = f2u(y);
+    uint32_t ab = b & 0x7FFFFFFFu;
+    asm volatile("" : "+v"(ab));  // keep |y| in a register: two-operand forms below, no abs modifiers
+    float ys = u2f(ab);
+    if constexpr (VT<V>::cls == CLS_LOW) ys = __builtin_amdgcn_ldexpf(ys, -f.j);
+    float rs = (ys + f.c0) - f.c0;
+    if constexpr (VT<V>::cls == CLS_LOW) rs = __builtin_amdgcn_ldexpf(rs, f.j);
+    // NaN fails the compare and takes the subnormal path, which keeps it NaN
+    return (f.thr <= u2f(ab)) ? y : u2f(f2u(rs) | (b & 0x80000000u));
 }
 
 // R_fmt(s + q) for two working-domain format values.
@@ -1372,6 +1395,14 @@ struct GemmArgs {
     float* __restrict__ C;
     int64_t lda, ldb, ldc;
     int32_t M, N, K;
+    int32_t ka, kb;  // staged A and B carry 2^ka, 2^kb (ka + kb = k of the accumulator, or both 0)
+};
+
+// How a product reaches the accumulator's working domain and is rounded:
+enum GemmProduct {
+    GP_LDEXP = 0,   // operands native: fl32(a * b) then 2^k, rounded (quant)
+    GP_SCALED = 1,  // operands pre-scaled at staging: a_w * b_w rounded (quant_w)
+    GP_FIT = 2,     // pre-scaled, and every product fits the significand (quant_fit)
 };
 
 constexpr int GT = 64;  // output tile GT x GT per block, 4 x 4 per thread
@@ -1382,7 +1413,7 @@ constexpr int GK = 16;  // k-tile staged in LDS
 // four rows are one 16-byte read); each thread then runs 16 independent
 // chains, one per output, adding its products in k order.  The work is the
 // VALU's: a product, its rounding and the rounded add per multiply-accumulate.
-template <int V, bool KAHAN>
+template <int V, bool KAHAN, int PM>
 __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa) {
     __shared__ __align__(16) float As[GK][GT + 4];  // As[k][m]; the pad spreads the staging writes over banks
     __shared__ __align__(16) float Bs[GK][GT + 4];  // Bs[k][n]
@@ -1406,9 +1437,11 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
         for (int r = 0; r < 4; ++r) {
             const int idx = t + BLOCK * r;
             const int64_t am = m0 + (idx >> 4), ak = k0 + (idx & 15);
-            ra[r] = (am < g.M && ak < g.K) ? quant_any(g.A[am * g.lda + ak], fi.k, fi) : 0.0f;
+            ra[r] = (am < g.M && ak < g.K) ? __builtin_amdgcn_ldexpf(quant_any(g.A[am * g.lda + ak], fi.k, fi), g.ka)
+                                           : 0.0f;
             const int64_t bk = k0 + (idx >> 6), bn = n0 + (idx & 63);
-            rb[r] = (bk < g.K && bn < g.N) ? quant_any(g.B[bk * g.ldb + bn], fi.k, fi) : 0.0f;
+            rb[r] = (bk < g.K && bn < g.N) ? __builtin_amdgcn_ldexpf(quant_any(g.B[bk * g.ldb + bn], fi.k, fi), g.kb)
+                                           : 0.0f;
         }
     };
     auto mac = [&](int kk, bool first) {
@@ -1421,7 +1454,13 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 // exact fp32 product of two input-format values, cast to the accumulator
-                const float p = quant<V>(a[i] * b[j], fa.k, fa, bad[i][j]);
+                float p;
+                if constexpr (PM == GP_LDEXP)
+                    p = quant<V>(a[i] * b[j], fa.k, fa, bad[i][j]);
+                else if constexpr (PM == GP_SCALED)
+                    p = quant_w<V>(a[i] * b[j], fa, bad[i][j]);
+                else
+                    p = quant_fit<V>(a[i] * b[j], fa);
                 if (first)
                     s[i][j] = p;
                 else
@@ -1742,6 +1781,38 @@ extern "C" int aps_dequantize(const float* Q, const void* codes, int64_t n, cons
     return launched();
 }
 
+// Instantiates only the product modes a variant can take: GP_FIT needs the
+// TOP or LOW class with m >= 1; INT-class formats (k = 0) are always scaled.
+template <int V>
+static void launch_lp_gemm_v(bool kahan, int pm, dim3 grid, hipStream_t s, const GemmArgs& g, const FmtK& fi,
+                             const FmtK& fa) {
+    constexpr bool can_fit = VT<V>::cls != CLS_INT && !VT<V>::m0;
+    constexpr bool can_ldexp = VT<V>::cls != CLS_INT;
+#define APS_G(K, P) hipLaunchKernelGGL((k_lp_gemm<V, K, P>), grid, dim3(BLOCK), 0, s, g, fi, fa)
+    if (pm == GP_FIT) {
+        if constexpr (can_fit) {
+            if (kahan) APS_G(true, GP_FIT); else APS_G(false, GP_FIT);
+            return;
+        }
+    }
+    if (pm == GP_LDEXP) {
+        if constexpr (can_ldexp) {
+            if (kahan) APS_G(true, GP_LDEXP); else APS_G(false, GP_LDEXP);
+            return;
+        }
+    }
+    if (kahan) APS_G(true, GP_SCALED); else APS_G(false, GP_SCALED);
+#undef APS_G
+}
+
+static void launch_lp_gemm(int variant, bool kahan, int pm, dim3 grid, hipStream_t s, const GemmArgs& g,
+                           const FmtK& fi, const FmtK& fa) {
+#define APS_LG(v) \
+    if (variant == (v)) launch_lp_gemm_v<v>(kahan, pm, grid, s, g, fi, fa);
+    APS_FOR_VARIANTS(APS_LG)
+#undef APS_LG
+}
+
 extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t ldb, float* C, int64_t ldc,
                            int32_t M, int32_t N, int32_t K, aps_format in_fmt, aps_format acc_fmt,
                            int32_t accumulator, void* stream) {
@@ -1761,18 +1832,20 @@ extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t 
     if (2 * (emin_in - in_fmt.m) < -149 && 2 * (in_fmt.m + 1) > emin_acc - acc_fmt.m + 149) return APS_ERR_UNSUPPORTED;
     if (!has_out) return APS_OK;
     const FmtK fi = make_fmtk(in_fmt), fa = make_fmtk(acc_fmt);
-    GemmArgs g{A, B, C, lda, ldb, ldc, M, N, K};
-    const dim3 grid((unsigned)((N + GT - 1) / GT), (unsigned)((M + GT - 1) / GT));
-    hipStream_t s = (hipStream_t)stream;
-    const bool kahan = accumulator == APS_ACC_KAHAN;
-#define APS_LAUNCH_G(v)                                                                          \
-    if (fa.variant == (v)) {                                                                     \
-        if (kahan)                                                                               \
-            hipLaunchKernelGGL((k_lp_gemm<v, true>), grid, dim3(BLOCK), 0, s, g, fi, fa);         \
-        else                                                                                     \
-            hipLaunchKernelGGL((k_lp_gemm<v, false>), grid, dim3(BLOCK), 0, s, g, fi, fa);        \
+    GemmArgs g{A, B, C, lda, ldb, ldc, M, N, K, 0, 0};
+    // Pre-scale the staged operands by 2^ka and 2^kb (ka + kb = k) when both
+    // stay below 2^128: a value below 2^(emax_in+1) times 2^(127-emax_in) does.
+    const int room = 127 - fi.emax;
+    int pm = GP_LDEXP;
+    if (fa.k <= 2 * room) {
+        g.ka = fa.k < room ? fa.k : room;
+        g.kb = fa.k - g.ka;
+        pm = GP_SCALED;
+        // every product has at most 2(m_in+1) significant bits
+        const int cls = fa.variant <= V_INT_M0 ? CLS_INT : (fa.variant <= V_TOP_M0 ? CLS_TOP : CLS_LOW);
+        if (cls != CLS_INT && acc_fmt.m > 0 && 2 * (in_fmt.m + 1) <= acc_fmt.m + 1) pm = GP_FIT;
     }
-    APS_FOR_VARIANTS(APS_LAUNCH_G)
-#undef APS_LAUNCH_G
+    const dim3 grid((unsigned)((N + GT - 1) / GT), (unsigned)((M + GT - 1) / GT));
+    launch_lp_gemm(fa.variant, accumulator == APS_ACC_KAHAN, pm, grid, (hipStream_t)stream, g, fi, fa);
     return launched();
 }

@@ -520,6 +520,10 @@ GEMM_PAIRS = [
     (F(4, 3), F(5, 0)),     # m = 0, TOP class
     (F(2, 1), F(2, 0)),     # m = 0, LOW class: the 3-bit accumulator
     (F(8, 3), F(8, 0)),     # m = 0, INT class
+    (F(5, 2), F(5, 10)),    # products fit the accumulator's significand: TOP class
+    (F(2, 1), F(4, 6)),     # products fit: LOW class
+    (F(8, 3), F(5, 10)),    # bf16-range inputs cannot be pre-scaled: one ldexp per product, TOP
+    (F(8, 2), F(4, 3)),     # the same, LOW class
 ]
 GEMM_SHAPES = [(1, 1, 1), (70, 130, 37), (64, 64, 16), (5, 200, 0), (128, 96, 300), (3, 65, 17)]
 
