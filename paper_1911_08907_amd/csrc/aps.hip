@@ -1444,9 +1444,7 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
                                            : 0.0f;
         }
     };
-    auto mac = [&](int kk, bool first) {
-        const f4 av = *(const f4*)&As[kk][ty * 4];
-        const f4 bv = *(const f4*)&Bs[kk][tx * 4];
+    auto mac_v = [&](const f4& av, const f4& bv, bool first) {
         const float a[4] = {av.x, av.y, av.z, av.w};
         const float b[4] = {bv.x, bv.y, bv.z, bv.w};
 #pragma unroll
@@ -1467,6 +1465,9 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
                     chain_step<V, KAHAN>(s[i][j], c[i][j], p, fa, bad[i][j]);
             }
     };
+    auto mac = [&](int kk, bool first) {
+        mac_v(*(const f4*)&As[kk][ty * 4], *(const f4*)&Bs[kk][tx * 4], first);
+    };
     if (g.K > 0) fetch(0);
     for (int64_t k0 = 0; k0 < g.K; k0 += GK) {
         __syncthreads();  // the previous k-tile is consumed
@@ -1479,14 +1480,27 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
         __syncthreads();
         if (k0 + GK < g.K) fetch(k0 + GK);  // the next k-tile's loads overlap this tile's math
         const int kend = (int)min((int64_t)GK, g.K - k0);
-        int kk = 0;
-        if (k0 == 0) {
-            mac(0, true);  // an output's chain starts with its first product
-            kk = 1;
-        }
-        if (kend == GK) {
-            for (; kk < GK; ++kk) mac(kk, false);
+        if (k0 > 0 && kend == GK) {
+            // software-pipelined: step kk+1's LDS reads are issued before step kk's math
+            f4 av = *(const f4*)&As[0][ty * 4], bv = *(const f4*)&Bs[0][tx * 4];
+#pragma unroll
+            for (int kk = 0; kk < GK; ++kk) {
+                f4 an = av, bn = bv;
+                if (kk + 1 < GK) {
+                    an = *(const f4*)&As[kk + 1][ty * 4];
+                    bn = *(const f4*)&Bs[kk + 1][tx * 4];
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                mac_v(av, bv, false);
+                av = an;
+                bv = bn;
+            }
         } else {
+            int kk = 0;
+            if (k0 == 0) {
+                mac(0, true);  // an output's chain starts with its first product
+                kk = 1;
+            }
 #pragma unroll 1
             for (; kk < kend; ++kk) mac(kk, false);
         }
