@@ -3,14 +3,19 @@
 
 A step is one APS synchronisation of W simulated workers over a synthetic,
 HBM-resident gradient set (Algorithm 1 of arXiv 1911.08907): per-layer
-max-abs, per-layer scale exponents, and the fused scale / cast / rounded
-W-worker sum / unscale kernel.  The default workload is the ResNet-50-shaped
-set with W = 256 workers (161 tensors, 25,557,032 elements per worker,
-26.2 GB of fp32 worker gradients) in the 1-5-2 format.
+max-abs, per-layer scale exponents, and scale / cast / rounded W-worker sum /
+unscale, through one aps_sync call (pass 1 + pass 2).  On the one-pass route
+pass 1 reads the W rows once and forms the sum unscaled; pass 2 computes the
+scales and recomputes the few elements whose inputs reach the format's
+subnormal range.  The default workload is the ResNet-50-shaped set with
+W = 256 workers (161 tensors, 25,557,032 elements per worker, 26.2 GB of fp32
+worker gradients) in the 1-5-2 format.
 
 Prints one JSON line: whole-step throughput (worker-gradient elements per
-second), the fused kernel's HBM roofline figures measured with HIP events on
-the launch stream, and the CPU oracle's throughput on a bounded sample.
+second), the dominant kernel's HBM roofline figures measured with HIP events
+on the launch stream, the two-pass step (max-abs, scales, fused reduce) and
+the other calls timed beside it, and the CPU oracle's throughput on a
+bounded sample.
 """
 from __future__ import annotations
 
@@ -18,6 +23,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -32,10 +38,15 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_1911_08907_amd", "csrc", f) for f in
 
 
 def source_digest() -> str:
+    """Digest of the kernel sources' code: comments and whitespace are
+    dropped, so a change to a comment does not count as a kernel change."""
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(p, "rb") as fh:
-            h.update(fh.read())
+        with open(p) as fh:
+            txt = fh.read()
+        txt = re.sub(r"/\*.*?\*/", " ", txt, flags=re.S)
+        txt = re.sub(r"//[^\n]*", " ", txt)
+        h.update(" ".join(txt.split()).encode())
     return h.hexdigest()[:16]
 
 
@@ -70,10 +81,10 @@ def copy_calibration(gib: float, reps: int = 5) -> None:
     print(json.dumps({"copy_bytes_per_dispatch": nbytes, "reps": reps}), flush=True)
 
 
-def traffic_from_profile(config: str, palette: str, launch_bytes: float):
-    """HBM bytes per launch from the committed counter summary, if it was
-    taken on the current kernel source."""
-    path = os.path.join(PROFILES, f"sim_reduce_{config}_{palette}_counters.json")
+def traffic_from_profile(kernel: str, config: str, palette: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary,
+    if it was taken on the current kernel source."""
+    path = os.path.join(PROFILES, f"{kernel}_{config}_{palette}_counters.json")
     if not os.path.exists(path):
         return None, "no counter summary"
     with open(path) as fh:
@@ -83,6 +94,39 @@ def traffic_from_profile(config: str, palette: str, launch_bytes: float):
     fetch = c["fetch_kib_per_dispatch"] * 1024 * c["fetch_scale"]
     write = c["write_kib_per_dispatch"] * 1024 * c["write_scale"]
     return fetch + write, f"{os.path.basename(path)}"
+
+
+def event_timed(fns, reps: int = 5):
+    """Median over reps of the event-timed span of each callable in fns,
+    run back to back on the current stream."""
+    import torch
+
+    for fn in fns:
+        fn()
+    torch.cuda.synchronize()
+    spans = [[] for _ in fns]
+    for _ in range(reps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)]
+        ev[0].record()
+        for k, fn in enumerate(fns):
+            fn()
+            ev[k + 1].record()
+        torch.cuda.synchronize()
+        for k in range(len(fns)):
+            spans[k].append(ev[k].elapsed_time(ev[k + 1]))
+    return [sorted(t)[len(t) // 2] for t in spans]
+
+
+def two_pass_step(A, G, gs, pal, idx_t, offs_t, mab, se, out):
+    """The step as three calls (max-abs, scales, fused reduce): two full
+    reads of the W rows."""
+    W, n = gs.W, gs.n
+    t1, t2, t3 = event_timed([lambda: A.aps_layer_maxabs(G, n, offs_t, mab),
+                              lambda: A.aps_layer_scales(mab, W, pal, idx_t, se),
+                              lambda: A.aps_sim_reduce(G, n, offs_t, se, pal, idx_t, 0, out=out)])
+    return {"ms": t1 + t2 + t3, "elements_per_s": W * n / ((t1 + t2 + t3) * 1e-3),
+            "kernels_ms": {"k_maxabs": t1, "k_scales": t2, "k_sim_reduce": t3},
+            "k_sim_reduce_GBps": (4.0 * W * n + 4.0 * n) / (t3 * 1e-3) / 1e9}
 
 
 def other_calls(A, G, gs, pal, idx_t, offs_t, se, out, reps: int = 5):
@@ -318,24 +362,27 @@ def main():
     mab = torch.empty(L, dtype=torch.int32, device=dev)
     se = torch.empty(L, dtype=torch.int32, device=dev)
     out = torch.empty(n, dtype=torch.float32, device=dev)
+    ws = torch.empty(A.aps_sync_workspace_bytes(n, L), dtype=torch.uint8, device=dev)
     G = gs.G
+    aps = args.mode == "aps"
+    one = aps and A.aps_sync_one_pass(W, pal)
 
     ev = []
 
     def step(record: bool):
         if record:
-            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
             e[0].record()
-        A.aps_layer_maxabs(G, n, offs_t, mab)
+        if aps:
+            A.aps_sync(G, n, offs_t, pal, idx_t, A.APS_SYNC_PASS1, mab, se, out, ws)
         if record:
             e[1].record()
-        if args.mode == "aps":
-            A.aps_layer_scales(mab, W, pal, idx_t, se)
+        if aps:
+            A.aps_sync(G, n, offs_t, pal, idx_t, A.APS_SYNC_PASS2, mab, se, out, ws)
+        else:  # casting without APS: no maxima, no scales
+            A.aps_sim_reduce(G, n, offs_t, None, pal, idx_t, 0, out=out)
         if record:
             e[2].record()
-        A.aps_sim_reduce(G, n, offs_t, se if args.mode == "aps" else None, pal, idx_t, 0, out=out)
-        if record:
-            e[3].record()
             ev.append(e)
 
     for _ in range(args.warmup):
@@ -347,18 +394,27 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
-    k1 = sum(e[0].elapsed_time(e[1]) for e in ev) / len(ev)
-    k2 = sum(e[1].elapsed_time(e[2]) for e in ev) / len(ev)
-    k4 = sum(e[2].elapsed_time(e[3]) for e in ev) / len(ev)
-    assert bool(torch.isfinite(out).all()) or args.mode == "raw"
+    p1 = sum(e[0].elapsed_time(e[1]) for e in ev) / len(ev)
+    p2 = sum(e[1].elapsed_time(e[2]) for e in ev) / len(ev)
+    assert bool(torch.isfinite(out).all()) or not aps
 
-    other = {} if args.no_other_calls else other_calls(A, G, gs, pal, idx_t, offs_t, se, out)
+    other = {}
+    if aps:
+        other["two_pass_step"] = two_pass_step(A, G, gs, pal, idx_t, offs_t, mab, se, out)
     if not args.no_other_calls:
+        other.update(other_calls(A, G, gs, pal, idx_t, offs_t, se if aps else None, out))
         other["lp_gemm"] = lp_gemm_calls(A, dev)
 
+    # the dominant kernel: the one that reads the W rows and writes the sum
     alg_bytes = 4.0 * W * n + 4.0 * n     # read every worker row once, write the fp32 sum
-    achieved = alg_bytes / (k4 * 1e-3) / 1e9
-    traffic, traffic_src = traffic_from_profile(args.config, palette, alg_bytes)
+    if one:
+        kernel, k_ms = "k_sync_spec", p1
+        note = "pass-1 span: k_sync_spec plus the zeroing of the L maxima (k_fill_u32, a few us)"
+    else:
+        kernel, k_ms = "k_sim_reduce", p2
+        note = "pass-2 span: k_sim_reduce plus k_scales (a few us)" if aps else "k_sim_reduce alone"
+    achieved = alg_bytes / (k_ms * 1e-3) / 1e9
+    traffic, traffic_src = traffic_from_profile(kernel[2:], args.config, palette)
     res = {
         "metric": METRIC,
         "value": W * n / (ms_per_step * 1e-3),
@@ -373,7 +429,8 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": args.config, "W": W, "n": n, "tensors": L, "format": palette,
-                   "mode": args.mode, "layout": "[W][ld] fp32 worker-major, HBM resident"},
+                   "mode": args.mode, "route": "one pass" if one else "two passes",
+                   "layout": "[W][ld] fp32 worker-major, HBM resident"},
         "roofline": {
             "bound": "hbm",
             "achieved": achieved,
@@ -381,18 +438,17 @@ def main():
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
             "traffic": traffic,
-            "kernel": "k_sim_reduce",
+            "kernel": kernel,
             "algorithmic_bytes_per_launch": alg_bytes,
-            "avg_launch_ms": k4,
+            "avg_launch_ms": k_ms,
+            "timed_span": note,
             "traffic_source": traffic_src,
         },
-        "kernels_ms": {"layer_maxabs": k1, "layer_scales": k2, "sim_reduce": k4},
+        "passes_ms": {"pass1": p1, "pass2": p2},
         "other_calls": other,
-        "sim_reduce_elements_per_s": W * n / (k4 * 1e-3),
-        "maxabs_GBps": 4.0 * W * n / (k1 * 1e-3) / 1e9,
         "kernel_source": source_digest(),
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and aps:
         res["cpu_baseline"] = cpu_baseline(G, gs, pal, args.cpu_seconds)
     print(json.dumps(res), flush=True)
 

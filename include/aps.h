@@ -172,6 +172,77 @@ int aps_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n,
                    const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,
                    uint32_t flags, float* out, void* codes_out, void* stream);
 
+/* aps_sync flags: one or both passes, and optionally a route */
+#define APS_SYNC_PASS1 1u    /* read G: layer maxima (and, on the one-pass route, the
+                              * unscaled rounded sums and the workspace bytes) */
+#define APS_SYNC_PASS2 2u    /* scale exponents, then the rest of the sum */
+#define APS_SYNC_ONE_PASS 4u /* take the one-pass route wherever it applies */
+#define APS_SYNC_TWO_PASS 8u /* always read G twice */
+
+/*
+ * Bytes of workspace aps_sync needs for n elements and L layers, with
+ * C = ceil(n / 1024) chunks: round_up(1024 * C, 256) + round_up(4 * C, 256)
+ * + round_up(4 * L, 256) + 256 + round_up(4 * C, 256).  Host-only.
+ * Returns 0 for negative arguments or n > APS_MAX_ELEMS.
+ */
+uint64_t aps_sync_workspace_bytes(int64_t n, int32_t L);
+
+/*
+ * One whole APS synchronisation of W simulated workers (Algorithm 1 with the
+ * low-precision accumulator of Sec. 5), with N = W:
+ *   maxabs_bits  as aps_layer_maxabs
+ *   scale_exp    as aps_layer_scales with N = W
+ *   out          as aps_sim_reduce with flags 0 (the unscaled sum)
+ * The three arrays hold exactly what those three calls in sequence produce,
+ * whichever route is taken.
+ *
+ * The one-pass route reads G once instead of twice.  Power-of-two scaling
+ * commutes with rounding to m+1 significant bits (Sec. 3.3.1), so pass 1
+ * forms the rounded sum on the unscaled values while it takes the layer
+ * maxima, and records one byte per element.  Pass 2 computes the scales
+ * and recomputes through the scaled path only the elements for which the
+ * unscaled sum can differ: those with a nonzero input below
+ * T = max(2^(emin - ft), 2^-126) (the format's subnormal range after
+ * scaling) that is not swamped, i.e. that comes from worker 0 or meets a
+ * partial sum below 2^(m+3) * T, and every element of a layer whose max is
+ * INF or NaN or whose N * ghat exceeds 2^127.  The route applies when W is a power of two and
+ * every palette format has m <= 10.  With APS_SYNC_ONE_PASS it is then
+ * always taken.  With no route flag it is taken only when the format's range
+ * leaves few elements to recompute (W^2 * 2^(emin - emax + 2) <= 2^-7 for
+ * every palette format).  Otherwise, or with APS_SYNC_TWO_PASS, pass 1 is
+ * aps_layer_maxabs and pass 2 is aps_layer_scales followed by aps_sim_reduce.
+ *
+ *   G          [W][ld] fp32 (16-byte aligned, ld % 4 == 0); not aliased by out
+ *   flags      APS_SYNC_PASS1, APS_SYNC_PASS2 or both, plus at most one of
+ *              APS_SYNC_ONE_PASS, APS_SYNC_TWO_PASS.  Run separately, pass 2
+ *              must follow pass 1 with the same arguments and route flag on
+ *              the same stream, with the workspace untouched in between; after
+ *              pass 1 alone, maxabs_bits is final and out holds intermediate
+ *              values
+ *   maxabs_bits uint32[L] out
+ *   scale_exp  int32[L] out
+ *   out        fp32[n] out (16-byte aligned)
+ *   workspace  device memory of at least aps_sync_workspace_bytes(n, L)
+ *              bytes, 256-byte aligned, owned by the caller; its contents on
+ *              entry do not matter
+ * Calls that share a workspace must not overlap.  Errors as aps_sim_reduce;
+ * a small workspace returns APS_ERR_SIZE; no pass bit, an unknown bit or both
+ * route bits return APS_ERR_UNSUPPORTED.
+ */
+/*
+ * Which route aps_sync takes for W workers, this palette and these flags
+ * (only the route bits of flags matter): 1 for the one-pass route, 0 for
+ * two passes, or a negative status (W out of range, a bad palette, both
+ * route bits).  Host-only.
+ */
+int aps_sync_one_pass(int32_t W, const aps_format* fmts, int32_t n_fmts, uint32_t flags);
+
+int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n,
+             const int64_t* offsets, int32_t L,
+             const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,
+             uint32_t flags, uint32_t* maxabs_bits, int32_t* scale_exp, float* out,
+             void* workspace, uint64_t workspace_bytes, void* stream);
+
 /* Summation order and accumulator of aps_sim_reduce_ex. */
 enum { APS_ACC_SEQUENTIAL = 0, APS_ACC_KAHAN = 1 };
 typedef struct {

@@ -29,10 +29,15 @@ APS_MAX_FORMATS = 8
 
 EXPORTS = ("aps_format_supported", "aps_layer_maxabs", "aps_layer_scales", "aps_quantize",
            "aps_sim_reduce", "aps_sim_reduce_ex", "aps_sim_reduce_codes", "aps_dequantize", "aps_lp_gemm",
-           "aps_strerror")
+           "aps_sync_workspace_bytes", "aps_sync_one_pass", "aps_sync", "aps_strerror")
 
 APS_ACC_SEQUENTIAL = 0
 APS_ACC_KAHAN = 1
+
+APS_SYNC_PASS1 = 1
+APS_SYNC_PASS2 = 2
+APS_SYNC_ONE_PASS = 4
+APS_SYNC_TWO_PASS = 8
 
 
 class ApsError(RuntimeError):
@@ -100,6 +105,9 @@ def lib() -> ctypes.CDLL:
                                                  ctypes.POINTER(aps_reduce_opts), P, P, P]),
             "aps_dequantize": (ctypes.c_int, [P, P, i64, P, i32, P, FP, i32, P, P, P]),
             "aps_lp_gemm": (ctypes.c_int, [P, i64, P, i64, P, i64, i32, i32, i32, aps_format, aps_format, i32, P]),
+            "aps_sync_workspace_bytes": (ctypes.c_uint64, [i64, i32]),
+            "aps_sync_one_pass": (ctypes.c_int, [i32, FP, i32, u32]),
+            "aps_sync": (ctypes.c_int, [P, i32, i64, i64, P, i32, FP, i32, P, u32, P, P, P, P, ctypes.c_uint64, P]),
             "aps_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         }
         for name, (res, args) in sig.items():
@@ -248,6 +256,47 @@ def aps_lp_gemm(A, B, fin: Format, facc: Format, accumulator: int = APS_ACC_SEQU
     _check("aps_lp_gemm", lib().aps_lp_gemm(_ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, M, N, K, fin.c(),
                                             facc.c(), int(accumulator), _stream(stream)))
     return C
+
+
+def aps_sync_workspace_bytes(n: int, L: int) -> int:
+    return int(lib().aps_sync_workspace_bytes(int(n), int(L)))
+
+
+def aps_sync_one_pass(W: int, fmts, flags: int = 0) -> bool:
+    """Whether aps_sync takes the one-pass route for W workers and this
+    palette (only the route bits of ``flags`` matter)."""
+    pal, nf = _palette(fmts)
+    st = lib().aps_sync_one_pass(int(W), pal, nf, int(flags))
+    if st < 0:
+        raise ApsError("aps_sync_one_pass", st)
+    return st == 1
+
+
+def aps_sync(G, n: int, offsets, fmts, fmt_idx=None, flags: int = APS_SYNC_PASS1 | APS_SYNC_PASS2,
+             maxabs_bits=None, scale_exp=None, out=None, workspace=None, stream=None):
+    """One APS synchronisation in one call (N = W): max-abs, scales and the
+    rounded W-worker sum, reading G once where the library can.  ``flags``
+    selects the passes and optionally the route.  Missing output or
+    workspace tensors are allocated here.  Returns
+    (out, scale_exp, maxabs_bits, workspace)."""
+    import torch
+    W, ld = _rows(G)
+    L = offsets.numel() - 1
+    dev = G.device
+    if maxabs_bits is None:
+        maxabs_bits = torch.empty(L, dtype=torch.int32, device=dev)
+    if scale_exp is None:
+        scale_exp = torch.empty(L, dtype=torch.int32, device=dev)
+    if out is None:
+        out = torch.empty(max(n, 1), dtype=torch.float32, device=dev)[:n]
+    need = aps_sync_workspace_bytes(n, L)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    pal, nf = _palette(fmts)
+    _check("aps_sync", lib().aps_sync(_ptr(G), W, ld, n, _ptr(offsets), L, pal, nf, _ptr(fmt_idx), int(flags),
+                                      _ptr(maxabs_bits), _ptr(scale_exp), _ptr(out), _ptr(workspace),
+                                      workspace.numel() * workspace.element_size(), _stream(stream)))
+    return out, scale_exp, maxabs_bits, workspace
 
 
 def code_bytes(count: int, bits: int) -> int:

@@ -207,3 +207,66 @@ def test_lp_gemm_validation(lib):
     assert g(fin=A.Format(8, 11).c(), facc=F8) == A.APS_ERR_UNSUPPORTED
     # empty output: nothing to do (and nothing checked beyond the sizes)
     assert g(M=0, a=None, b=None, c=None) == A.APS_OK
+
+
+def test_sync_workspace_bytes(lib):
+    f = A.aps_sync_workspace_bytes
+    up = lambda b: (b + 255) // 256 * 256
+    for n, L in ((0, 1), (1, 1), (1024, 64), (1025, 65), (25557032, 161), (335141888, 391)):
+        C = (n + 1023) // 1024
+        assert f(n, L) == up(1024 * C) + up(4 * C) + up(4 * L) + 256 + up(4 * C), (n, L)
+    assert f(-1, 3) == 0 and f(5, -1) == 0 and f((1 << 30) + 1, 1) == 0
+
+
+@no_gpu
+def test_sync_validation(lib):
+    f = lib.aps_sync
+    pal = _pal(A.Format(5, 2))
+    ws = A.aps_sync_workspace_bytes(64, 1)
+    ok = dict(G=GOOD, W=2, ld=64, n=64, off=GOOD, L=1, pal=pal, nf=1, idx=None, ph=3, mab=GOOD, se=GOOD,
+              out=GOOD, ws=GOOD, wsb=ws)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["G"], a["W"], a["ld"], a["n"], a["off"], a["L"], a["pal"], a["nf"], a["idx"], a["ph"],
+                 a["mab"], a["se"], a["out"], a["ws"], a["wsb"], None)
+
+    assert call(G=None, ph=0) == A.APS_ERR_NULL
+    assert call(mab=None) == A.APS_ERR_NULL
+    assert call(se=None) == A.APS_ERR_NULL
+    assert call(out=None) == A.APS_ERR_NULL
+    assert call(ws=None) == A.APS_ERR_NULL
+    assert call(ph=0) == A.APS_ERR_UNSUPPORTED
+    assert call(ph=4) == A.APS_ERR_UNSUPPORTED                  # a route but no pass
+    assert call(ph=16 | 3) == A.APS_ERR_UNSUPPORTED             # unknown bit
+    assert call(ph=3 | 4 | 8) == A.APS_ERR_UNSUPPORTED          # both routes
+    assert call(out=MIS) == A.APS_ERR_ALIGN
+    assert call(ws=P(4096 + 128)) == A.APS_ERR_ALIGN       # workspace needs 256-byte alignment
+    assert call(wsb=ws - 1) == A.APS_ERR_SIZE
+    assert call(W=0) == A.APS_ERR_SIZE
+    assert call(pal=_pal(A.Format(9, 2))) == A.APS_ERR_FORMAT
+    assert call(nf=0) == A.APS_ERR_SIZE
+
+
+def test_sync_route_choice(lib):
+    F = A.Format
+    one, two = A.APS_SYNC_ONE_PASS, A.APS_SYNC_TWO_PASS
+    # the default takes one pass when the format's range leaves few elements to recompute
+    assert A.aps_sync_one_pass(256, [F(5, 2)]) is True
+    assert A.aps_sync_one_pass(8, [F(5, 2)]) is True
+    assert A.aps_sync_one_pass(8, [F(5, 10), F(5, 2)]) is True
+    assert A.aps_sync_one_pass(256, [F(8, 7)]) is True
+    assert A.aps_sync_one_pass(256, [F(4, 3)]) is False
+    assert A.aps_sync_one_pass(8, [F(3, 0)]) is False
+    # forced routes; the one-pass route needs a power-of-two W and m <= 10
+    assert A.aps_sync_one_pass(256, [F(4, 3)], one) is True
+    assert A.aps_sync_one_pass(256, [F(5, 2)], two) is False
+    assert A.aps_sync_one_pass(12, [F(5, 2)], one) is False
+    assert A.aps_sync_one_pass(8, [F(5, 12)], one) is False
+    assert A.aps_sync_one_pass(8, [F(5, 2), F(8, 23)], one) is False
+    with pytest.raises(A.ApsError):
+        A.aps_sync_one_pass(8, [F(5, 2)], one | two)
+    with pytest.raises(A.ApsError):
+        A.aps_sync_one_pass(0, [F(5, 2)])
+    with pytest.raises(A.ApsError):
+        A.aps_sync_one_pass(8, [F(9, 2)])

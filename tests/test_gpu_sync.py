@@ -1,0 +1,274 @@
+"""GPU parity of aps_sync, one whole APS synchronisation per call, against
+the CPU oracle.
+
+aps_sync must return exactly what the oracle's max-abs, scales (N = W) and
+rounded W-worker sum give (Algorithm 1 with the low-precision accumulator of
+Sec. 5), whichever route the library takes: the one-pass route (the sum
+formed unscaled while the maxima are taken, then the elements whose inputs
+reach the format's subnormal range recomputed through the scaled path), or
+the two-pass fallback (W not a power of two, or m > 10).  The cases put
+inputs exactly at, just above and just below each layer's threshold
+2^(emin - ft), in fp32's subnormal range, in layers with INF/NaN or with a
+maximum near fp32's top, and make chunks with few and with many elements to
+recompute, so that both repair routes run."""
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_1911_08907_amd import aps as A
+from paper_1911_08907_amd import workloads as WL
+from tests._util import first_diff, log, ofmt, same_f32, same_maxabs
+from tests.sync_cases import LAYER_MAXIMA, threshold_values
+from tests.test_gpu_parity import _layout, _oracle_maxabs_streamed, _sample_idx, _sampled_oracle, _values
+
+pytestmark = pytest.mark.gpu
+
+F = A.Format
+CH = 1024
+SPARSE_MAX = 16
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    A.lib()  # the HIP library must be there: no fallback
+    return torch.device("cuda:0")
+
+
+def _flagged(ws, n, offs):
+    """Elements the second pass recomputed (read back from the workspace):
+    exponent byte below the layer's threshold."""
+    if n == 0:
+        return np.zeros(0, bool)
+    L = offs.size - 1
+    up = lambda b: (b + 255) // 256 * 256
+    C = (n + CH - 1) // CH
+    t0 = up(CH * C) + up(4 * C)
+    w = ws.cpu().numpy()
+    minb = w[:n]
+    thr = w[t0:t0 + 4 * L].view(np.int32)
+    layer = np.searchsorted(offs, np.arange(n), side="right") - 1
+    return minb.astype(np.int32) < thr[layer]
+
+
+def one_pass(W, pal, route):
+    if route == A.APS_SYNC_TWO_PASS or W & (W - 1) or any(f.m > 10 for f in pal):
+        return False
+    if route == A.APS_SYNC_ONE_PASS:
+        return True
+    lw = int(W).bit_length() - 1
+    return all(2 * lw + (1 - f.b) - f.emax + 2 <= -7 for f in pal)
+
+
+def sync_case(dev, G, n, offs, pal, fmt_idx=None, tag="", split=False, garbage=True, route=A.APS_SYNC_ONE_PASS):
+    W, ld = G.shape
+    L = offs.size - 1
+    opal = [ofmt(f) for f in pal]
+    G_t = torch.from_numpy(G).to(dev)
+    offs_t = torch.from_numpy(offs).to(dev)
+    idx_t = None if fmt_idx is None else torch.from_numpy(fmt_idx).to(dev)
+    ws = torch.empty(A.aps_sync_workspace_bytes(n, L), dtype=torch.uint8, device=dev)
+    if garbage:  # the workspace's contents on entry must not matter
+        ws.copy_(torch.randint(0, 256, ws.shape, dtype=torch.uint8, device=dev))
+    out = torch.full((max(n, 1),), float("nan"), dtype=torch.float32, device=dev)
+    mab = torch.full((L,), -1, dtype=torch.int32, device=dev)
+    se = torch.full((L,), 12345, dtype=torch.int32, device=dev)
+    if split:
+        A.aps_sync(G_t, n, offs_t, pal, idx_t, A.APS_SYNC_PASS1 | route, mab, se, out, ws)
+        A.aps_sync(G_t, n, offs_t, pal, idx_t, A.APS_SYNC_PASS2 | route, mab, se, out, ws)
+    else:
+        A.aps_sync(G_t, n, offs_t, pal, idx_t, A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | route, mab, se, out, ws)
+    torch.cuda.synchronize()
+    o_mab = O.layer_maxabs(G, n, offs)
+    assert same_maxabs(mab.cpu().numpy(), o_mab), f"{tag} maxabs"
+    o_se = O.layer_scales(o_mab, W, opal, fmt_idx)
+    assert np.array_equal(se.cpu().numpy(), o_se), f"{tag} scales"
+    o_out = O.sim_reduce(G, n, offs, o_se, opal, fmt_idx)
+    g = out.cpu().numpy()[:n]
+    assert same_f32(g, o_out), f"{tag} sum {first_diff(g, o_out)}"
+    flagged = _flagged(ws, n, offs) if one_pass(W, pal, route) else None
+    return flagged
+
+
+# ----------------------------------------------------------- edge layouts
+
+FORMATS = [F(5, 2), F(4, 3), F(3, 0), F(2, 0), F(2, 1), F(3, 2), F(5, 10), F(8, 7), F(8, 0), F(6, 1),
+           F(4, 3, 5), F(5, 2, 20), F(7, 5), F(5, 12), F(8, 23)]
+SIZES = [0, 1, 3, 5, 7, 1023, 1024, 1025, 2049, 0, 64, 13, 4095, 2, 3000]
+
+
+@pytest.mark.parametrize("f", FORMATS, ids=str)
+@pytest.mark.parametrize("kind", ["normal", "special", "tiny"])
+def test_sync_edge_layouts(dev, f, kind):
+    rng = np.random.default_rng(hash(("sync", str(f), kind)) & 0xFFFF)
+    offs, n, ld = _layout(SIZES)
+    for W in (1, 2, 4, 8, 16, 3, 13):
+        G = _values(rng, W, ld, offs, kind)
+        tag = f"{f} {kind} W={W}"
+        log("case", tag)
+        sync_case(dev, G, n, offs, [f], tag=tag, split=(W == 4))
+        if W in (2, 8):
+            sync_case(dev, G, n, offs, [f], tag=tag + " default route", route=0)
+            sync_case(dev, G, n, offs, [f], tag=tag + " two passes", route=A.APS_SYNC_TWO_PASS, split=(W == 2))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_sync_mixed_palette(dev, seed):
+    rng = np.random.default_rng(300 + seed)
+    pal_choices = [[F(5, 2), F(4, 3), F(3, 0), F(2, 1)], [F(5, 10), F(5, 2), F(8, 7)],
+                   [F(5, 2), F(4, 3), F(6, 1), F(3, 4)], [F(8, 23), F(5, 2), F(3, 0)]]
+    pal = pal_choices[seed]
+    sizes = [int(v) for v in rng.choice([0, 1, 2, 3, 5, 17, 255, 1000, 1023, 1024, 1500, 4096], 40)]
+    offs, n, ld = _layout(sizes)
+    fmt_idx = rng.integers(0, len(pal), len(sizes)).astype(np.uint8)
+    for W in (2, 8, 5):
+        for kind in ("normal", "special", "tiny"):
+            G = _values(rng, W, ld, offs, kind)
+            tag = f"mixed seed={seed} W={W} {kind}"
+            log("case", tag)
+            sync_case(dev, G, n, offs, pal, fmt_idx=fmt_idx, tag=tag)
+
+
+def test_sync_empty_gradient(dev):
+    offs = np.zeros(4, np.int64)
+    G = np.zeros((4, 4), np.float32)
+    sync_case(dev, G, 0, offs, [F(5, 2)], tag="empty")
+
+
+# ------------------------------------------------- thresholds and repair
+
+@pytest.mark.parametrize("f", [F(5, 2), F(4, 3), F(3, 0), F(2, 1), F(5, 10), F(8, 7), F(6, 1), F(4, 3, 5)], ids=str)
+def test_sync_threshold_inputs(dev, f):
+    rng = np.random.default_rng(500 + f.e * 16 + f.m)
+    sizes = [1, 7, 1024, 3000, 2, 5000, 64, 1025]
+    offs, n, ld = _layout(sizes)
+    for W in (1, 2, 4, 8, 64):
+        # maxima spread from tiny (threshold below 2^-126) to near fp32's top
+        G = threshold_values(rng, W, ld, offs, f, LAYER_MAXIMA)
+        tag = f"{f} thresholds W={W}"
+        log("case", tag)
+        fl = sync_case(dev, G, n, offs, [f], tag=tag)
+        assert fl is not None and fl.any(), "no element was recomputed: the case tests nothing"
+
+
+def _chunk_counts(flagged):
+    n = flagged.size
+    nch = (n + CH - 1) // CH
+    pad = np.zeros(nch * CH, bool)
+    pad[:n] = flagged
+    return pad.reshape(nch, CH).sum(1)
+
+
+def test_sync_sparse_and_dense_repairs(dev):
+    """Chunks with 1..16 elements to recompute (one wave each) and with more
+    (the whole chunk again), in the same call; W = 512 also walks the
+    casts in two batches of 256 workers."""
+    f = F(5, 2)
+    for W in (8, 512):
+        n = 40 * CH
+        ld = n
+        rng = np.random.default_rng(W)
+        G = (rng.standard_normal((W, ld)) * 0.1).astype(np.float32)
+        G[0, 0] = 1.0
+        ft = O.scale_one(int(np.float32(1.0).view(np.uint32)), W, ofmt(f))
+        T = np.float32(2.0 ** (1 - f.b - ft))
+        G[np.abs(G) < 64 * T] = 64 * T   # nothing flagged by chance
+        # chunk c gets c elements whose first worker's input is below the
+        # threshold (a first term is never swamped)
+        planted = np.zeros(n, bool)
+        for c in range(40):
+            cols = c * CH + rng.choice(CH, c, replace=False)
+            G[0, cols] = T * np.float32(0.75) * np.where(rng.random(c) < 0.5, -1, 1)
+            planted[cols] = True
+        # and below-threshold inputs from worker 1 meeting a first term of
+        # 0.5: swamped, so nothing to recompute there
+        sw = rng.choice(np.nonzero(~planted & (np.arange(n) > 0))[0], 500, replace=False)
+        G[0, sw] = np.float32(0.5)
+        G[1, sw] = T * np.float32(0.5)
+        offs = np.array([0, n], np.int64)
+        fl = sync_case(dev, G, n, offs, [f], tag=f"sparse/dense W={W}")
+        cnt = _chunk_counts(fl)
+        assert np.array_equal(cnt, np.arange(40)), cnt
+        assert ((cnt > 0) & (cnt <= SPARSE_MAX)).any() and (cnt > SPARSE_MAX).any()
+
+
+def test_sync_unsafe_layers(dev):
+    """Layers whose max is INF or NaN, whose N * ghat overflows fp32, or
+    exceeds 2^127: recomputed whole, through the scaled path."""
+    f = F(5, 2)
+    W = 4
+    sizes = [300, 300, 300, 300, 300, 2000]
+    offs, n, ld = _layout(sizes)
+    rng = np.random.default_rng(9)
+    G = (rng.standard_normal((W, ld)) * 1e-3).astype(np.float32)
+    G[2, 10] = np.inf                       # layer 0: INF
+    G[1, 310] = np.nan                      # layer 1: NaN
+    with np.errstate(over="ignore"):
+        G[:, 600:900] *= np.float32(3e38 / 4e-3)  # layer 2: N * ghat = INF
+    G[0, 905] = np.float32(5e37)            # layer 3: N * ghat = 2e38, finite but above 2^127
+    G[1, 906] = np.float32(-5e37)
+    G[:, n:] = np.nan
+    fl = sync_case(dev, G, n, offs, [f], tag="unsafe layers")
+    assert fl[:1200].all()
+
+
+# --------------------------------------------------- paper-shaped sets
+
+@pytest.mark.parametrize("name,palette", [("mlp", "1-4-3"), ("resnet20", "1-5-2"), ("resnet20", "1-4-3"),
+                                          ("resnet20", "1-3-0")])
+def test_sync_config_full(dev, name, palette):
+    gs = WL.generate(name, palette, device="cpu")
+    pal = [A.Format(p.e, p.m, p.bias) for p in gs.palette]
+    fl = sync_case(dev, gs.G.numpy(), gs.n, gs.offsets, pal, fmt_idx=gs.fmt_idx, tag=f"{name} {palette}")
+    log(name, palette, "recomputed", int(fl.sum()), "of", gs.n)
+
+
+@pytest.mark.parametrize("name,palette", [("resnet50_w8", "1-5-2"), ("resnet50_w256", "1-5-2"),
+                                          ("resnet50_w256", "1-4-3"), ("bert_large", "hybrid")])
+def test_sync_config_large(dev, name, palette):
+    """Full sizes: maxima and scales against the oracle in full, the sum
+    against the two-pass kernels in full and against the oracle on sampled
+    columns, the recomputed elements among them."""
+    t0 = time.time()
+    gs = WL.generate(name, palette, device=dev)
+    G_t, W, n = gs.G, gs.W, gs.n
+    pal = [A.Format(p.e, p.m, p.bias) for p in gs.palette]
+    opal = [ofmt(f) for f in pal]
+    offs_t = torch.from_numpy(gs.offsets).to(dev)
+    idx_t = None if gs.fmt_idx is None else torch.from_numpy(gs.fmt_idx).to(dev)
+    route = A.APS_SYNC_ONE_PASS   # the one-pass kernels at full size, also where the default would not take them
+    out, se, mab, ws = A.aps_sync(G_t, n, offs_t, pal, idx_t, A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | route)
+    ref, se2, mab2 = A.aps_step(G_t, n, offs_t, pal, idx_t)
+    dflt, _, _, _ = A.aps_sync(G_t, n, offs_t, pal, idx_t)
+    torch.cuda.synchronize()
+    log(name, palette, "gpu done", f"{time.time() - t0:.1f}s")
+    o_mab = _oracle_maxabs_streamed(G_t, gs)
+    assert same_maxabs(mab.cpu().numpy(), o_mab), "maxabs"
+    o_se = O.layer_scales(o_mab, W, opal, gs.fmt_idx)
+    assert np.array_equal(se.cpu().numpy(), o_se), "scales"
+    assert torch.equal(out.view(torch.int32), ref.view(torch.int32)), "one-pass vs two-pass sum"
+    assert torch.equal(dflt.view(torch.int32), ref.view(torch.int32)), "default route vs two-pass sum"
+    fl = _flagged(ws, n, gs.offsets)
+    log(name, palette, "recomputed", int(fl.sum()), "of", n, f"{time.time() - t0:.1f}s")
+    rng = np.random.default_rng(11)
+    if name == "resnet50_w8":
+        G = G_t.cpu().numpy()
+        o_out = O.sim_reduce(G, n, gs.offsets, o_se, opal, gs.fmt_idx)
+        g = out.cpu().numpy()
+        assert same_f32(g, o_out), first_diff(g, o_out)
+    else:
+        idx = _sample_idx(rng, gs.offsets, n)
+        fidx = np.nonzero(fl)[0]
+        if fidx.size:
+            idx = np.unique(np.concatenate([idx, rng.choice(fidx, min(fidx.size, 4000), replace=False)]))
+        o_s = _sampled_oracle(G_t, gs, pal, idx, o_se, gs.fmt_idx, W)
+        g = out[torch.from_numpy(idx).to(dev)].cpu().numpy()
+        assert same_f32(g, o_s), first_diff(g, o_s)
+        log("sampled parity on", idx.size, "columns,", int(fl[idx].sum()), "of them recomputed")
+    assert bool(torch.isfinite(out).all())
+    del G_t, gs
+    torch.cuda.empty_cache()
