@@ -20,6 +20,7 @@ bounded sample.
 from __future__ import annotations
 
 import argparse
+import glob
 import hashlib
 import json
 import os
@@ -34,7 +35,8 @@ if ROOT not in sys.path:
 METRIC = "APS gradient elements/s (quantize+W-way sim reduce) and % of HBM peak GB/s"
 HBM_PEAK_GBPS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_1911_08907_amd", "csrc", f) for f in ("aps.hip", "aps_format.hpp")]
+KERNEL_SOURCES = sorted(glob.glob(os.path.join(ROOT, "paper_1911_08907_amd", "csrc", "*.hip"))
+                        + glob.glob(os.path.join(ROOT, "paper_1911_08907_amd", "csrc", "*.hpp")))
 
 
 def source_digest() -> str:
@@ -409,7 +411,7 @@ def main():
     alg_bytes = 4.0 * W * n + 4.0 * n     # read every worker row once, write the fp32 sum
     if one:
         kernel, k_ms = "k_sync_spec", p1
-        note = "pass-1 span: k_sync_spec plus the zeroing of the L maxima (k_fill_u32, a few us)"
+        note = "pass-1 span: k_sync_spec plus the zeroing of the L maxima (k_sync_clear, a few us)"
     else:
         kernel, k_ms = "k_sim_reduce", p2
         note = "pass-2 span: k_sim_reduce plus k_scales (a few us)" if aps else "k_sim_reduce alone"

@@ -1,0 +1,206 @@
+// aps_gemm.hip -- a GEMM on a multiply-accumulate unit of a chosen low
+// precision, CPD's low-precision-accumulator GEMM (Sec. 5).
+#include "aps_common.hpp"
+
+namespace aps {
+
+// ================================================== K6: low-precision GEMM
+
+struct GemmArgs {
+    const float* __restrict__ A;
+    const float* __restrict__ B;
+    float* __restrict__ C;
+    int64_t lda, ldb, ldc;
+    int32_t M, N, K;
+    int32_t ka, kb;  // staged A and B carry 2^ka, 2^kb (ka + kb = k of the accumulator, or both 0)
+};
+
+// How a product reaches the accumulator's working domain and is rounded:
+enum GemmProduct {
+    GP_LDEXP = 0,   // operands native: fl32(a * b) then 2^k, rounded (quant)
+    GP_SCALED = 1,  // operands pre-scaled at staging: a_w * b_w rounded (quant_w)
+    GP_FIT = 2,     // pre-scaled, and every product fits the significand (quant_fit)
+};
+
+constexpr int GT = 64;  // output tile GT x GT per block, 4 x 4 per thread
+constexpr int GK = 16;  // k-tile staged in LDS
+
+// One block computes a GT x GT tile of C.  Each k-tile of A and B is cast to
+// the input format while it is staged into LDS (A transposed, so a thread's
+// four rows are one 16-byte read); each thread then runs 16 independent
+// chains, one per output, adding its products in k order.  The work is the
+// VALU's: a product, its rounding and the rounded add per multiply-accumulate.
+template <int V, bool KAHAN, int PM>
+__global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa) {
+    __shared__ __align__(16) float As[GK][GT + 4];  // As[k][m]; the pad spreads the staging writes over banks
+    __shared__ __align__(16) float Bs[GK][GT + 4];  // Bs[k][n]
+    const int t = threadIdx.x;
+    const int tx = t & 15, ty = t >> 4;
+    const int64_t m0 = (int64_t)blockIdx.y * GT, n0 = (int64_t)blockIdx.x * GT;
+    float s[4][4], c[4][4];
+    bool bad[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            s[i][j] = 0.0f;
+            c[i][j] = 0.0f;
+            bad[i][j] = false;
+        }
+    float ra[4], rb[4];
+    // global -> registers, cast to the input format; outside A and B: 0
+    auto fetch = [&](int64_t k0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int idx = t + BLOCK * r;
+            const int64_t am = m0 + (idx >> 4), ak = k0 + (idx & 15);
+            ra[r] = (am < g.M && ak < g.K) ? __builtin_amdgcn_ldexpf(quant_any(g.A[am * g.lda + ak], fi.k, fi), g.ka)
+                                           : 0.0f;
+            const int64_t bk = k0 + (idx >> 6), bn = n0 + (idx & 63);
+            rb[r] = (bk < g.K && bn < g.N) ? __builtin_amdgcn_ldexpf(quant_any(g.B[bk * g.ldb + bn], fi.k, fi), g.kb)
+                                           : 0.0f;
+        }
+    };
+    auto mac_v = [&](const f4& av, const f4& bv, bool first) {
+        const float a[4] = {av.x, av.y, av.z, av.w};
+        const float b[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                // exact fp32 product of two input-format values, cast to the accumulator
+                float p;
+                if constexpr (PM == GP_LDEXP)
+                    p = quant<V>(a[i] * b[j], fa.k, fa, bad[i][j]);
+                else if constexpr (PM == GP_SCALED)
+                    p = quant_w<V>(a[i] * b[j], fa, bad[i][j]);
+                else
+                    p = quant_fit<V>(a[i] * b[j], fa);
+                if (first)
+                    s[i][j] = p;
+                else
+                    chain_step<V, KAHAN>(s[i][j], c[i][j], p, fa, bad[i][j]);
+            }
+    };
+    auto mac = [&](int kk, bool first) {
+        mac_v(*(const f4*)&As[kk][ty * 4], *(const f4*)&Bs[kk][tx * 4], first);
+    };
+    if (g.K > 0) fetch(0);
+    for (int64_t k0 = 0; k0 < g.K; k0 += GK) {
+        __syncthreads();  // the previous k-tile is consumed
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int idx = t + BLOCK * r;
+            As[idx & 15][idx >> 4] = ra[r];
+            Bs[idx >> 6][idx & 63] = rb[r];
+        }
+        __syncthreads();
+        if (k0 + GK < g.K) fetch(k0 + GK);  // the next k-tile's loads overlap this tile's math
+        const int kend = (int)min((int64_t)GK, g.K - k0);
+        if (k0 > 0 && kend == GK) {
+            // software-pipelined: step kk+1's LDS reads are issued before step kk's math
+            f4 av = *(const f4*)&As[0][ty * 4], bv = *(const f4*)&Bs[0][tx * 4];
+#pragma unroll
+            for (int kk = 0; kk < GK; ++kk) {
+                f4 an = av, bn = bv;
+                if (kk + 1 < GK) {
+                    an = *(const f4*)&As[kk + 1][ty * 4];
+                    bn = *(const f4*)&Bs[kk + 1][tx * 4];
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                mac_v(av, bv, false);
+                av = an;
+                bv = bn;
+            }
+        } else {
+            int kk = 0;
+            if (k0 == 0) {
+                mac(0, true);  // an output's chain starts with its first product
+                kk = 1;
+            }
+#pragma unroll 1
+            for (; kk < kend; ++kk) mac(kk, false);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t m = m0 + ty * 4 + i;
+        if (m >= g.M) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t n = n0 + tx * 4 + j;
+            if (n < g.N) g.C[m * g.ldc + n] = __builtin_amdgcn_ldexpf(finish<V>(s[i][j], bad[i][j]), -fa.k);
+        }
+    }
+}
+
+}  // namespace aps
+
+using namespace aps;
+
+template <int V>
+static void launch_lp_gemm_v(bool kahan, int pm, dim3 grid, hipStream_t s, const GemmArgs& g, const FmtK& fi,
+                             const FmtK& fa) {
+    constexpr bool can_fit = VT<V>::cls != CLS_INT && !VT<V>::m0;
+    constexpr bool can_ldexp = VT<V>::cls != CLS_INT;
+#define APS_G(K, P) hipLaunchKernelGGL((k_lp_gemm<V, K, P>), grid, dim3(BLOCK), 0, s, g, fi, fa)
+    if (pm == GP_FIT) {
+        if constexpr (can_fit) {
+            if (kahan) APS_G(true, GP_FIT); else APS_G(false, GP_FIT);
+            return;
+        }
+    }
+    if (pm == GP_LDEXP) {
+        if constexpr (can_ldexp) {
+            if (kahan) APS_G(true, GP_LDEXP); else APS_G(false, GP_LDEXP);
+            return;
+        }
+    }
+    if (kahan) APS_G(true, GP_SCALED); else APS_G(false, GP_SCALED);
+#undef APS_G
+}
+
+static void launch_lp_gemm(int variant, bool kahan, int pm, dim3 grid, hipStream_t s, const GemmArgs& g,
+                           const FmtK& fi, const FmtK& fa) {
+#define APS_LG(v) \
+    if (variant == (v)) launch_lp_gemm_v<v>(kahan, pm, grid, s, g, fi, fa);
+    APS_FOR_VARIANTS(APS_LG)
+#undef APS_LG
+}
+
+extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t ldb, float* C, int64_t ldc,
+                           int32_t M, int32_t N, int32_t K, aps_format in_fmt, aps_format acc_fmt,
+                           int32_t accumulator, void* stream) {
+    if (M < 0 || N < 0 || K < 0 || M > APS_MAX_GEMM_DIM || N > APS_MAX_GEMM_DIM || K > APS_MAX_GEMM_DIM)
+        return APS_ERR_SIZE;
+    const bool has_out = (int64_t)M * N > 0;
+    if (has_out && (!C || (K > 0 && (!A || !B)))) return APS_ERR_NULL;
+    if (has_out && (ldc < N || (K > 0 && (lda < K || ldb < N)))) return APS_ERR_SIZE;
+    int st = fmt_status(in_fmt);
+    if (st != APS_OK) return st;
+    st = fmt_status(acc_fmt);
+    if (st != APS_OK) return st;
+    if (accumulator != APS_ACC_SEQUENTIAL && accumulator != APS_ACC_KAHAN) return APS_ERR_UNSUPPORTED;
+    // the product of two input values must be exact in fp32, or round to zero anyway
+    const int emin_in = 1 - in_fmt.bias, emin_acc = 1 - acc_fmt.bias;
+    if (in_fmt.m > 11) return APS_ERR_UNSUPPORTED;
+    if (2 * (emin_in - in_fmt.m) < -149 && 2 * (in_fmt.m + 1) > emin_acc - acc_fmt.m + 149) return APS_ERR_UNSUPPORTED;
+    if (!has_out) return APS_OK;
+    const FmtK fi = make_fmtk(in_fmt), fa = make_fmtk(acc_fmt);
+    GemmArgs g{A, B, C, lda, ldb, ldc, M, N, K, 0, 0};
+    // Pre-scale the staged operands by 2^ka and 2^kb (ka + kb = k) when both
+    // stay below 2^128: a value below 2^(emax_in+1) times 2^(127-emax_in) does.
+    const int room = 127 - fi.emax;
+    int pm = GP_LDEXP;
+    if (fa.k <= 2 * room) {
+        g.ka = fa.k < room ? fa.k : room;
+        g.kb = fa.k - g.ka;
+        pm = GP_SCALED;
+        // every product has at most 2(m_in+1) significant bits
+        const int cls = fa.variant <= V_INT_M0 ? CLS_INT : (fa.variant <= V_TOP_M0 ? CLS_TOP : CLS_LOW);
+        if (cls != CLS_INT && acc_fmt.m > 0 && 2 * (in_fmt.m + 1) <= acc_fmt.m + 1) pm = GP_FIT;
+    }
+    const dim3 grid((unsigned)((N + GT - 1) / GT), (unsigned)((M + GT - 1) / GT));
+    launch_lp_gemm(fa.variant, accumulator == APS_ACC_KAHAN, pm, grid, (hipStream_t)stream, g, fi, fa);
+    return launched();
+}

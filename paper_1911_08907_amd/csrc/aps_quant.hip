@@ -1,0 +1,249 @@
+// aps_quant.hip -- scale and cast (Algorithm 1, g * 2^ft then Cast), and
+// cast back and unscale (Cast(low_g, 8, 23), g / 2^ft), with packed codes.
+#include "aps_common.hpp"
+
+namespace aps {
+
+// ======================================================= K3: quantize
+
+struct QuantArgs {
+    const float* X;
+    float* Q;  // may alias X: each element is read before its own store
+    uint8_t* __restrict__ codes;
+    int64_t ld;
+    int32_t W;
+    int32_t code_cls;
+};
+
+template <int V>
+__device__ __forceinline__ void quantize_tail(const QuantArgs& a, const FmtK& f, int64_t j, int64_t end,
+                                           const int32_t ft[4]) {
+#pragma unroll 1
+    for (int64_t r = 0; r < a.W; ++r) {
+        const int64_t off = r * a.ld + j;
+        uint32_t cc[4] = {0, 0, 0, 0};
+        for (int e = 0; e < 4 && j + e < end; ++e) {
+            const float v = quant_native<V>(a.X[off + e], ft[e] + f.k, f);
+            if (a.Q) a.Q[off + e] = v;
+            cc[e] = encode(v, f);
+        }
+        if (a.codes) store_codes4(a.codes + code_byte(r * a.ld, a.code_cls), j, cc, a.code_cls, end);
+    }
+}
+
+// The cast alone does not depend on the accumulator width, so the F32 and F64
+// variants of a class cast alike; the F64 form reads the tie-bit width from the
+// format (1 whenever the F32 form applies).
+__host__ __device__ constexpr int cast_variant(int v) {
+    return v == V_INT_F32 ? V_INT_F64 : (v == V_TOP_F32 ? V_TOP_F64 : (v == V_LOW_F32 ? V_LOW_F64 : v));
+}
+
+// What one k_quantize launch writes per row.
+enum QuantOut { QO_Q = 0, QO_CODES4 = 1, QO_CODES8 = 2, QO_CODES16 = 3, QO_BOTH = 4 };
+
+// One block walks a range of chunks; for each chunk its threads stream all W
+// rows (two register sets of rows in flight), cast each row and store it.
+// The stores of a row are fixed at compile time (OUT): a store that is
+// conditional inside the streamed loop makes the compiler's load-counter
+// waits at the loop's joins far more conservative.
+template <int V, int OUT>
+__global__ __launch_bounds__(BLOCK) void k_quantize(QuantArgs a, Layers ly, Pal pal) {
+    constexpr bool HQ = OUT == QO_Q || OUT == QO_BOTH;
+    constexpr bool HC = OUT != QO_Q;
+    const int64_t nchunks = (ly.n + CH - 1) / CH;
+    int64_t cb, ce;
+    block_range(nchunks, cb, ce);
+    int hint = 0;
+    for (int64_t c = cb; c < ce; ++c) {
+        const int64_t start = c * CH;
+        const int64_t end = min(start + CH, ly.n);
+        const ChunkInfo ci = chunk_layers(ly, start, end, hint);
+        hint = ci.i0;
+        if (ci.mixed) continue;  // handled by k_quantize_mixed
+        const FmtK& f = pal.f[ci.pidx];
+        if (cast_variant(f.variant) != V) continue;
+        const int64_t j = start + (int64_t)threadIdx.x * VEC;
+        if (j >= end) continue;
+        int32_t ft[4];
+        if (ci.i0 == ci.i1) {
+            const int32_t t = ly.scale_exp ? clamp_exp(cld(ly.scale_exp, ci.i0)) : 0;
+            ft[0] = ft[1] = ft[2] = ft[3] = t;
+        } else {
+            elem_scales(ly, ci, j, ft);
+        }
+        if (j + 4 > end) {
+            quantize_tail<V>(a, f, j, end, ft);
+            continue;
+        }
+        const float* p = a.X + j;
+        const int64_t ld = a.ld;
+        const int cls = OUT == QO_CODES4 ? 0 : (OUT == QO_CODES8 ? 1 : (OUT == QO_CODES16 ? 2 : a.code_cls));
+        int64_t r = 0;  // row of the next callback
+        auto row = [&](const f4& x, bool valid) {
+            if (valid) {
+                const f4 v = {quant_native<V>(x.x, ft[0] + f.k, f), quant_native<V>(x.y, ft[1] + f.k, f),
+                              quant_native<V>(x.z, ft[2] + f.k, f), quant_native<V>(x.w, ft[3] + f.k, f)};
+                if constexpr (HQ) __builtin_nontemporal_store(v, (f4*)(a.Q + j + r * ld));
+                if constexpr (HC) {
+                    const uint32_t cc[4] = {encode(v.x, f), encode(v.y, f), encode(v.z, f), encode(v.w, f)};
+                    store_codes4_full(a.codes + code_byte(r * ld, cls), j, cc, cls);
+                }
+            }
+            ++r;
+        };
+        stream_rows(
+            a.W, [&](int rr) { return ld4(p + (int64_t)rr * ld); }, [&]() {}, [&](const f4& x) { row(x, true); }, row);
+    }
+}
+
+
+// Mixed-format chunks, all W rows; grid (boundary, worker); element pairs
+// per thread as in k_sim_reduce_mixed.
+__global__ __launch_bounds__(BLOCK) void k_quantize_mixed(QuantArgs a, Layers ly, Pal pal) {
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    pal_to_lds(pal, spal);
+    int64_t start, end;
+    if (!mixed_chunk_of_boundary(ly, blockIdx.x, start, end)) return;
+    const int64_t w = blockIdx.y;
+    uint8_t* row = a.codes ? a.codes + code_byte(w * a.ld, a.code_cls) : nullptr;
+    for (int64_t j0 = start + 2 * (int64_t)threadIdx.x; j0 < end; j0 += 2 * BLOCK) {
+        uint32_t c[2] = {0, 0};
+        for (int e = 0; e < 2; ++e) {
+            const int64_t j = j0 + e;
+            if (j >= end) break;
+            const int li = find_layer(ly.offsets, ly.L, j, 0);
+            const FmtK& f = spal[ly.fmt_idx[li]];
+            const int32_t ft = ly.scale_exp ? clamp_exp(ly.scale_exp[li]) : 0;
+            const int64_t off = w * a.ld + j;
+            const float v = quant_any(a.X[off], ft + f.k, f);  // Q may alias X: same element
+            if (a.Q) a.Q[off] = v;
+            c[e] = encode(v, f);
+            if (row && a.code_cls != 0) put_code(row, j, c[e], a.code_cls);
+        }
+        if (row && a.code_cls == 0) {
+            uint8_t* pb = row + (j0 >> 1);
+            *pb = (j0 + 1 < end) ? (uint8_t)((c[0] & 15u) | ((c[1] & 15u) << 4))
+                                 : (uint8_t)((*pb & 0xF0u) | (c[0] & 15u));
+        }
+    }
+}
+
+// ===================================================== K5: dequantize
+
+struct DeqArgs {
+    const float* Q;  // may alias out
+    const uint8_t* __restrict__ codes;
+    float* out;
+    int32_t code_cls;
+};
+
+__global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal pal) {
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    pal_to_lds(pal, spal);
+    const int64_t nchunks = (ly.n + CH - 1) / CH;
+    int64_t cb, ce;
+    block_range(nchunks, cb, ce);
+    int hint = 0;
+    for (int64_t c = cb; c < ce; ++c) {
+        const int64_t start = c * CH;
+        const int64_t end = min(start + CH, ly.n);
+        const ChunkInfo ci = chunk_layers(ly, start, end, hint);
+        hint = ci.i0;
+        const int64_t j = start + (int64_t)threadIdx.x * VEC;
+        if (j >= end) continue;
+        if (ci.i0 == ci.i1 && j + 4 <= end) {
+            // one layer: uniform format and exponent, 16-byte accesses
+            const FmtK& f = pal.f[ci.pidx];
+            const int32_t ft = ly.scale_exp ? clamp_exp(cld(ly.scale_exp, ci.i0)) : 0;
+            f4 v;
+            if (a.Q) {
+                v = *(const f4*)(a.Q + j);
+            } else {
+                v.x = decode(load_code(a.codes, j, a.code_cls), f);
+                v.y = decode(load_code(a.codes, j + 1, a.code_cls), f);
+                v.z = decode(load_code(a.codes, j + 2, a.code_cls), f);
+                v.w = decode(load_code(a.codes, j + 3, a.code_cls), f);
+            }
+            const f4 o = {__builtin_amdgcn_ldexpf(v.x, -ft), __builtin_amdgcn_ldexpf(v.y, -ft),
+                          __builtin_amdgcn_ldexpf(v.z, -ft), __builtin_amdgcn_ldexpf(v.w, -ft)};
+            __builtin_nontemporal_store(o, (f4*)(a.out + j));  // out may alias Q: same elements
+            continue;
+        }
+        int li = ci.i0;
+        for (int e = 0; e < 4; ++e) {
+            const int64_t jj = j + e;
+            if (jj >= end) break;
+            while (ly.offsets[li + 1] <= jj) ++li;
+            const FmtK& f = spal[ly.fmt_idx ? ly.fmt_idx[li] : 0];
+            const int32_t ft = ly.scale_exp ? clamp_exp(ly.scale_exp[li]) : 0;
+            const float v = a.Q ? a.Q[jj] : decode(load_code(a.codes, jj, a.code_cls), f);
+            a.out[jj] = __builtin_amdgcn_ldexpf(v, -ft);
+        }
+    }
+}
+
+}  // namespace aps
+
+using namespace aps;
+
+extern "C" int aps_quantize(const float* X, int32_t W, int64_t ld, int64_t n, const int64_t* offsets, int32_t L,
+                            const int32_t* scale_exp, const aps_format* fmts, int32_t n_fmts,
+                            const uint8_t* fmt_idx, float* Q, void* codes, void* stream) {
+    int st = check_rows(X, W, ld, n, offsets, L);
+    if (st != APS_OK) return st;
+    if (!Q && !codes && n > 0) return APS_ERR_NULL;
+    if ((Q && !aligned16(Q)) || (codes && !aligned16(codes))) return APS_ERR_ALIGN;
+    Pal pal;
+    int ccls = 0;
+    st = check_palette(fmts, n_fmts, pal, &ccls);
+    if (st != APS_OK) return st;
+    if (codes && (ccls < 0 || ccls > 2)) return APS_ERR_UNSUPPORTED;
+    if (n == 0) return APS_OK;
+    hipStream_t s = (hipStream_t)stream;
+    Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
+    QuantArgs a{X, Q, (uint8_t*)codes, ld, W, ccls};
+    const int64_t nchunks = (n + CH - 1) / CH;
+    const dim3 grid((unsigned)grid_for(nchunks, BLOCKS_PER_CU));
+    unsigned cm = 0;  // cast variants present
+    for (int i = 0; i < n_fmts; ++i) cm |= 1u << cast_variant(pal.f[i].variant);
+    const int out = !codes ? QO_Q : (Q ? QO_BOTH : QO_CODES4 + ccls);
+#define APS_LAUNCH_Q(v)                                                                                    \
+    if (cm & (1u << (v))) {                                                                                \
+        switch (out) {                                                                                     \
+            case QO_Q: hipLaunchKernelGGL((k_quantize<v, QO_Q>), grid, dim3(BLOCK), 0, s, a, ly, pal); break; \
+            case QO_CODES4: hipLaunchKernelGGL((k_quantize<v, QO_CODES4>), grid, dim3(BLOCK), 0, s, a, ly, pal); break; \
+            case QO_CODES8: hipLaunchKernelGGL((k_quantize<v, QO_CODES8>), grid, dim3(BLOCK), 0, s, a, ly, pal); break; \
+            case QO_CODES16: hipLaunchKernelGGL((k_quantize<v, QO_CODES16>), grid, dim3(BLOCK), 0, s, a, ly, pal); break; \
+            default: hipLaunchKernelGGL((k_quantize<v, QO_BOTH>), grid, dim3(BLOCK), 0, s, a, ly, pal); break; \
+        }                                                                                                  \
+    }
+    APS_LAUNCH_Q(V_INT_F64) APS_LAUNCH_Q(V_INT_EXACT) APS_LAUNCH_Q(V_INT_M0) APS_LAUNCH_Q(V_TOP_F64)
+    APS_LAUNCH_Q(V_TOP_M0) APS_LAUNCH_Q(V_LOW_F64) APS_LAUNCH_Q(V_LOW_M0)
+#undef APS_LAUNCH_Q
+    if (fmt_idx && n_fmts > 1 && L > 1)
+        hipLaunchKernelGGL(k_quantize_mixed, dim3((unsigned)L, (unsigned)W), dim3(BLOCK), 0, s, a, ly, pal);
+    return launched();
+}
+
+extern "C" int aps_dequantize(const float* Q, const void* codes, int64_t n, const int64_t* offsets, int32_t L,
+                              const int32_t* scale_exp, const aps_format* fmts, int32_t n_fmts,
+                              const uint8_t* fmt_idx, float* out, void* stream) {
+    if (!offsets || ((!out || (!Q && !codes)) && n > 0)) return APS_ERR_NULL;
+    if (L < 1 || n < 0 || n > APS_MAX_ELEMS) return APS_ERR_SIZE;
+    if ((Q && !aligned16(Q)) || (codes && !aligned16(codes)) || !aligned16(out)) return APS_ERR_ALIGN;
+    Pal pal;
+    int ccls = 0;
+    int st = check_palette(fmts, n_fmts, pal, &ccls);
+    if (st != APS_OK) return st;
+    if (!Q && (ccls < 0 || ccls > 2)) return APS_ERR_UNSUPPORTED;
+    if (n == 0) return APS_OK;
+    Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
+    DeqArgs a{Q, (const uint8_t*)codes, out, ccls};
+    const int64_t nchunks = (n + CH - 1) / CH;
+    hipLaunchKernelGGL(k_dequantize, dim3((unsigned)grid_for(nchunks, BLOCKS_PER_CU)), dim3(BLOCK), 0, (hipStream_t)stream, a,
+                       ly, pal);
+    return launched();
+}
+
+// Instantiates only the product modes a variant can take: GP_FIT needs the
+// TOP or LOW class with m >= 1; INT-class formats (k = 0) are always scaled.

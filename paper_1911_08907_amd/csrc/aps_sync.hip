@@ -1,0 +1,559 @@
+// aps_sync.hip -- one whole APS synchronisation in one call (Algorithm 1 with
+// the low-precision accumulator of Sec. 5), reading the W workers'
+// gradients once where it can.
+#include "aps_common.hpp"
+
+namespace aps {
+
+// ============================================ K5: one-pass synchronisation
+//
+// A layer's scale 2^ft is known only after the max over every worker and
+// element of the layer, which would make the fused sum a second full read
+// of the W rows.  It need not be.  Power-of-two scaling commutes with
+// rounding to m+1 significant bits (Sec. 3.3.1); only the format's
+// subnormal range and its overflow depend on ft.  So the first pass sums
+// the UNSCALED values, rounding to m+1 significant bits with an unbounded
+// exponent (rho below), while it takes the max.  Once the scales are known,
+// its result is the exact result of the scaled path for every element in
+// which each nonzero input x_k satisfies |x_k| >= T = max(2^(emin - ft),
+// 2^-126), or arrives (k >= 1) when the unscaled partial sum has
+// |s_(k-1)| >= 2^(m+3) * T, in a layer with 0 < N * ghat <= 2^127 (or an
+// all-zero layer), when N = W is a power of two:
+//   * an x with |x| >= T is an fp32 normal, x * 2^ft is exact and in the
+//     format's normal range, so R(x * 2^ft) = 2^ft * rho(x);
+//   * a smaller x casts to at most T * 2^ft scaled (T unscaled), at most a
+//     quarter of the partial sum's smallest gap once |s| >= 2^(m+3) * T,
+//     so both chains leave the sum unchanged;
+//   * partial sums are then multiples of 2^(emin - ft - m): a sum below
+//     2^(emin - ft) is exact both ways, one above rounds the same way both
+//     ways (fp32 add + rho = rho of the exact sum for m <= 10);
+//   * nothing overflows: every |q| <= 2^emax / N, and the worst chain, all
+//     q equal to that bound, counts exactly up to min(N, 2^(m+1)) of them
+//     and then stays (ties to even; m = 0: 1, 2, 4, 4, ...), so every
+//     partial sum stays at or below 2^emax; unscaled, at or below 2^127.
+// The first pass keeps per element one byte: the exponent field of
+// min_k max(|x_k|, |s_(k-1)| * 2^-(m+3)) over the nonzero x_k (the first
+// term alone), less one ulp; it lies below T's exponent whenever the test
+// fails.  The second pass lists the chunks holding such an element (from
+// one byte per 256 elements), then recomputes those elements through the
+// scaled path: one wave per element when few elements of a chunk fail, the
+// whole chunk with the streaming kernel's row walk when many do.
+
+// Zero the layer maxima before pass 1 accumulates them with atomicMax.
+__global__ void k_sync_clear(uint32_t* __restrict__ maxabs, int32_t L) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < L) maxabs[i] = 0u;
+}
+
+// rho: round an fp32 bit pattern to m+1 significant bits, ties to the even
+// significand (m = 0: up, the even multiple of the quantum), exponent
+// unbounded.  lw is the width of the tie bit (1, or 0 when m = 0).
+__device__ __forceinline__ uint32_t rho(uint32_t b, uint32_t half, uint32_t sh, uint32_t lw, uint32_t mask) {
+    return (b + half + __builtin_amdgcn_ubfe(b, sh, lw)) & mask;
+}
+
+// Device view of the caller's workspace (layout in sync_layout()).
+struct SyncWs {
+    uint8_t* __restrict__ minb;  // [round_up(n, CH)] per-element exponent byte
+    uint8_t* __restrict__ wmin;  // [4 per chunk] min of minb over each wave's 256 elements
+    int32_t* __restrict__ thr;   // [L] repair threshold per layer
+    uint32_t* __restrict__ count;  // chunks listed for repair
+    int32_t* __restrict__ list;    // [nchunks] those chunks
+};
+
+struct SyncArgs {
+    const float* __restrict__ G;
+    float* __restrict__ out;
+    int64_t ld;
+    int32_t W;
+};
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+    for (int o = 32; o > 0; o >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, o, 64));
+    return v;
+}
+
+// A thread's finished first-pass results for 4 elements, stored after the
+// next chunk's loads have been issued (see PendingOut); lane 0 of a wave also
+// holds the wave's minimum byte.
+struct PendingSync {
+    f4 o;
+    uint32_t mb;  // the 4 exponent bytes, element j in the low byte
+    uint32_t wb;  // wave minimum (lane 0)
+    int64_t j, lim, c;
+    bool valid;
+};
+
+__device__ __forceinline__ void flush_sync(const SyncArgs& a, const SyncWs& ws, PendingSync& pd) {
+    if (!pd.valid) return;
+    pd.valid = false;
+    const int64_t j = pd.j, lim = pd.lim;
+    if (j + 4 <= lim) {
+        __builtin_nontemporal_store(pd.o, (f4*)(a.out + j));
+    } else {
+        if (j < lim) a.out[j] = pd.o.x;
+        if (j + 1 < lim) a.out[j + 1] = pd.o.y;
+        if (j + 2 < lim) a.out[j + 2] = pd.o.z;
+    }
+    // the byte array is padded to whole chunks: a full word is always in bounds
+    __builtin_nontemporal_store(pd.mb, (uint32_t*)(ws.minb + j));
+    if ((threadIdx.x & 63) == 0) ws.wmin[pd.c * 4 + (threadIdx.x >> 6)] = (uint8_t)pd.wb;
+}
+
+__global__ __launch_bounds__(BLOCK) void k_sync_spec(SyncArgs a, SyncWs ws, Layers ly, Pal pal,
+                                                    uint32_t* __restrict__ maxabs) {
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    __shared__ uint32_t red[BLOCK / 64];
+    pal_to_lds(pal, spal);
+    const int64_t nchunks = (ly.n + CH - 1) / CH;
+    int64_t cb, ce;
+    block_range(nchunks, cb, ce);
+    int hint = 0;
+    uint32_t run = 0;  // running max of layer run_layer (chunks inside one layer)
+    int run_layer = -1;
+    PendingSync pd;
+    pd.valid = false;
+    const f4 neg0 = {-0.0f, -0.0f, -0.0f, -0.0f};
+    for (int64_t c = cb; c < ce; ++c) {
+        const int64_t start = c * CH;
+        const int64_t end = min(start + CH, ly.n);
+        const ChunkInfo ci = chunk_layers(ly, start, end, hint);
+        hint = ci.i0;
+        const int64_t j = start + (int64_t)threadIdx.x * VEC;
+        uint32_t mx0 = 0, mx1 = 0, mx2 = 0, mx3 = 0;
+        uint32_t tmin = 255u;  // this thread's smallest exponent byte
+        if (j < end) {
+            uint32_t hf[4], sh[4], lw[4], mk[4];
+            float sc[4];  // 2^-(m+3)
+            if (!ci.mixed) {
+                const FmtK& f = pal.f[ci.pidx];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    hf[e] = f.half;
+                    sh[e] = f.sh;
+                    lw[e] = f.lsbw;
+                    mk[e] = f.mask;
+                    sc[e] = u2f((uint32_t)(124 - f.m) << 23);
+                }
+            } else {
+                int li = ci.i0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    while (li < ci.i1 && ly.offsets[li + 1] <= j + e) ++li;
+                    const FmtK& f = spal[ly.fmt_idx[li]];
+                    hf[e] = f.half;
+                    sh[e] = f.sh;
+                    lw[e] = f.lsbw;
+                    mk[e] = f.mask;
+                    sc[e] = u2f((uint32_t)(124 - f.m) << 23);
+                }
+            }
+            uint32_t mn0, mn1, mn2, mn3;
+            float s0, s1, s2, s3;
+            const float* p = a.G + j;
+            const int64_t ld = a.ld;
+            stream_rows(
+                a.W, [&](int r) { return ld4(p + (int64_t)r * ld); },
+                [&]() { flush_sync(a, ws, pd); },
+                [&](const f4& x) {
+                    const uint32_t b0 = f2u(x.x), b1 = f2u(x.y), b2 = f2u(x.z), b3 = f2u(x.w);
+                    mx0 = b0 & 0x7FFFFFFFu;
+                    mx1 = b1 & 0x7FFFFFFFu;
+                    mx2 = b2 & 0x7FFFFFFFu;
+                    mx3 = b3 & 0x7FFFFFFFu;
+                    mn0 = mx0 - 1u;  // a zero wraps to the top and never wins the min
+                    mn1 = mx1 - 1u;
+                    mn2 = mx2 - 1u;
+                    mn3 = mx3 - 1u;
+                    s0 = u2f(rho(b0, hf[0], sh[0], lw[0], mk[0]));
+                    s1 = u2f(rho(b1, hf[1], sh[1], lw[1], mk[1]));
+                    s2 = u2f(rho(b2, hf[2], sh[2], lw[2], mk[2]));
+                    s3 = u2f(rho(b3, hf[3], sh[3], lw[3], mk[3]));
+                },
+                [&](const f4& r, bool valid) {
+                    // a row past the last one counts as -0: no change to any of the four
+                    const f4 v = valid ? r : neg0;
+                    const uint32_t b0 = f2u(v.x), b1 = f2u(v.y), b2 = f2u(v.z), b3 = f2u(v.w);
+                    const uint32_t a0 = b0 & 0x7FFFFFFFu, a1 = b1 & 0x7FFFFFFFu;
+                    const uint32_t a2 = b2 & 0x7FFFFFFFu, a3 = b3 & 0x7FFFFFFFu;
+                    mx0 = max(mx0, a0);
+                    mx1 = max(mx1, a1);
+                    mx2 = max(mx2, a2);
+                    mx3 = max(mx3, a3);
+                    // the term's magnitude, or the sum it meets scaled down by 2^(m+3)
+                    mn0 = min(mn0, max(a0 - 1u, f2u(u2f(f2u(s0) & 0x7FFFFFFFu) * sc[0])));
+                    mn1 = min(mn1, max(a1 - 1u, f2u(u2f(f2u(s1) & 0x7FFFFFFFu) * sc[1])));
+                    mn2 = min(mn2, max(a2 - 1u, f2u(u2f(f2u(s2) & 0x7FFFFFFFu) * sc[2])));
+                    mn3 = min(mn3, max(a3 - 1u, f2u(u2f(f2u(s3) & 0x7FFFFFFFu) * sc[3])));
+                    s0 = u2f(rho(f2u(s0 + u2f(rho(b0, hf[0], sh[0], lw[0], mk[0]))), hf[0], sh[0], lw[0], mk[0]));
+                    s1 = u2f(rho(f2u(s1 + u2f(rho(b1, hf[1], sh[1], lw[1], mk[1]))), hf[1], sh[1], lw[1], mk[1]));
+                    s2 = u2f(rho(f2u(s2 + u2f(rho(b2, hf[2], sh[2], lw[2], mk[2]))), hf[2], sh[2], lw[2], mk[2]));
+                    s3 = u2f(rho(f2u(s3 + u2f(rho(b3, hf[3], sh[3], lw[3], mk[3]))), hf[3], sh[3], lw[3], mk[3]));
+                });
+            const uint32_t e0 = min(mn0 >> 23, 255u), e1 = min(mn1 >> 23, 255u);
+            const uint32_t e2 = min(mn2 >> 23, 255u), e3 = min(mn3 >> 23, 255u);
+            pd.o.x = s0;
+            pd.o.y = s1;
+            pd.o.z = s2;
+            pd.o.w = s3;
+            pd.mb = e0 | (e1 << 8) | (e2 << 16) | (e3 << 24);
+            pd.j = j;
+            pd.lim = end;
+            pd.c = c;
+            pd.valid = true;
+            // elements past the end of the gradient (row padding) do not count
+            tmin = e0;
+            if (j + 1 < end) tmin = min(tmin, e1); else mx1 = 0;
+            if (j + 2 < end) tmin = min(tmin, e2); else mx2 = 0;
+            if (j + 3 < end) tmin = min(tmin, e3); else mx3 = 0;
+        }
+        // every lane of the wave takes part; lane 0 has the wave's first
+        // element, so its pending record exists whenever the wave has one
+        pd.wb = wave_min_u32(tmin);
+        if (ci.i0 == ci.i1) {
+            const uint32_t v = max(max(mx0, mx1), max(mx2, mx3));
+            if (ci.i0 != run_layer) {
+                if (run_layer >= 0) block_max_atomic(run, maxabs + run_layer, red);
+                run_layer = ci.i0;
+                run = 0;
+            }
+            run = max(run, v);
+        } else {
+            const uint32_t mv[4] = {mx0, mx1, mx2, mx3};
+            for (int li = ci.i0; li <= ci.i1; ++li) {
+                const int64_t lo = cld(ly.offsets, li), hi = cld(ly.offsets, li + 1);
+                uint32_t v = 0;
+                if (j < end)
+                    for (int e = 0; e < 4; ++e)
+                        if (j + e >= lo && j + e < hi) v = max(v, mv[e]);
+                block_max_atomic(v, maxabs + li, red);
+            }
+        }
+    }
+    if (run_layer >= 0) block_max_atomic(run, maxabs + run_layer, red);
+    flush_sync(a, ws, pd);
+}
+
+// Scale exponents (as k_scales) and the per-layer repair threshold: an
+// element is recomputed when its exponent byte is below thr[i].  thr = 256
+// recomputes the whole layer (ghat INF/NaN, N * ghat = INF or above 2^127);
+// an all-zero layer needs nothing.  Also clears the repair list.
+__global__ void k_sync_layers(const uint32_t* __restrict__ maxabs, int32_t L, int32_t N, Pal pal,
+                              const uint8_t* __restrict__ fmt_idx, int32_t* __restrict__ scale_exp, SyncWs ws) {
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    pal_to_lds(pal, spal);
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i == 0) *ws.count = 0u;
+    if (i >= L) return;
+    const FmtK& f = spal[fmt_idx ? fmt_idx[i] : 0];
+    const uint32_t gb = maxabs[i] & 0x7FFFFFFFu;
+    int32_t r = 0, th = 256;
+    if (gb == 0) {
+        th = 0;
+    } else if (gb < 0x7F800000u) {
+        const float t = (float)N * u2f(gb);
+        const uint32_t tb = f2u(t);
+        if (tb < 0x7F800000u) {
+            const int cl = ceil_log2_bits(tb);
+            r = f.emax - cl;
+            // smallest safe nonzero magnitude: 2^max(emin - ft, -126), as an exponent field
+            if (cl <= 127) th = max(f.emin - r + 127, 1);
+        }
+    }
+    scale_exp[i] = r;
+    ws.thr[i] = th;
+}
+
+// Largest i in [0, L-1] with offsets[i] <= pos, for pos < n (per lane).
+__device__ __forceinline__ int layer_of(const int64_t* __restrict__ off, int L, int64_t pos) {
+    int lo = 0, hi = L;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (off[mid] <= pos) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+// One thread per chunk: list the chunks (single palette entry) holding an
+// element whose byte is below its layer's threshold.  The test is on the
+// chunk's minimum byte against the largest threshold among its layers, so
+// it never misses one; the repair looks at each element.
+__global__ void k_sync_scan(Layers ly, SyncWs ws) {
+    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t nchunks = (ly.n + CH - 1) / CH;
+    if (c >= nchunks) return;
+    const int64_t start = c * CH;
+    const int64_t end = min(start + CH, ly.n);
+    const uint32_t w4 = *(const uint32_t*)(ws.wmin + 4 * c);
+    uint32_t cm = 255u;
+    for (int wv = 0; wv < 4; ++wv)
+        if (start + 256 * wv < end) cm = min(cm, (w4 >> (8 * wv)) & 0xFFu);
+    const int i0 = layer_of(ly.offsets, ly.L, start), i1 = layer_of(ly.offsets, ly.L, end - 1);
+    int32_t th = 0;
+    bool mixed = false;
+    const int p0 = ly.fmt_idx ? ly.fmt_idx[i0] : 0;
+    for (int i = i0; i <= i1; ++i) {
+        if (ly.offsets[i] == ly.offsets[i + 1]) continue;  // empty layer
+        th = max(th, ws.thr[i]);
+        if (ly.fmt_idx && ly.fmt_idx[i] != p0) mixed = true;
+    }
+    if (!mixed && (int32_t)cm < th) ws.list[atomicAdd(ws.count, 1u)] = (int32_t)c;
+}
+
+constexpr int SPARSE_MAX = 16;  // flagged elements per chunk repaired one wave each
+
+// The exact scaled path for one element, run by a whole wave: each lane
+// loads and casts a different worker's value, then every lane walks the
+// casts in worker order (one readlane per add) and lane 0 stores.
+template <int V>
+__device__ void repair_one(const ReduceArgs& a, const FmtK& f, int64_t j, int F) {
+    const int lane = threadIdx.x & 63;
+    const float* p = a.G + j;
+    bool badl = false, bads = false;
+    float s = 0.0f;
+    for (int base = 0; base < a.W; base += 256) {
+        float q[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int r = base + 64 * u + lane;
+            q[u] = quant<V>(r < a.W ? p[(int64_t)r * a.ld] : -0.0f, F, f, badl);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int r0 = base + 64 * u;
+            const int cnt = min(64, a.W - r0);
+            for (int t = 0; t < cnt; ++t) {
+                const float qt = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(q[u]), t));
+                if (r0 + t == 0)
+                    s = qt;
+                else
+                    s = accum<V>(s, qt, f, bads);
+            }
+        }
+    }
+    const bool bad = bads || (__ballot(badl) != 0);
+    s = finish<V>(s, bad);
+    if (lane == 0) a.out[j] = __builtin_amdgcn_ldexpf(s, -F);
+}
+
+// Second pass over the listed chunks of one variant's format, one wave per
+// chunk: find the flagged elements (16 bytes per lane), then repair them one
+// after another (at most SPARSE_MAX), or rerun the whole chunk through the
+// streaming row walk, a quarter at a time.  Waves stride over the list; its
+// length is read on the device.
+template <int V>
+__global__ __launch_bounds__(BLOCK) void k_sync_repair(ReduceArgs a, Layers ly, Pal pal, SyncWs ws) {
+    const uint32_t total = *ws.count;
+    const int lane = threadIdx.x & 63;
+    const int64_t nw = (int64_t)gridDim.x * (BLOCK / 64);
+    for (int64_t k = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * (BLOCK / 64) + (threadIdx.x >> 6))); k < total;
+         k += nw) {
+        const int64_t start = (int64_t)cld(ws.list, k) * CH;
+        const int64_t end = min(start + CH, ly.n);
+        const ChunkInfo ci = chunk_layers(ly, start, end, 0);
+        const FmtK& f = pal.f[ci.pidx];
+        if (f.variant != V) continue;  // another launch owns this format
+        // 16 consecutive elements per lane; the byte array is padded to whole chunks
+        const int64_t j0 = start + 16 * lane;
+        const u4v w = *(const u4v*)(ws.minb + j0);
+        uint32_t mask = 0;
+        if (ci.i0 == ci.i1) {  // one layer: one threshold, read once
+            const int32_t th = cld(ws.thr, ci.i0);
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const uint32_t byte = (w[e >> 2] >> (8 * (e & 3))) & 0xFFu;
+                if ((int32_t)byte < th && j0 + e < end) mask |= 1u << e;
+            }
+        } else {
+            int li = ci.i0;
+            int64_t next = ly.offsets[li + 1];
+            int32_t th = ws.thr[li];
+            for (int e = 0; e < 16; ++e) {
+                const int64_t jj = j0 + e;
+                if (jj >= end) break;
+                while (li < ci.i1 && next <= jj) {
+                    ++li;
+                    next = ly.offsets[li + 1];
+                    th = ws.thr[li];
+                }
+                const uint32_t byte = (w[e >> 2] >> (8 * (e & 3))) & 0xFFu;
+                if ((int32_t)byte < th) mask |= 1u << e;
+            }
+        }
+        int cnt = __builtin_popcount(mask);
+        for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+        if (cnt > SPARSE_MAX) {
+#pragma unroll 1
+            for (int qtr = 0; qtr < 4; ++qtr) {
+                const int64_t j = start + (int64_t)qtr * 256 + 4 * lane;
+                if (j >= end) continue;
+                int32_t ft[4];
+                if (ci.i0 == ci.i1) {
+                    const int32_t t = clamp_exp(cld(ly.scale_exp, ci.i0));
+                    ft[0] = ft[1] = ft[2] = ft[3] = t;
+                } else {
+                    elem_scales(ly, ci, j, ft);
+                }
+                PendingOut pd;
+                pd.valid = false;
+                reduce_vec<V>(a, f, j, end, ft, pd);
+                flush_out(a, pd);
+            }
+        } else {
+            uint64_t lanes = __ballot(mask != 0);
+            while (lanes) {
+                const int l = __builtin_ctzll(lanes);
+                lanes &= lanes - 1;
+                uint32_t m = (uint32_t)__builtin_amdgcn_readlane((int)mask, l);
+                while (m) {
+                    const int e = __builtin_ctz(m);
+                    m &= m - 1;
+                    const int64_t jj = start + 16 * l + e;
+                    const int lj = find_layer(ly.offsets, ly.L, jj, ci.i0);
+                    repair_one<V>(a, f, jj, clamp_exp(cld(ly.scale_exp, lj)) + f.k);
+                }
+            }
+        }
+    }
+}
+
+// Flagged elements of chunks that mix palette entries, element by element.
+__global__ __launch_bounds__(BLOCK) void k_sync_repair_mixed(ReduceArgs a, Layers ly, Pal pal, SyncWs ws) {
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    pal_to_lds(pal, spal);
+    int64_t start, end;
+    if (!mixed_chunk_of_boundary(ly, blockIdx.x, start, end)) return;
+    for (int64_t j = start + threadIdx.x; j < end; j += BLOCK) {
+        const int li = find_layer(ly.offsets, ly.L, j, 0);
+        if ((int32_t)ws.minb[j] >= ws.thr[li]) continue;
+        const FmtK& f = spal[ly.fmt_idx[li]];
+        const int F = clamp_exp(ly.scale_exp[li]) + f.k;
+        a.out[j] = __builtin_amdgcn_ldexpf(reduce_elem_any(a, f, j, F), -F);
+    }
+}
+
+}  // namespace aps
+
+using namespace aps;
+
+// Workspace of aps_sync, in 256-byte aligned parts: the per-element exponent
+// bytes (padded to whole chunks), four bytes per chunk, the int32 layer
+// thresholds, the list counter, the int32 chunk list.
+struct SyncLayout {
+    uint64_t minb, wmin, thr, count, list, total;
+};
+
+static uint64_t up256(uint64_t b) { return (b + 255u) & ~(uint64_t)255u; }
+
+static SyncLayout sync_layout(int64_t n, int32_t L) {
+    const uint64_t nch = (uint64_t)((n + CH - 1) / CH);
+    SyncLayout o;
+    o.minb = 0;
+    o.wmin = o.minb + up256(nch * (uint64_t)CH);
+    o.thr = o.wmin + up256(4u * nch);
+    o.count = o.thr + up256(4u * (uint64_t)L);
+    o.list = o.count + 256u;
+    o.total = o.list + up256(4u * nch);
+    return o;
+}
+
+extern "C" uint64_t aps_sync_workspace_bytes(int64_t n, int32_t L) {
+    if (n < 0 || L < 0 || n > APS_MAX_ELEMS) return 0;
+    return sync_layout(n, L).total;
+}
+
+// Which route aps_sync takes.  The one-pass route applies when N = W is a
+// power of two (exact N * ghat, no overflow) and every format has m <= 10
+// (an fp32 add then one rounding equals rounding the exact sum).  Without a
+// route flag it is taken when it is also expected to pay: for layers of
+// normally distributed values (max about 5 sigma) the threshold sits at
+// W * 2^(emin - emax) of the layer's max, each input falls below it with
+// probability about W * 2^(emin - emax + 2), and an element is recomputed
+// with probability up to W^2 * 2^(emin - emax + 2); above 2^-7 most chunks
+// would be recomputed and two passes cost less.
+static bool sync_one_pass(int32_t W, const Pal& pal, int32_t n_fmts, uint32_t flags) {
+    if (flags & APS_SYNC_TWO_PASS) return false;
+    if (W & (W - 1)) return false;
+    int lw = 0;
+    while ((1 << lw) < W) ++lw;
+    for (int i = 0; i < n_fmts; ++i) {
+        if (pal.f[i].m > 10) return false;
+        if (!(flags & APS_SYNC_ONE_PASS) && 2 * lw + pal.f[i].emin - pal.f[i].emax + 2 > -7) return false;
+    }
+    return true;
+}
+
+extern "C" int aps_sync_one_pass(int32_t W, const aps_format* fmts, int32_t n_fmts, uint32_t flags) {
+    if (W < 1 || W > APS_MAX_WORKERS) return APS_ERR_SIZE;
+    if ((flags & APS_SYNC_ONE_PASS) && (flags & APS_SYNC_TWO_PASS)) return APS_ERR_UNSUPPORTED;
+    Pal pal;
+    const int st = check_palette(fmts, n_fmts, pal, nullptr);
+    if (st != APS_OK) return st;
+    return sync_one_pass(W, pal, n_fmts, flags) ? 1 : 0;
+}
+
+extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const int64_t* offsets, int32_t L,
+                        const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx, uint32_t flags,
+                        uint32_t* maxabs_bits, int32_t* scale_exp, float* out, void* workspace,
+                        uint64_t workspace_bytes, void* stream) {
+    int st = check_rows(G, W, ld, n, offsets, L);
+    if (st != APS_OK) return st;
+    if (!maxabs_bits || !scale_exp || !workspace || (!out && n > 0)) return APS_ERR_NULL;
+    const uint32_t phases = flags & (APS_SYNC_PASS1 | APS_SYNC_PASS2);
+    if (phases == 0 || (flags & ~(APS_SYNC_PASS1 | APS_SYNC_PASS2 | APS_SYNC_ONE_PASS | APS_SYNC_TWO_PASS)) ||
+        ((flags & APS_SYNC_ONE_PASS) && (flags & APS_SYNC_TWO_PASS)))
+        return APS_ERR_UNSUPPORTED;
+    if ((out && !aligned16(out)) || ((uintptr_t)workspace & 255u)) return APS_ERR_ALIGN;
+    const SyncLayout lay = sync_layout(n, L);
+    if (workspace_bytes < lay.total) return APS_ERR_SIZE;
+    Pal pal;
+    st = check_palette(fmts, n_fmts, pal, nullptr);
+    if (st != APS_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t nchunks = (n + CH - 1) / CH;
+    uint8_t* wb = (uint8_t*)workspace;
+    SyncWs ws{wb + lay.minb, wb + lay.wmin, (int32_t*)(wb + lay.thr), (uint32_t*)(wb + lay.count),
+              (int32_t*)(wb + lay.list)};
+    Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
+    const bool one = sync_one_pass(W, pal, n_fmts, flags);
+    if (!one) {
+        // two passes: exactly the three calls of the step
+        if (phases & APS_SYNC_PASS1) {
+            st = aps_layer_maxabs(G, W, ld, n, offsets, L, maxabs_bits, stream);
+            if (st != APS_OK) return st;
+        }
+        if (phases & APS_SYNC_PASS2) {
+            st = aps_layer_scales(maxabs_bits, L, W, fmts, n_fmts, fmt_idx, scale_exp, stream);
+            if (st != APS_OK) return st;
+            st = aps_sim_reduce(G, W, ld, n, offsets, L, scale_exp, fmts, n_fmts, fmt_idx, 0u, out, nullptr, stream);
+            if (st != APS_OK) return st;
+        }
+        return APS_OK;
+    }
+    const dim3 lgrid((unsigned)((L + 255) / 256));
+    const bool mixed = fmt_idx && n_fmts > 1 && L > 1;
+    if (phases & APS_SYNC_PASS1) {
+        hipLaunchKernelGGL(k_sync_clear, lgrid, dim3(256), 0, s, maxabs_bits, L);
+        if (n > 0) {
+            SyncArgs sa{G, out, ld, W};
+            hipLaunchKernelGGL(k_sync_spec, dim3((unsigned)grid_for(nchunks, BLOCKS_PER_CU)), dim3(BLOCK), 0, s, sa, ws,
+                               ly, pal, maxabs_bits);
+        }
+    }
+    if (phases & APS_SYNC_PASS2) {
+        hipLaunchKernelGGL(k_sync_layers, lgrid, dim3(256), 0, s, maxabs_bits, L, W, pal, fmt_idx, scale_exp, ws);
+        if (n > 0) {
+            hipLaunchKernelGGL(k_sync_scan, dim3((unsigned)((nchunks + 255) / 256)), dim3(256), 0, s, ly, ws);
+            ReduceArgs a{G, out, nullptr, ld, W, 0u, 0};
+            const unsigned vm = variant_mask(pal, n_fmts);
+            const dim3 grid((unsigned)grid_for(nchunks, BLOCKS_PER_CU));
+#define APS_LAUNCH_S(v) \
+    if (vm & (1u << (v))) hipLaunchKernelGGL(k_sync_repair<v>, grid, dim3(BLOCK), 0, s, a, ly, pal, ws);
+            APS_LAUNCH_S(V_INT_F32) APS_LAUNCH_S(V_INT_M0) APS_LAUNCH_S(V_TOP_F32) APS_LAUNCH_S(V_TOP_M0)
+            APS_LAUNCH_S(V_LOW_F32) APS_LAUNCH_S(V_LOW_M0)
+#undef APS_LAUNCH_S
+            if (mixed) hipLaunchKernelGGL(k_sync_repair_mixed, dim3((unsigned)L), dim3(BLOCK), 0, s, a, ly, pal, ws);
+        }
+    }
+    return launched();
+}
