@@ -111,7 +111,9 @@ __global__ __launch_bounds__(BLOCK) void k_sim_reduce_ex(ReduceArgs a, Layers ly
         const ChunkInfo ci = chunk_layers(ly, start, end, hint);
         hint = ci.i0;
         const int64_t seg = ring_segment(start, ly.n, od.ng);
-        if (ci.mixed || seg != ring_segment(end - 1, ly.n, od.ng)) continue;  // k_sim_reduce_ex_slow
+        // chunks that mix palette entries: k_sim_reduce_ex_slow; chunks that
+        // cross ring segments: k_sim_reduce_ex_cross
+        if (ci.mixed || seg != ring_segment(end - 1, ly.n, od.ng)) continue;
         const FmtK& f = pal.f[ci.pidx];
         if (f.variant != V) continue;
         const int64_t j = start + (int64_t)threadIdx.x * VEC;
@@ -126,6 +128,60 @@ __global__ __launch_bounds__(BLOCK) void k_sim_reduce_ex(ReduceArgs a, Layers ly
         reduce_vec_ex<V, KAHAN>(a, f, j, end, ft, (int)seg, od, pd);
     }
     flush_out(a, pd);
+}
+
+// Chunks of one palette entry that cross ring segments, one block per
+// segment boundary (the block of the first boundary inside a chunk owns it):
+// one row walk per segment the chunk touches; after each, the elements of
+// that segment are stored at once (a thread owns both nibbles of its code
+// bytes, so the read-modify-writes of a byte split between segments come in
+// program order).  A kernel of its own, so that the usual chunk keeps the
+// register footprint of a single walk.
+template <int V, bool KAHAN>
+__global__ __launch_bounds__(BLOCK) void k_sim_reduce_ex_cross(ReduceArgs a, Layers ly, Pal pal, Order od) {
+    const int64_t s1 = (int64_t)blockIdx.x + 1;                // boundary: first element of segment s1
+    const int64_t p = (s1 * ly.n + od.ng - 1) / od.ng;
+    if (p <= 0 || p >= ly.n || p % CH == 0) return;           // at a chunk edge: nothing crosses
+    const int64_t start = p / CH * CH;
+    if (s1 > 1 && ((s1 - 1) * ly.n + od.ng - 1) / od.ng > start) return;  // an earlier boundary owns it
+    const int64_t end = min(start + CH, ly.n);
+    const ChunkInfo ci = chunk_layers(ly, start, end, 0);
+    if (ci.mixed) return;  // k_sim_reduce_ex_slow
+    const FmtK& f = pal.f[ci.pidx];
+    if (f.variant != V) return;
+    const int64_t j = start + (int64_t)threadIdx.x * VEC;
+    if (j >= end) return;
+    int32_t ft[4];
+    if (ci.i0 == ci.i1) {
+        const int32_t t = ly.scale_exp ? clamp_exp(cld(ly.scale_exp, ci.i0)) : 0;
+        ft[0] = ft[1] = ft[2] = ft[3] = t;
+    } else {
+        elem_scales(ly, ci, j, ft);
+    }
+    const int64_t seg_last = ring_segment(end - 1, ly.n, od.ng);
+    for (int64_t sg = ring_segment(start, ly.n, od.ng); sg <= seg_last; ++sg) {
+        PendingOut part;
+        part.valid = false;
+        reduce_vec_ex<V, KAHAN>(a, f, j, end, ft, (int)sg, od, part);
+        // segment sg holds the elements i with floor(i * ng / n) = sg
+        const int64_t lo = (sg * ly.n + od.ng - 1) / od.ng;
+        const int64_t hi = min(((sg + 1) * ly.n + od.ng - 1) / od.ng, end);
+        const float po[4] = {part.o.x, part.o.y, part.o.z, part.o.w};
+        for (int e = 0; e < 4; ++e) {
+            const int64_t jj = j + e;
+            if (jj < lo || jj >= hi) continue;
+            if (a.out) a.out[jj] = po[e];
+            if (a.codes) {
+                if (a.code_cls == 0) {
+                    uint8_t* pb = a.codes + (jj >> 1);
+                    *pb = (jj & 1) ? (uint8_t)((*pb & 0x0Fu) | ((part.c[e] & 15u) << 4))
+                                   : (uint8_t)((*pb & 0xF0u) | (part.c[e] & 15u));
+                } else {
+                    put_code(a.codes, jj, part.c[e], a.code_cls);
+                }
+            }
+        }
+    }
 }
 
 // One element through the whole ordered chain, any variant.
@@ -162,9 +218,9 @@ __device__ float reduce_elem_ex_any(const ReduceArgs& a, const FmtK& f, int64_t 
     }
 }
 
-// Chunks that mix palette entries or cross a ring-segment boundary, one block
-// per chunk (blocks of other chunks return at once); element pairs per
-// thread so that a byte of nibble codes has one writer.
+// Chunks that mix palette entries, one block per chunk (blocks of other
+// chunks return at once); element pairs per thread so that a byte of nibble
+// codes has one writer.
 template <bool KAHAN>
 __global__ __launch_bounds__(BLOCK) void k_sim_reduce_ex_slow(ReduceArgs a, Layers ly, Pal pal, Order od) {
     __shared__ FmtK spal[APS_MAX_FORMATS];
@@ -173,7 +229,7 @@ __global__ __launch_bounds__(BLOCK) void k_sim_reduce_ex_slow(ReduceArgs a, Laye
     if (start >= ly.n) return;
     const int64_t end = min(start + CH, ly.n);
     const ChunkInfo ci = chunk_layers(ly, start, end, 0);
-    if (!ci.mixed && ring_segment(start, ly.n, od.ng) == ring_segment(end - 1, ly.n, od.ng)) return;
+    if (!ci.mixed) return;
     for (int64_t j0 = start + 2 * (int64_t)threadIdx.x; j0 < end; j0 += 2 * BLOCK) {
         uint32_t cd[2] = {0, 0};
         for (int e = 0; e < 2; ++e) {
@@ -234,18 +290,26 @@ extern "C" int aps_sim_reduce_ex(const float* G, int32_t W, int64_t ld, int64_t 
     const int64_t nchunks = (n + CH - 1) / CH;
     const dim3 grid((unsigned)grid_for(nchunks, BLOCKS_PER_CU));
     const unsigned vm = variant_mask(pal, n_fmts);
-#define APS_LAUNCH_X(v)                                                                                   \
-    if (vm & (1u << (v))) {                                                                               \
-        if (acc == APS_ACC_KAHAN)                                                                         \
-            hipLaunchKernelGGL((k_sim_reduce_ex<v, true>), grid, dim3(BLOCK), 0, s, a, ly, pal, od);     \
-        else                                                                                              \
-            hipLaunchKernelGGL((k_sim_reduce_ex<v, false>), grid, dim3(BLOCK), 0, s, a, ly, pal, od);    \
+    const dim3 bgrid((unsigned)(od.ng > 1 ? od.ng - 1 : 1));  // one block per ring-segment boundary
+#define APS_LAUNCH_X(v)                                                                                     \
+    if (vm & (1u << (v))) {                                                                                 \
+        if (acc == APS_ACC_KAHAN) {                                                                         \
+            hipLaunchKernelGGL((k_sim_reduce_ex<v, true>), grid, dim3(BLOCK), 0, s, a, ly, pal, od);       \
+            if (od.ng > 1)                                                                                  \
+                hipLaunchKernelGGL((k_sim_reduce_ex_cross<v, true>), bgrid, dim3(BLOCK), 0, s, a, ly, pal, od); \
+        } else {                                                                                            \
+            hipLaunchKernelGGL((k_sim_reduce_ex<v, false>), grid, dim3(BLOCK), 0, s, a, ly, pal, od);      \
+            if (od.ng > 1)                                                                                  \
+                hipLaunchKernelGGL((k_sim_reduce_ex_cross<v, false>), bgrid, dim3(BLOCK), 0, s, a, ly, pal, od); \
+        }                                                                                                   \
     }
     APS_FOR_VARIANTS(APS_LAUNCH_X)
 #undef APS_LAUNCH_X
-    if (acc == APS_ACC_KAHAN)
-        hipLaunchKernelGGL(k_sim_reduce_ex_slow<true>, dim3((unsigned)nchunks), dim3(BLOCK), 0, s, a, ly, pal, od);
-    else
-        hipLaunchKernelGGL(k_sim_reduce_ex_slow<false>, dim3((unsigned)nchunks), dim3(BLOCK), 0, s, a, ly, pal, od);
+    if (fmt_idx && n_fmts > 1 && L > 1) {  // chunks that mix palette entries
+        if (acc == APS_ACC_KAHAN)
+            hipLaunchKernelGGL(k_sim_reduce_ex_slow<true>, dim3((unsigned)nchunks), dim3(BLOCK), 0, s, a, ly, pal, od);
+        else
+            hipLaunchKernelGGL(k_sim_reduce_ex_slow<false>, dim3((unsigned)nchunks), dim3(BLOCK), 0, s, a, ly, pal, od);
+    }
     return launched();
 }

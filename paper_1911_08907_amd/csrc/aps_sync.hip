@@ -536,8 +536,11 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
         hipLaunchKernelGGL(k_sync_clear, lgrid, dim3(256), 0, s, maxabs_bits, L);
         if (n > 0) {
             SyncArgs sa{G, out, ld, W};
-            hipLaunchKernelGGL(k_sync_spec, dim3((unsigned)grid_for(nchunks, BLOCKS_PER_CU)), dim3(BLOCK), 0, s, sa, ws,
-                               ly, pal, maxabs_bits);
+            // launch width measured on MI355X: 24 blocks per CU for many rows,
+            // 32 when each chunk is only a few rows (shorter work per chunk)
+            const int per_cu = W >= 64 ? 24 : 32;
+            hipLaunchKernelGGL(k_sync_spec, dim3((unsigned)grid_for(nchunks, per_cu)), dim3(BLOCK), 0, s, sa, ws, ly,
+                               pal, maxabs_bits);
         }
     }
     if (phases & APS_SYNC_PASS2) {

@@ -244,6 +244,8 @@ def test_sync_validation(lib):
     assert call(ws=P(4096 + 128)) == A.APS_ERR_ALIGN       # workspace needs 256-byte alignment
     assert call(wsb=ws - 1) == A.APS_ERR_SIZE
     assert call(W=0) == A.APS_ERR_SIZE
+    assert call(W=(1 << 24) + 1) == A.APS_ERR_SIZE
+    assert call(n=(1 << 30) + 4, ld=(1 << 30) + 4) == A.APS_ERR_SIZE   # above APS_MAX_ELEMS
     assert call(pal=_pal(A.Format(9, 2))) == A.APS_ERR_FORMAT
     assert call(nf=0) == A.APS_ERR_SIZE
 

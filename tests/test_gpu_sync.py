@@ -272,3 +272,62 @@ def test_sync_config_large(dev, name, palette):
     assert bool(torch.isfinite(out).all())
     del G_t, gs
     torch.cuda.empty_cache()
+
+
+# --------------------------------------------------------- maximum sizes
+
+class _Set:
+    """The fields of a generated gradient set the sampling helpers read."""
+
+    def __init__(self, G_t, offsets):
+        self.G, self.offsets = G_t, offsets
+        self.W, self.n = G_t.shape[0], int(offsets[-1])
+
+
+def test_sync_maximum_elements(dev):
+    """n = APS_MAX_ELEMS (2^30 elements per worker), W = 2: maxima and scales
+    in full, the sum on sampled columns (layer edges, chunk edges, both ends,
+    random), both routes."""
+    n = 1 << 30
+    sizes = [1, 1000, (1 << 29) - 1001, 7, (1 << 29) - 7]
+    offs = np.zeros(len(sizes) + 1, np.int64)
+    offs[1:] = np.cumsum(sizes)
+    assert offs[-1] == n
+    g = torch.Generator(device=dev).manual_seed(1911)
+    G_t = torch.randn((2, n), generator=g, device=dev) * 1e-3
+    G_t[:, 1:1001] *= 1e-30
+    offs_t = torch.from_numpy(offs).to(dev)
+    pal = [F(5, 2)]
+    t0 = time.time()
+    out, se, mab, _ = A.aps_sync(G_t, n, offs_t, pal, None, A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | A.APS_SYNC_ONE_PASS)
+    out2, _, _, _ = A.aps_sync(G_t, n, offs_t, pal, None, A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | A.APS_SYNC_TWO_PASS)
+    torch.cuda.synchronize()
+    log("n = 2^30 sync done", f"{time.time() - t0:.1f}s")
+    gs = _Set(G_t, offs)
+    o_mab = _oracle_maxabs_streamed(G_t, gs, rows=1)
+    assert same_maxabs(mab.cpu().numpy(), o_mab), "maxabs"
+    o_se = O.layer_scales(o_mab, 2, [ofmt(f) for f in pal])
+    assert np.array_equal(se.cpu().numpy(), o_se), "scales"
+    assert torch.equal(out.view(torch.int32), out2.view(torch.int32)), "one pass vs two passes"
+    idx = _sample_idx(np.random.default_rng(5), offs, n)
+    o_s = _sampled_oracle(G_t, gs, pal, idx, o_se, None, 2)
+    gv = out[torch.from_numpy(idx).to(dev)].cpu().numpy()
+    assert same_f32(gv, o_s), first_diff(gv, o_s)
+    del G_t, out, out2
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("W", [1 << 20, 1 << 24])
+def test_sync_maximum_workers(dev, W):
+    """W up to APS_MAX_WORKERS (2^24) on a 5-element gradient: the default
+    route and the one-pass route, against the oracle in full."""
+    n, ld = 5, 8
+    offs = np.array([0, 2, 5], np.int64)
+    rng = np.random.default_rng(W)
+    G = (rng.standard_normal((W, ld)) * 1e-2).astype(np.float32)
+    G[:, n:] = np.nan
+    routes = [0] if W == 1 << 24 else [0, A.APS_SYNC_ONE_PASS]
+    for route in routes:
+        t0 = time.time()
+        sync_case(dev, G, n, offs, [F(5, 2)], tag=f"W={W} route={route}", route=route, garbage=False)
+        log("W", W, "route", route, f"{time.time() - t0:.1f}s")
