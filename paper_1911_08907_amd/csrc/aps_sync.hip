@@ -100,11 +100,12 @@ __device__ __forceinline__ void flush_sync(const SyncArgs& a, const SyncWs& ws, 
     if ((threadIdx.x & 63) == 0) ws.wmin[pd.c * 4 + (threadIdx.x >> 6)] = (uint8_t)pd.wb;
 }
 
+// Pass 1 over the chunks of one palette entry (chunks that mix entries:
+// k_sync_spec_mixed).  The format's rounding constants are uniform, so they
+// sit in scalar registers.
 __global__ __launch_bounds__(BLOCK) void k_sync_spec(SyncArgs a, SyncWs ws, Layers ly, Pal pal,
                                                     uint32_t* __restrict__ maxabs) {
-    __shared__ FmtK spal[APS_MAX_FORMATS];
     __shared__ uint32_t red[BLOCK / 64];
-    pal_to_lds(pal, spal);
     const int64_t nchunks = (ly.n + CH - 1) / CH;
     int64_t cb, ce;
     block_range(nchunks, cb, ce);
@@ -119,35 +120,14 @@ __global__ __launch_bounds__(BLOCK) void k_sync_spec(SyncArgs a, SyncWs ws, Laye
         const int64_t end = min(start + CH, ly.n);
         const ChunkInfo ci = chunk_layers(ly, start, end, hint);
         hint = ci.i0;
+        if (ci.mixed) continue;  // k_sync_spec_mixed
         const int64_t j = start + (int64_t)threadIdx.x * VEC;
         uint32_t mx0 = 0, mx1 = 0, mx2 = 0, mx3 = 0;
         uint32_t tmin = 255u;  // this thread's smallest exponent byte
         if (j < end) {
-            uint32_t hf[4], sh[4], lw[4], mk[4];
-            float sc[4];  // 2^-(m+3)
-            if (!ci.mixed) {
-                const FmtK& f = pal.f[ci.pidx];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    hf[e] = f.half;
-                    sh[e] = f.sh;
-                    lw[e] = f.lsbw;
-                    mk[e] = f.mask;
-                    sc[e] = u2f((uint32_t)(124 - f.m) << 23);
-                }
-            } else {
-                int li = ci.i0;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    while (li < ci.i1 && ly.offsets[li + 1] <= j + e) ++li;
-                    const FmtK& f = spal[ly.fmt_idx[li]];
-                    hf[e] = f.half;
-                    sh[e] = f.sh;
-                    lw[e] = f.lsbw;
-                    mk[e] = f.mask;
-                    sc[e] = u2f((uint32_t)(124 - f.m) << 23);
-                }
-            }
+            const FmtK& f = pal.f[ci.pidx];
+            const uint32_t hf = f.half, sh = f.sh, lw = f.lsbw, mk = f.mask;
+            const float sc = u2f((uint32_t)(124 - f.m) << 23);  // 2^-(m+3)
             uint32_t mn0, mn1, mn2, mn3;
             float s0, s1, s2, s3;
             const float* p = a.G + j;
@@ -165,10 +145,10 @@ __global__ __launch_bounds__(BLOCK) void k_sync_spec(SyncArgs a, SyncWs ws, Laye
                     mn1 = mx1 - 1u;
                     mn2 = mx2 - 1u;
                     mn3 = mx3 - 1u;
-                    s0 = u2f(rho(b0, hf[0], sh[0], lw[0], mk[0]));
-                    s1 = u2f(rho(b1, hf[1], sh[1], lw[1], mk[1]));
-                    s2 = u2f(rho(b2, hf[2], sh[2], lw[2], mk[2]));
-                    s3 = u2f(rho(b3, hf[3], sh[3], lw[3], mk[3]));
+                    s0 = u2f(rho(b0, hf, sh, lw, mk));
+                    s1 = u2f(rho(b1, hf, sh, lw, mk));
+                    s2 = u2f(rho(b2, hf, sh, lw, mk));
+                    s3 = u2f(rho(b3, hf, sh, lw, mk));
                 },
                 [&](const f4& r, bool valid) {
                     // a row past the last one counts as -0: no change to any of the four
@@ -181,14 +161,14 @@ __global__ __launch_bounds__(BLOCK) void k_sync_spec(SyncArgs a, SyncWs ws, Laye
                     mx2 = max(mx2, a2);
                     mx3 = max(mx3, a3);
                     // the term's magnitude, or the sum it meets scaled down by 2^(m+3)
-                    mn0 = min(mn0, max(a0 - 1u, f2u(u2f(f2u(s0) & 0x7FFFFFFFu) * sc[0])));
-                    mn1 = min(mn1, max(a1 - 1u, f2u(u2f(f2u(s1) & 0x7FFFFFFFu) * sc[1])));
-                    mn2 = min(mn2, max(a2 - 1u, f2u(u2f(f2u(s2) & 0x7FFFFFFFu) * sc[2])));
-                    mn3 = min(mn3, max(a3 - 1u, f2u(u2f(f2u(s3) & 0x7FFFFFFFu) * sc[3])));
-                    s0 = u2f(rho(f2u(s0 + u2f(rho(b0, hf[0], sh[0], lw[0], mk[0]))), hf[0], sh[0], lw[0], mk[0]));
-                    s1 = u2f(rho(f2u(s1 + u2f(rho(b1, hf[1], sh[1], lw[1], mk[1]))), hf[1], sh[1], lw[1], mk[1]));
-                    s2 = u2f(rho(f2u(s2 + u2f(rho(b2, hf[2], sh[2], lw[2], mk[2]))), hf[2], sh[2], lw[2], mk[2]));
-                    s3 = u2f(rho(f2u(s3 + u2f(rho(b3, hf[3], sh[3], lw[3], mk[3]))), hf[3], sh[3], lw[3], mk[3]));
+                    mn0 = min(mn0, max(a0 - 1u, f2u(u2f(f2u(s0) & 0x7FFFFFFFu) * sc)));
+                    mn1 = min(mn1, max(a1 - 1u, f2u(u2f(f2u(s1) & 0x7FFFFFFFu) * sc)));
+                    mn2 = min(mn2, max(a2 - 1u, f2u(u2f(f2u(s2) & 0x7FFFFFFFu) * sc)));
+                    mn3 = min(mn3, max(a3 - 1u, f2u(u2f(f2u(s3) & 0x7FFFFFFFu) * sc)));
+                    s0 = u2f(rho(f2u(s0 + u2f(rho(b0, hf, sh, lw, mk))), hf, sh, lw, mk));
+                    s1 = u2f(rho(f2u(s1 + u2f(rho(b1, hf, sh, lw, mk))), hf, sh, lw, mk));
+                    s2 = u2f(rho(f2u(s2 + u2f(rho(b2, hf, sh, lw, mk))), hf, sh, lw, mk));
+                    s3 = u2f(rho(f2u(s3 + u2f(rho(b3, hf, sh, lw, mk))), hf, sh, lw, mk));
                 });
             const uint32_t e0 = min(mn0 >> 23, 255u), e1 = min(mn1 >> 23, 255u);
             const uint32_t e2 = min(mn2 >> 23, 255u), e3 = min(mn3 >> 23, 255u);
@@ -232,6 +212,38 @@ __global__ __launch_bounds__(BLOCK) void k_sync_spec(SyncArgs a, SyncWs ws, Laye
     }
     if (run_layer >= 0) block_max_atomic(run, maxabs + run_layer, red);
     flush_sync(a, ws, pd);
+}
+
+// Pass 1 over the chunks that mix palette entries, one block per layer
+// boundary (the block of the first boundary inside a chunk owns it), one
+// element per thread: the same chain, maximum and byte as k_sync_spec.  The
+// scan skips these chunks; k_sync_repair_mixed reads their bytes.
+__global__ __launch_bounds__(BLOCK) void k_sync_spec_mixed(SyncArgs a, SyncWs ws, Layers ly, Pal pal,
+                                                          uint32_t* __restrict__ maxabs) {
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    pal_to_lds(pal, spal);
+    int64_t start, end;
+    if (!mixed_chunk_of_boundary(ly, blockIdx.x, start, end)) return;
+    for (int64_t j = start + threadIdx.x; j < end; j += BLOCK) {
+        const int li = find_layer(ly.offsets, ly.L, j, 0);
+        const FmtK& f = spal[ly.fmt_idx[li]];
+        const float sc = u2f((uint32_t)(124 - f.m) << 23);  // 2^-(m+3)
+        const float* p = a.G + j;
+        uint32_t b = f2u(p[0]);
+        uint32_t mx = b & 0x7FFFFFFFu;
+        uint32_t mn = mx - 1u;  // a zero wraps to the top and never wins the min
+        float s = u2f(rho(b, f.half, f.sh, f.lsbw, f.mask));
+        for (int w = 1; w < a.W; ++w) {
+            b = f2u(p[(int64_t)w * a.ld]);
+            const uint32_t ab = b & 0x7FFFFFFFu;
+            mx = max(mx, ab);
+            mn = min(mn, max(ab - 1u, f2u(u2f(f2u(s) & 0x7FFFFFFFu) * sc)));
+            s = u2f(rho(f2u(s + u2f(rho(b, f.half, f.sh, f.lsbw, f.mask))), f.half, f.sh, f.lsbw, f.mask));
+        }
+        a.out[j] = s;
+        ws.minb[j] = (uint8_t)min(mn >> 23, 255u);
+        if (mx) atomicMax(maxabs + li, mx);
+    }
 }
 
 // Scale exponents (as k_scales) and the per-layer repair threshold: an
@@ -541,6 +553,8 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
             const int per_cu = W >= 64 ? 24 : 32;
             hipLaunchKernelGGL(k_sync_spec, dim3((unsigned)grid_for(nchunks, per_cu)), dim3(BLOCK), 0, s, sa, ws, ly,
                                pal, maxabs_bits);
+            if (mixed)
+                hipLaunchKernelGGL(k_sync_spec_mixed, dim3((unsigned)L), dim3(BLOCK), 0, s, sa, ws, ly, pal, maxabs_bits);
         }
     }
     if (phases & APS_SYNC_PASS2) {
