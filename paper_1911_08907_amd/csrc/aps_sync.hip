@@ -187,9 +187,12 @@ __global__ __launch_bounds__(BLOCK) void k_sync_spec(SyncArgs a, SyncWs ws, Laye
             if (j + 2 < end) tmin = min(tmin, e2); else mx2 = 0;
             if (j + 3 < end) tmin = min(tmin, e3); else mx3 = 0;
         }
-        // every lane of the wave takes part; lane 0 has the wave's first
-        // element, so its pending record exists whenever the wave has one
-        pd.wb = wave_min_u32(tmin);
+        // every lane of the wave takes part in the minimum; lane 0 has the
+        // wave's first element, so it holds this chunk's record whenever the
+        // wave has one.  A lane without an element here keeps the record of
+        // an earlier chunk, whose minimum must stay as it is.
+        const uint32_t wmin_here = wave_min_u32(tmin);
+        if (j < end) pd.wb = wmin_here;
         if (ci.i0 == ci.i1) {
             const uint32_t v = max(max(mx0, mx1), max(mx2, mx3));
             if (ci.i0 != run_layer) {

@@ -331,3 +331,41 @@ def test_sync_maximum_workers(dev, W):
         t0 = time.time()
         sync_case(dev, G, n, offs, [F(5, 2)], tag=f"W={W} route={route}", route=route, garbage=False)
         log("W", W, "route", route, f"{time.time() - t0:.1f}s")
+
+
+def test_sync_short_last_chunk_keeps_the_previous_chunks_bytes(dev):
+    """A block that owns several chunks, the last of them short (300
+    elements, so two of its waves hold no element): the chunk before it keeps
+    its per-wave bytes, and its flagged elements in those waves' ranges are
+    recomputed.  With W = 2 the launch has 8192 blocks, so 16385 chunks give
+    two or three per block."""
+    f = F(5, 2)
+    W = 2
+    n = 16384 * CH + 300
+    ld = (n + 63) // 64 * 64
+    g = torch.Generator(device=dev).manual_seed(7)
+    G_t = torch.randn((W, ld), generator=g, device=dev) * 0.1
+    G_t[0, 0] = 1.0
+    ft = O.scale_one(int(np.float32(1.0).view(np.uint32)), W, ofmt(f))
+    T = float(2.0 ** (1 - f.b - ft))
+    G_t[G_t.abs() < 64 * T] = 64 * T                 # nothing below the threshold by chance
+    c = 16383                                         # the chunk before the short last one
+    # flagged elements of chunk c only in its waves 2 and 3 (elements 512..1023):
+    # were their per-wave bytes lost, nothing would list the chunk
+    planted = np.array([100 * CH + 5, c * CH + 600, c * CH + 900, c * CH + 1023, 16384 * CH + 10, 16384 * CH + 299])
+    pt = torch.from_numpy(planted).to(dev)
+    G_t[0, pt] = 0.6 * T                              # casts to 0.5 T scaled, 0.625 T unscaled
+    G_t[1, pt] = 0.0
+    offs = np.array([0, n], np.int64)
+    offs_t = torch.from_numpy(offs).to(dev)
+    out, se, mab, ws = A.aps_sync(G_t, n, offs_t, [f], None, A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | A.APS_SYNC_ONE_PASS)
+    torch.cuda.synchronize()
+    fl = _flagged(ws, n, offs)
+    assert fl[planted].all()
+    gs = _Set(G_t[:, :n], offs)
+    o_se = O.layer_scales(O.layer_maxabs(G_t.cpu().numpy(), n, offs), W, ofmt(f))
+    assert np.array_equal(se.cpu().numpy(), o_se)
+    idx = np.unique(np.concatenate([planted, _sample_idx(np.random.default_rng(3), offs, n)]))
+    o_s = _sampled_oracle(G_t, gs, [f], idx, o_se, None, W)
+    gv = out[torch.from_numpy(idx).to(dev)].cpu().numpy()
+    assert same_f32(gv, o_s), first_diff(gv, o_s)
