@@ -225,6 +225,8 @@ uint64_t aps_sync_workspace_bytes(int64_t n, int32_t L);
  *   workspace  device memory of at least aps_sync_workspace_bytes(n, L)
  *              bytes, 256-byte aligned, owned by the caller; its contents on
  *              entry do not matter
+ * Every pass enqueues kernels only (no memset, no allocation, no host
+ * synchronisation), so a call can be captured in a HIP graph and replayed.
  * Calls that share a workspace must not overlap.  Errors as aps_sim_reduce;
  * a small workspace returns APS_ERR_SIZE; no pass bit, an unknown bit or both
  * route bits return APS_ERR_UNSUPPORTED.

@@ -369,3 +369,49 @@ def test_sync_short_last_chunk_keeps_the_previous_chunks_bytes(dev):
     o_s = _sampled_oracle(G_t, gs, [f], idx, o_se, None, W)
     gv = out[torch.from_numpy(idx).to(dev)].cpu().numpy()
     assert same_f32(gv, o_s), first_diff(gv, o_s)
+
+
+@pytest.mark.parametrize("route", [A.APS_SYNC_ONE_PASS, A.APS_SYNC_TWO_PASS], ids=["one_pass", "two_passes"])
+def test_sync_hip_graph_replays(dev, route):
+    """aps_sync enqueues kernels only (no memset, no allocation), so it can be
+    captured in a HIP graph: three replays on new inputs, with eager work
+    between them, each against the oracle."""
+    gs = WL.generate("resnet20", "1-5-2", device=dev)
+    W, n, L = gs.W, gs.n, len(gs.sizes)
+    pal = [F(5, 2)]
+    opal = [ofmt(f) for f in pal]
+    offs_t = torch.from_numpy(gs.offsets).to(dev)
+    G = gs.G.clone()
+    mab = torch.empty(L, dtype=torch.int32, device=dev)
+    se = torch.empty(L, dtype=torch.int32, device=dev)
+    out = torch.empty(n, dtype=torch.float32, device=dev)
+    ws = torch.empty(A.aps_sync_workspace_bytes(n, L), dtype=torch.uint8, device=dev)
+    flags = A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | route
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        A.aps_sync(G, n, offs_t, pal, None, flags, mab, se, out, ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        A.aps_sync(G, n, offs_t, pal, None, flags, mab, se, out, ws)
+    gen = torch.Generator(device=dev).manual_seed(23)
+    for trial in range(3):
+        # new inputs in place: rescaled rows plus noise, some exact zeros
+        G.mul_(2.0 ** (trial - 1)).add_(torch.randn(G.shape, generator=gen, device=dev) * 1e-6)
+        G[:, ::97] = 0.0
+        eager = torch.empty_like(out)
+        A.aps_sync(G, n, offs_t, pal, None, A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | A.APS_SYNC_TWO_PASS, out=eager)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        Gh = G.cpu().numpy()
+        o_mab = O.layer_maxabs(Gh, n, gs.offsets)
+        assert same_maxabs(mab.cpu().numpy(), o_mab), f"replay {trial} maxabs"
+        o_se = O.layer_scales(o_mab, W, opal)
+        assert np.array_equal(se.cpu().numpy(), o_se), f"replay {trial} scales"
+        o_out = O.sim_reduce(Gh, n, gs.offsets, o_se, opal)
+        g = out.cpu().numpy()
+        assert same_f32(g, o_out), f"replay {trial} {first_diff(g, o_out)}"
+        assert torch.equal(out.view(torch.int32), eager.view(torch.int32)), f"replay {trial} vs eager"
