@@ -385,8 +385,8 @@ __device__ __forceinline__ void touch(const f4& v) { asm volatile("" ::"v"(v.x),
 
 // Streams W rows of one thread's 16-byte column slice through the callbacks:
 // first(row 0), then step(row w, valid) for w = 1, 2, ... in order.  Two
-// register sets of UNROLL rows are in flight: while one set is consumed, the
-// loads of the next UNROLL rows are outstanding; the scheduling barrier keeps
+// register sets of U rows (UNROLL by default) are in flight: while one set is
+// consumed, the loads of the next U rows are outstanding; the scheduling barrier keeps
 // those loads ahead of the math.  Rows past W-1 are loaded from row W-1 and
 // handed to step() with valid = false, so every path issues the same loads
 // and the compiler waits for exactly the row it is about to use.
@@ -399,47 +399,47 @@ __device__ __forceinline__ void touch(const f4& v) { asm volatile("" ::"v"(v.x),
 // exit in its body: an exit in the middle of the body is merged by the
 // compiler's control-flow structurizer into the back edge, and the loads it
 // would leave outstanding then force waits at the top of every iteration.
-template <class Load, class AfterIssue, class First, class Step>
+template <int U = UNROLL, class Load, class AfterIssue, class First, class Step>
 __device__ __forceinline__ void stream_rows(int W, Load load, AfterIssue after_issue, First first, Step step) {
-    f4 A[UNROLL], B[UNROLL];
+    f4 A[U], B[U];
 #pragma unroll
-    for (int u = 0; u < UNROLL; ++u) A[u] = load(min(u, W - 1));
+    for (int u = 0; u < U; ++u) A[u] = load(min(u, W - 1));
 #pragma unroll
-    for (int u = 0; u < UNROLL; ++u) B[u] = load(min(UNROLL + u, W - 1));
+    for (int u = 0; u < U; ++u) B[u] = load(min(U + u, W - 1));
     __builtin_amdgcn_sched_barrier(0);
     after_issue();
     first(A[0]);
-    const int nsets = (W + UNROLL - 1) / UNROLL;
+    const int nsets = (W + U - 1) / U;
     if (nsets == 1) {
 #pragma unroll
-        for (int u = 1; u < UNROLL; ++u) {
+        for (int u = 1; u < U; ++u) {
             touch(A[u]);
             step(A[u], u < W);
         }
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) {
+        for (int u = 0; u < U; ++u) {
             touch(B[u]);
             step(B[u], false);
         }
         return;
     }
 #pragma unroll
-    for (int u = 1; u < UNROLL; ++u) step(A[u], true);
-    int w = UNROLL;  // first row of the set being consumed
-#define APS_FULL(CUR, NXT)                                                     \
-    {                                                                          \
-        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u)                     \
-            NXT[u] = load(min(w + UNROLL + u, W - 1));                         \
-        __builtin_amdgcn_sched_barrier(0);                                     \
-        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u) step(CUR[u], true); \
-        w += UNROLL;                                                           \
+    for (int u = 1; u < U; ++u) step(A[u], true);
+    int w = U;  // first row of the set being consumed
+#define APS_FULL(CUR, NXT)                                                \
+    {                                                                     \
+        _Pragma("unroll") for (int u = 0; u < U; ++u)                     \
+            NXT[u] = load(min(w + U + u, W - 1));                         \
+        __builtin_amdgcn_sched_barrier(0);                                \
+        _Pragma("unroll") for (int u = 0; u < U; ++u) step(CUR[u], true); \
+        w += U;                                                           \
     }
-#define APS_LAST(CUR)                                                          \
-    {                                                                          \
-        _Pragma("unroll") for (int u = 0; u < UNROLL; ++u) {                   \
-            touch(CUR[u]);                                                     \
-            step(CUR[u], w + u < W);                                           \
-        }                                                                      \
+#define APS_LAST(CUR)                                     \
+    {                                                     \
+        _Pragma("unroll") for (int u = 0; u < U; ++u) {   \
+            touch(CUR[u]);                                \
+            step(CUR[u], w + u < W);                      \
+        }                                                 \
     }
     const int nfull = nsets - 2;
 #pragma unroll 1
