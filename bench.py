@@ -324,7 +324,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(the multi-GPU path is a design, not part of this build)", file=sys.stderr)
+              "(the multi-GPU path is a design only; this library runs on one GPU)", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration > 0:
         copy_calibration(args.copy_calibration)
