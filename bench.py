@@ -7,7 +7,9 @@ max-abs, per-layer scale exponents, and scale / cast / rounded W-worker sum /
 unscale, through one aps_sync call (pass 1 + pass 2).  On the one-pass route
 pass 1 reads the W rows once and forms the sum unscaled; pass 2 computes the
 scales and recomputes the few elements whose inputs reach the format's
-subnormal range.  The default workload is the ResNet-50-shaped set with
+subnormal range.  On the guessed-scale route (formats of narrow range at
+large W) pass 1 forms the scaled sum with exponents guessed from every 32nd
+worker; pass 2 reruns the layers whose guess was wrong.  The default workload is the ResNet-50-shaped set with
 W = 256 workers (161 tensors, 25,557,032 elements per worker, 26.2 GB of fp32
 worker gradients) in the 1-5-2 format.
 
@@ -367,7 +369,9 @@ def main():
     ws = torch.empty(A.aps_sync_workspace_bytes(n, L), dtype=torch.uint8, device=dev)
     G = gs.G
     aps = args.mode == "aps"
-    one = aps and A.aps_sync_one_pass(W, pal)
+    route = A.aps_sync_route(W, n, pal) if aps else None
+    one = route == A.APS_SYNC_ROUTE_ONE_PASS
+    guess = route == A.APS_SYNC_ROUTE_GUESS
 
     ev = []
 
@@ -400,6 +404,13 @@ def main():
     p2 = sum(e[1].elapsed_time(e[2]) for e in ev) / len(ev)
     assert bool(torch.isfinite(out).all()) or not aps
 
+    if guess:
+        # the layers pass 2 reran: threshold 1 in the workspace's int32[L] part
+        up = lambda b: (b + 255) // 256 * 256
+        C = (n + 1023) // 1024
+        t0_ = up(1024 * C) + up(4 * C)
+        rr = ws[t0_:t0_ + 4 * L].cpu().numpy().view("int32") != 0
+        rerun = {"layers": int(rr.sum()), "elements": int(sum(sz for sz, r in zip(gs.sizes, rr) if r))}
     other = {}
     if aps:
         other["two_pass_step"] = two_pass_step(A, G, gs, pal, idx_t, offs_t, mab, se, out)
@@ -412,6 +423,12 @@ def main():
     if one:
         kernel, k_ms = "k_sync_spec", p1
         note = "pass-1 span: k_sync_spec plus the zeroing of the L maxima (k_sync_clear, a few us)"
+    elif guess:
+        # pass 1 also reads every 32nd worker row for the sampled maxima
+        alg_bytes += 4.0 * ((W + 31) // 32) * n
+        kernel, k_ms = "k_guess_spec", p1
+        note = ("pass-1 span: k_guess_spec plus the sampled maxima (k_maxabs over every 32nd worker row), "
+                "bytes of both")
     else:
         kernel, k_ms = "k_sim_reduce", p2
         note = "pass-2 span: k_sim_reduce plus k_scales (a few us)" if aps else "k_sim_reduce alone"
@@ -431,7 +448,8 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": args.config, "W": W, "n": n, "tensors": L, "format": palette,
-                   "mode": args.mode, "route": "one pass" if one else "two passes",
+                   "mode": args.mode,
+                   "route": "one pass" if one else ("guessed scales" if guess else "two passes"),
                    "layout": "[W][ld] fp32 worker-major, HBM resident"},
         "roofline": {
             "bound": "hbm",
@@ -447,6 +465,7 @@ def main():
             "traffic_source": traffic_src,
         },
         "passes_ms": {"pass1": p1, "pass2": p2},
+        **({"guess_reruns": rerun} if guess else {}),
         "other_calls": other,
         "kernel_source": source_digest(),
     }

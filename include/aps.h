@@ -178,6 +178,12 @@ int aps_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n,
 #define APS_SYNC_PASS2 2u    /* scale exponents, then the rest of the sum */
 #define APS_SYNC_ONE_PASS 4u /* take the one-pass route wherever it applies */
 #define APS_SYNC_TWO_PASS 8u /* always read G twice */
+#define APS_SYNC_GUESS 16u   /* take the guessed-scale route */
+
+/* the routes, as aps_sync_route returns them */
+#define APS_SYNC_ROUTE_TWO_PASS 0
+#define APS_SYNC_ROUTE_ONE_PASS 1
+#define APS_SYNC_ROUTE_GUESS 2
 
 /*
  * Bytes of workspace aps_sync needs for n elements and L layers, with
@@ -186,6 +192,14 @@ int aps_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n,
  * Returns 0 for negative arguments or n > APS_MAX_ELEMS.
  */
 uint64_t aps_sync_workspace_bytes(int64_t n, int32_t L);
+
+/*
+ * Which route aps_sync takes for W workers, n elements, this palette and
+ * these flags (only the route bits of flags matter): APS_SYNC_ROUTE_*, or a
+ * negative status (W or n out of range, a bad palette, more than one route
+ * bit).  Host-only.
+ */
+int aps_sync_route(int32_t W, int64_t n, const aps_format* fmts, int32_t n_fmts, uint32_t flags);
 
 /*
  * One whole APS synchronisation of W simulated workers (Algorithm 1 with the
@@ -205,19 +219,35 @@ uint64_t aps_sync_workspace_bytes(int64_t n, int32_t L);
  * T = max(2^(emin - ft), 2^-126) (the format's subnormal range after
  * scaling) that is not swamped, i.e. that comes from worker 0 or meets a
  * partial sum below 2^(m+3) * T, and every element of a layer whose max is
- * INF or NaN or whose N * ghat exceeds 2^127.  The route applies when W is a power of two and
- * every palette format has m <= 10.  With APS_SYNC_ONE_PASS it is then
- * always taken.  With no route flag it is taken only when the format's range
- * leaves few elements to recompute (W^2 * 2^(emin - emax + 2) <= 2^-7 for
- * every palette format).  Otherwise, or with APS_SYNC_TWO_PASS, pass 1 is
- * aps_layer_maxabs and pass 2 is aps_layer_scales followed by aps_sim_reduce.
+ * INF or NaN or whose N * ghat exceeds 2^127.  The route applies when W is
+ * a power of two and every palette format has m <= 10.
+ *
+ * The guessed-scale route applies to every W and format.  Pass 1 takes the
+ * layer maxima of every 32nd worker (rows 0, 32, 64, ...), guesses each
+ * layer's scale exponent from them (allowing for the growth of a normal
+ * sample's max with the sample size), and then, reading G once, forms the
+ * scaled sums with the guesses while it takes the full maxima.  Pass 2
+ * computes the true exponents and reruns through the scaled path every
+ * chunk of a layer whose guess differs.  The results never depend on the
+ * guess; its cost is ceil(W/32) rows read plus the rerun layers.
+ *
+ * The two-pass route: pass 1 is aps_layer_maxabs, pass 2 aps_layer_scales
+ * followed by aps_sim_reduce.
+ *
+ * Route choice: APS_SYNC_TWO_PASS and APS_SYNC_GUESS force their routes;
+ * APS_SYNC_ONE_PASS takes the one-pass route wherever it applies (else two
+ * passes).  With no route bit, the one-pass route is taken where it applies
+ * and the format's range leaves few elements to recompute
+ * (W^2 * 2^(emin - emax + 2) <= 2^-7 for every palette format); otherwise
+ * the guessed-scale route when W * n >= 2^26, else two passes.
  *
  *   G          [W][ld] fp32 (16-byte aligned, ld % 4 == 0); not aliased by out
  *   flags      APS_SYNC_PASS1, APS_SYNC_PASS2 or both, plus at most one of
- *              APS_SYNC_ONE_PASS, APS_SYNC_TWO_PASS.  Run separately, pass 2
- *              must follow pass 1 with the same arguments and route flag on
- *              the same stream, with the workspace untouched in between; after
- *              pass 1 alone, maxabs_bits is final and out holds intermediate
+ *              APS_SYNC_ONE_PASS, APS_SYNC_TWO_PASS, APS_SYNC_GUESS.  Run
+ *              separately, pass 2 must follow pass 1 with the same arguments
+ *              and route flag on the same stream, with the workspace,
+ *              scale_exp and out untouched in between; after pass 1 alone,
+ *              maxabs_bits is final and scale_exp and out hold intermediate
  *              values
  *   maxabs_bits uint32[L] out
  *   scale_exp  int32[L] out
@@ -228,17 +258,9 @@ uint64_t aps_sync_workspace_bytes(int64_t n, int32_t L);
  * Every pass enqueues kernels only (no memset, no allocation, no host
  * synchronisation), so a call can be captured in a HIP graph and replayed.
  * Calls that share a workspace must not overlap.  Errors as aps_sim_reduce;
- * a small workspace returns APS_ERR_SIZE; no pass bit, an unknown bit or both
- * route bits return APS_ERR_UNSUPPORTED.
+ * a small workspace returns APS_ERR_SIZE; no pass bit, an unknown bit or more
+ * than one route bit return APS_ERR_UNSUPPORTED.
  */
-/*
- * Which route aps_sync takes for W workers, this palette and these flags
- * (only the route bits of flags matter): 1 for the one-pass route, 0 for
- * two passes, or a negative status (W out of range, a bad palette, both
- * route bits).  Host-only.
- */
-int aps_sync_one_pass(int32_t W, const aps_format* fmts, int32_t n_fmts, uint32_t flags);
-
 int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n,
              const int64_t* offsets, int32_t L,
              const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,

@@ -29,7 +29,7 @@ APS_MAX_FORMATS = 8
 
 EXPORTS = ("aps_format_supported", "aps_layer_maxabs", "aps_layer_scales", "aps_quantize",
            "aps_sim_reduce", "aps_sim_reduce_ex", "aps_sim_reduce_codes", "aps_dequantize", "aps_lp_gemm",
-           "aps_sync_workspace_bytes", "aps_sync_one_pass", "aps_sync", "aps_strerror")
+           "aps_sync_workspace_bytes", "aps_sync_route", "aps_sync", "aps_strerror")
 
 APS_ACC_SEQUENTIAL = 0
 APS_ACC_KAHAN = 1
@@ -38,6 +38,10 @@ APS_SYNC_PASS1 = 1
 APS_SYNC_PASS2 = 2
 APS_SYNC_ONE_PASS = 4
 APS_SYNC_TWO_PASS = 8
+APS_SYNC_GUESS = 16
+APS_SYNC_ROUTE_TWO_PASS = 0
+APS_SYNC_ROUTE_ONE_PASS = 1
+APS_SYNC_ROUTE_GUESS = 2
 
 
 class ApsError(RuntimeError):
@@ -106,7 +110,7 @@ def lib() -> ctypes.CDLL:
             "aps_dequantize": (ctypes.c_int, [P, P, i64, P, i32, P, FP, i32, P, P, P]),
             "aps_lp_gemm": (ctypes.c_int, [P, i64, P, i64, P, i64, i32, i32, i32, aps_format, aps_format, i32, P]),
             "aps_sync_workspace_bytes": (ctypes.c_uint64, [i64, i32]),
-            "aps_sync_one_pass": (ctypes.c_int, [i32, FP, i32, u32]),
+            "aps_sync_route": (ctypes.c_int, [i32, i64, FP, i32, u32]),
             "aps_sync": (ctypes.c_int, [P, i32, i64, i64, P, i32, FP, i32, P, u32, P, P, P, P, ctypes.c_uint64, P]),
             "aps_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         }
@@ -262,14 +266,14 @@ def aps_sync_workspace_bytes(n: int, L: int) -> int:
     return int(lib().aps_sync_workspace_bytes(int(n), int(L)))
 
 
-def aps_sync_one_pass(W: int, fmts, flags: int = 0) -> bool:
-    """Whether aps_sync takes the one-pass route for W workers and this
-    palette (only the route bits of ``flags`` matter)."""
+def aps_sync_route(W: int, n: int, fmts, flags: int = 0) -> int:
+    """The route aps_sync takes for W workers, n elements and this palette
+    (only the route bits of ``flags`` matter): one of APS_SYNC_ROUTE_*."""
     pal, nf = _palette(fmts)
-    st = lib().aps_sync_one_pass(int(W), pal, nf, int(flags))
+    st = lib().aps_sync_route(int(W), int(n), pal, nf, int(flags))
     if st < 0:
-        raise ApsError("aps_sync_one_pass", st)
-    return st == 1
+        raise ApsError("aps_sync_route", st)
+    return st
 
 
 def aps_sync(G, n: int, offsets, fmts, fmt_idx=None, flags: int = APS_SYNC_PASS1 | APS_SYNC_PASS2,

@@ -496,9 +496,12 @@ __device__ __forceinline__ void flush_out(const ReduceArgs& a, PendingOut& pd) {
     if (a.codes) store_codes4(a.codes, pd.j, pd.c, a.code_cls, pd.lim);
 }
 
-template <int V>
+// The fused scale + cast + rounded sum + unscale of 4 consecutive elements
+// over the W rows.  With MAX it also returns the largest |x| bit pattern of
+// each of the 4 columns in mx (rows past the end read as -0: no effect).
+template <int V, bool MAX = false>
 __device__ __forceinline__ void reduce_vec(const ReduceArgs& a, const FmtK& f, int64_t j, int64_t lim,
-                                           const int32_t ft[4], PendingOut& pd) {
+                                           const int32_t ft[4], PendingOut& pd, uint32_t* mx = nullptr) {
     const bool inq = a.flags & APS_INPUT_QUANTIZED;
     const bool outs = a.flags & APS_OUTPUT_SCALED;
     int F[4], Fo[4];
@@ -511,6 +514,7 @@ __device__ __forceinline__ void reduce_vec(const ReduceArgs& a, const FmtK& f, i
     const float* p = a.G + j;
     const int64_t ld = a.ld;
     float s0, s1, s2, s3;
+    uint32_t m0 = 0, m1 = 0, m2 = 0, m3 = 0;
     // a row past the last one counts as -0, which leaves every sum unchanged
     // (s + -0 == s, signs of zero included)
     const f4 neg0 = {-0.0f, -0.0f, -0.0f, -0.0f};
@@ -518,6 +522,12 @@ __device__ __forceinline__ void reduce_vec(const ReduceArgs& a, const FmtK& f, i
         a.W, [&](int r) { return ld4(p + (int64_t)r * ld); },
         [&]() { flush_out(a, pd); },  // the previous chunk's outputs, behind this chunk's loads
         [&](const f4& x) {
+            if constexpr (MAX) {
+                m0 = f2u(x.x) & 0x7FFFFFFFu;
+                m1 = f2u(x.y) & 0x7FFFFFFFu;
+                m2 = f2u(x.z) & 0x7FFFFFFFu;
+                m3 = f2u(x.w) & 0x7FFFFFFFu;
+            }
             s0 = quant<V>(x.x, F[0], f, bad0);
             s1 = quant<V>(x.y, F[1], f, bad1);
             s2 = quant<V>(x.z, F[2], f, bad2);
@@ -525,11 +535,23 @@ __device__ __forceinline__ void reduce_vec(const ReduceArgs& a, const FmtK& f, i
         },
         [&](const f4& r, bool valid) {
             const f4 v = valid ? r : neg0;
+            if constexpr (MAX) {
+                m0 = max(m0, f2u(v.x) & 0x7FFFFFFFu);
+                m1 = max(m1, f2u(v.y) & 0x7FFFFFFFu);
+                m2 = max(m2, f2u(v.z) & 0x7FFFFFFFu);
+                m3 = max(m3, f2u(v.w) & 0x7FFFFFFFu);
+            }
             s0 = accum<V>(s0, quant<V>(v.x, F[0], f, bad0), f, bad0);
             s1 = accum<V>(s1, quant<V>(v.y, F[1], f, bad1), f, bad1);
             s2 = accum<V>(s2, quant<V>(v.z, F[2], f, bad2), f, bad2);
             s3 = accum<V>(s3, quant<V>(v.w, F[3], f, bad3), f, bad3);
         });
+    if constexpr (MAX) {
+        mx[0] = m0;
+        mx[1] = m1;
+        mx[2] = m2;
+        mx[3] = m3;
+    }
     s0 = finish<V>(s0, bad0);
     s1 = finish<V>(s1, bad1);
     s2 = finish<V>(s2, bad2);

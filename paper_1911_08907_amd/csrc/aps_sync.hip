@@ -292,17 +292,22 @@ __device__ __forceinline__ int layer_of(const int64_t* __restrict__ off, int L, 
 // One thread per chunk: list the chunks (single palette entry) holding an
 // element whose byte is below its layer's threshold.  The test is on the
 // chunk's minimum byte against the largest threshold among its layers, so
-// it never misses one; the repair looks at each element.
-__global__ void k_sync_scan(Layers ly, SyncWs ws) {
+// it never misses one; the repair looks at each element.  With every (the
+// guessed-scale route, no bytes) each element counts as byte 0, so a chunk
+// is listed when one of its layers has a nonzero threshold.
+__global__ void k_sync_scan(Layers ly, SyncWs ws, bool every) {
     const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t nchunks = (ly.n + CH - 1) / CH;
     if (c >= nchunks) return;
     const int64_t start = c * CH;
     const int64_t end = min(start + CH, ly.n);
-    const uint32_t w4 = *(const uint32_t*)(ws.wmin + 4 * c);
-    uint32_t cm = 255u;
-    for (int wv = 0; wv < 4; ++wv)
-        if (start + 256 * wv < end) cm = min(cm, (w4 >> (8 * wv)) & 0xFFu);
+    uint32_t cm = 0u;
+    if (!every) {
+        const uint32_t w4 = *(const uint32_t*)(ws.wmin + 4 * c);
+        cm = 255u;
+        for (int wv = 0; wv < 4; ++wv)
+            if (start + 256 * wv < end) cm = min(cm, (w4 >> (8 * wv)) & 0xFFu);
+    }
     const int i0 = layer_of(ly.offsets, ly.L, start), i1 = layer_of(ly.offsets, ly.L, end - 1);
     int32_t th = 0;
     bool mixed = false;
@@ -355,24 +360,29 @@ __device__ void repair_one(const ReduceArgs& a, const FmtK& f, int64_t j, int F)
 // chunk: find the flagged elements (16 bytes per lane), then repair them one
 // after another (at most SPARSE_MAX), or rerun the whole chunk through the
 // streaming row walk, a quarter at a time.  Waves stride over the list; its
-// length is read on the device.
+// length is read on the device.  With every, each listed chunk is rerun
+// whole (the guessed-scale route lists only such chunks and keeps no bytes),
+// its four quarters by four waves: few listed chunks still spread over many
+// waves.
 template <int V>
-__global__ __launch_bounds__(BLOCK) void k_sync_repair(ReduceArgs a, Layers ly, Pal pal, SyncWs ws) {
-    const uint32_t total = *ws.count;
+__global__ __launch_bounds__(BLOCK) void k_sync_repair(ReduceArgs a, Layers ly, Pal pal, SyncWs ws, bool every) {
+    const int64_t total = (int64_t)*ws.count * (every ? 4 : 1);
     const int lane = threadIdx.x & 63;
     const int64_t nw = (int64_t)gridDim.x * (BLOCK / 64);
     for (int64_t k = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * (BLOCK / 64) + (threadIdx.x >> 6))); k < total;
          k += nw) {
-        const int64_t start = (int64_t)cld(ws.list, k) * CH;
+        const int64_t start = (int64_t)cld(ws.list, every ? k >> 2 : k) * CH;
         const int64_t end = min(start + CH, ly.n);
         const ChunkInfo ci = chunk_layers(ly, start, end, 0);
         const FmtK& f = pal.f[ci.pidx];
         if (f.variant != V) continue;  // another launch owns this format
         // 16 consecutive elements per lane; the byte array is padded to whole chunks
         const int64_t j0 = start + 16 * lane;
-        const u4v w = *(const u4v*)(ws.minb + j0);
         uint32_t mask = 0;
-        if (ci.i0 == ci.i1) {  // one layer: one threshold, read once
+        if (every) {
+            mask = ~0u;  // more than SPARSE_MAX: the whole chunk below
+        } else if (ci.i0 == ci.i1) {  // one layer: one threshold, read once
+            const u4v w = *(const u4v*)(ws.minb + j0);
             const int32_t th = cld(ws.thr, ci.i0);
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
@@ -380,6 +390,7 @@ __global__ __launch_bounds__(BLOCK) void k_sync_repair(ReduceArgs a, Layers ly, 
                 if ((int32_t)byte < th && j0 + e < end) mask |= 1u << e;
             }
         } else {
+            const u4v w = *(const u4v*)(ws.minb + j0);
             int li = ci.i0;
             int64_t next = ly.offsets[li + 1];
             int32_t th = ws.thr[li];
@@ -398,8 +409,9 @@ __global__ __launch_bounds__(BLOCK) void k_sync_repair(ReduceArgs a, Layers ly, 
         int cnt = __builtin_popcount(mask);
         for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
         if (cnt > SPARSE_MAX) {
+            const int q0 = every ? (int)(k & 3) : 0, q1 = every ? q0 + 1 : 4;
 #pragma unroll 1
-            for (int qtr = 0; qtr < 4; ++qtr) {
+            for (int qtr = q0; qtr < q1; ++qtr) {
                 const int64_t j = start + (int64_t)qtr * 256 + 4 * lane;
                 if (j >= end) continue;
                 int32_t ft[4];
@@ -432,19 +444,150 @@ __global__ __launch_bounds__(BLOCK) void k_sync_repair(ReduceArgs a, Layers ly, 
     }
 }
 
-// Flagged elements of chunks that mix palette entries, element by element.
-__global__ __launch_bounds__(BLOCK) void k_sync_repair_mixed(ReduceArgs a, Layers ly, Pal pal, SyncWs ws) {
+// Flagged elements of chunks that mix palette entries, element by element
+// (with every: all of their elements).
+__global__ __launch_bounds__(BLOCK) void k_sync_repair_mixed(ReduceArgs a, Layers ly, Pal pal, SyncWs ws,
+                                                            bool every) {
     __shared__ FmtK spal[APS_MAX_FORMATS];
     pal_to_lds(pal, spal);
     int64_t start, end;
     if (!mixed_chunk_of_boundary(ly, blockIdx.x, start, end)) return;
     for (int64_t j = start + threadIdx.x; j < end; j += BLOCK) {
         const int li = find_layer(ly.offsets, ly.L, j, 0);
-        if ((int32_t)ws.minb[j] >= ws.thr[li]) continue;
+        if (!every && (int32_t)ws.minb[j] >= ws.thr[li]) continue;
         const FmtK& f = spal[ly.fmt_idx[li]];
         const int F = clamp_exp(ly.scale_exp[li]) + f.k;
         a.out[j] = __builtin_amdgcn_ldexpf(reduce_elem_any(a, f, j, F), -F);
     }
+}
+
+// ======================================= K5b: the guessed-scale route
+//
+// For a format of narrow range at large W most elements have an input in
+// the scaled subnormal range, and the one-pass route would recompute nearly
+// all of them.  There pass 1 runs the scaled path itself, with a guessed
+// exponent per layer, and takes the true maxima alongside.  Wherever the
+// guess equals the exponent the maxima give, pass 1 did exactly the scaled
+// path's arithmetic; pass 2 reruns every chunk of a layer whose guess was
+// wrong.  The guess comes from the maxima of every GUESS_ROW_STRIDE-th
+// worker (a sample of n_s values of a layer, K = W / rows times fewer than
+// the layer has).  The max over all workers is larger than the sample's: for
+// normal values the max of n draws grows like sqrt(2 ln n), so by about
+// sqrt(1 + ln K / ln n_s).  The guess takes the sample's fl32(N * max) times
+// that factor.  It affects only how much pass 2 reruns, never a result.
+
+constexpr int GUESS_ROW_STRIDE = 32;
+
+// The guessed exponent of each layer from the sampled maxima (rows sampled
+// rows of N), into scale_exp: as k_scales, on the sample's N * max raised by
+// the expected growth of the max.
+__global__ void k_guess_scales(const uint32_t* __restrict__ maxabs, Layers ly, int32_t N, int32_t rows, Pal pal,
+                               int32_t* __restrict__ scale_exp) {
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    pal_to_lds(pal, spal);
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= ly.L) return;
+    const FmtK& f = spal[ly.fmt_idx ? ly.fmt_idx[i] : 0];
+    const uint32_t gb = maxabs[i] & 0x7FFFFFFFu;
+    int32_t r = 0;
+    if (gb != 0 && gb < 0x7F800000u) {
+        const float t = (float)N * u2f(gb);
+        uint32_t tb = f2u(t);
+        if (tb < 0x7F800000u) {
+            const float ns = (float)(ly.offsets[i + 1] - ly.offsets[i]) * (float)rows;
+            const float grow = sqrtf(1.0f + logf((float)N / (float)rows) / logf(fmaxf(ns, 2.0f)));
+            const uint32_t tn = f2u(t * grow);
+            if (tn < 0x7F800000u) tb = tn;
+            r = f.emax - ceil_log2_bits(tb);
+        }
+    }
+    scale_exp[i] = r;
+}
+
+// Pass 1 of the guessed-scale route over the chunks of one variant's format:
+// the fused scaled sum of k_sim_reduce with the guessed exponents, plus the
+// layer maxima (chunks that mix palette entries: maxima by
+// k_sync_spec_mixed, sums in pass 2).
+template <int V>
+__global__ __launch_bounds__(BLOCK) void k_guess_spec(ReduceArgs a, Layers ly, Pal pal,
+                                                     uint32_t* __restrict__ maxabs) {
+    __shared__ uint32_t red[BLOCK / 64];
+    const int64_t nchunks = (ly.n + CH - 1) / CH;
+    int64_t cb, ce;
+    block_range(nchunks, cb, ce);
+    int hint = 0;
+    uint32_t run = 0;  // running max of layer run_layer (chunks inside one layer)
+    int run_layer = -1;
+    PendingOut pd;
+    pd.valid = false;
+    for (int64_t c = cb; c < ce; ++c) {
+        const int64_t start = c * CH;
+        const int64_t end = min(start + CH, ly.n);
+        const ChunkInfo ci = chunk_layers(ly, start, end, hint);
+        hint = ci.i0;
+        if (ci.mixed) continue;
+        const FmtK& f = pal.f[ci.pidx];
+        if (f.variant != V) continue;  // another launch owns this format
+        const int64_t j = start + (int64_t)threadIdx.x * VEC;
+        uint32_t mx[4] = {0u, 0u, 0u, 0u};
+        if (j < end) {
+            int32_t ft[4];
+            if (ci.i0 == ci.i1) {
+                const int32_t t = clamp_exp(cld(ly.scale_exp, ci.i0));
+                ft[0] = ft[1] = ft[2] = ft[3] = t;
+            } else {
+                elem_scales(ly, ci, j, ft);
+            }
+            reduce_vec<V, true>(a, f, j, end, ft, pd, mx);
+            // elements past the end of the gradient (row padding) do not count
+            if (j + 1 >= end) mx[1] = 0;
+            if (j + 2 >= end) mx[2] = 0;
+            if (j + 3 >= end) mx[3] = 0;
+        }
+        if (ci.i0 == ci.i1) {
+            const uint32_t v = max(max(mx[0], mx[1]), max(mx[2], mx[3]));
+            if (ci.i0 != run_layer) {
+                if (run_layer >= 0) block_max_atomic(run, maxabs + run_layer, red);
+                run_layer = ci.i0;
+                run = 0;
+            }
+            run = max(run, v);
+        } else {
+            for (int li = ci.i0; li <= ci.i1; ++li) {
+                const int64_t lo = cld(ly.offsets, li), hi = cld(ly.offsets, li + 1);
+                uint32_t v = 0;
+                if (j < end)
+                    for (int e = 0; e < 4; ++e)
+                        if (j + e >= lo && j + e < hi) v = max(v, mx[e]);
+                block_max_atomic(v, maxabs + li, red);
+            }
+        }
+    }
+    if (run_layer >= 0) block_max_atomic(run, maxabs + run_layer, red);
+    flush_out(a, pd);
+}
+
+// Pass 2 of the guessed-scale route: the exponents (as k_scales) replace the
+// guesses in scale_exp; thr = 1 marks a layer whose guess differed (all of
+// its chunks are rerun), 0 one whose pass-1 sums stand.  Also clears the
+// repair list.
+__global__ void k_guess_layers(const uint32_t* __restrict__ maxabs, int32_t L, int32_t N, Pal pal,
+                               const uint8_t* __restrict__ fmt_idx, int32_t* __restrict__ scale_exp, SyncWs ws) {
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    pal_to_lds(pal, spal);
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i == 0) *ws.count = 0u;
+    if (i >= L) return;
+    const FmtK& f = spal[fmt_idx ? fmt_idx[i] : 0];
+    const uint32_t gb = maxabs[i] & 0x7FFFFFFFu;
+    int32_t r = 0;
+    if (gb != 0 && gb < 0x7F800000u) {
+        const float t = (float)N * u2f(gb);
+        const uint32_t tb = f2u(t);
+        if (tb < 0x7F800000u) r = f.emax - ceil_log2_bits(tb);
+    }
+    ws.thr[i] = clamp_exp(r) != clamp_exp(scale_exp[i]) ? 1 : 0;
+    scale_exp[i] = r;
 }
 
 }  // namespace aps
@@ -485,26 +628,46 @@ extern "C" uint64_t aps_sync_workspace_bytes(int64_t n, int32_t L) {
 // W * 2^(emin - emax) of the layer's max, each input falls below it with
 // probability about W * 2^(emin - emax + 2), and an element is recomputed
 // with probability up to W^2 * 2^(emin - emax + 2); above 2^-7 most chunks
-// would be recomputed and two passes cost less.
-static bool sync_one_pass(int32_t W, const Pal& pal, int32_t n_fmts, uint32_t flags) {
-    if (flags & APS_SYNC_TWO_PASS) return false;
+// would be recomputed.  Then the guessed-scale route is taken for sets of
+// at least GUESS_MIN_WORK element-workers (its sample and extra launches
+// cost more than they save on smaller ones), else two passes.
+constexpr int64_t GUESS_MIN_WORK = (int64_t)1 << 26;
+
+static bool one_pass_applies(int32_t W, const Pal& pal, int32_t n_fmts) {
     if (W & (W - 1)) return false;
-    int lw = 0;
-    while ((1 << lw) < W) ++lw;
-    for (int i = 0; i < n_fmts; ++i) {
+    for (int i = 0; i < n_fmts; ++i)
         if (pal.f[i].m > 10) return false;
-        if (!(flags & APS_SYNC_ONE_PASS) && 2 * lw + pal.f[i].emin - pal.f[i].emax + 2 > -7) return false;
-    }
     return true;
 }
 
-extern "C" int aps_sync_one_pass(int32_t W, const aps_format* fmts, int32_t n_fmts, uint32_t flags) {
-    if (W < 1 || W > APS_MAX_WORKERS) return APS_ERR_SIZE;
-    if ((flags & APS_SYNC_ONE_PASS) && (flags & APS_SYNC_TWO_PASS)) return APS_ERR_UNSUPPORTED;
+static int sync_route(int32_t W, int64_t n, const Pal& pal, int32_t n_fmts, uint32_t flags) {
+    if (flags & APS_SYNC_TWO_PASS) return APS_SYNC_ROUTE_TWO_PASS;
+    if (flags & APS_SYNC_GUESS) return APS_SYNC_ROUTE_GUESS;
+    const bool applies = one_pass_applies(W, pal, n_fmts);
+    if (flags & APS_SYNC_ONE_PASS) return applies ? APS_SYNC_ROUTE_ONE_PASS : APS_SYNC_ROUTE_TWO_PASS;
+    bool pays = applies;
+    int lw = 0;
+    while ((1 << lw) < W) ++lw;
+    for (int i = 0; i < n_fmts; ++i)
+        if (2 * lw + pal.f[i].emin - pal.f[i].emax + 2 > -7) pays = false;
+    if (pays) return APS_SYNC_ROUTE_ONE_PASS;
+    return (int64_t)W * n >= GUESS_MIN_WORK ? APS_SYNC_ROUTE_GUESS : APS_SYNC_ROUTE_TWO_PASS;
+}
+
+static constexpr uint32_t ROUTE_BITS = APS_SYNC_ONE_PASS | APS_SYNC_TWO_PASS | APS_SYNC_GUESS;
+
+static bool route_bits_ok(uint32_t flags) {
+    const uint32_t r = flags & ROUTE_BITS;
+    return (r & (r - 1)) == 0;  // at most one
+}
+
+extern "C" int aps_sync_route(int32_t W, int64_t n, const aps_format* fmts, int32_t n_fmts, uint32_t flags) {
+    if (W < 1 || W > APS_MAX_WORKERS || n < 0 || n > APS_MAX_ELEMS) return APS_ERR_SIZE;
+    if (!route_bits_ok(flags)) return APS_ERR_UNSUPPORTED;
     Pal pal;
     const int st = check_palette(fmts, n_fmts, pal, nullptr);
     if (st != APS_OK) return st;
-    return sync_one_pass(W, pal, n_fmts, flags) ? 1 : 0;
+    return sync_route(W, n, pal, n_fmts, flags);
 }
 
 extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const int64_t* offsets, int32_t L,
@@ -515,8 +678,7 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
     if (st != APS_OK) return st;
     if (!maxabs_bits || !scale_exp || !workspace || (!out && n > 0)) return APS_ERR_NULL;
     const uint32_t phases = flags & (APS_SYNC_PASS1 | APS_SYNC_PASS2);
-    if (phases == 0 || (flags & ~(APS_SYNC_PASS1 | APS_SYNC_PASS2 | APS_SYNC_ONE_PASS | APS_SYNC_TWO_PASS)) ||
-        ((flags & APS_SYNC_ONE_PASS) && (flags & APS_SYNC_TWO_PASS)))
+    if (phases == 0 || (flags & ~(APS_SYNC_PASS1 | APS_SYNC_PASS2 | ROUTE_BITS)) || !route_bits_ok(flags))
         return APS_ERR_UNSUPPORTED;
     if ((out && !aligned16(out)) || ((uintptr_t)workspace & 255u)) return APS_ERR_ALIGN;
     const SyncLayout lay = sync_layout(n, L);
@@ -530,8 +692,8 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
     SyncWs ws{wb + lay.minb, wb + lay.wmin, (int32_t*)(wb + lay.thr), (uint32_t*)(wb + lay.count),
               (int32_t*)(wb + lay.list)};
     Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
-    const bool one = sync_one_pass(W, pal, n_fmts, flags);
-    if (!one) {
+    const int route = sync_route(W, n, pal, n_fmts, flags);
+    if (route == APS_SYNC_ROUTE_TWO_PASS) {
         // two passes: exactly the three calls of the step
         if (phases & APS_SYNC_PASS1) {
             st = aps_layer_maxabs(G, W, ld, n, offsets, L, maxabs_bits, stream);
@@ -547,10 +709,30 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
     }
     const dim3 lgrid((unsigned)((L + 255) / 256));
     const bool mixed = fmt_idx && n_fmts > 1 && L > 1;
-    if (phases & APS_SYNC_PASS1) {
+    const unsigned vm = variant_mask(pal, n_fmts);
+    const dim3 grid((unsigned)grid_for(nchunks, BLOCKS_PER_CU));
+    ReduceArgs ra{G, out, nullptr, ld, W, 0u, 0};
+    SyncArgs sa{G, out, ld, W};
+    const bool guess = route == APS_SYNC_ROUTE_GUESS;
+    if (guess && (phases & APS_SYNC_PASS1)) {
+        // the maxima of every GUESS_ROW_STRIDE-th worker give the guesses
+        const int32_t rows = (W + GUESS_ROW_STRIDE - 1) / GUESS_ROW_STRIDE;
+        st = aps_layer_maxabs(G, rows, rows > 1 ? ld * GUESS_ROW_STRIDE : ld, n, offsets, L, maxabs_bits, stream);
+        if (st != APS_OK) return st;
+        hipLaunchKernelGGL(k_guess_scales, lgrid, dim3(256), 0, s, maxabs_bits, ly, W, rows, pal, scale_exp);
+        if (n > 0) {
+            // the full maxima accumulate on top of the sampled ones
+#define APS_LAUNCH_G(v) \
+    if (vm & (1u << (v))) hipLaunchKernelGGL(k_guess_spec<v>, grid, dim3(BLOCK), 0, s, ra, ly, pal, maxabs_bits);
+            APS_FOR_VARIANTS(APS_LAUNCH_G)
+#undef APS_LAUNCH_G
+            if (mixed)
+                hipLaunchKernelGGL(k_sync_spec_mixed, dim3((unsigned)L), dim3(BLOCK), 0, s, sa, ws, ly, pal, maxabs_bits);
+        }
+    }
+    if (!guess && (phases & APS_SYNC_PASS1)) {
         hipLaunchKernelGGL(k_sync_clear, lgrid, dim3(256), 0, s, maxabs_bits, L);
         if (n > 0) {
-            SyncArgs sa{G, out, ld, W};
             // launch width measured on MI355X: 24 blocks per CU for many rows,
             // 32 when each chunk is only a few rows (shorter work per chunk)
             const int per_cu = W >= 64 ? 24 : 32;
@@ -561,18 +743,18 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
         }
     }
     if (phases & APS_SYNC_PASS2) {
-        hipLaunchKernelGGL(k_sync_layers, lgrid, dim3(256), 0, s, maxabs_bits, L, W, pal, fmt_idx, scale_exp, ws);
+        if (guess)
+            hipLaunchKernelGGL(k_guess_layers, lgrid, dim3(256), 0, s, maxabs_bits, L, W, pal, fmt_idx, scale_exp, ws);
+        else
+            hipLaunchKernelGGL(k_sync_layers, lgrid, dim3(256), 0, s, maxabs_bits, L, W, pal, fmt_idx, scale_exp, ws);
         if (n > 0) {
-            hipLaunchKernelGGL(k_sync_scan, dim3((unsigned)((nchunks + 255) / 256)), dim3(256), 0, s, ly, ws);
-            ReduceArgs a{G, out, nullptr, ld, W, 0u, 0};
-            const unsigned vm = variant_mask(pal, n_fmts);
-            const dim3 grid((unsigned)grid_for(nchunks, BLOCKS_PER_CU));
+            hipLaunchKernelGGL(k_sync_scan, dim3((unsigned)((nchunks + 255) / 256)), dim3(256), 0, s, ly, ws, guess);
 #define APS_LAUNCH_S(v) \
-    if (vm & (1u << (v))) hipLaunchKernelGGL(k_sync_repair<v>, grid, dim3(BLOCK), 0, s, a, ly, pal, ws);
-            APS_LAUNCH_S(V_INT_F32) APS_LAUNCH_S(V_INT_M0) APS_LAUNCH_S(V_TOP_F32) APS_LAUNCH_S(V_TOP_M0)
-            APS_LAUNCH_S(V_LOW_F32) APS_LAUNCH_S(V_LOW_M0)
+    if (vm & (1u << (v))) hipLaunchKernelGGL(k_sync_repair<v>, grid, dim3(BLOCK), 0, s, ra, ly, pal, ws, guess);
+            APS_FOR_VARIANTS(APS_LAUNCH_S)
 #undef APS_LAUNCH_S
-            if (mixed) hipLaunchKernelGGL(k_sync_repair_mixed, dim3((unsigned)L), dim3(BLOCK), 0, s, a, ly, pal, ws);
+            if (mixed)
+                hipLaunchKernelGGL(k_sync_repair_mixed, dim3((unsigned)L), dim3(BLOCK), 0, s, ra, ly, pal, ws, guess);
         }
     }
     return launched();

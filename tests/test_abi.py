@@ -238,8 +238,10 @@ def test_sync_validation(lib):
     assert call(ws=None) == A.APS_ERR_NULL
     assert call(ph=0) == A.APS_ERR_UNSUPPORTED
     assert call(ph=4) == A.APS_ERR_UNSUPPORTED                  # a route but no pass
-    assert call(ph=16 | 3) == A.APS_ERR_UNSUPPORTED             # unknown bit
-    assert call(ph=3 | 4 | 8) == A.APS_ERR_UNSUPPORTED          # both routes
+    assert call(ph=32 | 3) == A.APS_ERR_UNSUPPORTED             # unknown bit
+    assert call(ph=3 | 4 | 8) == A.APS_ERR_UNSUPPORTED          # two routes
+    assert call(ph=3 | 4 | 16) == A.APS_ERR_UNSUPPORTED
+    assert call(ph=3 | 8 | 16) == A.APS_ERR_UNSUPPORTED
     assert call(out=MIS) == A.APS_ERR_ALIGN
     assert call(ws=P(4096 + 128)) == A.APS_ERR_ALIGN       # workspace needs 256-byte alignment
     assert call(wsb=ws - 1) == A.APS_ERR_SIZE
@@ -252,23 +254,40 @@ def test_sync_validation(lib):
 
 def test_sync_route_choice(lib):
     F = A.Format
-    one, two = A.APS_SYNC_ONE_PASS, A.APS_SYNC_TWO_PASS
+    one, two, guess = A.APS_SYNC_ONE_PASS, A.APS_SYNC_TWO_PASS, A.APS_SYNC_GUESS
+    ONE, TWO, GUESS = A.APS_SYNC_ROUTE_ONE_PASS, A.APS_SYNC_ROUTE_TWO_PASS, A.APS_SYNC_ROUTE_GUESS
+    r = A.aps_sync_route
+    big, small = 25557032, 272474          # ResNet-50 and ResNet-20 element counts
     # the default takes one pass when the format's range leaves few elements to recompute
-    assert A.aps_sync_one_pass(256, [F(5, 2)]) is True
-    assert A.aps_sync_one_pass(8, [F(5, 2)]) is True
-    assert A.aps_sync_one_pass(8, [F(5, 10), F(5, 2)]) is True
-    assert A.aps_sync_one_pass(256, [F(8, 7)]) is True
-    assert A.aps_sync_one_pass(256, [F(4, 3)]) is False
-    assert A.aps_sync_one_pass(8, [F(3, 0)]) is False
+    assert r(256, big, [F(5, 2)]) == ONE
+    assert r(8, small, [F(5, 2)]) == ONE
+    assert r(8, big, [F(5, 10), F(5, 2)]) == ONE
+    assert r(256, big, [F(8, 7)]) == ONE
+    # otherwise the guessed-scale route for at least 2^26 element-workers, else two passes
+    assert r(256, big, [F(4, 3)]) == GUESS
+    assert r(256, (1 << 18) - 1, [F(4, 3)]) == TWO
+    assert r(256, 1 << 18, [F(4, 3)]) == GUESS
+    assert r(8, small, [F(3, 0)]) == TWO
+    assert r(8, small, [F(4, 3)]) == TWO
+    assert r(12, big, [F(5, 2)]) == GUESS        # W not a power of two
+    assert r(8, big, [F(5, 12)]) == GUESS        # m > 10
+    assert r(12, small, [F(5, 2)]) == TWO
     # forced routes; the one-pass route needs a power-of-two W and m <= 10
-    assert A.aps_sync_one_pass(256, [F(4, 3)], one) is True
-    assert A.aps_sync_one_pass(256, [F(5, 2)], two) is False
-    assert A.aps_sync_one_pass(12, [F(5, 2)], one) is False
-    assert A.aps_sync_one_pass(8, [F(5, 12)], one) is False
-    assert A.aps_sync_one_pass(8, [F(5, 2), F(8, 23)], one) is False
+    assert r(256, big, [F(4, 3)], one) == ONE
+    assert r(256, big, [F(5, 2)], two) == TWO
+    assert r(256, big, [F(5, 2)], guess) == GUESS
+    assert r(3, 1, [F(5, 12)], guess) == GUESS
+    assert r(12, big, [F(5, 2)], one) == TWO
+    assert r(8, big, [F(5, 12)], one) == TWO
+    assert r(8, big, [F(5, 2), F(8, 23)], one) == TWO
+    for bad in (one | two, one | guess, two | guess):
+        with pytest.raises(A.ApsError):
+            r(8, big, [F(5, 2)], bad)
     with pytest.raises(A.ApsError):
-        A.aps_sync_one_pass(8, [F(5, 2)], one | two)
+        r(0, big, [F(5, 2)])
     with pytest.raises(A.ApsError):
-        A.aps_sync_one_pass(0, [F(5, 2)])
+        r(8, -1, [F(5, 2)])
     with pytest.raises(A.ApsError):
-        A.aps_sync_one_pass(8, [F(9, 2)])
+        r(8, (1 << 30) + 1, [F(5, 2)])
+    with pytest.raises(A.ApsError):
+        r(8, big, [F(9, 2)])

@@ -5,8 +5,9 @@ aps_sync must return exactly what the oracle's max-abs, scales (N = W) and
 rounded W-worker sum give (Algorithm 1 with the low-precision accumulator of
 Sec. 5), whichever route the library takes: the one-pass route (the sum
 formed unscaled while the maxima are taken, then the elements whose inputs
-reach the format's subnormal range recomputed through the scaled path), or
-the two-pass fallback (W not a power of two, or m > 10).  The cases put
+reach the format's subnormal range recomputed through the scaled path), the
+guessed-scale route (the scaled sum formed with exponents guessed from every
+32nd worker, layers whose guess was wrong rerun), or two passes.  The cases put
 inputs exactly at, just above and just below each layer's threshold
 2^(emin - ft), in fp32's subnormal range, in layers with INF/NaN or with a
 maximum near fp32's top, and make chunks with few and with many elements to
@@ -55,13 +56,17 @@ def _flagged(ws, n, offs):
     return minb.astype(np.int32) < thr[layer]
 
 
-def one_pass(W, pal, route):
-    if route == A.APS_SYNC_TWO_PASS or W & (W - 1) or any(f.m > 10 for f in pal):
-        return False
-    if route == A.APS_SYNC_ONE_PASS:
-        return True
-    lw = int(W).bit_length() - 1
-    return all(2 * lw + (1 - f.b) - f.emax + 2 <= -7 for f in pal)
+def _rerun_layers(ws, n, L):
+    """Layers the guessed-scale route reran (read back from the workspace):
+    threshold 1 where the guessed exponent differed."""
+    up = lambda b: (b + 255) // 256 * 256
+    C = (n + CH - 1) // CH
+    t0 = up(CH * C) + up(4 * C)
+    return ws.cpu().numpy()[t0:t0 + 4 * L].view(np.int32) != 0
+
+
+def _layer_mask(layers, n, offs):
+    return layers[np.searchsorted(offs, np.arange(n), side="right") - 1] if n else np.zeros(0, bool)
 
 
 def sync_case(dev, G, n, offs, pal, fmt_idx=None, tag="", split=False, garbage=True, route=A.APS_SYNC_ONE_PASS):
@@ -90,8 +95,12 @@ def sync_case(dev, G, n, offs, pal, fmt_idx=None, tag="", split=False, garbage=T
     o_out = O.sim_reduce(G, n, offs, o_se, opal, fmt_idx)
     g = out.cpu().numpy()[:n]
     assert same_f32(g, o_out), f"{tag} sum {first_diff(g, o_out)}"
-    flagged = _flagged(ws, n, offs) if one_pass(W, pal, route) else None
-    return flagged
+    taken = A.aps_sync_route(W, n, pal, route)
+    if taken == A.APS_SYNC_ROUTE_ONE_PASS:
+        return _flagged(ws, n, offs)
+    if taken == A.APS_SYNC_ROUTE_GUESS:
+        return _layer_mask(_rerun_layers(ws, n, L), n, offs)
+    return None
 
 
 # ----------------------------------------------------------- edge layouts
@@ -106,11 +115,12 @@ SIZES = [0, 1, 3, 5, 7, 1023, 1024, 1025, 2049, 0, 64, 13, 4095, 2, 3000]
 def test_sync_edge_layouts(dev, f, kind):
     rng = np.random.default_rng(hash(("sync", str(f), kind)) & 0xFFFF)
     offs, n, ld = _layout(SIZES)
-    for W in (1, 2, 4, 8, 16, 3, 13):
+    for W in (1, 2, 4, 8, 16, 3, 13, 40):
         G = _values(rng, W, ld, offs, kind)
         tag = f"{f} {kind} W={W}"
         log("case", tag)
         sync_case(dev, G, n, offs, [f], tag=tag, split=(W == 4))
+        sync_case(dev, G, n, offs, [f], tag=tag + " guessed scales", route=A.APS_SYNC_GUESS, split=(W == 3))
         if W in (2, 8):
             sync_case(dev, G, n, offs, [f], tag=tag + " default route", route=0)
             sync_case(dev, G, n, offs, [f], tag=tag + " two passes", route=A.APS_SYNC_TWO_PASS, split=(W == 2))
@@ -131,6 +141,7 @@ def test_sync_mixed_palette(dev, seed):
             tag = f"mixed seed={seed} W={W} {kind}"
             log("case", tag)
             sync_case(dev, G, n, offs, pal, fmt_idx=fmt_idx, tag=tag)
+            sync_case(dev, G, n, offs, pal, fmt_idx=fmt_idx, tag=tag + " guessed scales", route=A.APS_SYNC_GUESS)
 
 
 def test_sync_empty_gradient(dev):
@@ -216,6 +227,74 @@ def test_sync_unsafe_layers(dev):
     assert fl[:1200].all()
 
 
+def _guess_model(G, n, offs, W, f, stride=32):
+    """The guessed exponents as the guessed-scale route defines them: the
+    max over workers 0, 32, 64, ... (rows of them, n_s = rows * layer size
+    values); t = fl32(N * max) raised by the expected growth of a normal
+    sample's max, sqrt(1 + ln(N / rows) / ln max(n_s, 2)), where that stays
+    finite; exponent emax - ceil(log2 t); 0 for a zero, INF or NaN max."""
+    rows = (W + stride - 1) // stride
+    ms = O.layer_maxabs(G[::stride], n, offs).view(np.float32)
+    sizes = np.diff(offs)
+    out = np.zeros(ms.size, np.int64)
+    for i, m in enumerate(ms):
+        if not (np.isfinite(m) and m > 0):
+            continue
+        t = np.float32(np.float32(W) * m)
+        if not np.isfinite(t):
+            continue
+        grow = np.sqrt(1.0 + np.log(W / rows) / np.log(max(sizes[i] * rows, 2)))
+        tn = np.float32(t * np.float32(grow))
+        if np.isfinite(tn):
+            t = tn
+        fr, e = np.frexp(np.float64(t))
+        out[i] = f.emax - (e - 1 if fr == 0.5 else e)
+    return out
+
+
+def test_sync_guess_reruns(dev):
+    """The guessed-scale route with W = 40 (sampled workers 0 and 32, a
+    300-element layer's max taken 1.21 times larger): layers whose guess is
+    right (pass-1 sums kept) and wrong (rerun) of every kind: the max in an
+    unsampled worker, a sampled max that the growth factor takes into the
+    next binade with and without the full max getting there, INF outside the
+    sample, NaN inside it, zeros, a max only outside the sample.  Sums
+    against the oracle; the rerun layers against the guess rule."""
+    f = F(4, 3)
+    W = 40
+    P = np.float32(4.0 / W)  # N * ghat = 4 * (this multiple of P)
+    sizes = [300, 3000, 300, 300, 5000, 300, 300, 300, 1, 700, 2500, 300]
+    offs, n, ld = _layout(sizes)
+    rng = np.random.default_rng(40)
+    G = (rng.standard_normal((W, ld)) * 0.01).astype(np.float32)
+    G[:, n:] = np.nan
+    lo = lambda i: int(offs[i])
+    for i in range(4):
+        G[:, lo(i):lo(i + 1)] = np.clip(G[:, lo(i):lo(i + 1)], -0.05, 0.05)
+    G[32, lo(0) + 7] = 0.75 * P                    # 0: max sampled; 3.0 * 1.21 < 4: right
+    G[0, lo(1) + 9] = 0.75 * P
+    G[5, lo(1) + 2000] = 3.0 * P                    # 1: max outside the sample: wrong
+    G[32, lo(2) + 1] = -0.9 * P                     # 2: 3.6 * 1.21 > 4, the full max stays below: wrong
+    G[32, lo(3) + 3] = 0.9 * P
+    G[7, lo(3) + 4] = 1.2 * P                       # 3: ... and the full max gets there: right
+    G[9, lo(4) + 4321] = np.inf                     # 4: INF outside the sample: wrong
+    G[0, lo(5) + 5] = np.nan                        # 5: NaN in the sample: right (exponent 0 both ways)
+    G[:, lo(6):lo(7)] = 0.0                         # 6: all zero: right
+    G[::32, lo(7):lo(8)] = 0.0                      # 7: zero in the sample: wrong
+    G[:, lo(8)] = 0.0
+    G[39, lo(8)] = 1e-3                             # 8: one element, only worker 39: wrong
+    guess = _guess_model(G, n, offs, W, f)
+    o_se = O.layer_scales(O.layer_maxabs(G, n, offs), W, ofmt(f))
+    want = guess != o_se
+    assert list(np.nonzero(want)[0][:5]) == [1, 2, 4, 7, 8], want
+    assert not want[[0, 3, 5, 6]].any()
+    for split in (False, True):
+        rerun = sync_case(dev, G, n, offs, [f], tag=f"guess reruns split={split}", route=A.APS_SYNC_GUESS,
+                          split=split)
+        got = rerun[offs[:-1][np.array(sizes) > 0]]
+        assert np.array_equal(got, want[np.array(sizes) > 0]), (got, want)
+
+
 # --------------------------------------------------- paper-shaped sets
 
 @pytest.mark.parametrize("name,palette", [("mlp", "1-4-3"), ("resnet20", "1-5-2"), ("resnet20", "1-4-3"),
@@ -225,6 +304,9 @@ def test_sync_config_full(dev, name, palette):
     pal = [A.Format(p.e, p.m, p.bias) for p in gs.palette]
     fl = sync_case(dev, gs.G.numpy(), gs.n, gs.offsets, pal, fmt_idx=gs.fmt_idx, tag=f"{name} {palette}")
     log(name, palette, "recomputed", int(fl.sum()), "of", gs.n)
+    fl = sync_case(dev, gs.G.numpy(), gs.n, gs.offsets, pal, fmt_idx=gs.fmt_idx, tag=f"{name} {palette} guessed",
+                   route=A.APS_SYNC_GUESS)
+    log(name, palette, "guessed scales: rerun", int(fl.sum()), "of", gs.n)
 
 
 @pytest.mark.parametrize("name,palette", [("resnet50_w8", "1-5-2"), ("resnet50_w256", "1-5-2"),
@@ -244,7 +326,14 @@ def test_sync_config_large(dev, name, palette):
     out, se, mab, ws = A.aps_sync(G_t, n, offs_t, pal, idx_t, A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | route)
     ref, se2, mab2 = A.aps_step(G_t, n, offs_t, pal, idx_t)
     dflt, _, _, _ = A.aps_sync(G_t, n, offs_t, pal, idx_t)
+    gsd, gse, gmab, gws = A.aps_sync(G_t, n, offs_t, pal, idx_t, A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | A.APS_SYNC_GUESS)
     torch.cuda.synchronize()
+    assert torch.equal(gsd.view(torch.int32), ref.view(torch.int32)), "guessed-scale vs two-pass sum"
+    assert torch.equal(gse, se2) and torch.equal(gmab, mab2), "guessed-scale scales / maxima"
+    rr = _rerun_layers(gws, n, len(gs.sizes))
+    log(name, palette, "guessed scales: rerun", int(rr.sum()), "layers,",
+        int(np.array(gs.sizes)[rr].sum()), "of", n, "elements")
+    del gsd, gws
     log(name, palette, "gpu done", f"{time.time() - t0:.1f}s")
     o_mab = _oracle_maxabs_streamed(G_t, gs)
     assert same_maxabs(mab.cpu().numpy(), o_mab), "maxabs"
@@ -301,8 +390,12 @@ def test_sync_maximum_elements(dev):
     t0 = time.time()
     out, se, mab, _ = A.aps_sync(G_t, n, offs_t, pal, None, A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | A.APS_SYNC_ONE_PASS)
     out2, _, _, _ = A.aps_sync(G_t, n, offs_t, pal, None, A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | A.APS_SYNC_TWO_PASS)
+    out3, se3, _, _ = A.aps_sync(G_t, n, offs_t, pal, None, A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | A.APS_SYNC_GUESS)
     torch.cuda.synchronize()
     log("n = 2^30 sync done", f"{time.time() - t0:.1f}s")
+    assert torch.equal(out3.view(torch.int32), out2.view(torch.int32)), "guessed scales vs two passes"
+    assert torch.equal(se3, se)
+    del out3
     gs = _Set(G_t, offs)
     o_mab = _oracle_maxabs_streamed(G_t, gs, rows=1)
     assert same_maxabs(mab.cpu().numpy(), o_mab), "maxabs"
@@ -326,7 +419,7 @@ def test_sync_maximum_workers(dev, W):
     rng = np.random.default_rng(W)
     G = (rng.standard_normal((W, ld)) * 1e-2).astype(np.float32)
     G[:, n:] = np.nan
-    routes = [0] if W == 1 << 24 else [0, A.APS_SYNC_ONE_PASS]
+    routes = [0] if W == 1 << 24 else [0, A.APS_SYNC_ONE_PASS, A.APS_SYNC_GUESS]
     for route in routes:
         t0 = time.time()
         sync_case(dev, G, n, offs, [F(5, 2)], tag=f"W={W} route={route}", route=route, garbage=False)
@@ -371,7 +464,8 @@ def test_sync_short_last_chunk_keeps_the_previous_chunks_bytes(dev):
     assert same_f32(gv, o_s), first_diff(gv, o_s)
 
 
-@pytest.mark.parametrize("route", [A.APS_SYNC_ONE_PASS, A.APS_SYNC_TWO_PASS], ids=["one_pass", "two_passes"])
+@pytest.mark.parametrize("route", [A.APS_SYNC_ONE_PASS, A.APS_SYNC_TWO_PASS, A.APS_SYNC_GUESS],
+                         ids=["one_pass", "two_passes", "guessed_scales"])
 def test_sync_hip_graph_replays(dev, route):
     """aps_sync enqueues kernels only (no memset, no allocation), so it can be
     captured in a HIP graph: three replays on new inputs, with eager work
