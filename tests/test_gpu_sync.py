@@ -147,7 +147,8 @@ def test_sync_mixed_palette(dev, seed):
 def test_sync_empty_gradient(dev):
     offs = np.zeros(4, np.int64)
     G = np.zeros((4, 4), np.float32)
-    sync_case(dev, G, 0, offs, [F(5, 2)], tag="empty")
+    for route in (A.APS_SYNC_ONE_PASS, A.APS_SYNC_GUESS, A.APS_SYNC_TWO_PASS, 0):
+        sync_case(dev, G, 0, offs, [F(5, 2)], tag=f"empty route={route}", route=route)
 
 
 # ------------------------------------------------- thresholds and repair
