@@ -213,9 +213,11 @@ int aps_sync_route(int32_t W, int64_t n, const aps_format* fmts, int32_t n_fmts,
  * The one-pass route reads G once instead of twice.  Power-of-two scaling
  * commutes with rounding to m+1 significant bits (Sec. 3.3.1), so pass 1
  * forms the rounded sum on the unscaled values while it takes the layer
- * maxima, and records one byte per element.  Pass 2 computes the scales
+ * maxima, and records one byte per element (with fewer than 64 workers only
+ * the minimum byte of each 256-element group).  Pass 2 computes the scales
  * and recomputes through the scaled path only the elements for which the
- * unscaled sum can differ: those with a nonzero input below
+ * unscaled sum can differ (below 64 workers: the whole groups that hold
+ * one): those with a nonzero input below
  * T = max(2^(emin - ft), 2^-126) (the format's subnormal range after
  * scaling) that is not swamped, i.e. that comes from worker 0 or meets a
  * partial sum below 2^(m+3) * T, and every element of a layer whose max is

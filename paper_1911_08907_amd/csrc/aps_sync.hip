@@ -59,6 +59,21 @@ struct SyncWs {
     int32_t* __restrict__ thr;   // [L] repair threshold per layer
     uint32_t* __restrict__ count;  // chunks listed for repair
     int32_t* __restrict__ list;    // [nchunks] those chunks
+    bool bytes;                    // pass 1 stores minb for the single-entry chunks
+};
+
+// Fewer workers than this: pass 1 keeps only the per-wave minima, and pass 2
+// reruns each 256-element group whose minimum is below its chunk's largest
+// threshold.  Such a group is W rows of 1 KB, cheap to rerun at small W,
+// while the per-element byte stores slow pass 1 down by more than their
+// share of its traffic.
+constexpr int32_t SYNC_BYTES_MIN_W = 64;
+
+// What k_sync_repair does with a listed chunk.
+enum RepairMode {
+    RM_ELEMENTS = 0,  // find the flagged elements from their bytes
+    RM_CHUNKS = 1,    // rerun all four quarters (guessed-scale route)
+    RM_QUARTERS = 2,  // rerun the quarters whose wave minimum is below the chunk's threshold
 };
 
 struct SyncArgs {
@@ -96,7 +111,7 @@ __device__ __forceinline__ void flush_sync(const SyncArgs& a, const SyncWs& ws, 
         if (j + 2 < lim) a.out[j + 2] = pd.o.z;
     }
     // the byte array is padded to whole chunks: a full word is always in bounds
-    __builtin_nontemporal_store(pd.mb, (uint32_t*)(ws.minb + j));
+    if (ws.bytes) __builtin_nontemporal_store(pd.mb, (uint32_t*)(ws.minb + j));
     if ((threadIdx.x & 63) == 0) ws.wmin[pd.c * 4 + (threadIdx.x >> 6)] = (uint8_t)pd.wb;
 }
 
@@ -360,12 +375,14 @@ __device__ void repair_one(const ReduceArgs& a, const FmtK& f, int64_t j, int F)
 // chunk: find the flagged elements (16 bytes per lane), then repair them one
 // after another (at most SPARSE_MAX), or rerun the whole chunk through the
 // streaming row walk, a quarter at a time.  Waves stride over the list; its
-// length is read on the device.  With every, each listed chunk is rerun
-// whole (the guessed-scale route lists only such chunks and keeps no bytes),
-// its four quarters by four waves: few listed chunks still spread over many
-// waves.
+// length is read on the device.  Without bytes (RM_CHUNKS, RM_QUARTERS) a
+// listed chunk's four quarters are four tasks, so few listed chunks still
+// spread over many waves; RM_QUARTERS skips a quarter whose wave minimum is
+// not below the largest threshold of the chunk's layers (no element of it
+// can be flagged).
 template <int V>
-__global__ __launch_bounds__(BLOCK) void k_sync_repair(ReduceArgs a, Layers ly, Pal pal, SyncWs ws, bool every) {
+__global__ __launch_bounds__(BLOCK) void k_sync_repair(ReduceArgs a, Layers ly, Pal pal, SyncWs ws, int mode) {
+    const bool every = mode != RM_ELEMENTS;
     const int64_t total = (int64_t)*ws.count * (every ? 4 : 1);
     const int lane = threadIdx.x & 63;
     const int64_t nw = (int64_t)gridDim.x * (BLOCK / 64);
@@ -410,6 +427,11 @@ __global__ __launch_bounds__(BLOCK) void k_sync_repair(ReduceArgs a, Layers ly, 
         for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
         if (cnt > SPARSE_MAX) {
             const int q0 = every ? (int)(k & 3) : 0, q1 = every ? q0 + 1 : 4;
+            if (mode == RM_QUARTERS) {
+                int32_t th = 0;
+                for (int li = ci.i0; li <= ci.i1; ++li) th = max(th, cld(ws.thr, li));
+                if ((int32_t)ws.wmin[(start / CH) * 4 + q0] >= th) continue;
+            }
 #pragma unroll 1
             for (int qtr = q0; qtr < q1; ++qtr) {
                 const int64_t j = start + (int64_t)qtr * 256 + 4 * lane;
@@ -690,7 +712,7 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
     const int64_t nchunks = (n + CH - 1) / CH;
     uint8_t* wb = (uint8_t*)workspace;
     SyncWs ws{wb + lay.minb, wb + lay.wmin, (int32_t*)(wb + lay.thr), (uint32_t*)(wb + lay.count),
-              (int32_t*)(wb + lay.list)};
+              (int32_t*)(wb + lay.list), W >= SYNC_BYTES_MIN_W};
     Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
     const int route = sync_route(W, n, pal, n_fmts, flags);
     if (route == APS_SYNC_ROUTE_TWO_PASS) {
@@ -714,6 +736,7 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
     ReduceArgs ra{G, out, nullptr, ld, W, 0u, 0};
     SyncArgs sa{G, out, ld, W};
     const bool guess = route == APS_SYNC_ROUTE_GUESS;
+    const int rmode = guess ? RM_CHUNKS : (ws.bytes ? RM_ELEMENTS : RM_QUARTERS);
     if (guess && (phases & APS_SYNC_PASS1)) {
         // the maxima of every GUESS_ROW_STRIDE-th worker give the guesses
         const int32_t rows = (W + GUESS_ROW_STRIDE - 1) / GUESS_ROW_STRIDE;
@@ -750,7 +773,7 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
         if (n > 0) {
             hipLaunchKernelGGL(k_sync_scan, dim3((unsigned)((nchunks + 255) / 256)), dim3(256), 0, s, ly, ws, guess);
 #define APS_LAUNCH_S(v) \
-    if (vm & (1u << (v))) hipLaunchKernelGGL(k_sync_repair<v>, grid, dim3(BLOCK), 0, s, ra, ly, pal, ws, guess);
+    if (vm & (1u << (v))) hipLaunchKernelGGL(k_sync_repair<v>, grid, dim3(BLOCK), 0, s, ra, ly, pal, ws, rmode);
             APS_FOR_VARIANTS(APS_LAUNCH_S)
 #undef APS_LAUNCH_S
             if (mixed)

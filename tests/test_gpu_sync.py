@@ -40,9 +40,14 @@ def dev():
     return torch.device("cuda:0")
 
 
-def _flagged(ws, n, offs):
-    """Elements the second pass recomputed (read back from the workspace):
-    exponent byte below the layer's threshold."""
+BYTES_MIN_W = 64  # the one-pass route keeps per-element bytes from this many workers on
+
+
+def _flagged(ws, n, offs, W):
+    """Elements the second pass recomputed (read back from the workspace).
+    From BYTES_MIN_W workers on: exponent byte below the layer's threshold.
+    Below: every element of a 256-element group whose wave minimum is below
+    the largest threshold of its chunk's layers."""
     if n == 0:
         return np.zeros(0, bool)
     L = offs.size - 1
@@ -50,10 +55,18 @@ def _flagged(ws, n, offs):
     C = (n + CH - 1) // CH
     t0 = up(CH * C) + up(4 * C)
     w = ws.cpu().numpy()
-    minb = w[:n]
     thr = w[t0:t0 + 4 * L].view(np.int32)
     layer = np.searchsorted(offs, np.arange(n), side="right") - 1
-    return minb.astype(np.int32) < thr[layer]
+    if W >= BYTES_MIN_W:
+        return w[:n].astype(np.int32) < thr[layer]
+    wmin = w[up(CH * C):up(CH * C) + 4 * C].astype(np.int32).reshape(C, 4)
+    starts = np.arange(C) * CH
+    i0, i1 = layer[starts], layer[np.minimum(starts + CH, n) - 1]
+    th = thr[i0].copy()
+    for c in np.nonzero(i1 > i0)[0]:
+        th[c] = thr[i0[c]:i1[c] + 1].max()
+    groups = wmin < th[:, None]   # a group past n is never read below
+    return np.repeat(groups.reshape(-1), 256)[:n]
 
 
 def _rerun_layers(ws, n, L):
@@ -97,7 +110,7 @@ def sync_case(dev, G, n, offs, pal, fmt_idx=None, tag="", split=False, garbage=T
     assert same_f32(g, o_out), f"{tag} sum {first_diff(g, o_out)}"
     taken = A.aps_sync_route(W, n, pal, route)
     if taken == A.APS_SYNC_ROUTE_ONE_PASS:
-        return _flagged(ws, n, offs)
+        return _flagged(ws, n, offs, W)
     if taken == A.APS_SYNC_ROUTE_GUESS:
         return _layer_mask(_rerun_layers(ws, n, L), n, offs)
     return None
@@ -178,7 +191,8 @@ def _chunk_counts(flagged):
 def test_sync_sparse_and_dense_repairs(dev):
     """Chunks with 1..16 elements to recompute (one wave each) and with more
     (the whole chunk again), in the same call; W = 512 also walks the
-    casts in two batches of 256 workers."""
+    casts in two batches of 256 workers.  At W = 8 pass 1 keeps no
+    per-element bytes, and whole 256-element groups are rerun."""
     f = F(5, 2)
     for W in (8, 512):
         n = 40 * CH
@@ -204,8 +218,11 @@ def test_sync_sparse_and_dense_repairs(dev):
         offs = np.array([0, n], np.int64)
         fl = sync_case(dev, G, n, offs, [f], tag=f"sparse/dense W={W}")
         cnt = _chunk_counts(fl)
-        assert np.array_equal(cnt, np.arange(40)), cnt
-        assert ((cnt > 0) & (cnt <= SPARSE_MAX)).any() and (cnt > SPARSE_MAX).any()
+        if W >= BYTES_MIN_W:
+            assert np.array_equal(cnt, np.arange(40)), cnt
+            assert ((cnt > 0) & (cnt <= SPARSE_MAX)).any() and (cnt > SPARSE_MAX).any()
+        else:  # whole 256-element groups: every planted element among them, none in chunk 0
+            assert fl[planted].all() and cnt[0] == 0, cnt
 
 
 def test_sync_unsafe_layers(dev):
@@ -342,7 +359,7 @@ def test_sync_config_large(dev, name, palette):
     assert np.array_equal(se.cpu().numpy(), o_se), "scales"
     assert torch.equal(out.view(torch.int32), ref.view(torch.int32)), "one-pass vs two-pass sum"
     assert torch.equal(dflt.view(torch.int32), ref.view(torch.int32)), "default route vs two-pass sum"
-    fl = _flagged(ws, n, gs.offsets)
+    fl = _flagged(ws, n, gs.offsets, W)
     log(name, palette, "recomputed", int(fl.sum()), "of", n, f"{time.time() - t0:.1f}s")
     rng = np.random.default_rng(11)
     if name == "resnet50_w8":
@@ -454,7 +471,7 @@ def test_sync_short_last_chunk_keeps_the_previous_chunks_bytes(dev):
     offs_t = torch.from_numpy(offs).to(dev)
     out, se, mab, ws = A.aps_sync(G_t, n, offs_t, [f], None, A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | A.APS_SYNC_ONE_PASS)
     torch.cuda.synchronize()
-    fl = _flagged(ws, n, offs)
+    fl = _flagged(ws, n, offs, W)
     assert fl[planted].all()
     gs = _Set(G_t[:, :n], offs)
     o_se = O.layer_scales(O.layer_maxabs(G_t.cpu().numpy(), n, offs), W, ofmt(f))
