@@ -88,9 +88,9 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
     return v;
 }
 
-// A thread's finished first-pass results for 4 elements, stored after the
-// next chunk's loads have been issued (see PendingOut); lane 0 of a wave also
-// holds the wave's minimum byte.
+// A thread's finished first-pass results for 4 elements, handed on (to its
+// LDS slots below) after the next chunk's loads have been issued; lane 0 of
+// a wave also holds the wave's minimum byte.
 struct PendingSync {
     f4 o;
     uint32_t mb;  // the 4 exponent bytes, element j in the low byte
@@ -99,20 +99,49 @@ struct PendingSync {
     bool valid;
 };
 
-__device__ __forceinline__ void flush_sync(const SyncArgs& a, const SyncWs& ws, PendingSync& pd) {
+// A thread's finished records wait in LDS (its own slots: no other thread
+// reads them, so no barrier) and are written out STAGE chunks at a time, or
+// when the block is done.  Writes in the middle of the row reads cost pass 1
+// far more than their bytes; fewer, larger bursts of them cost less.
+constexpr int STAGE = 8;
+
+struct Stage {
+    f4* o;         // [STAGE][BLOCK] sums
+    uint32_t* mb;  // [STAGE][BLOCK] exponent bytes
+    int32_t* j;    // [STAGE][BLOCK] first element (n <= 2^30)
+    int cnt;       // this thread's filled slots
+};
+
+__device__ __forceinline__ void drain_stage(const SyncArgs& a, const SyncWs& ws, Stage& st, int64_t n) {
+    const int t = threadIdx.x;
+    for (int s = 0; s < st.cnt; ++s) {
+        const int64_t j = st.j[s * BLOCK + t];
+        const int64_t lim = min((j / CH) * CH + CH, n);
+        const f4 o = st.o[s * BLOCK + t];
+        if (j + 4 <= lim) {
+            __builtin_nontemporal_store(o, (f4*)(a.out + j));
+        } else {
+            if (j < lim) a.out[j] = o.x;
+            if (j + 1 < lim) a.out[j + 1] = o.y;
+            if (j + 2 < lim) a.out[j + 2] = o.z;
+        }
+        // the byte array is padded to whole chunks: a full word is always in bounds
+        if (ws.bytes) __builtin_nontemporal_store(st.mb[s * BLOCK + t], (uint32_t*)(ws.minb + j));
+    }
+    st.cnt = 0;
+}
+
+__device__ __forceinline__ void flush_sync(const SyncArgs& a, const SyncWs& ws, PendingSync& pd, Stage& st,
+                                           int64_t n) {
     if (!pd.valid) return;
     pd.valid = false;
-    const int64_t j = pd.j, lim = pd.lim;
-    if (j + 4 <= lim) {
-        __builtin_nontemporal_store(pd.o, (f4*)(a.out + j));
-    } else {
-        if (j < lim) a.out[j] = pd.o.x;
-        if (j + 1 < lim) a.out[j + 1] = pd.o.y;
-        if (j + 2 < lim) a.out[j + 2] = pd.o.z;
-    }
-    // the byte array is padded to whole chunks: a full word is always in bounds
-    if (ws.bytes) __builtin_nontemporal_store(pd.mb, (uint32_t*)(ws.minb + j));
+    const int t = threadIdx.x;
+    st.o[st.cnt * BLOCK + t] = pd.o;
+    st.mb[st.cnt * BLOCK + t] = pd.mb;
+    st.j[st.cnt * BLOCK + t] = (int32_t)pd.j;
+    ++st.cnt;
     if ((threadIdx.x & 63) == 0) ws.wmin[pd.c * 4 + (threadIdx.x >> 6)] = (uint8_t)pd.wb;
+    if (st.cnt == STAGE) drain_stage(a, ws, st, n);
 }
 
 // Pass 1 over the chunks of one palette entry (chunks that mix entries:
@@ -121,6 +150,10 @@ __device__ __forceinline__ void flush_sync(const SyncArgs& a, const SyncWs& ws, 
 __global__ __launch_bounds__(BLOCK) void k_sync_spec(SyncArgs a, SyncWs ws, Layers ly, Pal pal,
                                                     uint32_t* __restrict__ maxabs) {
     __shared__ uint32_t red[BLOCK / 64];
+    __shared__ f4 st_o[STAGE * BLOCK];
+    __shared__ uint32_t st_mb[STAGE * BLOCK];
+    __shared__ int32_t st_j[STAGE * BLOCK];
+    Stage st{st_o, st_mb, st_j, 0};
     const int64_t nchunks = (ly.n + CH - 1) / CH;
     int64_t cb, ce;
     block_range(nchunks, cb, ce);
@@ -149,7 +182,7 @@ __global__ __launch_bounds__(BLOCK) void k_sync_spec(SyncArgs a, SyncWs ws, Laye
             const int64_t ld = a.ld;
             stream_rows(
                 a.W, [&](int r) { return ld4(p + (int64_t)r * ld); },
-                [&]() { flush_sync(a, ws, pd); },
+                [&]() { flush_sync(a, ws, pd, st, ly.n); },
                 [&](const f4& x) {
                     const uint32_t b0 = f2u(x.x), b1 = f2u(x.y), b2 = f2u(x.z), b3 = f2u(x.w);
                     mx0 = b0 & 0x7FFFFFFFu;
@@ -229,7 +262,8 @@ __global__ __launch_bounds__(BLOCK) void k_sync_spec(SyncArgs a, SyncWs ws, Laye
         }
     }
     if (run_layer >= 0) block_max_atomic(run, maxabs + run_layer, red);
-    flush_sync(a, ws, pd);
+    flush_sync(a, ws, pd, st, ly.n);
+    drain_stage(a, ws, st, ly.n);
 }
 
 // Pass 1 over the chunks that mix palette entries, one block per layer
