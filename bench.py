@@ -226,39 +226,67 @@ def roundoff_study(groups=(4, 8, 16, 32, 64, 1)):
                                "1-5-2 with APS scales, synthetic", "error": result}), flush=True)
 
 
-def cpu_baseline(G_t, gs, pal, budget_s: float, slice_cols: int = 65536):
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _omp_threads(k: int | None) -> None:
+    """Set the OpenMP thread count of this process (the oracle's runtime)."""
+    import ctypes
+
+    if k is not None:
+        ctypes.CDLL("libgomp.so.1").omp_set_num_threads(int(k))
+
+
+def cpu_baseline(G_t, gs, pal, budget_s: float, slice_cols: int = 65536, single_s: float = 3.0):
     """The CPU oracle on successive column slices (all W workers) of the same
     gradient set until the time budget is used: max-abs, scales and the
-    rounded W-worker sum for each slice."""
+    rounded W-worker sum for each slice.  Run with all the OpenMP threads,
+    then on one thread over a shorter budget."""
     import numpy as np
 
     import oracle as O
 
     opal = [O.Format(f.e, f.m, f.bias) for f in pal]
     W, n = gs.W, gs.n
-    done = 0
-    spent = 0.0
-    start_col = 0
-    while spent < budget_s and start_col < n:
-        cols = min(slice_cols, n - start_col)
-        Gs = G_t[:, start_col:start_col + cols].cpu().numpy()
-        offs = gs.offsets
-        lo = np.searchsorted(offs, start_col, side="right") - 1
-        hi = np.searchsorted(offs, start_col + cols, side="left")
-        sub = np.clip(offs[lo:hi + 1] - start_col, 0, cols).astype(np.int64)
-        sub[0], sub[-1] = 0, cols
-        fi = None if gs.fmt_idx is None else gs.fmt_idx[lo:hi]
-        ldS = (cols + 3) // 4 * 4
-        Gp = np.zeros((W, ldS), np.float32)
-        Gp[:, :cols] = Gs
-        t0 = time.perf_counter()
-        mab = O.layer_maxabs(Gp, cols, sub)
-        se = O.layer_scales(mab, W, opal, fi)
-        O.sim_reduce(Gp, cols, sub, se, opal, fi)
-        spent += time.perf_counter() - t0
-        done += cols
-        start_col += cols
+
+    def run(budget):
+        done, spent, start_col = 0, 0.0, 0
+        while spent < budget and start_col < n:
+            cols = min(slice_cols, n - start_col)
+            Gs = G_t[:, start_col:start_col + cols].cpu().numpy()
+            offs = gs.offsets
+            lo = np.searchsorted(offs, start_col, side="right") - 1
+            hi = np.searchsorted(offs, start_col + cols, side="left")
+            sub = np.clip(offs[lo:hi + 1] - start_col, 0, cols).astype(np.int64)
+            sub[0], sub[-1] = 0, cols
+            fi = None if gs.fmt_idx is None else gs.fmt_idx[lo:hi]
+            ldS = (cols + 3) // 4 * 4
+            Gp = np.zeros((W, ldS), np.float32)
+            Gp[:, :cols] = Gs
+            t0 = time.perf_counter()
+            mab = O.layer_maxabs(Gp, cols, sub)
+            se = O.layer_scales(mab, W, opal, fi)
+            O.sim_reduce(Gp, cols, sub, se, opal, fi)
+            spent += time.perf_counter() - t0
+            done += cols
+            start_col += cols
+        return done, spent
+
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    O.lib()  # load the oracle (and its OpenMP runtime) before setting its thread count
+    _omp_threads(threads)
+    done, spent = run(budget_s)
+    _omp_threads(1)
+    done1, spent1 = run(single_s)
+    _omp_threads(threads)
     return {
         "value": W * done / spent,
         "unit": "elements/s",
@@ -266,6 +294,9 @@ def cpu_baseline(G_t, gs, pal, budget_s: float, slice_cols: int = 65536):
         "kind": "oracle",
         "sample": f"first {done} of {n} elements x all {W} workers, in {slice_cols}-element column slices "
                   f"(max-abs + scales + rounded W-worker sum), {spent:.1f} s",
+        "single_thread_value": W * done1 / spent1,
+        "single_thread_sample": f"first {done1} elements x all {W} workers, {spent1:.1f} s",
+        "cpu_model": _cpu_model(),
     }
 
 
@@ -438,6 +469,7 @@ def main():
         "metric": METRIC,
         "value": W * n / (ms_per_step * 1e-3),
         "unit": "elements/s",
+        "reduced_elements_per_s": n / (ms_per_step * 1e-3),
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
