@@ -1,6 +1,8 @@
 // aps_sync.hip -- one whole APS synchronisation in one call (Algorithm 1 with
 // the low-precision accumulator of Sec. 5), reading the W workers'
 // gradients once where it can.
+#include <algorithm>
+
 #include "aps_common.hpp"
 
 namespace aps {
@@ -790,9 +792,15 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
     if (!guess && (phases & APS_SYNC_PASS1)) {
         hipLaunchKernelGGL(k_sync_clear, lgrid, dim3(256), 0, s, maxabs_bits, L);
         if (n > 0) {
-            // launch width measured on MI355X: 24 blocks per CU for many rows,
-            // 32 when each chunk is only a few rows (shorter work per chunk)
-            const int per_cu = W >= 64 ? 24 : 32;
+            // launch width measured on MI355X: 24 blocks per CU for many rows;
+            // for few rows 32, except on large sets (2^17 chunks or more),
+            // which run fastest in blocks of about 2.5 chunks each
+            int per_cu = 24;
+            if (W < 64) {
+                const int dc = device_cus();
+                const int64_t cus = dc > 0 ? dc : 256;
+                per_cu = nchunks >= ((int64_t)1 << 17) ? (int)std::min<int64_t>(512, nchunks * 2 / (cus * 5)) : 32;
+            }
             hipLaunchKernelGGL(k_sync_spec, dim3((unsigned)grid_for(nchunks, per_cu)), dim3(BLOCK), 0, s, sa, ws, ly,
                                pal, maxabs_bits);
             if (mixed)
