@@ -217,7 +217,7 @@ extern "C" int aps_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n, 
     Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
     ReduceArgs a{G, out, (uint8_t*)codes_out, ld, W, flags, ccls};
     const int64_t nchunks = (n + CH - 1) / CH;
-    const dim3 grid((unsigned)grid_for(nchunks, BLOCKS_PER_CU));
+    const dim3 grid((unsigned)stream_grid(nchunks, W, BLOCKS_PER_CU));
     const unsigned vm = variant_mask(pal, n_fmts);
 #define APS_LAUNCH_R(v) \
     if (vm & (1u << (v))) hipLaunchKernelGGL(k_sim_reduce<v>, grid, dim3(BLOCK), 0, s, a, ly, pal);

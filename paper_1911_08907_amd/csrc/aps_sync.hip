@@ -1,8 +1,6 @@
 // aps_sync.hip -- one whole APS synchronisation in one call (Algorithm 1 with
 // the low-precision accumulator of Sec. 5), reading the W workers'
 // gradients once where it can.
-#include <algorithm>
-
 #include "aps_common.hpp"
 
 namespace aps {
@@ -768,7 +766,8 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
     const dim3 lgrid((unsigned)((L + 255) / 256));
     const bool mixed = fmt_idx && n_fmts > 1 && L > 1;
     const unsigned vm = variant_mask(pal, n_fmts);
-    const dim3 grid((unsigned)grid_for(nchunks, BLOCKS_PER_CU));
+    const dim3 grid((unsigned)stream_grid(nchunks, W, BLOCKS_PER_CU));  // pass-1 row walks
+    const dim3 rgrid((unsigned)grid_for(nchunks, BLOCKS_PER_CU));         // repairs: the list's length is on the device
     ReduceArgs ra{G, out, nullptr, ld, W, 0u, 0};
     SyncArgs sa{G, out, ld, W};
     const bool guess = route == APS_SYNC_ROUTE_GUESS;
@@ -792,17 +791,10 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
     if (!guess && (phases & APS_SYNC_PASS1)) {
         hipLaunchKernelGGL(k_sync_clear, lgrid, dim3(256), 0, s, maxabs_bits, L);
         if (n > 0) {
-            // launch width measured on MI355X: 24 blocks per CU for many rows;
-            // for few rows 32, except on large sets (2^17 chunks or more),
-            // which run fastest in blocks of about 2.5 chunks each
-            int per_cu = 24;
-            if (W < 64) {
-                const int dc = device_cus();
-                const int64_t cus = dc > 0 ? dc : 256;
-                per_cu = nchunks >= ((int64_t)1 << 17) ? (int)std::min<int64_t>(512, nchunks * 2 / (cus * 5)) : 32;
-            }
-            hipLaunchKernelGGL(k_sync_spec, dim3((unsigned)grid_for(nchunks, per_cu)), dim3(BLOCK), 0, s, sa, ws, ly,
-                               pal, maxabs_bits);
+            // launch width measured on MI355X: 24 blocks per CU for many rows,
+            // 32 for few (shorter work per chunk), wider on large sets
+            hipLaunchKernelGGL(k_sync_spec, dim3((unsigned)stream_grid(nchunks, W, W >= 64 ? 24 : 32)), dim3(BLOCK), 0,
+                               s, sa, ws, ly, pal, maxabs_bits);
             if (mixed)
                 hipLaunchKernelGGL(k_sync_spec_mixed, dim3((unsigned)L), dim3(BLOCK), 0, s, sa, ws, ly, pal, maxabs_bits);
         }
@@ -815,7 +807,7 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
         if (n > 0) {
             hipLaunchKernelGGL(k_sync_scan, dim3((unsigned)((nchunks + 255) / 256)), dim3(256), 0, s, ly, ws, guess);
 #define APS_LAUNCH_S(v) \
-    if (vm & (1u << (v))) hipLaunchKernelGGL(k_sync_repair<v>, grid, dim3(BLOCK), 0, s, ra, ly, pal, ws, rmode);
+    if (vm & (1u << (v))) hipLaunchKernelGGL(k_sync_repair<v>, rgrid, dim3(BLOCK), 0, s, ra, ly, pal, ws, rmode);
             APS_FOR_VARIANTS(APS_LAUNCH_S)
 #undef APS_LAUNCH_S
             if (mixed)
