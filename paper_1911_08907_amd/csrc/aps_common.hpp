@@ -498,12 +498,62 @@ __device__ __forceinline__ void flush_out(const ReduceArgs& a, PendingOut& pd) {
     if (a.codes) store_codes4(a.codes, pd.j, pd.c, a.code_cls, pd.lim);
 }
 
+// Finished fp32 outputs waiting in LDS, each thread in its own slots (no
+// other thread reads them, so no barrier), written OUT_STAGE chunks at a
+// time or when the block is done: writes in the middle of the row reads cost
+// the streaming kernels more than their bytes, and fewer, larger bursts of
+// them cost less.  For outputs without codes.
+constexpr int OUT_STAGE = 6;
+
+struct OutStage {
+    f4* o;        // [OUT_STAGE][BLOCK]
+    int32_t* j;   // first element (n <= 2^30)
+    int32_t* lim; // elements >= lim are not written
+    int cnt;      // this thread's filled slots
+};
+
+__device__ __forceinline__ void drain_out(const ReduceArgs& a, OutStage& st) {
+    const int t = threadIdx.x;
+    for (int s = 0; s < st.cnt; ++s) {
+        const int64_t j = st.j[s * BLOCK + t], lim = st.lim[s * BLOCK + t];
+        const f4 o = st.o[s * BLOCK + t];
+        if (j + 4 <= lim) {
+            __builtin_nontemporal_store(o, (f4*)(a.out + j));
+        } else {
+            if (j < lim) a.out[j] = o.x;
+            if (j + 1 < lim) a.out[j + 1] = o.y;
+            if (j + 2 < lim) a.out[j + 2] = o.z;
+        }
+    }
+    st.cnt = 0;
+}
+
+// Moves the pending record into the stage.  The caller drains a full stage
+// between chunks (drain_if_full), outside the row loop.
+__device__ __forceinline__ void stage_out(PendingOut& pd, OutStage& st) {
+    if (!pd.valid) return;
+    pd.valid = false;
+    const int t = threadIdx.x;
+    st.o[st.cnt * BLOCK + t] = pd.o;
+    st.j[st.cnt * BLOCK + t] = (int32_t)pd.j;
+    st.lim[st.cnt * BLOCK + t] = (int32_t)pd.lim;
+    ++st.cnt;
+}
+
+__device__ __forceinline__ void drain_if_full(const ReduceArgs& a, OutStage& st) {
+    if (st.cnt == OUT_STAGE) drain_out(a, st);
+}
+
+
 // The fused scale + cast + rounded sum + unscale of 4 consecutive elements
 // over the W rows.  With MAX it also returns the largest |x| bit pattern of
 // each of the 4 columns in mx (rows past the end read as -0: no effect).
+// With a stage (no codes), the previous chunk's outputs go to it instead of
+// straight to memory; the stage must have a free slot (drain_if_full).
 template <int V, bool MAX = false>
 __device__ __forceinline__ void reduce_vec(const ReduceArgs& a, const FmtK& f, int64_t j, int64_t lim,
-                                           const int32_t ft[4], PendingOut& pd, uint32_t* mx = nullptr) {
+                                           const int32_t ft[4], PendingOut& pd, uint32_t* mx = nullptr,
+                                           OutStage* st = nullptr) {
     const bool inq = a.flags & APS_INPUT_QUANTIZED;
     const bool outs = a.flags & APS_OUTPUT_SCALED;
     int F[4], Fo[4];
@@ -522,7 +572,12 @@ __device__ __forceinline__ void reduce_vec(const ReduceArgs& a, const FmtK& f, i
     const f4 neg0 = {-0.0f, -0.0f, -0.0f, -0.0f};
     stream_rows(
         a.W, [&](int r) { return ld4(p + (int64_t)r * ld); },
-        [&]() { flush_out(a, pd); },  // the previous chunk's outputs, behind this chunk's loads
+        [&]() {  // the previous chunk's outputs, behind this chunk's loads
+            if (st)
+                stage_out(pd, *st);
+            else
+                flush_out(a, pd);
+        },
         [&](const f4& x) {
             if constexpr (MAX) {
                 m0 = f2u(x.x) & 0x7FFFFFFFu;

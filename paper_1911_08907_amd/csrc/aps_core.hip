@@ -92,8 +92,13 @@ __global__ void k_scales(const uint32_t* __restrict__ maxabs, int32_t L, int32_t
     scale_exp[i] = r;
 }
 
-template <int V>
+// ST: the outputs go through an LDS stage (no codes written).
+template <int V, bool ST>
 __global__ __launch_bounds__(BLOCK) void k_sim_reduce(ReduceArgs a, Layers ly, Pal pal) {
+    __shared__ f4 st_o[ST ? OUT_STAGE * BLOCK : 1];
+    __shared__ int32_t st_j[ST ? OUT_STAGE * BLOCK : 1];
+    __shared__ int32_t st_lim[ST ? OUT_STAGE * BLOCK : 1];
+    OutStage stage{st_o, st_j, st_lim, 0};
     const int64_t nchunks = (ly.n + CH - 1) / CH;
     int64_t cb, ce;
     block_range(nchunks, cb, ce);
@@ -117,9 +122,16 @@ __global__ __launch_bounds__(BLOCK) void k_sim_reduce(ReduceArgs a, Layers ly, P
         } else {
             elem_scales(ly, ci, j, ft);
         }
-        reduce_vec<V>(a, f, j, end, ft, pd);
+        if constexpr (ST) drain_if_full(a, stage);
+        reduce_vec<V>(a, f, j, end, ft, pd, nullptr, ST ? &stage : nullptr);
     }
-    flush_out(a, pd);
+    if constexpr (ST) {
+        drain_if_full(a, stage);
+        stage_out(pd, stage);
+        drain_out(a, stage);
+    } else {
+        flush_out(a, pd);
+    }
 }
 
 // Chunks whose layers use different palette entries, element by element.
@@ -219,8 +231,13 @@ extern "C" int aps_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n, 
     const int64_t nchunks = (n + CH - 1) / CH;
     const dim3 grid((unsigned)stream_grid(nchunks, W, BLOCKS_PER_CU));
     const unsigned vm = variant_mask(pal, n_fmts);
-#define APS_LAUNCH_R(v) \
-    if (vm & (1u << (v))) hipLaunchKernelGGL(k_sim_reduce<v>, grid, dim3(BLOCK), 0, s, a, ly, pal);
+#define APS_LAUNCH_R(v)                                                                             \
+    if (vm & (1u << (v))) {                                                                         \
+        if (codes_out)                                                                              \
+            hipLaunchKernelGGL((k_sim_reduce<v, false>), grid, dim3(BLOCK), 0, s, a, ly, pal);       \
+        else                                                                                        \
+            hipLaunchKernelGGL((k_sim_reduce<v, true>), grid, dim3(BLOCK), 0, s, a, ly, pal);        \
+    }
     APS_FOR_VARIANTS(APS_LAUNCH_R)
 #undef APS_LAUNCH_R
     if (fmt_idx && n_fmts > 1 && L > 1)
