@@ -188,7 +188,7 @@ int aps_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n,
 /*
  * Bytes of workspace aps_sync needs for n elements and L layers, with
  * C = ceil(n / 1024) chunks: round_up(1024 * C, 256) + round_up(4 * C, 256)
- * + round_up(4 * L, 256) + 256 + round_up(4 * C, 256).  Host-only.
+ * + round_up(4 * L, 256) + 256 + round_up(4 * C, 256) + 2048 * C.  Host-only.
  * Returns 0 for negative arguments or n > APS_MAX_ELEMS.
  */
 uint64_t aps_sync_workspace_bytes(int64_t n, int32_t L);
@@ -214,7 +214,9 @@ int aps_sync_route(int32_t W, int64_t n, const aps_format* fmts, int32_t n_fmts,
  * commutes with rounding to m+1 significant bits (Sec. 3.3.1), so pass 1
  * forms the rounded sum on the unscaled values while it takes the layer
  * maxima, and records one byte per element (with fewer than 64 workers only
- * the minimum byte of each 256-element group).  Pass 2 computes the scales
+ * the minimum byte of each 256-element group).  From 128 workers on, with
+ * every palette format m <= 7, it keeps each sum in 2 bytes of the workspace
+ * (its fp32 pattern's low 16 bits are zero) and pass 2 widens them into out.  Pass 2 computes the scales
  * and recomputes through the scaled path only the elements for which the
  * unscaled sum can differ (below 64 workers: the whole groups that hold
  * one): those with a nonzero input below

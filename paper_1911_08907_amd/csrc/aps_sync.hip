@@ -59,8 +59,18 @@ struct SyncWs {
     int32_t* __restrict__ thr;   // [L] repair threshold per layer
     uint32_t* __restrict__ count;  // chunks listed for repair
     int32_t* __restrict__ list;    // [nchunks] those chunks
+    uint16_t* __restrict__ half;   // [round_up(n, CH)] top halves of the pass-1 sums, or null
     bool bytes;                    // pass 1 stores minb for the single-entry chunks
 };
+
+// From this many workers on, and when every palette entry has m <= 7, pass 1
+// writes each sum's top 16 bits instead of the fp32 value: the unscaled
+// chain keeps m+1 significant bits, so the low 16 bits of its fp32 pattern
+// are zero.  Pass 2 widens them into out (k_sync_widen).  Writes in the
+// middle of pass 1's row reads cost far more than their bytes at large W;
+// the widening is one short streaming pass.  At small W the writes cost
+// less and the widening more than it saves.
+constexpr int32_t SYNC_HALF_MIN_W = 128;
 
 // Fewer workers than this: pass 1 keeps only the per-wave minima, and pass 2
 // reruns each 256-element group whose minimum is below its chunk's largest
@@ -118,7 +128,12 @@ __device__ __forceinline__ void drain_stage(const SyncArgs& a, const SyncWs& ws,
         const int64_t j = st.j[s * BLOCK + t];
         const int64_t lim = min((j / CH) * CH + CH, n);
         const f4 o = st.o[s * BLOCK + t];
-        if (j + 4 <= lim) {
+        if (ws.half) {
+            // elements j, j+1 in the first word (low half first); the array is
+            // padded to whole chunks, so all 8 bytes are in bounds
+            const u2v h = {(f2u(o.x) >> 16) | (f2u(o.y) & 0xFFFF0000u), (f2u(o.z) >> 16) | (f2u(o.w) & 0xFFFF0000u)};
+            __builtin_nontemporal_store(h, (u2v*)(ws.half + j));
+        } else if (j + 4 <= lim) {
             __builtin_nontemporal_store(o, (f4*)(a.out + j));
         } else {
             if (j < lim) a.out[j] = o.x;
@@ -292,7 +307,10 @@ __global__ __launch_bounds__(BLOCK) void k_sync_spec_mixed(SyncArgs a, SyncWs ws
             mn = min(mn, max(ab - 1u, f2u(u2f(f2u(s) & 0x7FFFFFFFu) * sc)));
             s = u2f(rho(f2u(s + u2f(rho(b, f.half, f.sh, f.lsbw, f.mask))), f.half, f.sh, f.lsbw, f.mask));
         }
-        a.out[j] = s;
+        if (ws.half)
+            ws.half[j] = (uint16_t)(f2u(s) >> 16);
+        else
+            a.out[j] = s;
         ws.minb[j] = (uint8_t)min(mn >> 23, 255u);
         if (mx) atomicMax(maxabs + li, mx);
     }
@@ -517,6 +535,25 @@ __global__ __launch_bounds__(BLOCK) void k_sync_repair_mixed(ReduceArgs a, Layer
     }
 }
 
+// Pass 2, before the repairs: the pass-1 sums kept as top halves, widened
+// to fp32 into out (8 elements per thread).
+__global__ __launch_bounds__(BLOCK) void k_sync_widen(const uint16_t* __restrict__ half, float* __restrict__ out,
+                                                     int64_t n) {
+    const int64_t stride = (int64_t)gridDim.x * BLOCK * 8;
+    for (int64_t j = ((int64_t)blockIdx.x * BLOCK + threadIdx.x) * 8; j < n; j += stride) {
+        const u4v h = __builtin_nontemporal_load((const u4v*)(half + j));  // padded to whole chunks
+        const f4 a = {u2f(h.x << 16), u2f(h.x & 0xFFFF0000u), u2f(h.y << 16), u2f(h.y & 0xFFFF0000u)};
+        const f4 b = {u2f(h.z << 16), u2f(h.z & 0xFFFF0000u), u2f(h.w << 16), u2f(h.w & 0xFFFF0000u)};
+        if (j + 8 <= n) {
+            __builtin_nontemporal_store(a, (f4*)(out + j));
+            __builtin_nontemporal_store(b, (f4*)(out + j + 4));
+        } else {
+            const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+            for (int e = 0; e < 8 && j + e < n; ++e) out[j + e] = v[e];
+        }
+    }
+}
+
 // ======================================= K5b: the guessed-scale route
 //
 // For a format of narrow range at large W most elements have an input in
@@ -652,9 +689,10 @@ using namespace aps;
 
 // Workspace of aps_sync, in 256-byte aligned parts: the per-element exponent
 // bytes (padded to whole chunks), four bytes per chunk, the int32 layer
-// thresholds, the list counter, the int32 chunk list.
+// thresholds, the list counter, the int32 chunk list, two bytes per element
+// (padded to whole chunks) for the top halves of the pass-1 sums.
 struct SyncLayout {
-    uint64_t minb, wmin, thr, count, list, total;
+    uint64_t minb, wmin, thr, count, list, half, total;
 };
 
 static uint64_t up256(uint64_t b) { return (b + 255u) & ~(uint64_t)255u; }
@@ -667,7 +705,8 @@ static SyncLayout sync_layout(int64_t n, int32_t L) {
     o.thr = o.wmin + up256(4u * nch);
     o.count = o.thr + up256(4u * (uint64_t)L);
     o.list = o.count + 256u;
-    o.total = o.list + up256(4u * nch);
+    o.half = o.list + up256(4u * nch);
+    o.total = o.half + up256(2u * nch * (uint64_t)CH);
     return o;
 }
 
@@ -746,9 +785,14 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
     const int64_t nchunks = (n + CH - 1) / CH;
     uint8_t* wb = (uint8_t*)workspace;
     SyncWs ws{wb + lay.minb, wb + lay.wmin, (int32_t*)(wb + lay.thr), (uint32_t*)(wb + lay.count),
-              (int32_t*)(wb + lay.list), W >= SYNC_BYTES_MIN_W};
+              (int32_t*)(wb + lay.list), nullptr, W >= SYNC_BYTES_MIN_W};
     Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
     const int route = sync_route(W, n, pal, n_fmts, flags);
+    if (route == APS_SYNC_ROUTE_ONE_PASS && W >= SYNC_HALF_MIN_W) {
+        bool narrow = true;
+        for (int i = 0; i < n_fmts; ++i) narrow = narrow && pal.f[i].m <= 7;
+        if (narrow) ws.half = (uint16_t*)(wb + lay.half);
+    }
     if (route == APS_SYNC_ROUTE_TWO_PASS) {
         // two passes: exactly the three calls of the step
         if (phases & APS_SYNC_PASS1) {
@@ -806,6 +850,12 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
             hipLaunchKernelGGL(k_sync_layers, lgrid, dim3(256), 0, s, maxabs_bits, L, W, pal, fmt_idx, scale_exp, ws);
         if (n > 0) {
             hipLaunchKernelGGL(k_sync_scan, dim3((unsigned)((nchunks + 255) / 256)), dim3(256), 0, s, ly, ws, guess);
+            if (ws.half) {
+                const int64_t threads = (n + 7) / 8;
+                // one pass per thread: up to 64 blocks per CU
+                hipLaunchKernelGGL(k_sync_widen, dim3((unsigned)grid_for((threads + BLOCK - 1) / BLOCK, 64)), dim3(BLOCK),
+                                   0, s, ws.half, out, n);
+            }
 #define APS_LAUNCH_S(v) \
     if (vm & (1u << (v))) hipLaunchKernelGGL(k_sync_repair<v>, rgrid, dim3(BLOCK), 0, s, ra, ly, pal, ws, rmode);
             APS_FOR_VARIANTS(APS_LAUNCH_S)
