@@ -454,6 +454,10 @@ def main():
     if one:
         kernel, k_ms = "k_sync_spec", p1
         note = "pass-1 span: k_sync_spec plus the zeroing of the L maxima (k_sync_clear, a few us)"
+        if W >= 128 and all(f.m <= 7 for f in pal):
+            # pass 1 keeps each sum in 2 bytes; pass 2 widens them into the fp32 output
+            alg_bytes = 4.0 * W * n + 2.0 * n
+            note += "; the sums written as 2-byte top halves (pass 2 widens them)"
     elif guess:
         # pass 1 also reads every 32nd worker row for the sampled maxima
         alg_bytes += 4.0 * ((W + 31) // 32) * n
