@@ -128,7 +128,7 @@ SIZES = [0, 1, 3, 5, 7, 1023, 1024, 1025, 2049, 0, 64, 13, 4095, 2, 3000]
 def test_sync_edge_layouts(dev, f, kind):
     rng = np.random.default_rng(hash(("sync", str(f), kind)) & 0xFFFF)
     offs, n, ld = _layout(SIZES)
-    for W in (1, 2, 4, 8, 16, 3, 13, 40):
+    for W in (1, 2, 4, 8, 16, 3, 13, 40, 256):
         G = _values(rng, W, ld, offs, kind)
         tag = f"{f} {kind} W={W}"
         log("case", tag)
@@ -171,8 +171,9 @@ def test_sync_threshold_inputs(dev, f):
     rng = np.random.default_rng(500 + f.e * 16 + f.m)
     sizes = [1, 7, 1024, 3000, 2, 5000, 64, 1025]
     offs, n, ld = _layout(sizes)
-    for W in (1, 2, 4, 8, 64):
+    for W in (1, 2, 4, 8, 64, 256):
         # maxima spread from tiny (threshold below 2^-126) to near fp32's top
+        # (W = 256 with m <= 7: pass 1 keeps 2-byte sums)
         G = threshold_values(rng, W, ld, offs, f, LAYER_MAXIMA)
         tag = f"{f} thresholds W={W}"
         log("case", tag)
