@@ -148,7 +148,7 @@ def test_sync_mixed_palette(dev, seed):
     sizes = [int(v) for v in rng.choice([0, 1, 2, 3, 5, 17, 255, 1000, 1023, 1024, 1500, 4096], 40)]
     offs, n, ld = _layout(sizes)
     fmt_idx = rng.integers(0, len(pal), len(sizes)).astype(np.uint8)
-    for W in (2, 8, 5):
+    for W in (2, 8, 5, 256):  # 256: 2-byte pass-1 sums where every format has m <= 7
         for kind in ("normal", "special", "tiny"):
             G = _values(rng, W, ld, offs, kind)
             tag = f"mixed seed={seed} W={W} {kind}"
