@@ -37,7 +37,12 @@ namespace aps {
 // fails.  The second pass lists the chunks holding such an element (from
 // one byte per 256 elements), then recomputes those elements through the
 // scaled path: one wave per element when few elements of a chunk fail, the
-// whole chunk with the streaming kernel's row walk when many do.
+// whole chunk with the streaming kernel's row walk when many do.  With fewer
+// than SYNC_BYTES_MIN_W workers only the per-256 minima are kept and whole
+// 256-element groups are rerun; from SYNC_HALF_MIN_W workers on (m <= 7)
+// the sums themselves are kept in 2 bytes and widened in the second pass.
+// An accepted sum is a multiple of 2^(-126 - m) (T >= 2^-126), so its fp32
+// pattern, normal or not, has no bits below position 23 - m >= 16.
 
 // Zero the layer maxima before pass 1 accumulates them with atomicMax.
 __global__ void k_sync_clear(uint32_t* __restrict__ maxabs, int32_t L) {
