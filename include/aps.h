@@ -213,18 +213,18 @@ int aps_sync_route(int32_t W, int64_t n, const aps_format* fmts, int32_t n_fmts,
  * The one-pass route reads G once instead of twice.  Power-of-two scaling
  * commutes with rounding to m+1 significant bits (Sec. 3.3.1), so pass 1
  * forms the rounded sum on the unscaled values while it takes the layer
- * maxima, and records one byte per element (with fewer than 64 workers only
- * the minimum byte of each 256-element group).  From 128 workers on, with
- * every palette format m <= 7, it keeps each sum in 2 bytes of the workspace
- * (its fp32 pattern's low 16 bits are zero) and pass 2 widens them into out.  Pass 2 computes the scales
- * and recomputes through the scaled path only the elements for which the
- * unscaled sum can differ (below 64 workers: the whole groups that hold
- * one): those with a nonzero input below
- * T = max(2^(emin - ft), 2^-126) (the format's subnormal range after
- * scaling) that is not swamped, i.e. that comes from worker 0 or meets a
- * partial sum below 2^(m+3) * T, and every element of a layer whose max is
- * INF or NaN or whose N * ghat exceeds 2^127.  The route applies when W is
- * a power of two and every palette format has m <= 10.
+ * maxima.  Pass 2 computes the scales and recomputes through the scaled
+ * path only the elements for which the unscaled sum can differ: those with
+ * a nonzero input below T = max(2^(emin - ft), 2^-126) (the format's
+ * subnormal range after scaling) that is not swamped, i.e. that comes from
+ * worker 0 or meets a partial sum below 2^(m+3) * T, and every element of a
+ * layer whose max is INF or NaN or whose N * ghat exceeds 2^127.  Pass 1
+ * records one byte per element to find them (with fewer than 64 workers only
+ * the minimum byte of each 256-element group, and pass 2 reruns whole
+ * groups).  From 128 workers on, with every palette format m <= 7, pass 1
+ * keeps each sum in 2 bytes of the workspace (its fp32 pattern's low 16 bits
+ * are zero) and pass 2 widens them into out.  The route applies when W is a
+ * power of two and every palette format has m <= 10.
  *
  * The guessed-scale route applies to every W and format.  Pass 1 takes the
  * layer maxima of every 32nd worker (rows 0, 32, 64, ...), guesses each
