@@ -17,7 +17,10 @@ adds, rounding on fp32 bit patterns, the per-element byte and the per-layer
 threshold) in numpy; it shares nothing with the HIP library or the oracle.
 The tests check that every element the criterion accepts matches the oracle
 bit for bit, and that elements it rejects do differ in some of the cases
-(so the recomputation is needed and the test can fail)."""
+(so the recomputation is needed and the test can fail).  They also check
+what lets the route keep its sums in 2 bytes for m <= 7: an accepted sum is
+a multiple of 2^(-126 - m), so the low 16 bits of its fp32 pattern are
+zero."""
 import numpy as np
 import pytest
 
@@ -97,6 +100,9 @@ def _check(G, n, offs, f, W):
     nan = np.isnan(s[ok]) & np.isnan(ref[ok])
     bad = (a != b) & ~nan
     assert not bad.any(), (str(f), W, np.nonzero(ok)[0][bad][:5])
+    if f.m <= 7:
+        low = ((a & np.uint32(0xFFFF)) != 0) & ~nan
+        assert not low.any(), (str(f), W, "accepted sums with bits below 2^16", np.nonzero(ok)[0][low][:5])
     fa, fb = s[flagged], ref[flagged]
     differ = ~((fa.view(np.uint32) == fb.view(np.uint32)) | (np.isnan(fa) & np.isnan(fb)))
     return int(flagged.sum()), int(differ.sum())
@@ -107,7 +113,7 @@ def test_accepted_elements_match_the_oracle(f):
     rng = np.random.default_rng(700 + 16 * f.e + f.m)
     offs, n, ld = _layout([1, 7, 900, 2, 1500, 64, 300, 33])
     n_flag = n_diff = 0
-    for W in (1, 2, 4, 8, 64):
+    for W in (1, 2, 4, 8, 64, 256):
         G = threshold_values(rng, W, ld, offs, f, LAYER_MAXIMA)
         a, b = _check(G, n, offs, f, W)
         n_flag += a
