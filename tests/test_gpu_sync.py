@@ -11,7 +11,10 @@ guessed-scale route (the scaled sum formed with exponents guessed from every
 inputs exactly at, just above and just below each layer's threshold
 2^(emin - ft), in fp32's subnormal range, in layers with INF/NaN or with a
 maximum near fp32's top, and make chunks with few and with many elements to
-recompute, so that both repair routes run."""
+recompute, so that both repair routes run.  Worker counts span the three
+modes of the one-pass route's pass 1: fewer than 64 workers (no per-element
+bytes, whole 256-element groups rerun), 64 and more (per-element bytes), and
+from 128 with m <= 7 (the sums kept in 2 bytes and widened in pass 2)."""
 import time
 
 import numpy as np
