@@ -486,13 +486,15 @@ def test_sync_short_last_chunk_keeps_the_previous_chunks_bytes(dev):
     assert same_f32(gv, o_s), first_diff(gv, o_s)
 
 
-@pytest.mark.parametrize("route", [A.APS_SYNC_ONE_PASS, A.APS_SYNC_TWO_PASS, A.APS_SYNC_GUESS],
-                         ids=["one_pass", "two_passes", "guessed_scales"])
-def test_sync_hip_graph_replays(dev, route):
+@pytest.mark.parametrize("route,W", [(A.APS_SYNC_ONE_PASS, 8), (A.APS_SYNC_TWO_PASS, 8), (A.APS_SYNC_GUESS, 8),
+                                     (A.APS_SYNC_ONE_PASS, 256)],
+                         ids=["one_pass", "two_passes", "guessed_scales", "one_pass_two_byte_sums"])
+def test_sync_hip_graph_replays(dev, route, W):
     """aps_sync enqueues kernels only (no memset, no allocation), so it can be
     captured in a HIP graph: three replays on new inputs, with eager work
-    between them, each against the oracle."""
-    gs = WL.generate("resnet20", "1-5-2", device=dev)
+    between them, each against the oracle.  At W = 256 the one-pass route
+    keeps its sums in 2 bytes and widens them in pass 2."""
+    gs = WL.generate("resnet20", "1-5-2", device=dev, W=W)
     W, n, L = gs.W, gs.n, len(gs.sizes)
     pal = [F(5, 2)]
     opal = [ofmt(f) for f in pal]
