@@ -237,12 +237,16 @@ def _cpu_model() -> str:
     return "unknown"
 
 
-def _omp_threads(k: int | None) -> None:
-    """Set the OpenMP thread count of this process (the oracle's runtime)."""
+def _omp_threads(k: int) -> bool:
+    """Set the OpenMP thread count of this process (the oracle's runtime);
+    False if the runtime cannot be reached."""
     import ctypes
 
-    if k is not None:
+    try:
         ctypes.CDLL("libgomp.so.1").omp_set_num_threads(int(k))
+    except (OSError, AttributeError):
+        return False
+    return True
 
 
 def cpu_baseline(G_t, gs, pal, budget_s: float, slice_cols: int = 65536, single_s: float = 3.0):
@@ -282,11 +286,13 @@ def cpu_baseline(G_t, gs, pal, budget_s: float, slice_cols: int = 65536, single_
 
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     O.lib()  # load the oracle (and its OpenMP runtime) before setting its thread count
-    _omp_threads(threads)
+    can_set = _omp_threads(threads)
     done, spent = run(budget_s)
-    _omp_threads(1)
-    done1, spent1 = run(single_s)
-    _omp_threads(threads)
+    single = None
+    if can_set and _omp_threads(1):
+        done1, spent1 = run(single_s)
+        _omp_threads(threads)
+        single = (W * done1 / spent1, f"first {done1} elements x all {W} workers, {spent1:.1f} s")
     return {
         "value": W * done / spent,
         "unit": "elements/s",
@@ -294,8 +300,8 @@ def cpu_baseline(G_t, gs, pal, budget_s: float, slice_cols: int = 65536, single_
         "kind": "oracle",
         "sample": f"first {done} of {n} elements x all {W} workers, in {slice_cols}-element column slices "
                   f"(max-abs + scales + rounded W-worker sum), {spent:.1f} s",
-        "single_thread_value": W * done1 / spent1,
-        "single_thread_sample": f"first {done1} elements x all {W} workers, {spent1:.1f} s",
+        "single_thread_value": single[0] if single else None,
+        "single_thread_sample": single[1] if single else "OpenMP runtime not reachable: not measured",
         "cpu_model": _cpu_model(),
     }
 
