@@ -33,8 +33,9 @@
  * Algorithm 1's upper_bound_exp as emax and Table 2's ranges.
  *
  * Memory.  Every array argument except `fmts` is DEVICE memory owned by the
- * caller.  `fmts` is HOST memory, read during the call only.  The library
- * allocates nothing and keeps no state between calls.
+ * caller.  `fmts` is HOST memory, read during the call only.  The calls
+ * allocate nothing and keep no state between calls; the one static device
+ * array of aps_sync_noalloc (below) is the only memory the library holds.
  *
  * Streams.  `stream` is a hipStream_t (NULL = the default stream).  A call
  * validates its arguments on the host, enqueues its kernels on `stream` and
@@ -270,6 +271,34 @@ int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n,
              const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,
              uint32_t flags, uint32_t* maxabs_bits, int32_t* scale_exp, float* out,
              void* workspace, uint64_t workspace_bytes, void* stream);
+
+/*
+ * aps_sync for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  It
+ * takes no workspace argument; its workspace is a static device array of
+ * APS_SYNC_SCRATCH_BYTES bytes that the HIP runtime places on each GPU when
+ * it loads this library's code there, and that stays until the process
+ * ends.  The call itself allocates nothing: no hipMalloc, no hipFree, no
+ * allocating library routine.
+ *
+ * Arguments, results, routes, flags and errors are those of aps_sync.  In
+ * addition, a set whose aps_sync_workspace_bytes(n, L) exceeds
+ * APS_SYNC_SCRATCH_BYTES returns APS_ERR_SIZE before anything is enqueued
+ * (96 MiB holds sets up to about 33 M elements, e.g. the 25.6 M of a
+ * ResNet-50).  The stream must belong to the current device.
+ *
+ * Every call on one GPU uses that GPU's one array, whose contents the call
+ * does not rely on (each pass writes what it later reads).  Calls that
+ * overlap on one GPU (two streams, two threads, or pass 1 of one set issued
+ * between pass 1 and pass 2 of another) race on it and give undefined
+ * results; serialise them.
+ */
+#define APS_SYNC_SCRATCH_BYTES ((uint64_t)96 << 20)
+int aps_sync_noalloc(const float* G, int32_t W, int64_t ld, int64_t n,
+                     const int64_t* offsets, int32_t L,
+                     const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,
+                     uint32_t flags, uint32_t* maxabs_bits, int32_t* scale_exp, float* out,
+                     void* stream);
 
 /* Summation order and accumulator of aps_sim_reduce_ex. */
 enum { APS_ACC_SEQUENTIAL = 0, APS_ACC_KAHAN = 1 };

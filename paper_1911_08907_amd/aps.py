@@ -29,7 +29,7 @@ APS_MAX_FORMATS = 8
 
 EXPORTS = ("aps_format_supported", "aps_layer_maxabs", "aps_layer_scales", "aps_quantize",
            "aps_sim_reduce", "aps_sim_reduce_ex", "aps_sim_reduce_codes", "aps_dequantize", "aps_lp_gemm",
-           "aps_sync_workspace_bytes", "aps_sync_route", "aps_sync", "aps_strerror")
+           "aps_sync_workspace_bytes", "aps_sync_route", "aps_sync", "aps_sync_noalloc", "aps_strerror")
 
 APS_ACC_SEQUENTIAL = 0
 APS_ACC_KAHAN = 1
@@ -42,6 +42,7 @@ APS_SYNC_GUESS = 16
 APS_SYNC_ROUTE_TWO_PASS = 0
 APS_SYNC_ROUTE_ONE_PASS = 1
 APS_SYNC_ROUTE_GUESS = 2
+APS_SYNC_SCRATCH_BYTES = 96 << 20
 
 
 class ApsError(RuntimeError):
@@ -112,6 +113,7 @@ def lib() -> ctypes.CDLL:
             "aps_sync_workspace_bytes": (ctypes.c_uint64, [i64, i32]),
             "aps_sync_route": (ctypes.c_int, [i32, i64, FP, i32, u32]),
             "aps_sync": (ctypes.c_int, [P, i32, i64, i64, P, i32, FP, i32, P, u32, P, P, P, P, ctypes.c_uint64, P]),
+            "aps_sync_noalloc": (ctypes.c_int, [P, i32, i64, i64, P, i32, FP, i32, P, u32, P, P, P, P]),
             "aps_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         }
         for name, (res, args) in sig.items():
@@ -301,6 +303,19 @@ def aps_sync(G, n: int, offsets, fmts, fmt_idx=None, flags: int = APS_SYNC_PASS1
                                       _ptr(maxabs_bits), _ptr(scale_exp), _ptr(out), _ptr(workspace),
                                       workspace.numel() * workspace.element_size(), _stream(stream)))
     return out, scale_exp, maxabs_bits, workspace
+
+
+def aps_sync_noalloc(G, n: int, offsets, fmts, fmt_idx, maxabs_bits, scale_exp, out,
+                     flags: int = APS_SYNC_PASS1 | APS_SYNC_PASS2, stream=None) -> None:
+    """aps_sync with the library's static per-GPU workspace instead of a
+    caller's (nothing is allocated, here or in the library): every output
+    tensor is the caller's."""
+    W, ld = _rows(G)
+    L = offsets.numel() - 1
+    pal, nf = _palette(fmts)
+    _check("aps_sync_noalloc", lib().aps_sync_noalloc(_ptr(G), W, ld, n, _ptr(offsets), L, pal, nf, _ptr(fmt_idx),
+                                                      int(flags), _ptr(maxabs_bits), _ptr(scale_exp), _ptr(out),
+                                                      _stream(stream)))
 
 
 def code_bytes(count: int, bits: int) -> int:

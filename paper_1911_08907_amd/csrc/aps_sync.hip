@@ -1,6 +1,9 @@
 // aps_sync.hip -- one whole APS synchronisation in one call (Algorithm 1 with
 // the low-precision accumulator of Sec. 5), reading the W workers'
 // gradients once where it can.
+#include <atomic>
+#include <mutex>
+
 #include "aps_common.hpp"
 
 namespace aps {
@@ -870,4 +873,57 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
         }
     }
     return launched();
+}
+
+// ================================= aps_sync without a caller's workspace
+//
+// The workspace of aps_sync_noalloc: one static array per GPU, placed there by
+// the HIP runtime when it loads this code object on the device.  In host code
+// `scratch` names the host-side shadow of the symbol, not device memory, so
+// it is never passed to a kernel or a copy: the device address comes from
+// hipGetSymbolAddress, taken once per device with that device current and
+// kept in scratch_ptr.
+static __device__ __align__(256) uint8_t scratch[APS_SYNC_SCRATCH_BYTES];
+
+namespace {
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::atomic<void*> scratch_ptr[SCRATCH_MAX_DEVICES];
+std::mutex scratch_mu;
+
+// Device address of the current device's scratch array (APS_ERR_DEVICE if
+// the runtime cannot give it).
+int scratch_address(void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= SCRATCH_MAX_DEVICES) return APS_ERR_DEVICE;
+    void* p = scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(scratch_mu);
+        p = scratch_ptr[dev].load(std::memory_order_relaxed);
+        if (!p) {
+            if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return APS_ERR_DEVICE;
+            if ((uintptr_t)p & 255u) return APS_ERR_DEVICE;
+            scratch_ptr[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return APS_OK;
+}
+}  // namespace
+
+extern "C" int aps_sync_noalloc(const float* G, int32_t W, int64_t ld, int64_t n, const int64_t* offsets,
+                                int32_t L, const aps_format* fmts, int32_t n_fmts, const uint8_t* fmt_idx,
+                                uint32_t flags, uint32_t* maxabs_bits, int32_t* scale_exp, float* out,
+                                void* stream) {
+    // the checks aps_sync makes on these arguments come first, so that a bad
+    // call reports the same status; then the size against the array, all
+    // before the device is touched
+    int st = check_rows(G, W, ld, n, offsets, L);
+    if (st != APS_OK) return st;
+    if (!maxabs_bits || !scale_exp || (!out && n > 0)) return APS_ERR_NULL;
+    if (sync_layout(n, L).total > APS_SYNC_SCRATCH_BYTES) return APS_ERR_SIZE;
+    void* ws = nullptr;
+    st = scratch_address(&ws);
+    if (st != APS_OK) return st;
+    return aps_sync(G, W, ld, n, offsets, L, fmts, n_fmts, fmt_idx, flags, maxabs_bits, scale_exp, out, ws,
+                    APS_SYNC_SCRATCH_BYTES, stream);
 }

@@ -291,3 +291,37 @@ def test_sync_route_choice(lib):
         r(8, (1 << 30) + 1, [F(5, 2)])
     with pytest.raises(A.ApsError):
         r(8, big, [F(9, 2)])
+
+
+@no_gpu
+def test_sync_noalloc_validation(lib):
+    """aps_sync_noalloc checks what aps_sync checks, then the set's
+    workspace against its static array, all before touching the device."""
+    f = lib.aps_sync_noalloc
+    pal = _pal(A.Format(5, 2))
+    ok = dict(G=GOOD, W=2, ld=64, n=64, off=GOOD, L=1, pal=pal, nf=1, idx=None, ph=3, mab=GOOD, se=GOOD,
+              out=GOOD)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["G"], a["W"], a["ld"], a["n"], a["off"], a["L"], a["pal"], a["nf"], a["idx"], a["ph"],
+                 a["mab"], a["se"], a["out"], None)
+
+    assert call(G=None) == A.APS_ERR_NULL
+    assert call(off=None) == A.APS_ERR_NULL
+    assert call(mab=None) == A.APS_ERR_NULL
+    assert call(se=None) == A.APS_ERR_NULL
+    assert call(out=None) == A.APS_ERR_NULL
+    assert call(W=0) == A.APS_ERR_SIZE
+    assert call(n=65) == A.APS_ERR_SIZE                       # ld < n
+    assert call(G=MIS) == A.APS_ERR_ALIGN
+    # the largest n whose workspace fits the array, and the next chunk's worth
+    limit = A.APS_SYNC_SCRATCH_BYTES
+    n_fit = max(c * 1024 for c in range(1, 40000) if A.aps_sync_workspace_bytes(c * 1024, 1) <= limit)
+    assert A.aps_sync_workspace_bytes(n_fit + 1, 1) > limit
+    assert 25557032 <= n_fit < (1 << 30)                      # a ResNet-50's gradient fits
+    assert call(n=n_fit + 1, ld=n_fit + 4) == A.APS_ERR_SIZE
+    assert call(n=1 << 30, ld=1 << 30) == A.APS_ERR_SIZE
+    big_L = 1 << 24                                            # many layers need more thresholds
+    assert A.aps_sync_workspace_bytes(n_fit, big_L) > limit
+    assert call(n=n_fit, ld=n_fit, L=big_L) == A.APS_ERR_SIZE
