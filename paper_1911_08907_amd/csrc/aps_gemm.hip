@@ -13,6 +13,8 @@ struct GemmArgs {
     int64_t lda, ldb, ldc;
     int32_t M, N, K;
     int32_t ka, kb;  // staged A and B carry 2^ka, 2^kb (ka + kb = k of the accumulator, or both 0)
+    int64_t tiles;   // output tiles, ntn of them per row of tiles (n fastest)
+    int32_t ntn;
 };
 
 // How a product reaches the accumulator's working domain and is rounded:
@@ -36,100 +38,104 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
     __shared__ __align__(16) float Bs[GK][GT + 4];  // Bs[k][n]
     const int t = threadIdx.x;
     const int tx = t & 15, ty = t >> 4;
-    const int64_t m0 = (int64_t)blockIdx.y * GT, n0 = (int64_t)blockIdx.x * GT;
-    float s[4][4], c[4][4];
-    bool bad[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            s[i][j] = 0.0f;
-            c[i][j] = 0.0f;
-            bad[i][j] = false;
-        }
-    float ra[4], rb[4];
-    // global -> registers, cast to the input format; outside A and B: 0
-    auto fetch = [&](int64_t k0) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int idx = t + BLOCK * r;
-            const int64_t am = m0 + (idx >> 4), ak = k0 + (idx & 15);
-            ra[r] = (am < g.M && ak < g.K) ? __builtin_amdgcn_ldexpf(quant_any(g.A[am * g.lda + ak], fi.k, fi), g.ka)
-                                           : 0.0f;
-            const int64_t bk = k0 + (idx >> 6), bn = n0 + (idx & 63);
-            rb[r] = (bk < g.K && bn < g.N) ? __builtin_amdgcn_ldexpf(quant_any(g.B[bk * g.ldb + bn], fi.k, fi), g.kb)
-                                           : 0.0f;
-        }
-    };
-    auto mac_v = [&](const f4& av, const f4& bv, bool first) {
-        const float a[4] = {av.x, av.y, av.z, av.w};
-        const float b[4] = {bv.x, bv.y, bv.z, bv.w};
+    // a 1-D grid over the tiles (a grid's y extent is limited to 65535 blocks);
+    // a block takes a further tile only where the tiles outnumber the grid
+    for (int64_t tile = blockIdx.x; tile < g.tiles; tile += gridDim.x) {
+        const int64_t m0 = tile / g.ntn * GT, n0 = tile % g.ntn * GT;
+        float s[4][4], c[4][4];
+        bool bad[4][4];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                // exact fp32 product of two input-format values, cast to the accumulator
-                float p;
-                if constexpr (PM == GP_LDEXP)
-                    p = quant<V>(a[i] * b[j], fa.k, fa, bad[i][j]);
-                else if constexpr (PM == GP_SCALED)
-                    p = quant_w<V>(a[i] * b[j], fa, bad[i][j]);
-                else
-                    p = quant_fit<V>(a[i] * b[j], fa);
-                if (first)
-                    s[i][j] = p;
-                else
-                    chain_step<V, KAHAN>(s[i][j], c[i][j], p, fa, bad[i][j]);
+                s[i][j] = 0.0f;
+                c[i][j] = 0.0f;
+                bad[i][j] = false;
             }
-    };
-    auto mac = [&](int kk, bool first) {
-        mac_v(*(const f4*)&As[kk][ty * 4], *(const f4*)&Bs[kk][tx * 4], first);
-    };
-    if (g.K > 0) fetch(0);
-    for (int64_t k0 = 0; k0 < g.K; k0 += GK) {
-        __syncthreads();  // the previous k-tile is consumed
+        float ra[4], rb[4];
+        // global -> registers, cast to the input format; outside A and B: 0
+        auto fetch = [&](int64_t k0) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int idx = t + BLOCK * r;
-            As[idx & 15][idx >> 4] = ra[r];
-            Bs[idx >> 6][idx & 63] = rb[r];
-        }
-        __syncthreads();
-        if (k0 + GK < g.K) fetch(k0 + GK);  // the next k-tile's loads overlap this tile's math
-        const int kend = (int)min((int64_t)GK, g.K - k0);
-        if (k0 > 0 && kend == GK) {
-            // software-pipelined: step kk+1's LDS reads are issued before step kk's math
-            f4 av = *(const f4*)&As[0][ty * 4], bv = *(const f4*)&Bs[0][tx * 4];
+            for (int r = 0; r < 4; ++r) {
+                const int idx = t + BLOCK * r;
+                const int64_t am = m0 + (idx >> 4), ak = k0 + (idx & 15);
+                ra[r] = (am < g.M && ak < g.K) ? __builtin_amdgcn_ldexpf(quant_any(g.A[am * g.lda + ak], fi.k, fi), g.ka)
+                                               : 0.0f;
+                const int64_t bk = k0 + (idx >> 6), bn = n0 + (idx & 63);
+                rb[r] = (bk < g.K && bn < g.N) ? __builtin_amdgcn_ldexpf(quant_any(g.B[bk * g.ldb + bn], fi.k, fi), g.kb)
+                                               : 0.0f;
+            }
+        };
+        auto mac_v = [&](const f4& av, const f4& bv, bool first) {
+            const float a[4] = {av.x, av.y, av.z, av.w};
+            const float b[4] = {bv.x, bv.y, bv.z, bv.w};
 #pragma unroll
-            for (int kk = 0; kk < GK; ++kk) {
-                f4 an = av, bn = bv;
-                if (kk + 1 < GK) {
-                    an = *(const f4*)&As[kk + 1][ty * 4];
-                    bn = *(const f4*)&Bs[kk + 1][tx * 4];
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    // exact fp32 product of two input-format values, cast to the accumulator
+                    float p;
+                    if constexpr (PM == GP_LDEXP)
+                        p = quant<V>(a[i] * b[j], fa.k, fa, bad[i][j]);
+                    else if constexpr (PM == GP_SCALED)
+                        p = quant_w<V>(a[i] * b[j], fa, bad[i][j]);
+                    else
+                        p = quant_fit<V>(a[i] * b[j], fa);
+                    if (first)
+                        s[i][j] = p;
+                    else
+                        chain_step<V, KAHAN>(s[i][j], c[i][j], p, fa, bad[i][j]);
                 }
-                __builtin_amdgcn_sched_barrier(0);
-                mac_v(av, bv, false);
-                av = an;
-                bv = bn;
+        };
+        auto mac = [&](int kk, bool first) {
+            mac_v(*(const f4*)&As[kk][ty * 4], *(const f4*)&Bs[kk][tx * 4], first);
+        };
+        if (g.K > 0) fetch(0);
+        for (int64_t k0 = 0; k0 < g.K; k0 += GK) {
+            __syncthreads();  // the previous k-tile is consumed
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int idx = t + BLOCK * r;
+                As[idx & 15][idx >> 4] = ra[r];
+                Bs[idx >> 6][idx & 63] = rb[r];
             }
-        } else {
-            int kk = 0;
-            if (k0 == 0) {
-                mac(0, true);  // an output's chain starts with its first product
-                kk = 1;
-            }
+            __syncthreads();
+            if (k0 + GK < g.K) fetch(k0 + GK);  // the next k-tile's loads overlap this tile's math
+            const int kend = (int)min((int64_t)GK, g.K - k0);
+            if (k0 > 0 && kend == GK) {
+                // software-pipelined: step kk+1's LDS reads are issued before step kk's math
+                f4 av = *(const f4*)&As[0][ty * 4], bv = *(const f4*)&Bs[0][tx * 4];
+#pragma unroll
+                for (int kk = 0; kk < GK; ++kk) {
+                    f4 an = av, bn = bv;
+                    if (kk + 1 < GK) {
+                        an = *(const f4*)&As[kk + 1][ty * 4];
+                        bn = *(const f4*)&Bs[kk + 1][tx * 4];
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                    mac_v(av, bv, false);
+                    av = an;
+                    bv = bn;
+                }
+            } else {
+                int kk = 0;
+                if (k0 == 0) {
+                    mac(0, true);  // an output's chain starts with its first product
+                    kk = 1;
+                }
 #pragma unroll 1
-            for (; kk < kend; ++kk) mac(kk, false);
+                for (; kk < kend; ++kk) mac(kk, false);
+            }
         }
-    }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int64_t m = m0 + ty * 4 + i;
-        if (m >= g.M) continue;
+        for (int i = 0; i < 4; ++i) {
+            const int64_t m = m0 + ty * 4 + i;
+            if (m >= g.M) continue;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int64_t n = n0 + tx * 4 + j;
-            if (n < g.N) g.C[m * g.ldc + n] = __builtin_amdgcn_ldexpf(finish<V>(s[i][j], bad[i][j]), -fa.k);
+            for (int j = 0; j < 4; ++j) {
+                const int64_t n = n0 + tx * 4 + j;
+                if (n < g.N) g.C[m * g.ldc + n] = __builtin_amdgcn_ldexpf(finish<V>(s[i][j], bad[i][j]), -fa.k);
+            }
         }
     }
 }
@@ -187,7 +193,8 @@ extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t 
     if (2 * (emin_in - in_fmt.m) < -149 && 2 * (in_fmt.m + 1) > emin_acc - acc_fmt.m + 149) return APS_ERR_UNSUPPORTED;
     if (!has_out) return APS_OK;
     const FmtK fi = make_fmtk(in_fmt), fa = make_fmtk(acc_fmt);
-    GemmArgs g{A, B, C, lda, ldb, ldc, M, N, K, 0, 0};
+    const int64_t mt = (M + GT - 1) / GT, nt = (N + GT - 1) / GT;
+    GemmArgs g{A, B, C, lda, ldb, ldc, M, N, K, 0, 0, mt * nt, (int32_t)nt};
     // Pre-scale the staged operands by 2^ka and 2^kb (ka + kb = k) when both
     // stay below 2^128: a value below 2^(emax_in+1) times 2^(127-emax_in) does.
     const int room = 127 - fi.emax;
@@ -200,7 +207,7 @@ extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t 
         const int cls = fa.variant <= V_INT_M0 ? CLS_INT : (fa.variant <= V_TOP_M0 ? CLS_TOP : CLS_LOW);
         if (cls != CLS_INT && acc_fmt.m > 0 && 2 * (in_fmt.m + 1) <= acc_fmt.m + 1) pm = GP_FIT;
     }
-    const dim3 grid((unsigned)((N + GT - 1) / GT), (unsigned)((M + GT - 1) / GT));
+    const dim3 grid((unsigned)std::min<int64_t>(g.tiles, INT32_MAX));
     launch_lp_gemm(fa.variant, accumulator == APS_ACC_KAHAN, pm, grid, (hipStream_t)stream, g, fi, fa);
     return launched();
 }

@@ -97,36 +97,42 @@ __global__ __launch_bounds__(BLOCK) void k_quantize(QuantArgs a, Layers ly, Pal 
 }
 
 
-// Mixed-format chunks, all W rows; grid (boundary, worker); element pairs
-// per thread as in k_sim_reduce_mixed.
+// Mixed-format chunks, all W rows; grid (boundary, row group): block y takes
+// rows y, y + gridDim.y, ... (a grid's y extent is limited to 65535 blocks);
+// element pairs per thread as in k_sim_reduce_mixed.
 __global__ __launch_bounds__(BLOCK) void k_quantize_mixed(QuantArgs a, Layers ly, Pal pal) {
     __shared__ FmtK spal[APS_MAX_FORMATS];
     pal_to_lds(pal, spal);
     int64_t start, end;
     if (!mixed_chunk_of_boundary(ly, blockIdx.x, start, end)) return;
-    const int64_t w = blockIdx.y;
-    uint8_t* row = a.codes ? a.codes + code_byte(w * a.ld, a.code_cls) : nullptr;
-    for (int64_t j0 = start + 2 * (int64_t)threadIdx.x; j0 < end; j0 += 2 * BLOCK) {
-        uint32_t c[2] = {0, 0};
-        for (int e = 0; e < 2; ++e) {
-            const int64_t j = j0 + e;
-            if (j >= end) break;
-            const int li = find_layer(ly.offsets, ly.L, j, 0);
-            const FmtK& f = spal[ly.fmt_idx[li]];
-            const int32_t ft = ly.scale_exp ? clamp_exp(ly.scale_exp[li]) : 0;
-            const int64_t off = w * a.ld + j;
-            const float v = quant_any(a.X[off], ft + f.k, f);  // Q may alias X: same element
-            if (a.Q) a.Q[off] = v;
-            c[e] = encode(v, f);
-            if (row && a.code_cls != 0) put_code(row, j, c[e], a.code_cls);
-        }
-        if (row && a.code_cls == 0) {
-            uint8_t* pb = row + (j0 >> 1);
-            *pb = (j0 + 1 < end) ? (uint8_t)((c[0] & 15u) | ((c[1] & 15u) << 4))
-                                 : (uint8_t)((*pb & 0xF0u) | (c[0] & 15u));
+    for (int64_t w = blockIdx.y; w < a.W; w += gridDim.y) {
+        uint8_t* row = a.codes ? a.codes + code_byte(w * a.ld, a.code_cls) : nullptr;
+        for (int64_t j0 = start + 2 * (int64_t)threadIdx.x; j0 < end; j0 += 2 * BLOCK) {
+            uint32_t c[2] = {0, 0};
+            for (int e = 0; e < 2; ++e) {
+                const int64_t j = j0 + e;
+                if (j >= end) break;
+                const int li = find_layer(ly.offsets, ly.L, j, 0);
+                const FmtK& f = spal[ly.fmt_idx[li]];
+                const int32_t ft = ly.scale_exp ? clamp_exp(ly.scale_exp[li]) : 0;
+                const int64_t off = w * a.ld + j;
+                const float v = quant_any(a.X[off], ft + f.k, f);  // Q may alias X: same element
+                if (a.Q) a.Q[off] = v;
+                c[e] = encode(v, f);
+                if (row && a.code_cls != 0) put_code(row, j, c[e], a.code_cls);
+            }
+            if (row && a.code_cls == 0) {
+                uint8_t* pb = row + (j0 >> 1);
+                *pb = (j0 + 1 < end) ? (uint8_t)((c[0] & 15u) | ((c[1] & 15u) << 4))
+                                     : (uint8_t)((*pb & 0xF0u) | (c[0] & 15u));
+            }
         }
     }
 }
+
+// Row blocks per boundary of k_quantize_mixed: one row per block up to this
+// many workers, more rows per block beyond.
+constexpr int32_t MIXED_ROW_BLOCKS = 4096;
 
 // ===================================================== K5: dequantize
 
@@ -223,7 +229,8 @@ extern "C" int aps_quantize(const float* X, int32_t W, int64_t ld, int64_t n, co
     APS_LAUNCH_Q(V_TOP_M0) APS_LAUNCH_Q(V_LOW_F64) APS_LAUNCH_Q(V_LOW_M0)
 #undef APS_LAUNCH_Q
     if (fmt_idx && n_fmts > 1 && L > 1)
-        hipLaunchKernelGGL(k_quantize_mixed, dim3((unsigned)L, (unsigned)W), dim3(BLOCK), 0, s, a, ly, pal);
+        hipLaunchKernelGGL(k_quantize_mixed, dim3((unsigned)L, (unsigned)std::min<int32_t>(W, MIXED_ROW_BLOCKS)),
+                           dim3(BLOCK), 0, s, a, ly, pal);
     return launched();
 }
 
