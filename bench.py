@@ -67,6 +67,9 @@ def parse():
     ap.add_argument("--no-other-calls", action="store_true",
                     help="skip timing aps_quantize / aps_dequantize outside the step")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU oracle time budget")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip timing the other workloads (and RAW mode) after the headline step")
+    ap.add_argument("--other-steps", type=int, default=10, help="timed steps per other workload")
     ap.add_argument("--roundoff", action="store_true",
                     help="only run the group-size round-off study (Eq. 5) and print it")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
@@ -182,15 +185,32 @@ def other_calls(A, G, gs, pal, idx_t, offs_t, se, out, reps: int = 5):
     return res
 
 
-def roundoff_study(groups=(4, 8, 16, 32, 64, 1)):
-    """Sec. 4.2's round-off study on synthetic data: Eq. (5) for the first
-    convolution's gradient (64x3x7x7) with W = 256 workers in 1-5-2 with APS
-    scales, for hierarchical all-reduces of several group sizes (1 is the
-    ring over all workers), against the fp32 all-reduce.  Two draws: the
-    configs' recipe (workers independent, so their sum largely cancels) and
-    correlated workers (a shared gradient plus per-worker noise of the same
-    size, which is how data-parallel gradients relate)."""
+ROUNDOFF_GROUPS = (4, 8, 16, 32, 64, 1)
+
+
+def round_off_error(grad_h, grad_l) -> float:
+    """Eq. (5): the mean over the elements with grad_h != 0 of
+    |(grad_h - grad_l) / grad_h|, in double (0 when every grad_h is 0).
+    grad_h is the fp32 all-reduce, grad_l the low-precision one."""
     import numpy as np
+
+    h = np.asarray(grad_h, np.float32).astype(np.float64)
+    lo = np.asarray(grad_l, np.float32).astype(np.float64)
+    nz = h != 0
+    if not nz.any():
+        return 0.0
+    return float(np.mean(np.abs((h[nz] - lo[nz]) / h[nz])))
+
+
+def roundoff_arrays(groups=ROUNDOFF_GROUPS):
+    """The data of Sec. 4.2's round-off study on synthetic gradients: the
+    first convolution's gradient (64x3x7x7) for W = 256 workers, reduced in
+    fp32 (1-8-23, worker order) and in 1-5-2 with APS scales by hierarchical
+    all-reduces of several group sizes (1 is the ring over all workers).  Two
+    draws: the configs' recipe (workers independent, so their sum largely
+    cancels) and correlated workers (a shared gradient plus per-worker noise
+    of the same size, which is how data-parallel gradients relate).  Returns
+    {draw: (G, scale_exp, grad_h, {group name: grad_l})}, host arrays."""
     import torch
 
     from paper_1911_08907_amd import aps as A
@@ -207,34 +227,68 @@ def roundoff_study(groups=(4, 8, 16, 32, 64, 1)):
         "independent": torch.randn(W, ld, generator=g, device=dev) * s,
         "correlated": (torch.randn(1, ld, generator=g, device=dev) + torch.randn(W, ld, generator=g, device=dev)) * s,
     }
-    result = {}
+    out = {}
     for name, G in draws.items():
         G[:, n:] = 0
         hi = torch.empty(n, dtype=torch.float32, device=dev)
         A.aps_sim_reduce(G, n, offs_t, None, [A.Format(8, 23)], None, 0, out=hi)
         _, se, _ = A.aps_step(G, n, offs_t, [A.Format(5, 2)])
-        h = hi.double().cpu().numpy()
-        nz = h != 0
-        lo = torch.empty(n, dtype=torch.float32, device=dev)
-        rows = {}
+        lo = {}
         for k in groups:
-            A.aps_sim_reduce_ex(G, n, offs_t, se, [A.Format(5, 2)], None, 0, group=k, out=lo)
-            l = lo.double().cpu().numpy()
-            rows["ring_256" if k == 1 else f"group_{k}"] = float(np.mean(np.abs((h[nz] - l[nz]) / h[nz])))
-        result[name] = rows
-    print(json.dumps({"study": "Eq.5 round-off error vs all-reduce group size, 64x3x7x7 gradient, W=256, "
-                               "1-5-2 with APS scales, synthetic", "error": result}), flush=True)
+            t = torch.empty(n, dtype=torch.float32, device=dev)
+            A.aps_sim_reduce_ex(G, n, offs_t, se, [A.Format(5, 2)], None, 0, group=k, out=t)
+            lo["ring_256" if k == 1 else f"group_{k}"] = t
+        torch.cuda.synchronize()
+        out[name] = (G.cpu().numpy(), se.cpu().numpy(), hi.cpu().numpy(), {k: t.cpu().numpy() for k, t in lo.items()})
+    return out
 
 
-def _cpu_model() -> str:
+ROUNDOFF_STUDY = ("Eq.5 round-off error vs all-reduce group size, 64x3x7x7 gradient, W=256, "
+                  "1-5-2 with APS scales, synthetic")
+
+
+def roundoff_study(groups=ROUNDOFF_GROUPS) -> dict:
+    """Eq. (5) for each draw and group size of roundoff_arrays."""
+    return {name: {k: round_off_error(h, lo) for k, lo in lows.items()}
+            for name, (_, _, h, lows) in roundoff_arrays(groups).items()}
+
+
+def cpu_description() -> dict:
+    """The host CPU as lscpu reports it (model, sockets, physical cores,
+    logical CPUs), and the CPUs this process may run on."""
+    import subprocess
+
+    info = {}
     try:
-        with open("/proc/cpuinfo") as fh:
-            for line in fh:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
-    except OSError:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=20).stdout
+        for line in out.splitlines():
+            k, _, v = line.partition(":")
+            info[k.strip()] = v.strip()
+    except (OSError, subprocess.SubprocessError):
         pass
-    return "unknown"
+    model = info.get("Model name")
+    if not model:
+        try:
+            with open("/proc/cpuinfo") as fh:
+                model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), None)
+        except OSError:
+            model = None
+
+    def num(key):
+        try:
+            return int(info[key])
+        except (KeyError, ValueError):
+            return None
+
+    sockets, cores = num("Socket(s)"), num("Core(s) per socket")
+    try:
+        allowed = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        allowed = None
+    return {"cpu_model": model or "unknown", "sockets": sockets,
+            "physical_cores": sockets * cores if sockets and cores else None,
+            "logical_cpus": num("CPU(s)"), "threads_per_core": num("Thread(s) per core"),
+            "cpus_allowed": allowed}
 
 
 def _omp_threads(k: int) -> bool:
@@ -302,7 +356,7 @@ def cpu_baseline(G_t, gs, pal, budget_s: float, slice_cols: int = 65536, single_
                   f"(max-abs + scales + rounded W-worker sum), {spent:.1f} s",
         "single_thread_value": single[0] if single else None,
         "single_thread_sample": single[1] if single else "OpenMP runtime not reachable: not measured",
-        "cpu_model": _cpu_model(),
+        **cpu_description(),
     }
 
 
@@ -359,6 +413,147 @@ def lp_gemm_calls(A, dev, reps: int = 5):
     return res
 
 
+def measure_step(A, gs, pal, idx_t, offs_t, mode: str, steps: int, warmup: int) -> dict:
+    """Time `steps` APS synchronisations of a gradient set after `warmup`
+    untimed ones: aps_sync's pass 1 and pass 2 as two calls (APS mode), or
+    the reduce with every exponent 0 (RAW mode, casting without APS).  The
+    step time is wall-clock over steps run back to back; the pass spans come
+    from as many further steps with HIP events around each pass on the
+    launch stream.  Returns the step time, the pass times, the route and the
+    dominant kernel's roofline figures, plus the device arrays the step
+    wrote."""
+    import torch
+
+    dev = gs.G.device
+    G, W, n, L = gs.G, gs.W, gs.n, len(gs.sizes)
+    mab = torch.empty(L, dtype=torch.int32, device=dev)
+    se = torch.empty(L, dtype=torch.int32, device=dev)
+    out = torch.empty(n, dtype=torch.float32, device=dev)
+    ws = torch.empty(A.aps_sync_workspace_bytes(n, L), dtype=torch.uint8, device=dev)
+    aps = mode == "aps"
+    route = A.aps_sync_route(W, n, pal) if aps else None
+    one = route == A.APS_SYNC_ROUTE_ONE_PASS
+    guess = route == A.APS_SYNC_ROUTE_GUESS
+    ev = []
+
+    def step(record: bool):
+        if record:
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            e[0].record()
+        if aps:
+            A.aps_sync(G, n, offs_t, pal, idx_t, A.APS_SYNC_PASS1, mab, se, out, ws)
+        if record:
+            e[1].record()
+        if aps:
+            A.aps_sync(G, n, offs_t, pal, idx_t, A.APS_SYNC_PASS2, mab, se, out, ws)
+        else:  # casting without APS: no maxima, no scales
+            A.aps_sim_reduce(G, n, offs_t, None, pal, idx_t, 0, out=out)
+        if record:
+            e[2].record()
+            ev.append(e)
+
+    for _ in range(warmup):
+        step(False)
+    torch.cuda.synchronize()
+    # the step time: `steps` steps back to back with nothing between them
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step(False)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / steps
+    # the pass spans: as many steps again, with events around each pass
+    for _ in range(steps):
+        step(True)
+    torch.cuda.synchronize()
+    p1 = sum(e[0].elapsed_time(e[1]) for e in ev) / len(ev)
+    p2 = sum(e[1].elapsed_time(e[2]) for e in ev) / len(ev)
+    assert bool(torch.isfinite(out).all()) or not aps
+
+    rerun = None
+    if guess:
+        # the layers pass 2 reran: threshold 1 in the workspace's int32[L] part
+        up = lambda b: (b + 255) // 256 * 256
+        C = (n + 1023) // 1024
+        t0_ = up(1024 * C) + up(4 * C)
+        rr = ws[t0_:t0_ + 4 * L].cpu().numpy().view("int32") != 0
+        rerun = {"layers": int(rr.sum()), "elements": int(sum(sz for sz, r in zip(gs.sizes, rr) if r))}
+
+    # the dominant kernel: the one that reads the W rows and writes the sum
+    alg_bytes = 4.0 * W * n + 4.0 * n     # read every worker row once, write the fp32 sum
+    if one:
+        kernel, k_ms = "k_sync_spec", p1
+        note = "pass-1 span: k_sync_spec plus the zeroing of the L maxima (k_sync_clear, a few us)"
+        if W >= 128 and all(f.m <= 7 for f in pal):
+            # pass 1 keeps each sum in 2 bytes; pass 2 widens them into the fp32 output
+            alg_bytes = 4.0 * W * n + 2.0 * n
+            note += "; the sums written as 2-byte top halves (pass 2 widens them)"
+    elif guess:
+        # pass 1 also reads every 32nd worker row for the sampled maxima
+        alg_bytes += 4.0 * ((W + 31) // 32) * n
+        kernel, k_ms = "k_guess_spec", p1
+        note = ("pass-1 span: k_guess_spec plus the sampled maxima (k_maxabs over every 32nd worker row), "
+                "bytes of both")
+    else:
+        kernel, k_ms = "k_sim_reduce", p2
+        note = "pass-2 span: k_sim_reduce plus k_scales (a few us)" if aps else "k_sim_reduce alone"
+    achieved = alg_bytes / (k_ms * 1e-3) / 1e9
+    return {"ms_per_step": ms_per_step, "pass1_ms": p1, "pass2_ms": p2, "aps": aps, "one": one, "guess": guess,
+            "route": ("one pass" if one else ("guessed scales" if guess else "two passes")) if aps else "raw reduce",
+            "kernel": kernel, "kernel_ms": k_ms, "alg_bytes": alg_bytes, "achieved": achieved, "note": note,
+            "rerun": rerun, "arrays": (mab, se, out, ws)}
+
+
+# The other workloads timed after the headline step (each also in RAW mode,
+# casting without APS): config, palette, and whether its W rows fit the
+# 256 MB Infinity Cache (then a step is a few launches, bound by latency).
+OTHER_CONFIGS = [("resnet50_w256", "1-4-3", False), ("resnet50_w8", "1-5-2", False),
+                 ("bert_large", "hybrid", False), ("resnet20", "1-5-2", True), ("resnet20", "1-4-3", True),
+                 ("resnet20", "1-3-0", True), ("mlp", "1-4-3", True)]
+
+
+def other_configs(A, WL, dev, cfg0: str, pal0: str, held: dict, steps: int, warmup: int) -> dict:
+    """Each workload of OTHER_CONFIGS in APS and RAW mode, plus the headline
+    set in RAW mode.  held = {"config": cfg0, "gs": the headline GradSet}
+    is the only reference to the set in use: the headline set serves its own
+    config and is dropped before the next set is drawn."""
+    import torch
+
+    res = {}
+    plan = [(cfg0, pal0, "raw", False)] + [(c, p, m, cr) for c, p, cr in OTHER_CONFIGS for m in ("aps", "raw")
+                                            if (c, p) != (cfg0, pal0)]
+    plan.sort(key=lambda x: x[0] != cfg0)  # the headline set's own runs first, while it is held
+    for cfg, palette, mode, cache in plan:
+        if held["config"] != cfg:
+            held["config"], held["gs"] = None, None
+            torch.cuda.empty_cache()
+            held["gs"] = WL.generate(cfg, palette, device=dev)
+            held["config"] = cfg
+            torch.cuda.synchronize()
+        gs = held["gs"]
+        pal = [A.Format(p.e, p.m, p.bias) for p in WL.CONFIGS[cfg].palettes[palette]]
+        offs_t = torch.from_numpy(gs.offsets).to(dev)
+        idx_t = None if gs.fmt_idx is None else torch.from_numpy(gs.fmt_idx).to(dev)
+        m = measure_step(A, gs, pal, idx_t, offs_t, mode, steps, warmup)
+        del m["arrays"]
+        W, n = gs.W, gs.n
+        res[f"{cfg} {palette} {mode}"] = {
+            "W": W, "n": n, "ms_per_step": m["ms_per_step"], "elements_per_s": W * n / (m["ms_per_step"] * 1e-3),
+            "route": m["route"], "kernel": m["kernel"], "kernel_ms": m["kernel_ms"],
+            "algorithmic_bytes_per_launch": m["alg_bytes"], "achieved_GBps": m["achieved"],
+            "frac": m["achieved"] / HBM_PEAK_GBPS, "pass1_ms": m["pass1_ms"], "pass2_ms": m["pass2_ms"],
+            **({"guess_reruns": m["rerun"]} if m["rerun"] else {}),
+            "residency": ("cache-resident (the W rows fit the 256 MB Infinity Cache; a step is a few launches, "
+                          "bound by their latency)") if cache else "HBM",
+        }
+        print(f"# {cfg} {palette} {mode}: {m['ms_per_step']:.4f} ms/step, {m['route']}, "
+              f"{m['kernel']} {m['achieved'] / 1e3:.2f} TB/s", file=sys.stderr, flush=True)
+        del gs
+    held["config"], held["gs"] = None, None
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -369,7 +564,7 @@ def main():
         copy_calibration(args.copy_calibration)
         return
     if args.roundoff:
-        roundoff_study()
+        print(json.dumps({"study": ROUNDOFF_STUDY, "error": roundoff_study()}), flush=True)
         return
     if args.gemm:
         import torch
@@ -400,54 +595,12 @@ def main():
     W, n, L = gs.W, gs.n, len(gs.sizes)
     offs_t = torch.from_numpy(gs.offsets).to(dev)
     idx_t = None if gs.fmt_idx is None else torch.from_numpy(gs.fmt_idx).to(dev)
-    mab = torch.empty(L, dtype=torch.int32, device=dev)
-    se = torch.empty(L, dtype=torch.int32, device=dev)
-    out = torch.empty(n, dtype=torch.float32, device=dev)
-    ws = torch.empty(A.aps_sync_workspace_bytes(n, L), dtype=torch.uint8, device=dev)
     G = gs.G
     aps = args.mode == "aps"
-    route = A.aps_sync_route(W, n, pal) if aps else None
-    one = route == A.APS_SYNC_ROUTE_ONE_PASS
-    guess = route == A.APS_SYNC_ROUTE_GUESS
+    m = measure_step(A, gs, pal, idx_t, offs_t, args.mode, args.steps, args.warmup)
+    mab, se, out, _ = m.pop("arrays")
+    ms_per_step = m["ms_per_step"]
 
-    ev = []
-
-    def step(record: bool):
-        if record:
-            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-            e[0].record()
-        if aps:
-            A.aps_sync(G, n, offs_t, pal, idx_t, A.APS_SYNC_PASS1, mab, se, out, ws)
-        if record:
-            e[1].record()
-        if aps:
-            A.aps_sync(G, n, offs_t, pal, idx_t, A.APS_SYNC_PASS2, mab, se, out, ws)
-        else:  # casting without APS: no maxima, no scales
-            A.aps_sim_reduce(G, n, offs_t, None, pal, idx_t, 0, out=out)
-        if record:
-            e[2].record()
-            ev.append(e)
-
-    for _ in range(args.warmup):
-        step(False)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(True)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-    p1 = sum(e[0].elapsed_time(e[1]) for e in ev) / len(ev)
-    p2 = sum(e[1].elapsed_time(e[2]) for e in ev) / len(ev)
-    assert bool(torch.isfinite(out).all()) or not aps
-
-    if guess:
-        # the layers pass 2 reran: threshold 1 in the workspace's int32[L] part
-        up = lambda b: (b + 255) // 256 * 256
-        C = (n + 1023) // 1024
-        t0_ = up(1024 * C) + up(4 * C)
-        rr = ws[t0_:t0_ + 4 * L].cpu().numpy().view("int32") != 0
-        rerun = {"layers": int(rr.sum()), "elements": int(sum(sz for sz, r in zip(gs.sizes, rr) if r))}
     other = {}
     if aps:
         other["two_pass_step"] = two_pass_step(A, G, gs, pal, idx_t, offs_t, mab, se, out)
@@ -455,25 +608,7 @@ def main():
         other.update(other_calls(A, G, gs, pal, idx_t, offs_t, se if aps else None, out))
         other["lp_gemm"] = lp_gemm_calls(A, dev)
 
-    # the dominant kernel: the one that reads the W rows and writes the sum
-    alg_bytes = 4.0 * W * n + 4.0 * n     # read every worker row once, write the fp32 sum
-    if one:
-        kernel, k_ms = "k_sync_spec", p1
-        note = "pass-1 span: k_sync_spec plus the zeroing of the L maxima (k_sync_clear, a few us)"
-        if W >= 128 and all(f.m <= 7 for f in pal):
-            # pass 1 keeps each sum in 2 bytes; pass 2 widens them into the fp32 output
-            alg_bytes = 4.0 * W * n + 2.0 * n
-            note += "; the sums written as 2-byte top halves (pass 2 widens them)"
-    elif guess:
-        # pass 1 also reads every 32nd worker row for the sampled maxima
-        alg_bytes += 4.0 * ((W + 31) // 32) * n
-        kernel, k_ms = "k_guess_spec", p1
-        note = ("pass-1 span: k_guess_spec plus the sampled maxima (k_maxabs over every 32nd worker row), "
-                "bytes of both")
-    else:
-        kernel, k_ms = "k_sim_reduce", p2
-        note = "pass-2 span: k_sim_reduce plus k_scales (a few us)" if aps else "k_sim_reduce alone"
-    achieved = alg_bytes / (k_ms * 1e-3) / 1e9
+    kernel = m["kernel"]
     traffic, traffic_src = traffic_from_profile(kernel[2:], args.config, palette)
     res = {
         "metric": METRIC,
@@ -490,29 +625,34 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": args.config, "W": W, "n": n, "tensors": L, "format": palette,
-                   "mode": args.mode,
-                   "route": "one pass" if one else ("guessed scales" if guess else "two passes"),
+                   "mode": args.mode, "route": m["route"],
                    "layout": "[W][ld] fp32 worker-major, HBM resident"},
         "roofline": {
             "bound": "hbm",
-            "achieved": achieved,
+            "achieved": m["achieved"],
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBPS,
+            "frac": m["achieved"] / HBM_PEAK_GBPS,
             "traffic": traffic,
             "kernel": kernel,
-            "algorithmic_bytes_per_launch": alg_bytes,
-            "avg_launch_ms": k_ms,
-            "timed_span": note,
+            "algorithmic_bytes_per_launch": m["alg_bytes"],
+            "avg_launch_ms": m["kernel_ms"],
+            "timed_span": m["note"],
             "traffic_source": traffic_src,
         },
-        "passes_ms": {"pass1": p1, "pass2": p2},
-        **({"guess_reruns": rerun} if guess else {}),
+        "passes_ms": {"pass1": m["pass1_ms"], "pass2": m["pass2_ms"]},
+        **({"guess_reruns": m["rerun"]} if m["rerun"] else {}),
         "other_calls": other,
         "kernel_source": source_digest(),
     }
     if not args.no_cpu_baseline and aps:
         res["cpu_baseline"] = cpu_baseline(G, gs, pal, args.cpu_seconds)
+    if not args.no_other_calls:
+        res["roundoff_eq5"] = {"study": ROUNDOFF_STUDY, "error": roundoff_study()}
+    held = {"config": args.config, "gs": gs}
+    del mab, se, out, G, gs
+    if not args.no_other_configs:
+        res["other_configs"] = other_configs(A, WL, dev, args.config, palette, held, args.other_steps, 3)
     print(json.dumps(res), flush=True)
 
 

@@ -27,7 +27,7 @@ def test_bench_json_line():
         pytest.skip("no GPU")
     # the benchmark runs as a child process of its own
     r = subprocess.run([sys.executable, BENCH, "--config", "mlp", "--steps", "3", "--warmup", "1",
-                        "--cpu-seconds", "1", "--no-other-calls"],
+                        "--cpu-seconds", "1", "--no-other-calls", "--no-other-configs"],
                        capture_output=True, text=True, timeout=300, cwd=ROOT)
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [ln for ln in r.stdout.splitlines() if ln.strip()]
@@ -52,3 +52,4 @@ def test_bench_json_line():
     cb = res["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["unit"] == "elements/s"
     assert cb["value"] > 0 and cb["cores"] >= 1 and cb["sample"]
+    assert cb["cpu_model"] and "physical_cores" in cb and "logical_cpus" in cb
