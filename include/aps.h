@@ -8,10 +8,10 @@
  *
  *   aps_layer_maxabs   FindMaxExp input + AllReduce(MAX)   (Alg. 1, FindMaxExp)
  *   aps_layer_scales   ft = upper_bound_exp - max exponent (Alg. 1; Sec. 3.3.3)
- *   aps_quantize       g * 2^ft, Cast(g, exp_bit, man_bit) (Alg. 1; Sec. 3.3.1)
+ *   aps_quantize       scale by 2^ft, cast to the format   (Alg. 1; Sec. 3.3.1)
  *   aps_sim_reduce     scale, cast, AllReduce(SUM) with a low-precision
  *                      accumulator, cast back, unscale     (Alg. 1; Sec. 5)
- *   aps_dequantize     Cast(low_g, 8, 23) / 2^ft           (Alg. 1)
+ *   aps_dequantize     back to fp32, scale undone          (Alg. 1)
  *
  * Beside them, CPD's accumulation experiments (Sec. 5): aps_sim_reduce_ex
  * (summation orders, Kahan), aps_sim_reduce_codes (the sum over packed
@@ -134,8 +134,8 @@ int aps_layer_scales(const uint32_t* maxabs_bits, int32_t L, int32_t N,
                      int32_t* scale_exp, void* stream);
 
 /*
- * Scale and cast every element of every worker (Algorithm 1, g <- g * 2^ft
- * then Cast(g, exp_bit, man_bit)):
+ * Scale and cast every element of every worker (Algorithm 1: the gradient
+ * times 2^ft, then the cast to the custom format):
  *   Q[w][j] = R_fmt(fl32(X[w][j] * 2^scale_exp[i]))   for j in layer i.
  * The product is the fp32 value nearest to X * 2^ft; R_fmt is the format's
  * round-to-nearest-even described above.
@@ -332,11 +332,11 @@ int aps_sim_reduce_ex(const float* G, int32_t W, int64_t ld, int64_t n,
                       void* stream);
 
 /*
- * The SUM all-reduce of Algorithm 1 on low_g in the form the workers would
- * exchange it: W rows of packed codes of already scaled and cast values (as
- * written by aps_quantize), summed in worker order with the accumulator
- * rounded to the format after every add (Sec. 5), then cast back and
- * unscaled:
+ * The SUM all-reduce of Algorithm 1 on the cast gradients in the form the
+ * workers would exchange them: W rows of packed codes of already scaled and
+ * cast values (as written by aps_quantize), summed in worker order with the
+ * accumulator rounded to the format after every add (Sec. 5), then cast back
+ * and unscaled:
  *   s = decode(c_0[j]);  s = R_fmt(s + decode(c_w[j])) for w = 1..W-1
  *   out[j] = fl32(s / 2^ft)            (s itself with APS_OUTPUT_SCALED)
  * It is the kernel each owner of a slice would run in a multi-GPU
@@ -356,7 +356,7 @@ int aps_sim_reduce_codes(const void* codes, int32_t W, int64_t ld, int64_t n,
                          uint32_t flags, float* out, void* codes_out, void* stream);
 
 /*
- * Cast back and unscale (Algorithm 1, Cast(low_g, 8, 23) then g / 2^ft):
+ * Back to fp32 with the scale undone (Algorithm 1's last two steps):
  *   out[j] = fl32(V[j] / 2^scale_exp[i])
  * where V is Q (fp32 values) if Q is non-NULL, else the decoded codes.
  *

@@ -79,8 +79,9 @@ int oracle_format_ok(oracle_format f) {
 
 /* ------------------------------------------------------------- rounding */
 
-/* Cast(y, exp_bit, man_bit) of Algorithm 1 with the round-to-nearest-even
- * mode of Sec. 4 and readings R1-R5.  y is any real held exactly in a double.
+/* The cast to the custom format that Algorithm 1 applies to the scaled
+ * gradient, with the round-to-nearest-even mode of Sec. 4 and readings
+ * R1-R5.  y is any real held exactly in a double.
  *
  * For a = |y| in the binade [2^E, 2^(E+1)) the format spaces its values by
  * the quantum 2^(max(E, emin) - m); the result is the multiple of that
@@ -108,24 +109,31 @@ int oracle_ceil_log2(double t) {
     return (r == 0.5) ? E - 1 : E; /* exact power of two: log2 t = E - 1 */
 }
 
-/* FindMaxExp(g * N) of Algorithm 1, literally: the product is the fp32
- * multiply of the tensor by N, zeros are skipped, and the running maximum of
- * ceil(log2|v|) is kept.  Non-finite products are reported separately. */
+/* The exponent of one element of the tensor that Algorithm 1 hands to its
+ * exponent search, the gradient multiplied by the worker count: the fp32
+ * product v = fl32(N * g) has exponent ceil(log2 |v|) (Sec. 3.3.3).  A zero
+ * has none (INT32_MIN); an INF or NaN product sets *nonfinite. */
+static int32_t product_exponent(float g, int32_t N, int32_t* nonfinite) {
+    const float v = (float)N * g;
+    if (!isfinite(v)) {
+        *nonfinite = 1;
+        return INT32_MIN;
+    }
+    return v == 0.0f ? INT32_MIN : oracle_ceil_log2(fabs((double)v));
+}
+
+/* Sec. 3.3.3's exponent of a tensor taken element by element: the largest
+ * product_exponent over the tensor.  It is the route Algorithm 1 describes,
+ * kept beside the max-abs route (oracle_layer_maxabs, oracle_scale_one) so
+ * that a test can show the two agree. */
 int32_t oracle_find_max_exp(const float* g, int64_t cnt, int32_t N, int32_t* nonfinite) {
-    int32_t max_exp = INT32_MIN;
+    int32_t e = INT32_MIN;
     *nonfinite = 0;
     for (int64_t k = 0; k < cnt; ++k) {
-        const float v = (float)N * g[k];
-        if (!isfinite(v)) {
-            *nonfinite = 1;
-            continue;
-        }
-        if (v != 0.0f) {
-            const int32_t t = oracle_ceil_log2(fabs((double)v));
-            if (t > max_exp) max_exp = t;
-        }
+        const int32_t ek = product_exponent(g[k], N, nonfinite);
+        e = ek > e ? ek : e;
     }
-    return max_exp;
+    return e;
 }
 
 void oracle_layer_maxabs(const float* G, int32_t W, int64_t ld, int64_t n,
@@ -149,10 +157,11 @@ void oracle_layer_maxabs(const float* G, int32_t W, int64_t ld, int64_t n,
 }
 
 /* Sec. 3.3.3: the scale factor is f = 2^ft with
- *     ft = log2(p) - ceil(log2 |N * ghat|),   p = 2^emax,
- * which is Algorithm 1's  upper_bound_exp - AllReduce_MAX(FindMaxExp(g*N))
- * once the MAX over workers and elements is taken on ghat first (both
- * fl32(N*x) and ceil(log2 .) are monotone in |x|). */
+ *     ft = log2(p) - ceil(log2 |N * ghat|),   p = 2^emax.
+ * Algorithm 1 takes the largest exponent of N * g per worker, the MAX over
+ * workers, and subtracts it from the format's largest exponent; taking the
+ * MAX over workers and elements on ghat first gives the same number, since
+ * both fl32(N*x) and ceil(log2 .) are monotone in |x|. */
 int32_t oracle_scale_one(uint32_t maxabs_bits, int32_t N, oracle_format f) {
     const float ghat = f_of_bits(maxabs_bits & 0x7FFFFFFFu);
     if (!(ghat > 0.0f) || !isfinite(ghat)) return 0;            /* R6 */
@@ -172,9 +181,9 @@ void oracle_layer_scales(const uint32_t* maxabs_bits, int32_t L, int32_t N,
 
 /* ------------------------------------------------------- quantize/reduce */
 
-/* Algorithm 1 scales the gradient, g <- g * 2^ft; g is fp32, so the product is
- * the fp32 value nearest to x * 2^ft (a single rounding, exact unless the
- * result leaves fp32's normal range). */
+/* Algorithm 1 multiplies the fp32 gradient by 2^ft; the product is the fp32
+ * value nearest to x * 2^ft (a single rounding, exact unless the result
+ * leaves fp32's normal range). */
 static float scale_fp32(float x, int32_t ft) { return (float)ldexp((double)x, ft); }
 
 void oracle_quantize(const float* X, int32_t W, int64_t ld, int64_t n,
@@ -206,19 +215,19 @@ void oracle_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n,
             double s = 0.0;
             for (int32_t w = 0; w < W; ++w) {
                 const float x = G[(int64_t)w * ld + j];
-                /* g <- g * 2^ft (skipped when the input is already scaled) */
+                /* the scale by 2^ft (not when the input is already scaled) */
                 const float y = (flags & ORACLE_INPUT_QUANTIZED) ? x : scale_fp32(x, ft);
-                /* low_g <- Cast(g, exp_bit, man_bit) */
+                /* the cast to the format */
                 const double q = oracle_round((double)y, f);
-                /* low_g <- AllReduce(low_g, SUM) with a low-precision
-                 * accumulator: each partial sum is cast to the format.  The
-                 * double add of two format values followed by one rounding
-                 * equals rounding the exact sum (53 >= 2*24 + 2). */
+                /* the SUM all-reduce in worker order with a low-precision
+                 * accumulator (Sec. 5): every partial sum is rounded to the
+                 * format.  The double add of two format values followed by
+                 * one rounding equals rounding the exact sum (53 >= 2*24 + 2). */
                 s = (w == 0) ? q : oracle_round(s + q, f);
             }
-            /* g <- Cast(low_g, 8, 23): s is a format value, hence an fp32 value */
+            /* back to fp32: s is a format value, hence exactly an fp32 value */
             const float g = (float)s;
-            /* g <- g / 2^ft */
+            /* the scale undone */
             out[j] = (flags & ORACLE_OUTPUT_SCALED) ? g : (float)ldexp((double)g, -ft);
         }
     }
@@ -309,7 +318,7 @@ void oracle_dequantize(const float* Q, const void* codes, int64_t n,
         const int32_t ft = scale_exp ? scale_exp[i] : 0;
         for (int64_t j = offsets[i]; j < offsets[i + 1]; ++j) {
             const double v = Q ? (double)Q[j] : oracle_decode(get_code(codes, j, code_bits(f)), f);
-            out[j] = (float)ldexp(v, -ft); /* g <- Cast(low_g, 8, 23) / 2^ft */
+            out[j] = (float)ldexp(v, -ft); /* back to fp32, the scale undone */
         }
     }
 }
@@ -345,7 +354,7 @@ void oracle_sim_reduce_codes(const void* codes, int32_t W, int64_t ld, int64_t n
 
 /* ---------------------------------------------- summation order, Kahan */
 
-/* One add of a chain: plain (s = Cast(s + x)) or Kahan, where every
+/* One add of a chain: plain (s = R(s + x)) or Kahan, where every
  * intermediate is cast to the format as a low-precision accumulator would
  * hold it (Sec. 5). */
 static void chain_add(double* s, double* c, double x, oracle_format f, int32_t accumulator) {

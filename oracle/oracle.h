@@ -48,16 +48,17 @@ int oracle_emax(oracle_format f);
 double oracle_maxfinite(oracle_format f);
 double oracle_minsub(oracle_format f);
 
-/* Cast(y, e, m) of Algorithm 1: round-to-nearest-even of the real value y
+/* The cast of Algorithm 1, R(y): round-to-nearest-even of the real value y
  * to the format; result returned as a double that holds the format value. */
 double oracle_round(double y, oracle_format f);
 
 /* Exact ceil(log2 t) for finite t > 0. */
 int oracle_ceil_log2(double t);
 
-/* FindMaxExp of Algorithm 1 applied to fl32(N * g[k]), k < cnt: the largest
- * ceil(log2|v|) over the nonzero finite products.  Returns INT32_MIN when
- * there is none.  *nonfinite is set to 1 when some product is INF or NaN. */
+/* Sec. 3.3.3's exponent of the tensor N * g taken element by element, the
+ * route Algorithm 1 describes: the largest ceil(log2|v|) over the nonzero
+ * finite products v = fl32(N * g[k]), k < cnt.  Returns INT32_MIN when there
+ * is none.  *nonfinite is set to 1 when some product is INF or NaN. */
 int32_t oracle_find_max_exp(const float* g, int64_t cnt, int32_t N, int32_t* nonfinite);
 
 /* Per-layer max |G[w][j]| over all W workers and all j of the layer, as the
@@ -71,7 +72,7 @@ void oracle_layer_scales(const uint32_t* maxabs_bits, int32_t L, int32_t N,
                          const oracle_format* fmts, const uint8_t* fmt_idx,
                          int32_t* scale_exp);
 
-/* Q[w][j] = Cast(fl32(X[w][j] * 2^f_i)) for j in layer i (scale_exp NULL
+/* Q[w][j] = R(fl32(X[w][j] * 2^f_i)) for j in layer i (scale_exp NULL
  * means f_i = 0 for every layer). */
 void oracle_quantize(const float* X, int32_t W, int64_t ld, int64_t n,
                      const int64_t* offsets, int32_t L, const int32_t* scale_exp,
@@ -100,10 +101,11 @@ double oracle_decode(uint32_t code, oracle_format f);
 void oracle_pack_codes(const float* V, int64_t n, const int64_t* offsets, int32_t L,
                        const oracle_format* fmts, const uint8_t* fmt_idx, void* codes);
 
-/* The SUM all-reduce of Algorithm 1 applied to low_g as exchanged between
- * workers: W rows of packed codes (row stride ld elements, code layout as in
- * oracle_pack_codes), already scaled and cast.  Per element:
- * s = decode(c_0); s = Cast(s + decode(c_w)) for w = 1..W-1; out = s / 2^ft
+/* The SUM all-reduce of Algorithm 1 applied to the cast gradients as the
+ * workers would exchange them: W rows of packed codes (row stride ld
+ * elements, code layout as in oracle_pack_codes), already scaled and cast.
+ * Per element: s = decode(c_0); s = R(s + decode(c_w)) for w = 1..W-1;
+ * out = s / 2^ft
  * (or s with ORACLE_OUTPUT_SCALED). */
 void oracle_sim_reduce_codes(const void* codes, int32_t W, int64_t ld, int64_t n,
                              const int64_t* offsets, int32_t L, const int32_t* scale_exp,
@@ -111,7 +113,7 @@ void oracle_sim_reduce_codes(const void* codes, int32_t W, int64_t ld, int64_t n
                              uint32_t flags, float* out);
 
 /* Accumulation strategies of Sec. 5 (CPD) for a chain of adds. */
-#define ORACLE_ACC_SEQUENTIAL 0 /* s = Cast(s + x) */
+#define ORACLE_ACC_SEQUENTIAL 0 /* s = R(s + x) */
 #define ORACLE_ACC_KAHAN 1      /* Kahan's compensated summation, every op cast */
 
 /* The SUM all-reduce with the summation order of Sec. 4.2's hierarchical

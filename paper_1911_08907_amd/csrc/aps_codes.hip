@@ -1,6 +1,6 @@
 // aps_codes.hip -- the W-worker rounded sum over packed codes, the form in
-// which workers would exchange the cast gradients (Algorithm 1's AllReduce
-// SUM of low_g; Sec. 5).
+// which workers would exchange the cast gradients (Algorithm 1's SUM
+// all-reduce of the cast gradients; Sec. 5).
 #include "aps_common.hpp"
 
 namespace aps {

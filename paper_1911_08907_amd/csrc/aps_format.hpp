@@ -1,6 +1,6 @@
 // aps_format.hpp -- custom-float constants and device rounding for gfx950.
 //
-// Cast(g, exp_bit, man_bit) of Algorithm 1 (arXiv 1911.08907), with the
+// The cast to a custom float of Algorithm 1 (arXiv 1911.08907), with the
 // round-to-nearest-even mode of Sec. 4, the format layout that reproduces
 // Table 2, and the low-precision accumulator of Sec. 5.
 //

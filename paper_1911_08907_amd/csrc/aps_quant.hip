@@ -1,5 +1,6 @@
-// aps_quant.hip -- scale and cast (Algorithm 1, g * 2^ft then Cast), and
-// cast back and unscale (Cast(low_g, 8, 23), g / 2^ft), with packed codes.
+// aps_quant.hip -- scale and cast (Algorithm 1: the gradient times 2^ft,
+// rounded to the custom format), and back to fp32 with the scale undone,
+// with packed codes.
 #include "aps_common.hpp"
 
 namespace aps {

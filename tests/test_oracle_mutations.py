@@ -33,10 +33,15 @@ MUTANTS = {
                                 "out[j] = (flags & ORACLE_OUTPUT_SCALED) ? g : (float)ldexp((double)g, ft);"),
     "nan_ignored_in_maxabs": ("if (isnan(x))\n                    saw_nan = 1;", "if (0)\n                    saw_nan = 1;"),
     "scale_before_rounding_skipped": (
-        "(skipped when the input is already scaled) */\n"
+        "(not when the input is already scaled) */\n"
         "                const float y = (flags & ORACLE_INPUT_QUANTIZED) ? x : scale_fp32(x, ft);",
-        "(skipped when the input is already scaled) */\n"
+        "(not when the input is already scaled) */\n"
         "                const float y = x;"),
+    "format_ok_admits_emax_128": ("if (oracle_emax(f) > 127) return 0;", "if (oracle_emax(f) > 128) return 0;"),
+    "format_ok_admits_minsub_below_fp32": ("if (oracle_emin(f) - f.m < -149) return 0;",
+                                           "if (oracle_emin(f) - f.m < -150) return 0;"),
+    "literal_exponent_counts_zeros": ("return v == 0.0f ? INT32_MIN : oracle_ceil_log2(fabs((double)v));",
+                                      "return v == 0.0f ? -200 : oracle_ceil_log2(fabs((double)v));"),
     "kahan_compensation_sign": ("const double y = oracle_round(x - *c, f);",
                                 "const double y = oracle_round(x + *c, f);"),
     "ring_starts_one_master_late": ("const int32_t g = (int32_t)((seg + gi) % ng);",

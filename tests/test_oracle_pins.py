@@ -29,6 +29,32 @@ def _fp32(v):
     return float(np.float32(v))
 
 
+# ----------------------------------------------------- the formats modelled
+
+FP32_MAX = (2 - Fraction(1, 2 ** 23)) * 2 ** 127
+FP32_MIN_SUB = Fraction(1, 2 ** 149)
+
+
+def test_format_ok_accepts_exactly_the_formats_fp32_holds():
+    """A format is modelled when it has a sign, 2..8 exponent bits and 0..23
+    mantissa bits and every one of its finite values is an fp32 value: its
+    largest finite value (2 - 2^-m) * 2^emax at most fp32's, its smallest
+    subnormal 2^(emin - m) at least fp32's 2^-149.  Values computed as exact
+    rationals from the format's definition, across biases that put emax and
+    emin - m on both sides of those limits."""
+    for e in range(1, 10):
+        for m in range(0, 25):
+            dflt = (1 << (e - 1)) - 1
+            top = (1 << e) - 2          # emax = top - bias
+            biases = {dflt, dflt - 1, dflt + 1, top - 127, top - 128, top - 126, 150 - m, 149 - m, 151 - m, -5, 300}
+            for bias in sorted(biases):
+                emax, emin = top - bias, 1 - bias
+                maxfinite = (2 - Fraction(1, 2 ** m)) * Fraction(2) ** emax
+                minsub = Fraction(2) ** (emin - m)
+                want = 2 <= e <= 8 and 0 <= m <= 23 and maxfinite <= FP32_MAX and minsub >= FP32_MIN_SUB
+                assert O.format_ok(F(e, m, bias)) == want, (e, m, bias)
+
+
 # ------------------------------------------------------------------ Table 2
 
 def _table2():
@@ -255,7 +281,8 @@ def test_scale_matches_literal_findmaxexp():
             W, n = N, 500
             G = (rng.standard_normal((W, n)) * 2.0 ** rng.uniform(-40, 20)).astype(np.float32)
             G[:, rng.random(n) < 0.1] = 0
-            offs = np.array([0, 123, 123, 400, n], np.int64)
+            G[:, 400:450] = 0                      # an all-zero layer: no exponent, scale 0
+            offs = np.array([0, 123, 123, 400, 450, n], np.int64)
             mb = O.layer_maxabs(G, n, offs)
             se = O.layer_scales(mb, N, f)
             for i in range(len(offs) - 1):
@@ -263,6 +290,10 @@ def test_scale_matches_literal_findmaxexp():
                 mx = max(exps)
                 lit = 0 if mx == -2 ** 31 else ub - mx
                 assert se[i] == lit, (f, N, i)
+    # a zero has no exponent; INF and NaN products are reported apart
+    assert O.find_max_exp(np.zeros(3, np.float32), 8) == (-2 ** 31, False)
+    assert O.find_max_exp(np.array([0.0, 3.0, np.inf], np.float32), 2) == (3, True)
+    assert O.find_max_exp(np.array([np.nan, -0.75], np.float32), 1) == (0, True)
 
 
 def test_maxabs_nan_inf_zero():
