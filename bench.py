@@ -72,6 +72,9 @@ def parse():
     ap.add_argument("--other-steps", type=int, default=10, help="timed steps per other workload")
     ap.add_argument("--roundoff", action="store_true",
                     help="only run the group-size round-off study (Eq. 5) and print it")
+    ap.add_argument("--ceilings", action="store_true",
+                    help="only time the path's access patterns without arithmetic, and VALU issue rates")
+    ap.add_argument("--probe", default=None, help="with --ceilings: run only this probe")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only run device-to-device copies of this size (counter calibration)")
     return ap.parse_args()
@@ -86,6 +89,156 @@ def copy_calibration(gib: float, reps: int = 5) -> None:
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes_per_dispatch": nbytes, "reps": reps}), flush=True)
+
+
+# ------------------------------------------------------------- ceilings
+
+def _probe_lib():
+    import ctypes
+
+    from paper_1911_08907_amd import build as B
+
+    if not os.path.exists(B.PROBE_LIB):
+        raise RuntimeError(f"{B.PROBE_LIB} is missing: run paper_1911_08907_amd.build.build() first")
+    L = ctypes.CDLL(B.PROBE_LIB)
+    P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    for name, args in {"probe_rows": [i32, P, i32, i64, i64, P, P, P, i32, P],
+                       "probe_flat": [i32, P, i32, i64, i64, P, i32, P],
+                       "probe_copy": [P, P, i64, i32, P],
+                       "probe_widen": [i32, i32, P, P, i64, i32, P],
+                       "probe_valu": [i32, P, i32, i32, P]}.items():
+        fn = getattr(L, name)
+        fn.restype = ctypes.c_int
+        fn.argtypes = args
+    L.probe_device_cus.restype = ctypes.c_int
+    return L
+
+
+ROW_MODES = {"read": 0, "sum_f32": 1, "sum_half": 2, "sum_bytes": 3, "row_bytes": 4, "row_f32": 5}
+VALU_OPS = {"v_add_f32_e32": (0, 1), "v_mul_f32_e32": (1, 1), "v_and_b32_e32": (2, 1), "v_fma_f32": (3, 2),
+            "v_add3_u32": (4, 2), "v_bfe_u32": (5, 2), "v_ldexp_f32": (6, 2)}
+
+
+def ceilings(only: str | None = None, reps: int = 5) -> dict:
+    """The access patterns of the path's kernels with no arithmetic
+    (libaps_probe.so), timed with HIP events on the launch stream (median of
+    `reps`), and the VALU issue rate of single instructions.  Sizes are the
+    workloads': the ResNet-50 set at W = 256 and W = 8, BERT-large at W = 8."""
+    import torch
+
+    L = _probe_lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.init()
+    cus = L.probe_device_cus()
+    stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
+    ptr = lambda t: None if t is None else t.data_ptr()  # noqa: E731
+    res = {"device_cus": cus, "patterns": {}, "valu": {}}
+
+    def timed(name, fn, nbytes, **info):
+        if only and name != only:
+            return
+        st = fn()
+        if st != 0:
+            raise RuntimeError(f"probe {name}: status {st}")
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        t = sorted(ts)[len(ts) // 2]
+        res["patterns"][name] = {"ms": t, "bytes": nbytes, "TBps": nbytes / (t * 1e-3) / 1e12,
+                                 "frac_of_8TBps": nbytes / (t * 1e-3) / 1e12 / 8.0, **info}
+        print(f"# {name}: {t:.4f} ms, {nbytes / (t * 1e-3) / 1e12:.2f} TB/s", file=sys.stderr, flush=True)
+
+    def rows(tag, W, n_full, modes, widths):
+        n = n_full // 1024 * 1024
+        ld = (n_full + 63) // 64 * 64
+        if only and not any(only.startswith(f"rows_{m}_{tag}") for m in modes):
+            return
+        G = torch.zeros((W, ld), dtype=torch.float32, device=dev)
+        out = torch.empty(n, dtype=torch.float32, device=dev)
+        byt = torch.empty(n, dtype=torch.uint8, device=dev)
+        half = torch.empty(n, dtype=torch.int16, device=dev)
+        for m in modes:
+            extra = {"read": 0, "sum_f32": 4, "sum_half": 2, "sum_bytes": 5, "row_bytes": W, "row_f32": 4 * W}[m]
+            dst_o, dst_b = out, byt
+            if m == "row_bytes":
+                dst_b = torch.empty((W, ld), dtype=torch.uint8, device=dev)
+            if m == "row_f32":
+                dst_o = torch.empty((W, ld), dtype=torch.float32, device=dev)
+            for bpc in widths:
+                timed(f"rows_{m}_{tag}_{bpc}percu",
+                      lambda: L.probe_rows(ROW_MODES[m], ptr(G), W, ld, n, ptr(dst_o), ptr(dst_b), ptr(half), bpc,
+                                           stream()),
+                      4.0 * W * n + extra * n, W=W, n=n, blocks_per_cu=bpc)
+            del dst_o, dst_b
+            torch.cuda.empty_cache()
+        if any(m in ("row_bytes", "row_f32") for m in modes):
+            for outb in (1, 4):
+                dst = torch.empty((W, ld * outb), dtype=torch.uint8, device=dev)
+                for bpc in (8, 16, 32):
+                    timed(f"flat_{'bytes' if outb == 1 else 'f32'}_{tag}_{bpc}percu",
+                          lambda: L.probe_flat(outb, ptr(G), W, ld, n // 4096 * 4096, ptr(dst), bpc, stream()),
+                          (4.0 + outb) * W * (n // 4096 * 4096), W=W, n=n // 4096 * 4096, blocks_per_cu=bpc)
+                del dst
+                torch.cuda.empty_cache()
+        del G, out, byt, half
+        torch.cuda.empty_cache()
+
+    n50, n_bert = 25557032, 335141888
+    rows("resnet50_w256", 256, n50, ["read", "sum_f32", "sum_half", "sum_bytes", "row_bytes", "row_f32"], (16, 24))
+    rows("resnet50_w8", 8, n50, ["read", "sum_f32", "sum_bytes", "row_bytes"], (32, 64))
+    bert_wide = min(512, (n_bert // 1024) * 2 // (cus * 5))
+    rows("bert_large", 8, n_bert, ["read", "sum_f32", "sum_bytes"], (32, bert_wide))
+    if not only or only.startswith("copy"):
+        n = 1 << 29  # 2 GiB
+        a = torch.zeros(n, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        for bpc in (8, 32):
+            timed(f"copy_2GiB_{bpc}percu", lambda: L.probe_copy(ptr(a), ptr(b), n, bpc, stream()), 8.0 * n,
+                  n=n, blocks_per_cu=bpc)
+        del a, b
+        torch.cuda.empty_cache()
+    if not only or only.startswith("widen"):
+        n = n50 // 16 * 16
+        src = torch.zeros(2 * n, dtype=torch.uint8, device=dev)
+        dst = torch.empty(n, dtype=torch.float32, device=dev)
+        for ib, per in ((1, 4), (1, 16), (2, 16)):
+            for bpc in (8, 32):
+                timed(f"widen_{ib}B_{per}perthread_resnet50_{bpc}percu",
+                      lambda: L.probe_widen(ib, per, ptr(src), ptr(dst), n, bpc, stream()), (ib + 4.0) * n,
+                      n=n, in_bytes=ib, per_thread=per, blocks_per_cu=bpc)
+        del src, dst
+        torch.cuda.empty_cache()
+    if not only or only.startswith("valu"):
+        sink = torch.empty(256, dtype=torch.float32, device=dev)
+        iters, bpc = 2048, 16
+        blocks = cus * bpc
+        for name, (op, slots) in VALU_OPS.items():
+            if only and only != f"valu_{name}":
+                continue
+            L.probe_valu(op, ptr(sink), bpc, iters, stream())
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(reps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                L.probe_valu(op, ptr(sink), bpc, iters, stream())
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1))
+            t = sorted(ts)[len(ts) // 2]
+            lane_instr = blocks * 256.0 * iters * 64
+            rate = lane_instr / (t * 1e-3)
+            res["valu"][name] = {"ms": t, "lane_instr_per_s": rate,
+                                 "lanes_per_clk_per_cu_at_2.4GHz": rate / cus / 2.4e9,
+                                 "frac_of_78.6T": rate / (VALU_PEAK_T * 1e12), "issue_slots_assumed": slots}
+            print(f"# {name}: {rate / cus / 2.4e9:.1f} lanes/clk/CU", file=sys.stderr, flush=True)
+    return res
 
 
 def traffic_from_profile(kernel: str, config: str, palette: str):
@@ -562,6 +715,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration > 0:
         copy_calibration(args.copy_calibration)
+        return
+    if args.ceilings:
+        print(json.dumps(ceilings(args.probe)), flush=True)
         return
     if args.roundoff:
         print(json.dumps({"study": ROUNDOFF_STUDY, "error": roundoff_study()}), flush=True)

@@ -1,7 +1,9 @@
 """Build libaps.so (HIP kernels + C ABI) for gfx950 with hipcc, in-tree.
 
 Each kernel file under csrc/ is compiled to an object in parallel; the
-objects are then linked into one shared library."""
+objects are then linked into one shared library.  The benchmark's
+measurement probes (probe/*.hip, the path's access patterns without its
+arithmetic) are linked into a library of their own, libaps_probe.so."""
 from __future__ import annotations
 
 import glob
@@ -14,6 +16,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libaps.so")
+PROBE_DIR = os.path.join(PKG, "probe")
+PROBE_LIB = os.path.join(PKG, "libaps_probe.so")
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",
@@ -47,12 +51,19 @@ def _noise(stderr: str) -> list:
 
 
 def build(verbose: bool = False, jobs: int | None = None) -> str:
-    """Compile every csrc/*.hip file and link libaps.so next to this file."""
+    """Compile every csrc/*.hip file and link libaps.so next to this file,
+    then the probes into libaps_probe.so."""
+    _link(sources(), LIB, "libaps.so", verbose, jobs)
+    _link(sorted(glob.glob(os.path.join(PROBE_DIR, "*.hip"))), PROBE_LIB, "libaps_probe.so", verbose, jobs)
+    return LIB
+
+
+def _link(srcs: list, lib: str, name: str, verbose: bool, jobs: int | None) -> None:
     inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
     jobs = jobs or min(8, os.cpu_count() or 1)
     with tempfile.TemporaryDirectory(prefix="aps_build_") as tmp:
         objs, pending = [], []
-        for src in sources():
+        for src in srcs:
             obj = os.path.join(tmp, os.path.basename(src) + ".o")
             cmd = [hipcc(), *HIPCC_FLAGS, *inc, "-c", "-o", obj, src]
             if verbose:
@@ -74,17 +85,16 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
         if failed:
             for src, err in failed:
                 sys.stderr.write(f"--- {src}\n{err}")
-            raise RuntimeError("hipcc failed building libaps.so")
-        tmp_lib = LIB + ".tmp"
+            raise RuntimeError(f"hipcc failed building {name}")
+        tmp_lib = lib + ".tmp"
         cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp_lib, *objs]
         if verbose:
             print(" ".join(cmd), flush=True)
         res = subprocess.run(cmd, capture_output=True, text=True)
         if res.returncode != 0:
             sys.stderr.write(res.stderr)
-            raise RuntimeError("linking libaps.so failed")
-        os.replace(tmp_lib, LIB)
-    return LIB
+            raise RuntimeError(f"linking {name} failed")
+        os.replace(tmp_lib, lib)
 
 
 if __name__ == "__main__":
