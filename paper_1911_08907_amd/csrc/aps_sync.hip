@@ -47,10 +47,12 @@ namespace aps {
 // An accepted sum is a multiple of 2^(-126 - m) (T >= 2^-126), so its fp32
 // pattern, normal or not, has no bits below position 23 - m >= 16.
 
-// Zero the layer maxima before pass 1 accumulates them with atomicMax.
-__global__ void k_sync_clear(uint32_t* __restrict__ maxabs, int32_t L) {
+// Zero the layer maxima before pass 1 accumulates them with atomicMax, and
+// the repair list's length before pass 2 appends to it.
+__global__ void k_sync_clear(uint32_t* __restrict__ maxabs, int32_t L, uint32_t* __restrict__ count) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i < L) maxabs[i] = 0u;
+    if (i == 0) *count = 0u;
 }
 
 // rho: round an fp32 bit pattern to m+1 significant bits, ties to the even
@@ -68,6 +70,7 @@ struct SyncWs {
     uint32_t* __restrict__ count;  // chunks listed for repair
     int32_t* __restrict__ list;    // [nchunks] those chunks
     uint16_t* __restrict__ half;   // [round_up(n, CH)] top halves of the pass-1 sums, or null
+    int32_t* __restrict__ guess;   // [L] guessed exponents (guessed-scale route)
     bool bytes;                    // pass 1 stores minb for the single-entry chunks
 };
 
@@ -324,20 +327,14 @@ __global__ __launch_bounds__(BLOCK) void k_sync_spec_mixed(SyncArgs a, SyncWs ws
     }
 }
 
-// Scale exponents (as k_scales) and the per-layer repair threshold: an
-// element is recomputed when its exponent byte is below thr[i].  thr = 256
+// A layer's scale exponent (as k_scales) and its repair threshold: an
+// element is recomputed when its exponent byte is below th.  th = 256
 // recomputes the whole layer (ghat INF/NaN, N * ghat = INF or above 2^127);
-// an all-zero layer needs nothing.  Also clears the repair list.
-__global__ void k_sync_layers(const uint32_t* __restrict__ maxabs, int32_t L, int32_t N, Pal pal,
-                              const uint8_t* __restrict__ fmt_idx, int32_t* __restrict__ scale_exp, SyncWs ws) {
-    __shared__ FmtK spal[APS_MAX_FORMATS];
-    pal_to_lds(pal, spal);
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i == 0) *ws.count = 0u;
-    if (i >= L) return;
-    const FmtK& f = spal[fmt_idx ? fmt_idx[i] : 0];
-    const uint32_t gb = maxabs[i] & 0x7FFFFFFFu;
-    int32_t r = 0, th = 256;
+// an all-zero layer needs nothing (0).
+__device__ __forceinline__ void sync_layer(uint32_t maxabs_bits, int32_t N, const FmtK& f, int32_t& r, int32_t& th) {
+    const uint32_t gb = maxabs_bits & 0x7FFFFFFFu;
+    r = 0;
+    th = 256;
     if (gb == 0) {
         th = 0;
     } else if (gb < 0x7F800000u) {
@@ -350,49 +347,58 @@ __global__ void k_sync_layers(const uint32_t* __restrict__ maxabs, int32_t L, in
             if (cl <= 127) th = max(f.emin - r + 127, 1);
         }
     }
-    scale_exp[i] = r;
-    ws.thr[i] = th;
 }
 
-// Largest i in [0, L-1] with offsets[i] <= pos, for pos < n (per lane).
-__device__ __forceinline__ int layer_of(const int64_t* __restrict__ off, int L, int64_t pos) {
-    int lo = 0, hi = L;
-    while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (off[mid] <= pos) lo = mid; else hi = mid;
+// Pass 2's bookkeeping in one launch; thread t handles layer t and chunk t.
+//  * Layer t: its exponent into scale_exp and its threshold into thr (the
+//    one-pass route), or the exponent and a mark in thr, 1 where the guess
+//    in ws.guess differed (the guessed-scale route).
+//  * Chunk t (single palette entry): listed for repair when its minimum
+//    byte is below the largest threshold among its layers (one-pass: never
+//    misses a flagged element; the repair looks at each), or when one of its
+//    layers was guessed wrong (guessed scales).  The chunk's thresholds are
+//    recomputed here from the maxima, not read from thr, which other threads
+//    of this launch are writing.  The list's length was zeroed in pass 1.
+__global__ void k_sync_bookkeep(const uint32_t* __restrict__ maxabs, Layers ly, int32_t N, Pal pal,
+                                int32_t* __restrict__ scale_exp, SyncWs ws, bool guess) {
+    __shared__ FmtK spal[APS_MAX_FORMATS];
+    pal_to_lds(pal, spal);
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    // what decides a layer's repair: its threshold, or whether its guess was wrong
+    auto layer_th = [&](int i, int32_t& r) {
+        const FmtK& f = spal[ly.fmt_idx ? ly.fmt_idx[i] : 0];
+        int32_t th;
+        sync_layer(maxabs[i], N, f, r, th);
+        return guess ? (clamp_exp(r) != clamp_exp(ws.guess[i]) ? 1 : 0) : th;
+    };
+    if (t < ly.L) {
+        int32_t r;
+        const int32_t th = layer_th((int)t, r);
+        scale_exp[t] = r;
+        ws.thr[t] = th;
     }
-    return lo;
-}
-
-// One thread per chunk: list the chunks (single palette entry) holding an
-// element whose byte is below its layer's threshold.  The test is on the
-// chunk's minimum byte against the largest threshold among its layers, so
-// it never misses one; the repair looks at each element.  With every (the
-// guessed-scale route, no bytes) each element counts as byte 0, so a chunk
-// is listed when one of its layers has a nonzero threshold.
-__global__ void k_sync_scan(Layers ly, SyncWs ws, bool every) {
-    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t nchunks = (ly.n + CH - 1) / CH;
-    if (c >= nchunks) return;
-    const int64_t start = c * CH;
+    if (t >= nchunks) return;
+    const int64_t start = t * CH;
     const int64_t end = min(start + CH, ly.n);
-    uint32_t cm = 0u;
-    if (!every) {
-        const uint32_t w4 = *(const uint32_t*)(ws.wmin + 4 * c);
+    uint32_t cm = 0u;  // the guessed-scale route reruns whole chunks: every element counts as byte 0
+    if (!guess) {
+        const uint32_t w4 = *(const uint32_t*)(ws.wmin + 4 * t);
         cm = 255u;
         for (int wv = 0; wv < 4; ++wv)
             if (start + 256 * wv < end) cm = min(cm, (w4 >> (8 * wv)) & 0xFFu);
     }
-    const int i0 = layer_of(ly.offsets, ly.L, start), i1 = layer_of(ly.offsets, ly.L, end - 1);
+    const int i0 = find_layer(ly.offsets, ly.L, start, 0), i1 = find_layer(ly.offsets, ly.L, end - 1, i0);
     int32_t th = 0;
     bool mixed = false;
     const int p0 = ly.fmt_idx ? ly.fmt_idx[i0] : 0;
     for (int i = i0; i <= i1; ++i) {
         if (ly.offsets[i] == ly.offsets[i + 1]) continue;  // empty layer
-        th = max(th, ws.thr[i]);
+        int32_t r;
+        th = max(th, layer_th(i, r));
         if (ly.fmt_idx && ly.fmt_idx[i] != p0) mixed = true;
     }
-    if (!mixed && (int32_t)cm < th) ws.list[atomicAdd(ws.count, 1u)] = (int32_t)c;
+    if (!mixed && (int32_t)cm < th) ws.list[atomicAdd(ws.count, 1u)] = (int32_t)t;
 }
 
 constexpr int SPARSE_MAX = 16;  // flagged elements per chunk repaired one wave each
@@ -580,13 +586,14 @@ __global__ __launch_bounds__(BLOCK) void k_sync_widen(const uint16_t* __restrict
 constexpr int GUESS_ROW_STRIDE = 32;
 
 // The guessed exponent of each layer from the sampled maxima (rows sampled
-// rows of N), into scale_exp: as k_scales, on the sample's N * max raised by
-// the expected growth of the max.
+// rows of N), into guess: as k_scales, on the sample's N * max raised by the
+// expected growth of the max.  Also zeroes the repair list's length.
 __global__ void k_guess_scales(const uint32_t* __restrict__ maxabs, Layers ly, int32_t N, int32_t rows, Pal pal,
-                               int32_t* __restrict__ scale_exp) {
+                               int32_t* __restrict__ guess, uint32_t* __restrict__ count) {
     __shared__ FmtK spal[APS_MAX_FORMATS];
     pal_to_lds(pal, spal);
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i == 0) *count = 0u;
     if (i >= ly.L) return;
     const FmtK& f = spal[ly.fmt_idx ? ly.fmt_idx[i] : 0];
     const uint32_t gb = maxabs[i] & 0x7FFFFFFFu;
@@ -602,7 +609,7 @@ __global__ void k_guess_scales(const uint32_t* __restrict__ maxabs, Layers ly, i
             r = f.emax - ceil_log2_bits(tb);
         }
     }
-    scale_exp[i] = r;
+    guess[i] = r;
 }
 
 // Pass 1 of the guessed-scale route over the chunks of one variant's format:
@@ -668,29 +675,6 @@ __global__ __launch_bounds__(BLOCK) void k_guess_spec(ReduceArgs a, Layers ly, P
     flush_out(a, pd);
 }
 
-// Pass 2 of the guessed-scale route: the exponents (as k_scales) replace the
-// guesses in scale_exp; thr = 1 marks a layer whose guess differed (all of
-// its chunks are rerun), 0 one whose pass-1 sums stand.  Also clears the
-// repair list.
-__global__ void k_guess_layers(const uint32_t* __restrict__ maxabs, int32_t L, int32_t N, Pal pal,
-                               const uint8_t* __restrict__ fmt_idx, int32_t* __restrict__ scale_exp, SyncWs ws) {
-    __shared__ FmtK spal[APS_MAX_FORMATS];
-    pal_to_lds(pal, spal);
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i == 0) *ws.count = 0u;
-    if (i >= L) return;
-    const FmtK& f = spal[fmt_idx ? fmt_idx[i] : 0];
-    const uint32_t gb = maxabs[i] & 0x7FFFFFFFu;
-    int32_t r = 0;
-    if (gb != 0 && gb < 0x7F800000u) {
-        const float t = (float)N * u2f(gb);
-        const uint32_t tb = f2u(t);
-        if (tb < 0x7F800000u) r = f.emax - ceil_log2_bits(tb);
-    }
-    ws.thr[i] = clamp_exp(r) != clamp_exp(scale_exp[i]) ? 1 : 0;
-    scale_exp[i] = r;
-}
-
 }  // namespace aps
 
 using namespace aps;
@@ -698,9 +682,10 @@ using namespace aps;
 // Workspace of aps_sync, in 256-byte aligned parts: the per-element exponent
 // bytes (padded to whole chunks), four bytes per chunk, the int32 layer
 // thresholds, the list counter, the int32 chunk list, two bytes per element
-// (padded to whole chunks) for the top halves of the pass-1 sums.
+// (padded to whole chunks) for the top halves of the pass-1 sums, the int32
+// guessed exponents.
 struct SyncLayout {
-    uint64_t minb, wmin, thr, count, list, half, total;
+    uint64_t minb, wmin, thr, count, list, half, guess, total;
 };
 
 static uint64_t up256(uint64_t b) { return (b + 255u) & ~(uint64_t)255u; }
@@ -714,7 +699,8 @@ static SyncLayout sync_layout(int64_t n, int32_t L) {
     o.count = o.thr + up256(4u * (uint64_t)L);
     o.list = o.count + 256u;
     o.half = o.list + up256(4u * nch);
-    o.total = o.half + up256(2u * nch * (uint64_t)CH);
+    o.guess = o.half + up256(2u * nch * (uint64_t)CH);
+    o.total = o.guess + up256(4u * (uint64_t)L);
     return o;
 }
 
@@ -793,7 +779,7 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
     const int64_t nchunks = (n + CH - 1) / CH;
     uint8_t* wb = (uint8_t*)workspace;
     SyncWs ws{wb + lay.minb, wb + lay.wmin, (int32_t*)(wb + lay.thr), (uint32_t*)(wb + lay.count),
-              (int32_t*)(wb + lay.list), nullptr, W >= SYNC_BYTES_MIN_W};
+              (int32_t*)(wb + lay.list), nullptr, (int32_t*)(wb + lay.guess), W >= SYNC_BYTES_MIN_W};
     Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
     const int route = sync_route(W, n, pal, n_fmts, flags);
     if (route == APS_SYNC_ROUTE_ONE_PASS && W >= SYNC_HALF_MIN_W) {
@@ -829,11 +815,14 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
         const int32_t rows = (W + GUESS_ROW_STRIDE - 1) / GUESS_ROW_STRIDE;
         st = aps_layer_maxabs(G, rows, rows > 1 ? ld * GUESS_ROW_STRIDE : ld, n, offsets, L, maxabs_bits, stream);
         if (st != APS_OK) return st;
-        hipLaunchKernelGGL(k_guess_scales, lgrid, dim3(256), 0, s, maxabs_bits, ly, W, rows, pal, scale_exp);
+        hipLaunchKernelGGL(k_guess_scales, lgrid, dim3(256), 0, s, maxabs_bits, ly, W, rows, pal, ws.guess, ws.count);
         if (n > 0) {
-            // the full maxima accumulate on top of the sampled ones
+            // the full maxima accumulate on top of the sampled ones; the sums
+            // take the guessed exponents
+            Layers lg = ly;
+            lg.scale_exp = ws.guess;
 #define APS_LAUNCH_G(v) \
-    if (vm & (1u << (v))) hipLaunchKernelGGL(k_guess_spec<v>, grid, dim3(BLOCK), 0, s, ra, ly, pal, maxabs_bits);
+    if (vm & (1u << (v))) hipLaunchKernelGGL(k_guess_spec<v>, grid, dim3(BLOCK), 0, s, ra, lg, pal, maxabs_bits);
             APS_FOR_VARIANTS(APS_LAUNCH_G)
 #undef APS_LAUNCH_G
             if (mixed)
@@ -841,7 +830,7 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
         }
     }
     if (!guess && (phases & APS_SYNC_PASS1)) {
-        hipLaunchKernelGGL(k_sync_clear, lgrid, dim3(256), 0, s, maxabs_bits, L);
+        hipLaunchKernelGGL(k_sync_clear, lgrid, dim3(256), 0, s, maxabs_bits, L, ws.count);
         if (n > 0) {
             // launch width measured on MI355X: 24 blocks per CU for many rows,
             // 32 for few (shorter work per chunk), wider on large sets
@@ -852,12 +841,10 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
         }
     }
     if (phases & APS_SYNC_PASS2) {
-        if (guess)
-            hipLaunchKernelGGL(k_guess_layers, lgrid, dim3(256), 0, s, maxabs_bits, L, W, pal, fmt_idx, scale_exp, ws);
-        else
-            hipLaunchKernelGGL(k_sync_layers, lgrid, dim3(256), 0, s, maxabs_bits, L, W, pal, fmt_idx, scale_exp, ws);
+        const int64_t items = std::max<int64_t>(L, nchunks);
+        hipLaunchKernelGGL(k_sync_bookkeep, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, s, maxabs_bits, ly, W,
+                           pal, scale_exp, ws, guess);
         if (n > 0) {
-            hipLaunchKernelGGL(k_sync_scan, dim3((unsigned)((nchunks + 255) / 256)), dim3(256), 0, s, ly, ws, guess);
             if (ws.half) {
                 const int64_t threads = (n + 7) / 8;
                 // one pass per thread: up to 64 blocks per CU
