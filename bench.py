@@ -74,7 +74,7 @@ def parse():
                     help="only run the group-size round-off study (Eq. 5) and print it")
     ap.add_argument("--ceilings", action="store_true",
                     help="only time the path's access patterns without arithmetic, and VALU issue rates")
-    ap.add_argument("--probe", default=None, help="with --ceilings: run only this probe")
+    ap.add_argument("--probe", default=None, help="with --ceilings: run only the probes whose names start so")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only run device-to-device copies of this size (counter calibration)")
     return ap.parse_args()
@@ -104,6 +104,7 @@ def _probe_lib():
     P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     for name, args in {"probe_rows": [i32, P, i32, i64, i64, P, P, P, i32, P],
                        "probe_flat": [i32, P, i32, i64, i64, P, i32, P],
+                       "probe_rowmajor": [i32, i32, P, i32, i64, i64, P, i32, P],
                        "probe_copy": [P, P, i64, i32, P],
                        "probe_widen": [i32, i32, P, P, i64, i32, P],
                        "probe_valu": [i32, P, i32, i32, P]}.items():
@@ -134,8 +135,14 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
     ptr = lambda t: None if t is None else t.data_ptr()  # noqa: E731
     res = {"device_cus": cus, "patterns": {}, "valu": {}}
 
+    def want(name):
+        return not only or name.startswith(only)
+
+    def group(prefix):  # some probe named prefix... is wanted
+        return not only or prefix.startswith(only) or only.startswith(prefix)
+
     def timed(name, fn, nbytes, **info):
-        if only and name != only:
+        if not want(name):
             return
         st = fn()
         if st != 0:
@@ -157,13 +164,20 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
     def rows(tag, W, n_full, modes, widths):
         n = n_full // 1024 * 1024
         ld = (n_full + 63) // 64 * 64
-        if only and not any(only.startswith(f"rows_{m}_{tag}") for m in modes):
+        writes_rows = any(m in ("row_bytes", "row_f32") for m in modes)
+        names = [f"rows_{m}_{tag}_{b}percu" for m in modes for b in widths]
+        if writes_rows:
+            names += [f"{k}_{o}_{tag}" for k in ("flat", "rowmajor") for o in ("bytes", "f32")]
+            names += [f"rowmajor_{o}_{g}inflight_{tag}" for o in ("bytes", "f32") for g in (1, 4, 8)]
+        if only and not any(nm.startswith(only) or only.startswith(nm) for nm in names):
             return
         G = torch.zeros((W, ld), dtype=torch.float32, device=dev)
         out = torch.empty(n, dtype=torch.float32, device=dev)
         byt = torch.empty(n, dtype=torch.uint8, device=dev)
         half = torch.empty(n, dtype=torch.int16, device=dev)
         for m in modes:
+            if not any(want(f"rows_{m}_{tag}_{b}percu") for b in widths):
+                continue
             extra = {"read": 0, "sum_f32": 4, "sum_half": 2, "sum_bytes": 5, "row_bytes": W, "row_f32": 4 * W}[m]
             dst_o, dst_b = out, byt
             if m == "row_bytes":
@@ -177,13 +191,21 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
                       4.0 * W * n + extra * n, W=W, n=n, blocks_per_cu=bpc)
             del dst_o, dst_b
             torch.cuda.empty_cache()
-        if any(m in ("row_bytes", "row_f32") for m in modes):
+        if writes_rows:
             for outb in (1, 4):
+                kind = "bytes" if outb == 1 else "f32"
+                if not (group(f"flat_{kind}_{tag}") or group(f"rowmajor_{kind}_")):
+                    continue
                 dst = torch.empty((W, ld * outb), dtype=torch.uint8, device=dev)
                 for bpc in (8, 16, 32):
-                    timed(f"flat_{'bytes' if outb == 1 else 'f32'}_{tag}_{bpc}percu",
+                    timed(f"flat_{kind}_{tag}_{bpc}percu",
                           lambda: L.probe_flat(outb, ptr(G), W, ld, n // 4096 * 4096, ptr(dst), bpc, stream()),
                           (4.0 + outb) * W * (n // 4096 * 4096), W=W, n=n // 4096 * 4096, blocks_per_cu=bpc)
+                for g in (1, 4, 8):
+                    for bpc in (8, 16):
+                        timed(f"rowmajor_{kind}_{g}inflight_{tag}_{bpc}percu",
+                              lambda: L.probe_rowmajor(outb, g, ptr(G), W, ld, n, ptr(dst), bpc, stream()),
+                              (4.0 + outb) * W * n, W=W, n=n, chunks_in_flight=g, blocks_per_cu=bpc)
                 del dst
                 torch.cuda.empty_cache()
         del G, out, byt, half
@@ -194,7 +216,7 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
     rows("resnet50_w8", 8, n50, ["read", "sum_f32", "sum_bytes", "row_bytes"], (32, 64))
     bert_wide = min(512, (n_bert // 1024) * 2 // (cus * 5))
     rows("bert_large", 8, n_bert, ["read", "sum_f32", "sum_bytes"], (32, bert_wide))
-    if not only or only.startswith("copy"):
+    if group("copy_2GiB"):
         n = 1 << 29  # 2 GiB
         a = torch.zeros(n, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)
@@ -203,7 +225,7 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
                   n=n, blocks_per_cu=bpc)
         del a, b
         torch.cuda.empty_cache()
-    if not only or only.startswith("widen"):
+    if group("widen_"):
         n = n50 // 16 * 16
         src = torch.zeros(2 * n, dtype=torch.uint8, device=dev)
         dst = torch.empty(n, dtype=torch.float32, device=dev)
@@ -214,12 +236,12 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
                       n=n, in_bytes=ib, per_thread=per, blocks_per_cu=bpc)
         del src, dst
         torch.cuda.empty_cache()
-    if not only or only.startswith("valu"):
+    if group("valu_"):
         sink = torch.empty(256, dtype=torch.float32, device=dev)
         iters, bpc = 2048, 16
         blocks = cus * bpc
         for name, (op, slots) in VALU_OPS.items():
-            if only and only != f"valu_{name}":
+            if not want(f"valu_{name}"):
                 continue
             L.probe_valu(op, ptr(sink), bpc, iters, stream())
             torch.cuda.synchronize()

@@ -144,6 +144,49 @@ struct DeqArgs {
     int32_t code_cls;
 };
 
+// A thread's 4 elements of one chunk as loaded: the fp32 bit patterns, or
+// the 4 codes (one 2-, 4- or 8-byte load, by code class).
+struct DeqRaw {
+    uint32_t w[4];
+};
+
+template <int IN>  // 0: fp32 values; 1 + code class: codes
+__device__ __forceinline__ DeqRaw deq_load(const DeqArgs& a, int64_t j) {
+    DeqRaw r;
+    if constexpr (IN == 0) {
+        const f4 v = __builtin_nontemporal_load((const f4*)(a.Q + j));
+        r.w[0] = f2u(v.x);
+        r.w[1] = f2u(v.y);
+        r.w[2] = f2u(v.z);
+        r.w[3] = f2u(v.w);
+    } else if constexpr (IN == 1) {  // nibbles: elements j..j+3 in 2 bytes
+        const uint32_t h = __builtin_nontemporal_load((const uint16_t*)(a.codes + (j >> 1)));
+        r.w[0] = h & 15u;
+        r.w[1] = (h >> 4) & 15u;
+        r.w[2] = (h >> 8) & 15u;
+        r.w[3] = h >> 12;
+    } else if constexpr (IN == 2) {  // bytes
+        const uint32_t b = __builtin_nontemporal_load((const uint32_t*)(a.codes + j));
+        r.w[0] = b & 255u;
+        r.w[1] = (b >> 8) & 255u;
+        r.w[2] = (b >> 16) & 255u;
+        r.w[3] = b >> 24;
+    } else {  // little-endian uint16
+        const u2v b = __builtin_nontemporal_load((const u2v*)(a.codes + 2 * j));
+        r.w[0] = b.x & 0xFFFFu;
+        r.w[1] = b.x >> 16;
+        r.w[2] = b.y & 0xFFFFu;
+        r.w[3] = b.y >> 16;
+    }
+    return r;
+}
+
+// Chunks a block has in flight at once: their loads are issued together, so
+// each wave waits for memory once per DEQ_GROUP chunks (the work per chunk
+// is 4 elements per thread, too little to cover a load's latency).
+constexpr int DEQ_GROUP = 8;
+
+template <int IN>
 __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal pal) {
     __shared__ FmtK spal[APS_MAX_FORMATS];
     pal_to_lds(pal, spal);
@@ -151,40 +194,74 @@ __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal 
     int64_t cb, ce;
     block_range(nchunks, cb, ce);
     int hint = 0;
-    for (int64_t c = cb; c < ce; ++c) {
-        const int64_t start = c * CH;
-        const int64_t end = min(start + CH, ly.n);
-        const ChunkInfo ci = chunk_layers(ly, start, end, hint);
-        hint = ci.i0;
-        const int64_t j = start + (int64_t)threadIdx.x * VEC;
-        if (j >= end) continue;
-        if (ci.i0 == ci.i1 && j + 4 <= end) {
-            // one layer: uniform format and exponent, 16-byte accesses
-            const FmtK& f = pal.f[ci.pidx];
-            const int32_t ft = ly.scale_exp ? clamp_exp(cld(ly.scale_exp, ci.i0)) : 0;
-            f4 v;
-            if (a.Q) {
-                v = *(const f4*)(a.Q + j);
-            } else {
-                v.x = decode(load_code(a.codes, j, a.code_cls), f);
-                v.y = decode(load_code(a.codes, j + 1, a.code_cls), f);
-                v.z = decode(load_code(a.codes, j + 2, a.code_cls), f);
-                v.w = decode(load_code(a.codes, j + 3, a.code_cls), f);
+    // the group's loads are unconditional (a branch around each would make
+    // the compiler wait for it before the next): a thread past the end loads
+    // the gradient's last whole group of 4 instead and ignores it
+    const int64_t jlast = (ly.n & ~(int64_t)3) - 4;
+    auto one = [&](int64_t jj, int li) {  // element jj of layer li, on its own
+        const FmtK& f = spal[ly.fmt_idx ? ly.fmt_idx[li] : 0];
+        const int32_t ft = ly.scale_exp ? clamp_exp(ly.scale_exp[li]) : 0;
+        const float v = IN == 0 ? a.Q[jj] : decode(load_code(a.codes, jj, a.code_cls), f);
+        a.out[jj] = __builtin_amdgcn_ldexpf(v, -ft);
+    };
+    if (jlast < 0) {  // fewer than 4 elements: no whole group to load
+        if (blockIdx.x == 0 && threadIdx.x < ly.n) one(threadIdx.x, find_layer(ly.offsets, ly.L, threadIdx.x, 0));
+        return;
+    }
+    for (int64_t c0 = cb; c0 < ce; c0 += DEQ_GROUP) {
+        // the chunks' layers first (scalar loads, wave-uniform), then the
+        // group's data loads, all in flight together
+        ChunkInfo cis[DEQ_GROUP];
+        // usually the whole group lies in one layer: one lookup for all of it
+        const int64_t gend = min(min(c0 + DEQ_GROUP, ce) * CH, ly.n);
+        const ChunkInfo gi = chunk_layers(ly, c0 * CH, gend, hint);
+        hint = __builtin_amdgcn_readfirstlane(gi.i0);
+        if (gi.i0 == gi.i1) {
+#pragma unroll
+            for (int g = 0; g < DEQ_GROUP; ++g) cis[g] = gi;
+        } else {
+#pragma unroll
+            for (int g = 0; g < DEQ_GROUP; ++g) {
+                const int64_t c = min(c0 + g, ce - 1);
+                cis[g] = chunk_layers(ly, c * CH, min(c * CH + CH, ly.n), hint);
+                hint = __builtin_amdgcn_readfirstlane(cis[g].i0);
             }
-            const f4 o = {__builtin_amdgcn_ldexpf(v.x, -ft), __builtin_amdgcn_ldexpf(v.y, -ft),
-                          __builtin_amdgcn_ldexpf(v.z, -ft), __builtin_amdgcn_ldexpf(v.w, -ft)};
-            __builtin_nontemporal_store(o, (f4*)(a.out + j));  // out may alias Q: same elements
-            continue;
         }
-        int li = ci.i0;
-        for (int e = 0; e < 4; ++e) {
-            const int64_t jj = j + e;
-            if (jj >= end) break;
-            while (ly.offsets[li + 1] <= jj) ++li;
-            const FmtK& f = spal[ly.fmt_idx ? ly.fmt_idx[li] : 0];
-            const int32_t ft = ly.scale_exp ? clamp_exp(ly.scale_exp[li]) : 0;
-            const float v = a.Q ? a.Q[jj] : decode(load_code(a.codes, jj, a.code_cls), f);
-            a.out[jj] = __builtin_amdgcn_ldexpf(v, -ft);
+        DeqRaw raw[DEQ_GROUP];
+#pragma unroll
+        for (int g = 0; g < DEQ_GROUP; ++g) {
+            const int64_t j = (c0 + g) * CH + (int64_t)threadIdx.x * VEC;
+            raw[g] = deq_load<IN>(a, min(j, jlast));
+        }
+#pragma unroll
+        for (int g = 0; g < DEQ_GROUP; ++g) {
+            const int64_t c = c0 + g;
+            if (c >= ce) break;
+            const int64_t start = c * CH;
+            const int64_t end = min(start + CH, ly.n);
+            const ChunkInfo& ci = cis[g];
+            const int64_t j = start + (int64_t)threadIdx.x * VEC;
+            if (j >= end) continue;
+            if (ci.i0 == ci.i1 && j + 4 <= end) {
+                // one layer: uniform format and exponent, 16-byte stores
+                const FmtK& f = pal.f[ci.pidx];
+                const int32_t ft = ly.scale_exp ? clamp_exp(cld(ly.scale_exp, ci.i0)) : 0;
+                float v[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = IN == 0 ? u2f(raw[g].w[e]) : decode(raw[g].w[e], f);
+                const f4 o = {__builtin_amdgcn_ldexpf(v[0], -ft), __builtin_amdgcn_ldexpf(v[1], -ft),
+                              __builtin_amdgcn_ldexpf(v[2], -ft), __builtin_amdgcn_ldexpf(v[3], -ft)};
+                __builtin_nontemporal_store(o, (f4*)(a.out + j));  // out may alias Q: same elements
+                continue;
+            }
+            // several layers in the chunk, or the gradient's ragged end: element by element
+            int li = ci.i0;
+            for (int e = 0; e < 4; ++e) {
+                const int64_t jj = j + e;
+                if (jj >= end) break;
+                while (ly.offsets[li + 1] <= jj) ++li;
+                one(jj, li);
+            }
         }
     }
 }
@@ -250,8 +327,15 @@ extern "C" int aps_dequantize(const float* Q, const void* codes, int64_t n, cons
     Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
     DeqArgs a{Q, (const uint8_t*)codes, out, ccls};
     const int64_t nchunks = (n + CH - 1) / CH;
-    hipLaunchKernelGGL(k_dequantize, dim3((unsigned)grid_for(nchunks, BLOCKS_PER_CU)), dim3(BLOCK), 0, (hipStream_t)stream, a,
-                       ly, pal);
+    // 8 blocks per CU: all resident at once (the probe of this traffic is
+    // fastest there), each walking its range DEQ_GROUP chunks at a time
+    const dim3 grid((unsigned)grid_for(nchunks, 8));
+    hipStream_t s = (hipStream_t)stream;
+    const int in = Q ? 0 : 1 + ccls;
+    if (in == 0) hipLaunchKernelGGL(k_dequantize<0>, grid, dim3(BLOCK), 0, s, a, ly, pal);
+    else if (in == 1) hipLaunchKernelGGL(k_dequantize<1>, grid, dim3(BLOCK), 0, s, a, ly, pal);
+    else if (in == 2) hipLaunchKernelGGL(k_dequantize<2>, grid, dim3(BLOCK), 0, s, a, ly, pal);
+    else hipLaunchKernelGGL(k_dequantize<3>, grid, dim3(BLOCK), 0, s, a, ly, pal);
     return launched();
 }
 

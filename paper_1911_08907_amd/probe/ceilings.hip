@@ -23,6 +23,8 @@
 //   probe_flat   the same bytes as ROW_BYTES / ROW_F32 in a flat order:
 //                each thread reads 16 consecutive elements of one row and
 //                writes their 16 bytes (or 64 bytes) at once;
+//   probe_rowmajor  the same bytes again, each block walking its chunk range
+//                row after row (each row read and written in long runs);
 //   probe_copy   a 1:1 fp32 copy;
 //   probe_widen  read n codes of `in_bytes` bytes, write n fp32 values
 //                (aps_dequantize's traffic), `per` elements per thread;
@@ -117,6 +119,37 @@ __global__ __launch_bounds__(BLOCK) void k_flat(const float* __restrict__ G, uin
         } else {
 #pragma unroll
             for (int k = 0; k < 4; ++k) __builtin_nontemporal_store(x[k], (f4*)((float*)dst + w * ld + j + 4 * k));
+        }
+    }
+}
+
+// Row-major order inside a block's range of chunks: for each row, the block
+// walks all its chunks (G of them in flight), so each row is read and
+// written in one long run; OUTB = 1 writes a byte per element, 4 an fp32.
+template <int OUTB, int G>
+__global__ __launch_bounds__(BLOCK) void k_rowmajor(const float* __restrict__ X, uint8_t* __restrict__ dst, int64_t ld,
+                                                   int64_t n, int32_t W) {
+    const int64_t nchunks = n / CH;  // whole chunks only
+    int64_t cb, ce;
+    block_range(nchunks, cb, ce);
+    for (int64_t w = 0; w < W; ++w) {
+        for (int64_t c0 = cb; c0 < ce; c0 += G) {
+            f4 x[G];
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+                if (c0 + g < ce) x[g] = ld4(X + w * ld + (c0 + g) * CH + (int64_t)threadIdx.x * VEC);
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                if (c0 + g >= ce) break;
+                const int64_t j = (c0 + g) * CH + (int64_t)threadIdx.x * VEC;
+                if constexpr (OUTB == 1) {
+                    const uint32_t w4 = (f2u(x[g].x) >> 24) | ((f2u(x[g].y) >> 24) << 8) | ((f2u(x[g].z) >> 24) << 16) |
+                                        (f2u(x[g].w) & 0xFF000000u);
+                    __builtin_nontemporal_store(w4, (uint32_t*)(dst + w * ld + j));
+                } else {
+                    __builtin_nontemporal_store(x[g], (f4*)((float*)dst + w * ld + j));
+                }
+            }
         }
     }
 }
@@ -241,6 +274,20 @@ extern "C" int probe_flat(int outb, const float* G, int32_t W, int64_t ld, int64
     else
         return -5;
     return probe_done();
+}
+
+// Row-major walk (k_rowmajor): outb 1 or 4, g chunks in flight (1, 4 or 8).
+extern "C" int probe_rowmajor(int outb, int g, const float* X, int32_t W, int64_t ld, int64_t n, void* dst,
+                              int blocks_per_cu, void* stream) {
+    if (!X || !dst || W < 1 || n < CH || ld < n || (ld & 3) || blocks_per_cu < 1) return -2;
+    const dim3 grid((unsigned)grid_for(n / CH, blocks_per_cu));
+    hipStream_t s = (hipStream_t)stream;
+    uint8_t* d = (uint8_t*)dst;
+#define PROBE_RM(O, GG) \
+    if (outb == O && g == GG) { hipLaunchKernelGGL((k_rowmajor<O, GG>), grid, dim3(BLOCK), 0, s, X, d, ld, n, W); return probe_done(); }
+    PROBE_RM(1, 1) PROBE_RM(1, 4) PROBE_RM(1, 8) PROBE_RM(4, 1) PROBE_RM(4, 4) PROBE_RM(4, 8)
+#undef PROBE_RM
+    return -5;
 }
 
 extern "C" int probe_copy(const float* src, float* dst, int64_t n, int blocks_per_cu, void* stream) {
