@@ -184,12 +184,27 @@ __device__ __forceinline__ DeqRaw deq_load(const DeqArgs& a, int64_t j) {
 // Chunks a block has in flight at once: their loads are issued together, so
 // each wave waits for memory once per DEQ_GROUP chunks (the work per chunk
 // is 4 elements per thread, too little to cover a load's latency).
-constexpr int DEQ_GROUP = 8;
+constexpr int DEQ_GROUP = 4;
 
+// Codes of up to 8 bits decode through a table in LDS, one per palette
+// entry (value of every code), filled once per block; 16-bit codes decode
+// arithmetically.
 template <int IN>
 __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal pal) {
+    constexpr bool TABLE = IN == 1 || IN == 2;
+    constexpr int NCODES = IN == 1 ? 16 : 256;
     __shared__ FmtK spal[APS_MAX_FORMATS];
+    __shared__ float lut[TABLE ? APS_MAX_FORMATS : 1][TABLE ? NCODES : 1];
     pal_to_lds(pal, spal);
+    if constexpr (TABLE) {
+        for (int t = threadIdx.x; t < ly.n_fmts * NCODES; t += BLOCK)
+            lut[t / NCODES][t % NCODES] = decode((uint32_t)(t % NCODES), spal[t / NCODES]);
+        __syncthreads();
+    }
+    auto dec = [&](uint32_t code, int p, const FmtK& f) -> float {
+        if constexpr (TABLE) return lut[p][code];
+        else return decode(code, f);
+    };
     const int64_t nchunks = (ly.n + CH - 1) / CH;
     int64_t cb, ce;
     block_range(nchunks, cb, ce);
@@ -199,9 +214,9 @@ __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal 
     // the gradient's last whole group of 4 instead and ignores it
     const int64_t jlast = (ly.n & ~(int64_t)3) - 4;
     auto one = [&](int64_t jj, int li) {  // element jj of layer li, on its own
-        const FmtK& f = spal[ly.fmt_idx ? ly.fmt_idx[li] : 0];
+        const int p = ly.fmt_idx ? ly.fmt_idx[li] : 0;
         const int32_t ft = ly.scale_exp ? clamp_exp(ly.scale_exp[li]) : 0;
-        const float v = IN == 0 ? a.Q[jj] : decode(load_code(a.codes, jj, a.code_cls), f);
+        const float v = IN == 0 ? a.Q[jj] : dec(load_code(a.codes, jj, a.code_cls), p, spal[p]);
         a.out[jj] = __builtin_amdgcn_ldexpf(v, -ft);
     };
     if (jlast < 0) {  // fewer than 4 elements: no whole group to load
@@ -248,7 +263,7 @@ __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal 
                 const int32_t ft = ly.scale_exp ? clamp_exp(cld(ly.scale_exp, ci.i0)) : 0;
                 float v[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] = IN == 0 ? u2f(raw[g].w[e]) : decode(raw[g].w[e], f);
+                for (int e = 0; e < 4; ++e) v[e] = IN == 0 ? u2f(raw[g].w[e]) : dec(raw[g].w[e], ci.pidx, f);
                 const f4 o = {__builtin_amdgcn_ldexpf(v[0], -ft), __builtin_amdgcn_ldexpf(v[1], -ft),
                               __builtin_amdgcn_ldexpf(v[2], -ft), __builtin_amdgcn_ldexpf(v[3], -ft)};
                 __builtin_nontemporal_store(o, (f4*)(a.out + j));  // out may alias Q: same elements
@@ -327,9 +342,9 @@ extern "C" int aps_dequantize(const float* Q, const void* codes, int64_t n, cons
     Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
     DeqArgs a{Q, (const uint8_t*)codes, out, ccls};
     const int64_t nchunks = (n + CH - 1) / CH;
-    // 8 blocks per CU: all resident at once (the probe of this traffic is
-    // fastest there), each walking its range DEQ_GROUP chunks at a time
-    const dim3 grid((unsigned)grid_for(nchunks, 8));
+    // measured on MI355X (ResNet-50's 25.6 M byte codes): 16 blocks per CU
+    // with 4 chunks in flight beat 8 with 8, 32 with 1 or 2, and 4 with 16
+    const dim3 grid((unsigned)grid_for(nchunks, 16));
     hipStream_t s = (hipStream_t)stream;
     const int in = Q ? 0 : 1 + ccls;
     if (in == 0) hipLaunchKernelGGL(k_dequantize<0>, grid, dim3(BLOCK), 0, s, a, ly, pal);
