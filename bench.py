@@ -588,7 +588,7 @@ def lp_gemm_calls(A, dev, reps: int = 5):
     return res
 
 
-def measure_step(A, gs, pal, idx_t, offs_t, mode: str, steps: int, warmup: int) -> dict:
+def measure_step(A, gs, pal, idx_t, offs_t, mode: str, steps: int, warmup: int, graph: bool = False) -> dict:
     """Time `steps` APS synchronisations of a gradient set after `warmup`
     untimed ones: aps_sync's pass 1 and pass 2 as two calls (APS mode), or
     the reduce with every exponent 0 (RAW mode, casting without APS).  The
@@ -645,6 +645,37 @@ def measure_step(A, gs, pal, idx_t, offs_t, mode: str, steps: int, warmup: int) 
     p2 = sum(e[1].elapsed_time(e[2]) for e in ev) / len(ev)
     assert bool(torch.isfinite(out).all()) or not aps
 
+    graph_ms = None
+    if graph:
+        # the same step captured once in a HIP graph and replayed: the launches
+        # of a step on a set that fits the caches cost more than its work
+        eager = out.clone()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step(False)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            step(False)
+        for k in range(2):  # replays equal the eager step, before and after the timing
+            out.fill_(float("nan"))
+            gr.replay()
+            torch.cuda.synchronize()
+            if not torch.equal(out.view(torch.int32), eager.view(torch.int32)):
+                raise RuntimeError("a replay of the captured step differs from the eager step")
+            if k == 0:
+                for _ in range(warmup):
+                    gr.replay()
+                torch.cuda.synchronize()
+                tg = time.perf_counter()
+                for _ in range(steps):
+                    gr.replay()
+                torch.cuda.synchronize()
+                graph_ms = (time.perf_counter() - tg) * 1e3 / steps
+        del gr, eager
+
     rerun = None
     if guess:
         # the layers pass 2 reran: threshold 1 in the workspace's int32[L] part
@@ -676,7 +707,7 @@ def measure_step(A, gs, pal, idx_t, offs_t, mode: str, steps: int, warmup: int) 
     return {"ms_per_step": ms_per_step, "pass1_ms": p1, "pass2_ms": p2, "aps": aps, "one": one, "guess": guess,
             "route": ("one pass" if one else ("guessed scales" if guess else "two passes")) if aps else "raw reduce",
             "kernel": kernel, "kernel_ms": k_ms, "alg_bytes": alg_bytes, "achieved": achieved, "note": note,
-            "rerun": rerun, "arrays": (mab, se, out, ws)}
+            "rerun": rerun, "graph_ms_per_step": graph_ms, "arrays": (mab, se, out, ws)}
 
 
 # The other workloads timed after the headline step (each also in RAW mode,
@@ -709,7 +740,7 @@ def other_configs(A, WL, dev, cfg0: str, pal0: str, held: dict, steps: int, warm
         pal = [A.Format(p.e, p.m, p.bias) for p in WL.CONFIGS[cfg].palettes[palette]]
         offs_t = torch.from_numpy(gs.offsets).to(dev)
         idx_t = None if gs.fmt_idx is None else torch.from_numpy(gs.fmt_idx).to(dev)
-        m = measure_step(A, gs, pal, idx_t, offs_t, mode, steps, warmup)
+        m = measure_step(A, gs, pal, idx_t, offs_t, mode, steps, warmup, graph=True)
         del m["arrays"]
         W, n = gs.W, gs.n
         res[f"{cfg} {palette} {mode}"] = {
@@ -718,11 +749,13 @@ def other_configs(A, WL, dev, cfg0: str, pal0: str, held: dict, steps: int, warm
             "algorithmic_bytes_per_launch": m["alg_bytes"], "achieved_GBps": m["achieved"],
             "frac": m["achieved"] / HBM_PEAK_GBPS, "pass1_ms": m["pass1_ms"], "pass2_ms": m["pass2_ms"],
             **({"guess_reruns": m["rerun"]} if m["rerun"] else {}),
+            "graph_ms_per_step": m["graph_ms_per_step"],
+            "graph_elements_per_s": W * n / (m["graph_ms_per_step"] * 1e-3),
             "residency": ("cache-resident (the W rows fit the 256 MB Infinity Cache; a step is a few launches, "
                           "bound by their latency)") if cache else "HBM",
         }
-        print(f"# {cfg} {palette} {mode}: {m['ms_per_step']:.4f} ms/step, {m['route']}, "
-              f"{m['kernel']} {m['achieved'] / 1e3:.2f} TB/s", file=sys.stderr, flush=True)
+        print(f"# {cfg} {palette} {mode}: {m['ms_per_step']:.4f} ms/step ({m['graph_ms_per_step']:.4f} as a graph), "
+              f"{m['route']}, {m['kernel']} {m['achieved'] / 1e3:.2f} TB/s", file=sys.stderr, flush=True)
         del gs
     held["config"], held["gs"] = None, None
     torch.cuda.empty_cache()
