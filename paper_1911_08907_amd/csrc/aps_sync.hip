@@ -805,10 +805,14 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
     const bool mixed = fmt_idx && n_fmts > 1 && L > 1;
     const unsigned vm = variant_mask(pal, n_fmts);
     const dim3 grid((unsigned)stream_grid(nchunks, W, BLOCKS_PER_CU));  // pass-1 row walks
-    const dim3 rgrid((unsigned)grid_for(nchunks, BLOCKS_PER_CU));         // repairs: the list's length is on the device
+    // repairs: the list's length is only known on the device.  The one-pass
+    // route is taken where few elements need recomputing (often none), so a
+    // narrow grid, whose launch costs less; the guessed-scale route reruns
+    // whole layers, a quarter chunk per wave.
+    const bool guess = route == APS_SYNC_ROUTE_GUESS;
+    const dim3 rgrid((unsigned)grid_for(nchunks, guess ? BLOCKS_PER_CU : 4));
     ReduceArgs ra{G, out, nullptr, ld, W, 0u, 0};
     SyncArgs sa{G, out, ld, W};
-    const bool guess = route == APS_SYNC_ROUTE_GUESS;
     const int rmode = guess ? RM_CHUNKS : (ws.bytes ? RM_ELEMENTS : RM_QUARTERS);
     if (guess && (phases & APS_SYNC_PASS1)) {
         // the maxima of every GUESS_ROW_STRIDE-th worker give the guesses
