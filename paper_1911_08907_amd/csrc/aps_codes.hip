@@ -46,6 +46,11 @@ __global__ __launch_bounds__(BLOCK) void k_sim_reduce_codes(CodesArgs a, Layers 
     constexpr int EPT = CC == 0 ? 32 : (CC == 1 ? 16 : 8);
     constexpr int64_t CHC = (int64_t)BLOCK * EPT;
     __shared__ float lut[256];
+    // each wave's fp32 outputs pass through its own LDS slots, so that they
+    // leave in stores of consecutive 16-byte pieces per lane (a lane's EPT
+    // outputs written as EPT/4 stores 4*EPT bytes apart wrote up to 1.7x
+    // the output's bytes to HBM)
+    __shared__ __align__(16) float ostage[BLOCK * EPT];
     int lut_pidx = -1;
     const int64_t nchunks = (ly.n + CHC - 1) / CHC;
     int64_t cb, ce;
@@ -123,20 +128,31 @@ __global__ __launch_bounds__(BLOCK) void k_sim_reduce_codes(CodesArgs a, Layers 
                 else cw[e >> 1] |= (cd & 0xFFFFu) << ((e & 1) * 16);
             }
         }
-        if (j + EPT <= end) {
+        const int lane = threadIdx.x & 63;
+        const int64_t wbase = j - (int64_t)lane * EPT;  // the wave's first element
+        if (wbase + 64 * EPT <= end) {
+            // the whole wave is inside the gradient: every lane is here
             if (a.out) {
+                float* wbuf = ostage + (threadIdx.x - lane) * EPT;
 #pragma unroll
                 for (int q = 0; q < EPT / 4; ++q) {
                     const f4 v = {o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]};
-                    __builtin_nontemporal_store(v, (f4*)(a.out + j + 4 * q));
+                    *(f4*)(wbuf + lane * EPT + 4 * q) = v;
                 }
+                __builtin_amdgcn_wave_barrier();
+#pragma unroll
+                for (int q = 0; q < EPT / 4; ++q) {
+                    const f4 v = *(const f4*)(wbuf + 4 * lane + 256 * q);
+                    __builtin_nontemporal_store(v, (f4*)(a.out + wbase + 4 * lane + 256 * q));
+                }
+                __builtin_amdgcn_wave_barrier();
             }
             if (a.codes_out) {
                 const u4v v = {cw[0], cw[1], cw[2], cw[3]};
                 __builtin_nontemporal_store(v, (u4v*)(a.codes_out + code_byte(j, CC)));
             }
         } else {
-            // ragged end of the gradient: element by element
+            // the wave reaches the ragged end of the gradient: element by element
             for (int e = 0; e < EPT && j + e < end; ++e) {
                 if (a.out) a.out[j + e] = o[e];
                 if (a.codes_out) {

@@ -210,8 +210,9 @@ __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal 
     block_range(nchunks, cb, ce);
     int hint = 0;
     // the group's loads are unconditional (a branch around each would make
-    // the compiler wait for it before the next): a thread past the end loads
-    // the gradient's last whole group of 4 instead and ignores it
+    // the compiler wait for it before the next): past the block's last chunk
+    // a thread loads that chunk again, past the gradient's end its last whole
+    // group of 4, and ignores what it loaded
     const int64_t jlast = (ly.n & ~(int64_t)3) - 4;
     auto one = [&](int64_t jj, int li) {  // element jj of layer li, on its own
         const int p = ly.fmt_idx ? ly.fmt_idx[li] : 0;
@@ -245,7 +246,7 @@ __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal 
         DeqRaw raw[DEQ_GROUP];
 #pragma unroll
         for (int g = 0; g < DEQ_GROUP; ++g) {
-            const int64_t j = (c0 + g) * CH + (int64_t)threadIdx.x * VEC;
+            const int64_t j = min(c0 + g, ce - 1) * CH + (int64_t)threadIdx.x * VEC;
             raw[g] = deq_load<IN>(a, min(j, jlast));
         }
 #pragma unroll

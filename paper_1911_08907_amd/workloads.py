@@ -4,7 +4,9 @@ This module only draws inputs: it holds none of the APS arithmetic.  Both the
 HIP path (tests, benchmark) and the CPU oracle consume what it produces.
 
 A gradient set is W workers' flat fp32 gradients stored worker-major as a
-[W][ld] tensor (ld = n rounded up to 64, zero padded), plus the int64 layer
+[W][ld] tensor (ld = n rounded up to 256, zero padded: rows of fp32 start on
+1 KB boundaries and rows of 8-bit codes with the same stride on 256-byte
+ones, so no row shares a cache line with the next), plus the int64 layer
 offsets (one layer per parameter tensor, in parameter-registration order),
 and a per-layer palette index.
 
@@ -196,7 +198,7 @@ def generate(cfg_name: str, palette: str | None = None, device="cpu", seed: int 
     cfg, shapes, names, sizes, offs = layout(cfg_name)
     W = cfg.W if W is None else W
     n = int(offs[-1])
-    ld = (n + 63) // 64 * 64
+    ld = (n + 255) // 256 * 256
     pal_name = palette or next(iter(cfg.palettes))
     pal = cfg.palettes[pal_name]
     fmt_idx = None
