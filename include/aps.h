@@ -190,7 +190,7 @@ int aps_sim_reduce(const float* G, int32_t W, int64_t ld, int64_t n,
  * Bytes of workspace aps_sync needs for n elements and L layers, with
  * C = ceil(n / 1024) chunks: round_up(1024 * C, 256) + round_up(4 * C, 256)
  * + round_up(4 * L, 256) + 256 + round_up(4 * C, 256) + 2048 * C
- * + round_up(4 * L, 256).  Host-only.
+ * + round_up(4 * L, 256) + round_up(C, 256).  Host-only.
  * Returns 0 for negative arguments or n > APS_MAX_ELEMS.
  */
 uint64_t aps_sync_workspace_bytes(int64_t n, int32_t L);

@@ -71,13 +71,14 @@ struct SyncWs {
     int32_t* __restrict__ list;    // [nchunks] those chunks
     uint16_t* __restrict__ half;   // [round_up(n, CH)] top halves of the pass-1 sums, or null
     int32_t* __restrict__ guess;   // [L] guessed exponents (guessed-scale route)
+    uint8_t* __restrict__ listed;  // [nchunks] 1 where the chunk is on the repair list
     bool bytes;                    // pass 1 stores minb for the single-entry chunks
 };
 
 // From this many workers on, and when every palette entry has m <= 7, pass 1
 // writes each sum's top 16 bits instead of the fp32 value: the unscaled
 // chain keeps m+1 significant bits, so the low 16 bits of its fp32 pattern
-// are zero.  Pass 2 widens them into out (k_sync_widen).  Writes in the
+// are zero.  Pass 2 widens them into out (in k_sync_repair).  Writes in the
 // middle of pass 1's row reads cost far more than their bytes at large W;
 // the widening is one short streaming pass.  At small W the writes cost
 // less and the widening more than it saves.
@@ -398,7 +399,9 @@ __global__ void k_sync_bookkeep(const uint32_t* __restrict__ maxabs, Layers ly, 
         th = max(th, layer_th(i, r));
         if (ly.fmt_idx && ly.fmt_idx[i] != p0) mixed = true;
     }
-    if (!mixed && (int32_t)cm < th) ws.list[atomicAdd(ws.count, 1u)] = (int32_t)t;
+    const bool listed = !mixed && (int32_t)cm < th;
+    if (listed) ws.list[atomicAdd(ws.count, 1u)] = (int32_t)t;
+    ws.listed[t] = listed ? 1 : 0;
 }
 
 constexpr int SPARSE_MAX = 16;  // flagged elements per chunk repaired one wave each
@@ -446,19 +449,54 @@ __device__ void repair_one(const ReduceArgs& a, const FmtK& f, int64_t j, int F)
 // spread over many waves; RM_QUARTERS skips a quarter whose wave minimum is
 // not below the largest threshold of the chunk's layers (no element of it
 // can be flagged).
+// One wave widens a chunk's pass-1 sums, kept as top halves, into out: four
+// steps of 4 elements per lane, so that each step's loads (8 bytes per lane)
+// and stores (16) are contiguous across the wave.  The half array is padded
+// to whole chunks.
+__device__ __forceinline__ void widen_chunk(const SyncWs& ws, float* __restrict__ out, int64_t start, int64_t n) {
+    const int lane = threadIdx.x & 63;
+    u2v h[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) h[q] = __builtin_nontemporal_load((const u2v*)(ws.half + start + 256 * q + 4 * lane));
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int64_t j = start + 256 * q + 4 * lane;
+        const f4 v = {u2f(h[q].x << 16), u2f(h[q].x & 0xFFFF0000u), u2f(h[q].y << 16), u2f(h[q].y & 0xFFFF0000u)};
+        if (j + 4 <= n) {
+            __builtin_nontemporal_store(v, (f4*)(out + j));
+        } else {
+            for (int e = 0; e < 4 && j + e < n; ++e) out[j + e] = v[e];
+        }
+    }
+}
+
 template <int V>
-__global__ __launch_bounds__(BLOCK) void k_sync_repair(ReduceArgs a, Layers ly, Pal pal, SyncWs ws, int mode) {
+__global__ __launch_bounds__(BLOCK) void k_sync_repair(ReduceArgs a, Layers ly, Pal pal, SyncWs ws, int mode,
+                                                      bool widen_rest) {
     const bool every = mode != RM_ELEMENTS;
     const int64_t total = (int64_t)*ws.count * (every ? 4 : 1);
     const int lane = threadIdx.x & 63;
     const int64_t nw = (int64_t)gridDim.x * (BLOCK / 64);
-    for (int64_t k = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * (BLOCK / 64) + (threadIdx.x >> 6))); k < total;
-         k += nw) {
+    const int64_t wave = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * (BLOCK / 64) + (threadIdx.x >> 6)));
+    if (ws.half && widen_rest) {
+        // the sums kept as halves (pass 1 from SYNC_HALF_MIN_W workers on):
+        // one launch widens every chunk that is not listed, mixed ones
+        // included (k_sync_repair_mixed runs after it); a listed chunk is
+        // widened by the wave that repairs it, just before its repairs
+        const int64_t nchunks = (ly.n + CH - 1) / CH;
+        for (int64_t c = wave; c < nchunks; c += nw)
+            if (!ws.listed[c]) widen_chunk(ws, a.out, c * CH, ly.n);
+    }
+    for (int64_t k = wave; k < total; k += nw) {
         const int64_t start = (int64_t)cld(ws.list, every ? k >> 2 : k) * CH;
         const int64_t end = min(start + CH, ly.n);
         const ChunkInfo ci = chunk_layers(ly, start, end, 0);
         const FmtK& f = pal.f[ci.pidx];
         if (f.variant != V) continue;  // another launch owns this format
+        if (ws.half) {
+            widen_chunk(ws, a.out, start, ly.n);
+            __threadfence_block();  // the widened values are stored before any repair of the chunk
+        }
         // 16 consecutive elements per lane; the byte array is padded to whole chunks
         const int64_t j0 = start + 16 * lane;
         uint32_t mask = 0;
@@ -546,26 +584,6 @@ __global__ __launch_bounds__(BLOCK) void k_sync_repair_mixed(ReduceArgs a, Layer
         const FmtK& f = spal[ly.fmt_idx[li]];
         const int F = clamp_exp(ly.scale_exp[li]) + f.k;
         a.out[j] = __builtin_amdgcn_ldexpf(reduce_elem_any(a, f, j, F), -F);
-    }
-}
-
-// Pass 2, before the repairs: the pass-1 sums kept as top halves, widened
-// to fp32 into out, 4 elements per thread per step, so that each wave's
-// loads and stores are contiguous (8 bytes in and 16 out per lane; with 8
-// elements per lane, two 16-byte stores 32 bytes apart wrote about 7 % more
-// than the output's bytes to HBM).
-__global__ __launch_bounds__(BLOCK) void k_sync_widen(const uint16_t* __restrict__ half, float* __restrict__ out,
-                                                     int64_t n) {
-    const int64_t stride = (int64_t)gridDim.x * BLOCK * 4;
-    for (int64_t j = ((int64_t)blockIdx.x * BLOCK + threadIdx.x) * 4; j < n; j += stride) {
-        const u2v h = __builtin_nontemporal_load((const u2v*)(half + j));  // padded to whole chunks
-        const f4 a = {u2f(h.x << 16), u2f(h.x & 0xFFFF0000u), u2f(h.y << 16), u2f(h.y & 0xFFFF0000u)};
-        if (j + 4 <= n) {
-            __builtin_nontemporal_store(a, (f4*)(out + j));
-        } else {
-            const float v[4] = {a.x, a.y, a.z, a.w};
-            for (int e = 0; e < 4 && j + e < n; ++e) out[j + e] = v[e];
-        }
     }
 }
 
@@ -686,7 +704,7 @@ using namespace aps;
 // (padded to whole chunks) for the top halves of the pass-1 sums, the int32
 // guessed exponents.
 struct SyncLayout {
-    uint64_t minb, wmin, thr, count, list, half, guess, total;
+    uint64_t minb, wmin, thr, count, list, half, guess, listed, total;
 };
 
 static uint64_t up256(uint64_t b) { return (b + 255u) & ~(uint64_t)255u; }
@@ -701,7 +719,8 @@ static SyncLayout sync_layout(int64_t n, int32_t L) {
     o.list = o.count + 256u;
     o.half = o.list + up256(4u * nch);
     o.guess = o.half + up256(2u * nch * (uint64_t)CH);
-    o.total = o.guess + up256(4u * (uint64_t)L);
+    o.listed = o.guess + up256(4u * (uint64_t)L);
+    o.total = o.listed + up256(nch);
     return o;
 }
 
@@ -780,7 +799,7 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
     const int64_t nchunks = (n + CH - 1) / CH;
     uint8_t* wb = (uint8_t*)workspace;
     SyncWs ws{wb + lay.minb, wb + lay.wmin, (int32_t*)(wb + lay.thr), (uint32_t*)(wb + lay.count),
-              (int32_t*)(wb + lay.list), nullptr, (int32_t*)(wb + lay.guess), W >= SYNC_BYTES_MIN_W};
+              (int32_t*)(wb + lay.list), nullptr, (int32_t*)(wb + lay.guess), wb + lay.listed, W >= SYNC_BYTES_MIN_W};
     Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
     const int route = sync_route(W, n, pal, n_fmts, flags);
     if (route == APS_SYNC_ROUTE_ONE_PASS && W >= SYNC_HALF_MIN_W) {
@@ -811,7 +830,7 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
     // narrow grid, whose launch costs less; the guessed-scale route reruns
     // whole layers, a quarter chunk per wave.
     const bool guess = route == APS_SYNC_ROUTE_GUESS;
-    const dim3 rgrid((unsigned)grid_for(nchunks, guess ? BLOCKS_PER_CU : 4));
+    const dim3 rgrid((unsigned)grid_for(nchunks, (guess || ws.half) ? BLOCKS_PER_CU : 4));
     ReduceArgs ra{G, out, nullptr, ld, W, 0u, 0};
     SyncArgs sa{G, out, ld, W};
     const int rmode = guess ? RM_CHUNKS : (ws.bytes ? RM_ELEMENTS : RM_QUARTERS);
@@ -850,14 +869,13 @@ extern "C" int aps_sync(const float* G, int32_t W, int64_t ld, int64_t n, const 
         hipLaunchKernelGGL(k_sync_bookkeep, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, s, maxabs_bits, ly, W,
                            pal, scale_exp, ws, guess);
         if (n > 0) {
-            if (ws.half) {
-                const int64_t threads = (n + 3) / 4;
-                // one pass per thread: up to 64 blocks per CU
-                hipLaunchKernelGGL(k_sync_widen, dim3((unsigned)grid_for((threads + BLOCK - 1) / BLOCK, 64)), dim3(BLOCK),
-                                   0, s, ws.half, out, n);
-            }
-#define APS_LAUNCH_S(v) \
-    if (vm & (1u << (v))) hipLaunchKernelGGL(k_sync_repair<v>, rgrid, dim3(BLOCK), 0, s, ra, ly, pal, ws, rmode);
+            // the first repair launch also widens the sums kept as halves
+            bool first = true;
+#define APS_LAUNCH_S(v)                                                                                  \
+    if (vm & (1u << (v))) {                                                                              \
+        hipLaunchKernelGGL(k_sync_repair<v>, rgrid, dim3(BLOCK), 0, s, ra, ly, pal, ws, rmode, first); \
+        first = false;                                                                                   \
+    }
             APS_FOR_VARIANTS(APS_LAUNCH_S)
 #undef APS_LAUNCH_S
             if (mixed)

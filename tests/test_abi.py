@@ -214,7 +214,7 @@ def test_sync_workspace_bytes(lib):
     up = lambda b: (b + 255) // 256 * 256
     for n, L in ((0, 1), (1, 1), (1024, 64), (1025, 65), (25557032, 161), (335141888, 391)):
         C = (n + 1023) // 1024
-        assert f(n, L) == up(1024 * C) + up(4 * C) + up(4 * L) + 256 + up(4 * C) + 2048 * C + up(4 * L), (n, L)
+        assert f(n, L) == up(1024 * C) + up(4 * C) + up(4 * L) + 256 + up(4 * C) + 2048 * C + up(4 * L) + up(C), (n, L)
     assert f(-1, 3) == 0 and f(5, -1) == 0 and f((1 << 30) + 1, 1) == 0
 
 
