@@ -116,8 +116,11 @@ def _probe_lib():
 
 
 ROW_MODES = {"read": 0, "sum_f32": 1, "sum_half": 2, "sum_bytes": 3, "row_bytes": 4, "row_f32": 5}
-VALU_OPS = {"v_add_f32_e32": (0, 1), "v_mul_f32_e32": (1, 1), "v_and_b32_e32": (2, 1), "v_fma_f32": (3, 2),
-            "v_add3_u32": (4, 2), "v_bfe_u32": (5, 2), "v_ldexp_f32": (6, 2)}
+# probe op id, instructions per step of a chain
+VALU_OPS = {"v_add_f32_e32": (0, 1), "v_mul_f32_e32": (1, 1), "v_and_b32_e32": (2, 1), "v_fma_f32": (3, 1),
+            "v_add3_u32": (4, 1), "v_bfe_u32": (5, 1), "v_ldexp_f32": (6, 1), "v_and_or_b32": (7, 1),
+            "v_subrev_f32_e32": (8, 1), "v_cmp_nle_f32_e32+v_cndmask_b32_e32 (VCC)": (9, 2),
+            "v_cmp_nle_f32_e64+v_cndmask_b32_e64 (SGPR mask)": (10, 2)}
 
 
 def ceilings(only: str | None = None, reps: int = 5) -> dict:
@@ -163,7 +166,7 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
 
     def rows(tag, W, n_full, modes, widths):
         n = n_full // 1024 * 1024
-        ld = (n_full + 63) // 64 * 64
+        ld = (n_full + 255) // 256 * 256  # rows padded as the workloads pad them
         writes_rows = any(m in ("row_bytes", "row_f32") for m in modes)
         names = [f"rows_{m}_{tag}_{b}percu" for m in modes for b in widths]
         if writes_rows:
@@ -240,7 +243,7 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
         sink = torch.empty(256, dtype=torch.float32, device=dev)
         iters, bpc = 2048, 16
         blocks = cus * bpc
-        for name, (op, slots) in VALU_OPS.items():
+        for name, (op, per_step) in VALU_OPS.items():
             if not want(f"valu_{name}"):
                 continue
             L.probe_valu(op, ptr(sink), bpc, iters, stream())
@@ -254,11 +257,11 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
                 torch.cuda.synchronize()
                 ts.append(e0.elapsed_time(e1))
             t = sorted(ts)[len(ts) // 2]
-            lane_instr = blocks * 256.0 * iters * 64
+            lane_instr = blocks * 256.0 * iters * 64 * per_step
             rate = lane_instr / (t * 1e-3)
             res["valu"][name] = {"ms": t, "lane_instr_per_s": rate,
                                  "lanes_per_clk_per_cu_at_2.4GHz": rate / cus / 2.4e9,
-                                 "frac_of_78.6T": rate / (VALU_PEAK_T * 1e12), "issue_slots_assumed": slots}
+                                 "frac_of_78.6T": rate / (VALU_PEAK_T * 1e12)}
             print(f"# {name}: {rate / cus / 2.4e9:.1f} lanes/clk/CU", file=sys.stderr, flush=True)
     return res
 
@@ -537,16 +540,26 @@ def cpu_baseline(G_t, gs, pal, budget_s: float, slice_cols: int = 65536, single_
 
 # VALU peak: 256 CUs x 128 lanes/clk x 2.4 GHz = 78.6 T lane-instructions/s,
 # the published 157.3 TFLOP/s fp32 vector rate counted one lane-instruction
-# per FMA.  Two-operand (VOP2/VOPC) adds, multiplies and logic ops issue at
-# that rate; three-operand or modifier-carrying (VOP3) instructions such as
-# v_add3_u32, v_bfe_u32, v_ldexp_f32 or v_fma_f32 at half of it (measured:
-# about 54-71 against 87-112 lanes/clk/CU).
+# per FMA.
 VALU_PEAK_T = 256 * 128 * 2.4e9 / 1e12
+# Issue rates of the instructions of k_lp_gemm's k-loop, lanes per clock per
+# CU at 2.4 GHz, measured by bench.py --ceilings (chains of one instruction,
+# profiles/ceilings_patterns_and_valu.txt): two-operand adds, multiplies and
+# ands issue at about 112-120, v_bfe_u32 / v_add3_u32 / v_and_or_b32 at about
+# 62, and a compare into VCC followed by the select that reads it at about
+# 81 per instruction (the hazard wait between them included).
+VALU_RATES = {"v_and_b32": 119.9, "v_add_f32": 112.0, "v_sub_f32": 117.5, "v_mul_f32": 116.9,
+              "v_bfe_u32": 62.3, "v_add3_u32": 62.4, "v_and_or_b32": 62.0, "v_cmp+v_cndmask": 80.8}
 # k_lp_gemm's k-loop for 1-5-2 inputs and a 1-5-10 accumulator (products fit
-# the accumulator's significand), counted in the kernel's ISA per
-# multiply-accumulate: VALU instructions, and issue slots with a VOP3
-# instruction taking two.
-GEMM_VALU_PER_MAC = {"sequential": (11.125, 14.125), "kahan": (24.125, 33.125)}
+# the accumulator's significand), VALU instructions per multiply-accumulate,
+# counted in the kernel's ISA (256 multiply-accumulates per loop iteration;
+# the loop also issues 32 ds_read_b128, the operands from LDS).
+GEMM_LOOP_MIX = {
+    "sequential": {"v_and_b32": 2, "v_add_f32": 2, "v_mul_f32": 1, "v_sub_f32": 1, "v_and_or_b32": 1,
+                   "v_bfe_u32": 1, "v_add3_u32": 1, "v_cmp+v_cndmask": 2},
+    "kahan": {"v_and_b32": 5, "v_bfe_u32": 4, "v_add3_u32": 4, "v_sub_f32": 4, "v_add_f32": 2, "v_mul_f32": 1,
+              "v_and_or_b32": 1, "v_cmp+v_cndmask": 2},
+}
 GEMM_SHAPE = (4096, 1024, 4096)  # BERT-large FFN up-projection at 8 x 512 tokens: M, K, N
 
 
@@ -576,14 +589,17 @@ def lp_gemm_calls(A, dev, reps: int = 5):
             ts.append(e0.elapsed_time(e1))
         t = sorted(ts)[len(ts) // 2]
         macs = float(M) * N * K
-        instr, slots = GEMM_VALU_PER_MAC[name]
+        mix = GEMM_LOOP_MIX[name]
+        instr = float(sum(mix.values()))
         achieved = macs * instr / (t * 1e-3) / 1e12
-        ceiling = VALU_PEAK_T * 1e12 / slots  # MAC/s if every issue slot were used
+        # the mix's own ceiling: every CU issuing the loop's instructions at
+        # their measured rates, back to back
+        clk_per_lane_mac = sum(k / VALU_RATES[op] for op, k in mix.items())
+        ceiling = 256 * 2.4e9 / clk_per_lane_mac
         res[name] = {"ms": t, "MAC_per_s": macs / (t * 1e-3),
                      "roofline": {"bound": "alu", "achieved": achieved, "peak": VALU_PEAK_T,
                                   "unit": "T VALU lane-instructions/s", "frac": achieved / VALU_PEAK_T,
-                                  "valu_per_mac": instr, "issue_slots_per_mac": slots,
-                                  "mix_ceiling_MAC_per_s": ceiling,
+                                  "valu_per_mac": instr, "mix_ceiling_MAC_per_s": ceiling,
                                   "frac_of_mix_ceiling": macs / (t * 1e-3) / ceiling}}
     return res
 
