@@ -440,15 +440,6 @@ __device__ void repair_one(const ReduceArgs& a, const FmtK& f, int64_t j, int F)
     if (lane == 0) a.out[j] = __builtin_amdgcn_ldexpf(s, -F);
 }
 
-// Second pass over the listed chunks of one variant's format, one wave per
-// chunk: find the flagged elements (16 bytes per lane), then repair them one
-// after another (at most SPARSE_MAX), or rerun the whole chunk through the
-// streaming row walk, a quarter at a time.  Waves stride over the list; its
-// length is read on the device.  Without bytes (RM_CHUNKS, RM_QUARTERS) a
-// listed chunk's four quarters are four tasks, so few listed chunks still
-// spread over many waves; RM_QUARTERS skips a quarter whose wave minimum is
-// not below the largest threshold of the chunk's layers (no element of it
-// can be flagged).
 // One wave widens a chunk's pass-1 sums, kept as top halves, into out: four
 // steps of 4 elements per lane, so that each step's loads (8 bytes per lane)
 // and stores (16) are contiguous across the wave.  The half array is padded
@@ -470,6 +461,17 @@ __device__ __forceinline__ void widen_chunk(const SyncWs& ws, float* __restrict_
     }
 }
 
+// Second pass over the listed chunks of one variant's format, one wave per
+// chunk: find the flagged elements (16 bytes per lane), then repair them one
+// after another (at most SPARSE_MAX), or rerun the whole chunk through the
+// streaming row walk, a quarter at a time.  Waves stride over the list; its
+// length is read on the device.  Without bytes (RM_CHUNKS, RM_QUARTERS) a
+// listed chunk's four quarters are four tasks, so few listed chunks still
+// spread over many waves; RM_QUARTERS skips a quarter whose wave minimum is
+// not below the largest threshold of the chunk's layers (no element of it
+// can be flagged).
+// Halves are kept only on the one-pass route with bytes (RM_ELEMENTS), where
+// each listed chunk has one wave: it widens the chunk, then repairs it.
 template <int V>
 __global__ __launch_bounds__(BLOCK) void k_sync_repair(ReduceArgs a, Layers ly, Pal pal, SyncWs ws, int mode,
                                                       bool widen_rest) {
