@@ -94,9 +94,10 @@ enum {
 /*
  * Returns APS_OK if {e, m, bias} is a format the kernels implement, else
  * APS_ERR_FORMAT (outside e in [2,8], m in [0,23], emax <= 127,
- * emin - m >= -149) or APS_ERR_UNSUPPORTED (e = 8 with a bias other than
- * 127, or a format whose half-smallest-subnormal is below 2^-126).
- * Host-only; never touches the GPU.
+ * emin - m >= -149): every format whose values fp32 holds.  Formats with
+ * e = 8 and a bias other than 127, or whose half-smallest-subnormal lies
+ * below 2^-126, round in fp64 (slower) and are not taken by the one-pass
+ * route of aps_sync nor by aps_lp_gemm.  Host-only; never touches the GPU.
  */
 int aps_format_supported(aps_format f);
 
@@ -226,7 +227,8 @@ int aps_sync_route(int32_t W, int64_t n, const aps_format* fmts, int32_t n_fmts,
  * groups).  From 128 workers on, with every palette format m <= 7, pass 1
  * keeps each sum in 2 bytes of the workspace (its fp32 pattern's low 16 bits
  * are zero) and pass 2 widens them into out.  The route applies when W is a
- * power of two and every palette format has m <= 10.
+ * power of two and every palette format has m <= 10 and rounds in fp32
+ * (see aps_format_supported).
  *
  * The guessed-scale route applies to every W and format.  Pass 1 takes the
  * layer maxima of every 32nd worker (rows 0, 32, 64, ...), guesses each
@@ -388,8 +390,9 @@ int aps_dequantize(const float* Q, const void* codes, int64_t n,
  * rounded, which needs in_fmt.m <= 11, and either every product of two
  * in_fmt values a multiple of 2^-149 (2 * (emin_in - m_in) >= -149) or
  * every product too small for that rounding to zero in acc_fmt
- * (2 * (m_in + 1) <= emin_acc - m_acc + 149); other pairs return
- * APS_ERR_UNSUPPORTED.  M, N, K in [0, 2^22]; lda >= K, ldb >= N,
+ * (2 * (m_in + 1) <= emin_acc - m_acc + 149); other pairs, and formats
+ * rounded in fp64 (see aps_format_supported), return APS_ERR_UNSUPPORTED.
+ * M, N, K in [0, 2^22]; lda >= K, ldb >= N,
  * ldc >= N; A and B may be NULL when K = 0 or M * N = 0.
  */
 #define APS_MAX_GEMM_DIM (1 << 22)

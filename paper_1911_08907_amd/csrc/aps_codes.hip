@@ -205,6 +205,7 @@ __device__ float reduce_codes_any(const CodesArgs& a, const FmtK& f, int cc, int
         case V_TOP_M0: return reduce_codes_elem<V_TOP_M0>(a, f, cc, j);
         case V_LOW_F32: return reduce_codes_elem<V_LOW_F32>(a, f, cc, j);
         case V_LOW_F64: return reduce_codes_elem<V_LOW_F64>(a, f, cc, j);
+        case V_GEN: return reduce_codes_elem<V_GEN>(a, f, cc, j);
         default: return reduce_codes_elem<V_LOW_M0>(a, f, cc, j);
     }
 }

@@ -96,11 +96,27 @@ __device__ __forceinline__ int clamp_exp(int32_t ft) {
 
 template <int V>
 struct VT {
-    static constexpr int cls = V <= V_INT_M0 ? CLS_INT : (V <= V_TOP_M0 ? CLS_TOP : CLS_LOW);
+    static constexpr int cls = V == V_GEN ? CLS_GEN : (V <= V_INT_M0 ? CLS_INT : (V <= V_TOP_M0 ? CLS_TOP : CLS_LOW));
     static constexpr int acc = V == V_INT_EXACT ? ACC_EXACT
                                : ((V == V_INT_F64 || V == V_TOP_F64 || V == V_LOW_F64) ? ACC_F64 : ACC_F32);
     static constexpr bool m0 = (V == V_INT_M0 || V == V_TOP_M0 || V == V_LOW_M0);
 };
+
+// Class GEN: the format value of v (native, k = 0), rounded in fp64.  Above
+// 2^emin the fp64 pattern keeps m mantissa bits, ties to even (m = 0: up, the
+// even multiple); below, the magic constant puts v on the subnormal grid
+// 2^(emin - m) with fp64's own ties-to-even.  From 2^(emax + 1) up it is INF;
+// NaN stays NaN.  The result is a format value, so exact in fp32.
+__device__ __forceinline__ float round_gen(double v, const FmtK& f) {
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint64_t tie = f.m ? ((b >> f.sh64) & 1ull) : 0ull;
+    const double rn = __longlong_as_double((long long)((b + f.half64 + tie) & f.mask64));
+    const double a = __builtin_fabs(v);
+    const double rs = __builtin_copysign((a + f.c064) - f.c064, v);
+    double r = (a >= f.thr64) ? rn : rs;
+    r = (__builtin_fabs(r) >= f.ovf64) ? __builtin_copysign(__builtin_inf(), v) : r;
+    return (float)((v != v) ? v : r);
+}
 
 // Working-domain format value of y, a value already in the working domain
 // (fl32 of the scaled input).  Sets `bad` when y is NaN (m = 0 formats have
@@ -109,7 +125,9 @@ template <int V>
 __device__ __forceinline__ float quant_w(float y, const FmtK& f, bool& bad) {
     using T = VT<V>;
     if constexpr (T::m0) bad |= (y != y);
-    if constexpr (T::acc == ACC_EXACT) {
+    if constexpr (T::cls == CLS_GEN) {
+        return round_gen((double)y, f);
+    } else if constexpr (T::acc == ACC_EXACT) {
         return y;
     } else if constexpr (T::cls == CLS_INT) {
         const uint32_t b = f2u(y);
@@ -152,7 +170,7 @@ __device__ __forceinline__ float quant(float x, int F, const FmtK& f, bool& bad)
 // range rounds.  TOP and LOW classes, m >= 1.
 template <int V>
 __device__ __forceinline__ float quant_fit(float y, const FmtK& f) {
-    static_assert(VT<V>::cls != CLS_INT && !VT<V>::m0, "TOP or LOW class, m >= 1");
+    static_assert((VT<V>::cls == CLS_TOP || VT<V>::cls == CLS_LOW) && !VT<V>::m0, "TOP or LOW class, m >= 1");
     const uint32_t b = f2u(y);
     uint32_t ab = b & 0x7FFFFFFFu;
     asm volatile("" : "+v"(ab));  // keep |y| in a register: two-operand forms below, no abs modifiers
@@ -168,7 +186,12 @@ __device__ __forceinline__ float quant_fit(float y, const FmtK& f) {
 template <int V>
 __device__ __forceinline__ float accum(float s, float q, const FmtK& f, bool& bad) {
     using T = VT<V>;
-    if constexpr (T::acc == ACC_EXACT) {
+    if constexpr (T::cls == CLS_GEN) {
+        // the fp64 sum of two fp32 values, rounded to 53 then to m+1 <= 24
+        // bits, is the rounded exact sum (53 >= 2 * 24 + 2); below 2^emin the
+        // exact sum is a multiple of the subnormal step and exact in fp64
+        return round_gen((double)s + (double)q, f);
+    } else if constexpr (T::acc == ACC_EXACT) {
         return s + q;
     } else if constexpr (T::acc == ACC_F32) {
         const float t = s + q;
@@ -197,16 +220,19 @@ __device__ __forceinline__ float finish(float s, bool bad) {
 // ---------------------------------------------------------------- codes
 
 // code of a native-domain format value v.  Every case is computed and one is
-// selected, so the wave never splits on the value's class.
+// selected, so the wave never splits on the value's class.  Where 2^emin is
+// an fp32 subnormal (esh > 0) the normal case reads the pattern of v * 2^esh.
 __device__ __forceinline__ uint32_t encode(float v, const FmtK& f) {
     const uint32_t b = f2u(v);
     const uint32_t sign = (b >> 31) << (f.e + f.m);
     const uint32_t a = b & 0x7FFFFFFFu;
-    const uint32_t lo = (uint32_t)(f.emin + 127) << 23;  // bits of 2^emin
+    // bits of 2^emin (>= 2^-149: emin - m >= -149)
+    const uint32_t lo = f.emin >= -126 ? (uint32_t)(f.emin + 127) << 23 : 1u << (f.emin + 149);
     // below 2^emin: the subnormal code counts multiples of 2^(emin-m); the
     // clamp keeps the conversion's input finite when another case is taken
     const uint32_t c_sub = (uint32_t)__builtin_amdgcn_ldexpf(u2f(min(a, lo)), f.m - f.emin);
-    const uint32_t c_norm = (a >> (23 - f.m)) - ((uint32_t)(127 - f.bias) << f.m);
+    const uint32_t an = f2u(__builtin_amdgcn_ldexpf(u2f(a), f.esh));
+    const uint32_t c_norm = (an >> (23 - f.m)) - ((uint32_t)(127 + f.esh - f.bias) << f.m);
     const uint32_t c_nan = (uint32_t)f.emax_code | (f.m > 0 ? (1u << (f.m - 1)) : 0u);
     uint32_t c = a < lo ? c_sub : c_norm;
     c = a == 0x7F800000u ? (uint32_t)f.emax_code : c;
@@ -222,8 +248,9 @@ __device__ __forceinline__ float decode(uint32_t code, const FmtK& f) {
         a = mant ? __builtin_nanf("") : __builtin_inff();
     else if (ef == 0)
         a = __builtin_amdgcn_ldexpf((float)mant, f.emin - f.m);
-    else
-        a = u2f(((ef + 127u - (uint32_t)f.bias) << 23) | (mant << (23 - f.m)));
+    else  // built at 2^esh times the value (an fp32 normal), then scaled back exactly
+        a = __builtin_amdgcn_ldexpf(u2f(((ef + 127u + (uint32_t)f.esh - (uint32_t)f.bias) << 23) | (mant << (23 - f.m))),
+                                    -f.esh);
     return ((code >> (f.e + f.m)) & 1u) ? -a : a;
 }
 
@@ -685,6 +712,7 @@ __device__ inline float quant_any(float x, int F, const FmtK& f) {
         case V_TOP_M0: return quant_native<V_TOP_M0>(x, F, f);
         case V_LOW_F32: return quant_native<V_LOW_F32>(x, F, f);
         case V_LOW_F64: return quant_native<V_LOW_F64>(x, F, f);
+        case V_GEN: return quant_native<V_GEN>(x, F, f);
         default: return quant_native<V_LOW_M0>(x, F, f);
     }
 }
@@ -709,6 +737,7 @@ __device__ inline float reduce_elem_any(const ReduceArgs& a, const FmtK& f, int6
         case V_TOP_M0: return reduce_elem<V_TOP_M0>(a, f, j, F);
         case V_LOW_F32: return reduce_elem<V_LOW_F32>(a, f, j, F);
         case V_LOW_F64: return reduce_elem<V_LOW_F64>(a, f, j, F);
+        case V_GEN: return reduce_elem<V_GEN>(a, f, j, F);
         default: return reduce_elem<V_LOW_M0>(a, f, j, F);
     }
 }
@@ -797,4 +826,4 @@ static inline unsigned variant_mask(const Pal& pal, int32_t n_fmts) {
 }  // namespace aps
 
 // The kernels are templates over the variant; dispatch table per entry point.
-#define APS_FOR_VARIANTS(X) X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9)
+#define APS_FOR_VARIANTS(X) X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10)

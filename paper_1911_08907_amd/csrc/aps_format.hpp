@@ -9,9 +9,12 @@
 // format's overflow threshold coincides with fp32's.  Power-of-two scaling is
 // exact (Sec. 3.3.1), so rounding in the shifted domain and shifting back
 // gives the same result as rounding natively, as long as nothing below the
-// format's half-smallest-subnormal is decided by fp32's own underflow; the
-// host only accepts formats for which that holds (or e = 8, bias 127, where
-// k = 0).  In that domain:
+// format's half-smallest-subnormal is decided by fp32's own underflow: the
+// scaled input is an fp32 value, fl32(x * 2^ft), which fp32 itself has
+// already rounded once it lies below 2^-126.  For e = 8 with bias 127 the
+// shift is k = 0.  Formats for which that does not hold (e = 8 with another
+// bias, or a half-smallest-subnormal below 2^-126) take class GEN below.
+// In that domain:
 //   * a value with |y| >= 2^emin (format normal range) is rounded on its
 //     fp32 bit pattern: add half an ulp of the m-bit mantissa (plus the
 //     lowest kept bit, for ties to even) and clear the dropped bits.  A carry
@@ -23,7 +26,12 @@
 //     When c0 would not be an fp32 value (small e), the subtraction happens
 //     in a domain shifted down by j more bits (class LOW);
 //   * for e = 8 with bias 127 the format's subnormal grid is a coarsening of
-//     fp32's, so the bit-pattern rounding covers every magnitude (class INT).
+//     fp32's, so the bit-pattern rounding covers every magnitude (class INT);
+//   * class GEN keeps values native (k = 0; every format value is an fp32
+//     value) and rounds in fp64: the fp32 input fl32(x * 2^ft), or the sum of
+//     two format values, is rounded on its fp64 bit pattern in the normal
+//     range, onto the subnormal grid with the fp64 magic constant
+//     2^(emin - m + 52) below it, and to INF from 2^(emax + 1) up.
 // A sum of two format values whose magnitude is below 2^emin is a multiple
 // of the smallest subnormal and so exact, and for m <= 10 an fp32 add
 // followed by one rounding equals rounding the exact sum (24 >= 2(m+1) + 2,
@@ -32,11 +40,13 @@
 
 #include <stdint.h>
 
+#include <cmath>
+
 #include "aps.h"
 
 namespace aps {
 
-enum Cls : int32_t { CLS_INT = 0, CLS_TOP = 1, CLS_LOW = 2 };
+enum Cls : int32_t { CLS_INT = 0, CLS_TOP = 1, CLS_LOW = 2, CLS_GEN = 3 };
 enum Acc : int32_t { ACC_F32 = 0, ACC_F64 = 1, ACC_EXACT = 2 };
 
 // Kernel variants: one instantiation per (class, accumulator, m == 0).
@@ -51,7 +61,8 @@ enum Variant : int32_t {
     V_LOW_F32 = 7,
     V_LOW_F64 = 8,
     V_LOW_M0 = 9,
-    N_VARIANTS = 10
+    V_GEN = 10,
+    N_VARIANTS = 11
 };
 
 // Everything a kernel needs about one palette entry; built on the host.
@@ -67,9 +78,12 @@ struct FmtK {
     float thr;        // 2^emin in the working domain
     float c0;         // magic constant of the subnormal path (shifted by -j)
     uint32_t sh64;    // 52 - m  (fp64 accumulator)
-    uint32_t pad0;
-    uint64_t half64;  // 2^(sh64-1) - 1
+    int32_t esh;      // max(0, -126 - emin): codes scale by 2^esh so that 2^emin is an fp32 normal
+    uint64_t half64;  // 2^(sh64-1) - 1 (GEN with m = 0: 2^51, ties up)
     uint64_t mask64;  // clears the dropped fp64 bits
+    double thr64;     // GEN: 2^emin
+    double c064;      // GEN: 2^(emin - m + 52), the subnormal grid's magic constant
+    double ovf64;     // GEN: 2^(emax + 1), where a rounded value is INF
     int32_t code_bits;
     int32_t emax_code;  // all-ones exponent field << m
 };
@@ -81,9 +95,6 @@ inline int fmt_status(const aps_format& f) {
     const int emin = 1 - f.bias;
     const int emax = (1 << f.e) - 2 - f.bias;
     if (emax > 127 || emin > emax || emin - f.m < -149) return APS_ERR_FORMAT;
-    if (f.e == 8) return f.bias == 127 ? APS_OK : APS_ERR_UNSUPPORTED;
-    // below half the smallest subnormal fp32's own underflow must not matter
-    if (emin - f.m - 1 < -126) return APS_ERR_UNSUPPORTED;
     return APS_OK;
 }
 
@@ -104,7 +115,9 @@ inline FmtK make_fmtk(const aps_format& f) {
     o.emin = 1 - f.bias;
     o.emax = (1 << f.e) - 2 - f.bias;
     const bool is_int = (f.e == 8 && f.bias == 127);
-    o.k = is_int ? 0 : 127 - o.emax;
+    // the shifted domain would leave part of the subnormal grid to fp32's underflow
+    const bool is_gen = !is_int && (f.e == 8 || o.emin - f.m - 1 < -126);
+    o.k = (is_int || is_gen) ? 0 : 127 - o.emax;
     const int emin_w = o.emin + o.k;
     o.sh = 23u - (uint32_t)f.m;
     if (f.m == 0) {  // ties of a 1-bit significand go to the even multiple: up
@@ -124,6 +137,10 @@ inline FmtK make_fmtk(const aps_format& f) {
         cls = CLS_INT;
         o.j = 0;
         o.c0 = 0.f;
+    } else if (is_gen) {
+        cls = CLS_GEN;
+        o.j = 0;
+        o.c0 = 0.f;
     } else if (emin_w - f.m + 23 <= 127) {
         cls = CLS_TOP;
         o.j = 0;
@@ -141,9 +158,15 @@ inline FmtK make_fmtk(const aps_format& f) {
     else
         acc = ACC_F64;
     o.sh64 = 52u - (uint32_t)f.m;
-    o.half64 = (1ull << (o.sh64 - 1)) - 1ull;
+    o.esh = o.emin < -126 ? -126 - o.emin : 0;
+    o.half64 = (cls == CLS_GEN && f.m == 0) ? (1ull << 51) : (1ull << (o.sh64 - 1)) - 1ull;
     o.mask64 = ~((1ull << o.sh64) - 1ull);
-    if (cls == CLS_INT)
+    o.thr64 = std::ldexp(1.0, o.emin);
+    o.c064 = std::ldexp(1.0, o.emin - f.m + 52);
+    o.ovf64 = std::ldexp(1.0, o.emax + 1);
+    if (cls == CLS_GEN)
+        o.variant = V_GEN;
+    else if (cls == CLS_INT)
         o.variant = f.m == 0 ? V_INT_M0 : (acc == ACC_EXACT ? V_INT_EXACT : (acc == ACC_F64 ? V_INT_F64 : V_INT_F32));
     else if (cls == CLS_TOP)
         o.variant = f.m == 0 ? V_TOP_M0 : (acc == ACC_F64 ? V_TOP_F64 : V_TOP_F32);

@@ -147,8 +147,8 @@ using namespace aps;
 template <int V>
 static void launch_lp_gemm_v(bool kahan, int pm, dim3 grid, hipStream_t s, const GemmArgs& g, const FmtK& fi,
                              const FmtK& fa) {
-    constexpr bool can_fit = VT<V>::cls != CLS_INT && !VT<V>::m0;
-    constexpr bool can_ldexp = VT<V>::cls != CLS_INT;
+    constexpr bool can_fit = (VT<V>::cls == CLS_TOP || VT<V>::cls == CLS_LOW) && !VT<V>::m0;
+    constexpr bool can_ldexp = VT<V>::cls == CLS_TOP || VT<V>::cls == CLS_LOW;
 #define APS_G(K, P) hipLaunchKernelGGL((k_lp_gemm<V, K, P>), grid, dim3(BLOCK), 0, s, g, fi, fa)
     if (pm == GP_FIT) {
         if constexpr (can_fit) {
@@ -170,7 +170,7 @@ static void launch_lp_gemm(int variant, bool kahan, int pm, dim3 grid, hipStream
                            const FmtK& fi, const FmtK& fa) {
 #define APS_LG(v) \
     if (variant == (v)) launch_lp_gemm_v<v>(kahan, pm, grid, s, g, fi, fa);
-    APS_FOR_VARIANTS(APS_LG)
+    APS_LG(0) APS_LG(1) APS_LG(2) APS_LG(3) APS_LG(4) APS_LG(5) APS_LG(6) APS_LG(7) APS_LG(8) APS_LG(9)
 #undef APS_LG
 }
 
@@ -187,6 +187,8 @@ extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t 
     st = fmt_status(acc_fmt);
     if (st != APS_OK) return st;
     if (accumulator != APS_ACC_SEQUENTIAL && accumulator != APS_ACC_KAHAN) return APS_ERR_UNSUPPORTED;
+    // formats rounded in fp64 (class GEN) are not built into the GEMM
+    if (make_fmtk(in_fmt).variant == V_GEN || make_fmtk(acc_fmt).variant == V_GEN) return APS_ERR_UNSUPPORTED;
     // the product of two input values must be exact in fp32, or round to zero anyway
     const int emin_in = 1 - in_fmt.bias, emin_acc = 1 - acc_fmt.bias;
     if (in_fmt.m > 11) return APS_ERR_UNSUPPORTED;

@@ -214,6 +214,7 @@ __device__ float reduce_elem_ex_any(const ReduceArgs& a, const FmtK& f, int64_t 
         case V_TOP_M0: return reduce_elem_ex<V_TOP_M0, KAHAN>(a, f, j, F, seg, od);
         case V_LOW_F32: return reduce_elem_ex<V_LOW_F32, KAHAN>(a, f, j, F, seg, od);
         case V_LOW_F64: return reduce_elem_ex<V_LOW_F64, KAHAN>(a, f, j, F, seg, od);
+        case V_GEN: return reduce_elem_ex<V_GEN, KAHAN>(a, f, j, F, seg, od);
         default: return reduce_elem_ex<V_LOW_M0, KAHAN>(a, f, j, F, seg, od);
     }
 }

@@ -320,7 +320,7 @@ extern "C" int aps_quantize(const float* X, int32_t W, int64_t ld, int64_t n, co
         }                                                                                                  \
     }
     APS_LAUNCH_Q(V_INT_F64) APS_LAUNCH_Q(V_INT_EXACT) APS_LAUNCH_Q(V_INT_M0) APS_LAUNCH_Q(V_TOP_F64)
-    APS_LAUNCH_Q(V_TOP_M0) APS_LAUNCH_Q(V_LOW_F64) APS_LAUNCH_Q(V_LOW_M0)
+    APS_LAUNCH_Q(V_TOP_M0) APS_LAUNCH_Q(V_LOW_F64) APS_LAUNCH_Q(V_LOW_M0) APS_LAUNCH_Q(V_GEN)
 #undef APS_LAUNCH_Q
     if (fmt_idx && n_fmts > 1 && L > 1)
         hipLaunchKernelGGL(k_quantize_mixed, dim3((unsigned)L, (unsigned)std::min<int32_t>(W, MIXED_ROW_BLOCKS)),

@@ -733,7 +733,8 @@ extern "C" uint64_t aps_sync_workspace_bytes(int64_t n, int32_t L) {
 
 // Which route aps_sync takes.  The one-pass route applies when N = W is a
 // power of two (exact N * ghat, no overflow) and every format has m <= 10
-// (an fp32 add then one rounding equals rounding the exact sum).  Without a
+// (an fp32 add then one rounding equals rounding the exact sum) and rounds
+// in fp32 (not class GEN: its subnormal grid reaches below 2^-126).  Without a
 // route flag it is taken when it is also expected to pay: for layers of
 // normally distributed values (max about 5 sigma) the threshold sits at
 // W * 2^(emin - emax) of the layer's max, each input falls below it with
@@ -747,7 +748,7 @@ constexpr int64_t GUESS_MIN_WORK = (int64_t)1 << 26;
 static bool one_pass_applies(int32_t W, const Pal& pal, int32_t n_fmts) {
     if (W & (W - 1)) return false;
     for (int i = 0; i < n_fmts; ++i)
-        if (pal.f[i].m > 10) return false;
+        if (pal.f[i].m > 10 || pal.f[i].variant == V_GEN) return false;
     return true;
 }
 

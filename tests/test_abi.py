@@ -64,8 +64,8 @@ def test_strerror(lib):
     (A.Format(1, 2), A.APS_ERR_FORMAT), (A.Format(9, 2), A.APS_ERR_FORMAT),
     (A.Format(5, 24), A.APS_ERR_FORMAT), (A.Format(5, -1), A.APS_ERR_FORMAT),
     (A.Format(8, 7, 126), A.APS_ERR_FORMAT),      # emax 128
-    (A.Format(8, 7, 128), A.APS_ERR_UNSUPPORTED),  # e = 8 needs bias 127
-    (A.Format(7, 20, 127), A.APS_ERR_UNSUPPORTED),  # subnormals below 2^-126
+    (A.Format(8, 7, 128), A.APS_OK),               # e = 8, another bias: rounded in fp64
+    (A.Format(7, 20, 127), A.APS_OK),              # subnormals below 2^-126: rounded in fp64
     (A.Format(5, 2, 200), A.APS_ERR_FORMAT),       # smallest subnormal below 2^-149
 ])
 def test_format_supported(lib, f, ok):
@@ -141,8 +141,8 @@ def test_sim_reduce_validation(lib):
     assert f(GOOD, 2, 64, 64, GOOD, 1, None, pal, 1, None, 0, None, None, None) == A.APS_ERR_NULL
     assert f(GOOD, 2, 64, 64, GOOD, 1, None, pal, 1, None, 0, MIS, None, None) == A.APS_ERR_ALIGN
     assert f(GOOD, 2, 64, 64, GOOD, 1, None, pal, 1, None, 4, GOOD, None, None) == A.APS_ERR_UNSUPPORTED
-    assert f(GOOD, 2, 64, 64, GOOD, 1, None, _pal(A.Format(7, 20, 127)), 1, None, 0, GOOD, None,
-             None) == A.APS_ERR_UNSUPPORTED
+    assert f(GOOD, 2, 64, 64, GOOD, 1, None, _pal(A.Format(9, 2)), 1, None, 0, GOOD, None,
+             None) == A.APS_ERR_FORMAT
     assert f(None, 2, 64, 64, GOOD, 1, None, pal, 1, None, 0, GOOD, None, None) == A.APS_ERR_NULL
 
 
@@ -205,6 +205,9 @@ def test_lp_gemm_validation(lib):
     # bf16-range inputs with 12-bit significands: tiny products would need
     # fp32's subnormal rounding, which the fp32 accumulator format can see
     assert g(fin=A.Format(8, 11).c(), facc=F8) == A.APS_ERR_UNSUPPORTED
+    # formats rounded in fp64 are not built into the GEMM, as input or accumulator
+    assert g(fin=A.Format(5, 10, 120).c()) == A.APS_ERR_UNSUPPORTED
+    assert g(facc=A.Format(8, 7, 130).c()) == A.APS_ERR_UNSUPPORTED
     # empty output: nothing to do (and nothing checked beyond the sizes)
     assert g(M=0, a=None, b=None, c=None) == A.APS_OK
 
@@ -278,6 +281,9 @@ def test_sync_route_choice(lib):
     assert r(256, big, [F(5, 2)], guess) == GUESS
     assert r(3, 1, [F(5, 12)], guess) == GUESS
     assert r(12, big, [F(5, 2)], one) == TWO
+    # formats rounded in fp64 never take the one-pass route
+    assert r(8, big, [F(8, 7, 130)]) == GUESS
+    assert r(8, big, [F(5, 2), F(5, 10, 120)], one) == TWO
     assert r(8, big, [F(5, 12)], one) == TWO
     assert r(8, big, [F(5, 2), F(8, 23)], one) == TWO
     for bad in (one | two, one | guess, two | guess):

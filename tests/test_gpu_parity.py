@@ -167,6 +167,12 @@ def run_case(dev, G: np.ndarray, n: int, offs: np.ndarray, pal, fmt_idx=None, mo
 F = A.Format
 ALL_FORMATS = [F(5, 2), F(4, 3), F(3, 0), F(2, 0), F(2, 1), F(3, 2), F(5, 10), F(6, 9), F(8, 7), F(8, 23),
                F(8, 0), F(8, 15), F(5, 12), F(7, 23), F(4, 3, 5), F(5, 2, 20), F(6, 1), F(7, 5), F(2, 23)]
+# formats rounded in fp64: e = 8 with a bias other than 127, or a subnormal
+# grid that reaches below 2^-126 (the scaled input is fl32, rounded by fp32's
+# own underflow there)
+GEN_FORMATS = [F(8, 7, 130), F(8, 0, 140), F(8, 20, 128), F(7, 20, 127), F(5, 10, 120), F(4, 3, 140),
+               F(3, 0, 145), F(2, 1, 147)]
+ALL_FORMATS += GEN_FORMATS
 
 SIZES = [0, 1, 3, 5, 7, 1023, 1024, 1025, 2049, 0, 64, 13, 4095, 2, 3000]
 
@@ -291,7 +297,8 @@ def test_empty_gradient(dev):
 
 # ------------------------------------------------ exhaustive small formats
 
-SMALL = [F(5, 2), F(4, 3), F(3, 0), F(2, 0), F(2, 1), F(3, 2), F(6, 1), F(3, 4), F(4, 3, 5)]
+SMALL = [F(5, 2), F(4, 3), F(3, 0), F(2, 0), F(2, 1), F(3, 2), F(6, 1), F(3, 4), F(4, 3, 5),
+         F(4, 3, 140), F(3, 0, 145), F(2, 1, 147), F(5, 2, 140), F(8, 1, 140)]
 
 
 @pytest.mark.parametrize("f", SMALL, ids=str)
@@ -311,7 +318,8 @@ def test_every_code_and_midpoint(dev, f):
     run_case(dev, G, n, offs, [f], mode="raw", tag=f"{f} all codes/midpoints")
 
 
-@pytest.mark.parametrize("f", [F(5, 2), F(4, 3), F(3, 0), F(2, 1), F(3, 2)], ids=str)
+@pytest.mark.parametrize("f", [F(5, 2), F(4, 3), F(3, 0), F(2, 1), F(3, 2), F(4, 3, 140), F(3, 0, 145),
+                               F(5, 2, 140)], ids=str)
 def test_every_code_pair_sum(dev, f):
     vals = [float(v) for v in X.values(f.e, f.m, f.b)]
     vals = np.array(vals + [-v for v in vals[1:]] + [np.inf, -np.inf], np.float32)
@@ -439,7 +447,8 @@ def test_run_to_run_determinism(dev):
     assert torch.equal(a.view(torch.int32), b.view(torch.int32))
 
 
-@pytest.mark.parametrize("f", [F(5, 2), F(4, 3), F(3, 0), F(2, 1), F(5, 10), F(8, 7), F(3, 4), F(4, 3, 5)], ids=str)
+@pytest.mark.parametrize("f", [F(5, 2), F(4, 3), F(3, 0), F(2, 1), F(5, 10), F(8, 7), F(3, 4), F(4, 3, 5),
+                               F(4, 3, 140), F(3, 2, 140), F(5, 10, 120), F(3, 0, 145)], ids=str)
 def test_sim_reduce_codes_random_codes(dev, f):
     """Every code value (INF and NaN codes included) as input to the codes reduce."""
     rng = np.random.default_rng(40 + f.e * 3 + f.m)
@@ -486,7 +495,8 @@ def _run_ex(dev, G, n, offs, pal, fmt_idx, se, k, acc, tag):
 
 
 @pytest.mark.parametrize("acc", [A.APS_ACC_SEQUENTIAL, A.APS_ACC_KAHAN])
-@pytest.mark.parametrize("f", [F(5, 2), F(4, 3), F(3, 0), F(5, 10), F(8, 7), F(5, 12), F(8, 23)], ids=str)
+@pytest.mark.parametrize("f", [F(5, 2), F(4, 3), F(3, 0), F(5, 10), F(8, 7), F(5, 12), F(8, 23), F(8, 7, 130),
+                               F(5, 10, 120), F(3, 0, 145)], ids=str)
 def test_ordered_reduce_edge_layouts(dev, f, acc):
     rng = np.random.default_rng(60 + f.e * 5 + f.m + 100 * acc)
     offs, n, ld = _layout(SIZES)
