@@ -106,6 +106,9 @@ def _probe_lib():
                        "probe_flat": [i32, P, i32, i64, i64, P, i32, P],
                        "probe_rowmajor": [i32, i32, P, i32, i64, i64, P, i32, P],
                        "probe_copy": [P, P, i64, i32, P],
+                       "probe_rows_wide": [i32, i32, i32, P, i32, i64, i64, P, P, i32, P],
+                       "probe_read_flat": [P, i64, P, i32, P],
+                       "probe_copy_ranges": [P, P, i64, i32, P],
                        "probe_widen": [i32, i32, P, P, i64, i32, P],
                        "probe_valu": [i32, P, i32, i32, P]}.items():
         fn = getattr(L, name)
@@ -164,11 +167,12 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
                                  "frac_of_8TBps": nbytes / (t * 1e-3) / 1e12 / 8.0, **info}
         print(f"# {name}: {t:.4f} ms, {nbytes / (t * 1e-3) / 1e12:.2f} TB/s", file=sys.stderr, flush=True)
 
-    def rows(tag, W, n_full, modes, widths):
+    def rows(tag, W, n_full, modes, widths, wide=()):
         n = n_full // 1024 * 1024
         ld = (n_full + 255) // 256 * 256  # rows padded as the workloads pad them
         writes_rows = any(m in ("row_bytes", "row_f32") for m in modes)
         names = [f"rows_{m}_{tag}_{b}percu" for m in modes for b in widths]
+        names += [f"rows_wide{x}r{r}_{m}_{tag}_{b}percu" for x, r, m in wide for b in widths]
         if writes_rows:
             names += [f"{k}_{o}_{tag}" for k in ("flat", "rowmajor") for o in ("bytes", "f32")]
             names += [f"rowmajor_{o}_{g}inflight_{tag}" for o in ("bytes", "f32") for g in (1, 4, 8)]
@@ -194,6 +198,15 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
                       4.0 * W * n + extra * n, W=W, n=n, blocks_per_cu=bpc)
             del dst_o, dst_b
             torch.cuda.empty_cache()
+        # the same walk with chx chunks side by side per block step (each row read in runs of chx * 4 KB)
+        for chx, r, m in wide:
+            nw = n_full // (chx * 1024) * (chx * 1024)
+            extra = {"read": 0, "sum_half": 2, "sum_f32": 4}[m]
+            for bpc in widths:
+                timed(f"rows_wide{chx}r{r}_{m}_{tag}_{bpc}percu",
+                      lambda: L.probe_rows_wide(chx, r, {"read": 0, "sum_half": 1, "sum_f32": 2}[m], ptr(G), W, ld,
+                                                nw, ptr(out), ptr(half), bpc, stream()),
+                      4.0 * W * nw + extra * nw, W=W, n=nw, chunks_per_step=chx, rows_per_set=r, blocks_per_cu=bpc)
         if writes_rows:
             for outb in (1, 4):
                 kind = "bytes" if outb == 1 else "f32"
@@ -215,17 +228,32 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
         torch.cuda.empty_cache()
 
     n50, n_bert = 25557032, 335141888
-    rows("resnet50_w256", 256, n50, ["read", "sum_f32", "sum_half", "sum_bytes", "row_bytes", "row_f32"], (16, 24))
-    rows("resnet50_w8", 8, n50, ["read", "sum_f32", "sum_bytes", "row_bytes"], (32, 64))
+    rows("resnet50_w256", 256, n50, ["read", "sum_f32", "sum_half", "sum_bytes", "row_bytes", "row_f32"], (16, 24),
+         wide=[(2, 2, "read"), (4, 2, "read"), (2, 2, "sum_half"), (4, 2, "sum_half")])
+    rows("resnet50_w8", 8, n50, ["read", "sum_f32", "sum_bytes", "row_bytes"], (32, 64),
+         wide=[(2, 4, "sum_f32"), (4, 2, "sum_f32")])
     bert_wide = min(512, (n_bert // 1024) * 2 // (cus * 5))
-    rows("bert_large", 8, n_bert, ["read", "sum_f32", "sum_bytes"], (32, bert_wide))
-    if group("copy_2GiB"):
+    rows("bert_large", 8, n_bert, ["read", "sum_f32", "sum_bytes"], (32, bert_wide),
+         wide=[(2, 4, "sum_f32"), (4, 2, "sum_f32")])
+    if group("read_flat_8GiB"):
+        n = 1 << 31  # 8 GiB
+        a = torch.zeros(n, dtype=torch.float32, device=dev)
+        sink = torch.empty(256, dtype=torch.float32, device=dev)
+        for bpc in (8, 16, 32):
+            timed(f"read_flat_8GiB_{bpc}percu", lambda: L.probe_read_flat(ptr(a), n, ptr(sink), bpc, stream()),
+                  4.0 * n, n=n, blocks_per_cu=bpc)
+        del a, sink
+        torch.cuda.empty_cache()
+    if group("copy_2GiB") or group("copy_ranges_2GiB"):
         n = 1 << 29  # 2 GiB
         a = torch.zeros(n, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)
         for bpc in (8, 32):
             timed(f"copy_2GiB_{bpc}percu", lambda: L.probe_copy(ptr(a), ptr(b), n, bpc, stream()), 8.0 * n,
                   n=n, blocks_per_cu=bpc)
+        for bpc in (8, 16, 32):
+            timed(f"copy_ranges_2GiB_{bpc}percu", lambda: L.probe_copy_ranges(ptr(a), ptr(b), n, bpc, stream()),
+                  8.0 * n, n=n, blocks_per_cu=bpc)
         del a, b
         torch.cuda.empty_cache()
     if group("widen_"):

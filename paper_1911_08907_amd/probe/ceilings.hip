@@ -25,7 +25,17 @@
 //                writes their 16 bytes (or 64 bytes) at once;
 //   probe_rowmajor  the same bytes again, each block walking its chunk range
 //                row after row (each row read and written in long runs);
-//   probe_copy   a 1:1 fp32 copy;
+//   probe_rows_wide  the row walk with each block step covering CHX
+//                chunks side by side (each thread CHX 16-byte slices of
+//                a row, R rows per register set, two sets in flight), so
+//                every row is read in runs of CHX * 4 KB;
+//   probe_read_flat  a flat read of one contiguous buffer (each block a
+//                contiguous range of 16 KB tiles, four 16-byte loads per
+//                thread in flight): what HBM gives a pure read stream;
+//   probe_copy   a 1:1 fp32 copy, grid-stride (one 16-byte load per thread
+//                per step);
+//   probe_copy_ranges  the same copy with each block a contiguous range of
+//                16 KB tiles, four 16-byte loads per thread in flight;
 //   probe_widen  read n codes of `in_bytes` bytes, write n fp32 values
 //                (aps_dequantize's traffic), `per` elements per thread;
 //   probe_valu   16 independent chains per thread of one VALU instruction.
@@ -158,6 +168,106 @@ __global__ __launch_bounds__(BLOCK) void k_copy(const f4* __restrict__ src, f4* 
     const int64_t stride = (int64_t)gridDim.x * BLOCK;
     for (int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x; i < n4; i += stride)
         __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
+}
+
+// The row walk with CHX chunks per block step: thread t owns the 16-byte
+// slice at element 4t of each of the CHX chunks; R rows per register set,
+// two sets in flight (W a multiple of 2R).  OUT_NONE keeps an OR of the
+// bits, OUT_HALF writes one row of 2-byte halves, OUT_F32 one fp32 row.
+enum WideOut { OUT_NONE = 0, OUT_HALF = 1, OUT_F32 = 2 };
+
+template <int CHX, int R, int OUT>
+__global__ __launch_bounds__(BLOCK) void k_rows_wide(RowArgs a) {
+    constexpr int64_t C = CHX * CH;
+    int64_t gb, ge;
+    block_range(a.n / C, gb, ge);
+    u4v keep = {0u, 0u, 0u, 0u};
+    const int K = a.W / (2 * R);  // pairs of register sets
+    for (int64_t g = gb; g < ge; ++g) {
+        const int64_t j = g * C + (int64_t)threadIdx.x * VEC;
+        const float* p = a.G + j;
+        const int64_t ld = a.ld;
+        u4v acc[CHX];
+        f4 A[R][CHX], B[R][CHX];
+#pragma unroll
+        for (int u = 0; u < CHX; ++u) acc[u] = (u4v){0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int u = 0; u < CHX; ++u) A[r][u] = ld4(p + (int64_t)r * ld + u * CH);
+        for (int k = 0; k + 1 < K; ++k) {
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int u = 0; u < CHX; ++u) B[r][u] = ld4(p + (int64_t)(2 * k * R + R + r) * ld + u * CH);
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int u = 0; u < CHX; ++u) acc[u] |= __builtin_bit_cast(u4v, A[r][u]);
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int u = 0; u < CHX; ++u) A[r][u] = ld4(p + (int64_t)(2 * k * R + 2 * R + r) * ld + u * CH);
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int u = 0; u < CHX; ++u) acc[u] |= __builtin_bit_cast(u4v, B[r][u]);
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int u = 0; u < CHX; ++u) B[r][u] = ld4(p + (int64_t)(a.W - R + r) * ld + u * CH);
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int u = 0; u < CHX; ++u) acc[u] |= __builtin_bit_cast(u4v, A[r][u]) | __builtin_bit_cast(u4v, B[r][u]);
+#pragma unroll
+        for (int u = 0; u < CHX; ++u) {
+            const int64_t jj = j + u * CH;
+            const u4v o = acc[u];
+            if constexpr (OUT == OUT_NONE) keep |= o;
+            if constexpr (OUT == OUT_F32)
+                __builtin_nontemporal_store(__builtin_bit_cast(f4, o), (f4*)(a.out + jj));
+            if constexpr (OUT == OUT_HALF) {
+                const u2v h = {(o.x >> 16) | (o.y & 0xFFFF0000u), (o.z >> 16) | (o.w & 0xFFFF0000u)};
+                __builtin_nontemporal_store(h, (u2v*)(a.half + jj));
+            }
+        }
+    }
+    if constexpr (OUT == OUT_NONE)
+        if ((keep.x | keep.y | keep.z | keep.w) == a.magic) a.out[threadIdx.x] = 1.0f;
+}
+
+// A flat read of n4 16-byte items: each block a contiguous range of tiles of
+// 4 * BLOCK items, four loads per thread in flight.
+__global__ __launch_bounds__(BLOCK) void k_read_flat(const f4* __restrict__ src, int64_t n4, float* __restrict__ sink,
+                                                    uint32_t magic) {
+    int64_t tb, te;
+    block_range(n4 / (4 * BLOCK), tb, te);
+    u4v acc = {0u, 0u, 0u, 0u};
+    for (int64_t t = tb; t < te; ++t) {
+        const f4* p = src + t * 4 * BLOCK + threadIdx.x;
+        f4 x[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) x[u] = __builtin_nontemporal_load(p + u * BLOCK);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc |= __builtin_bit_cast(u4v, x[u]);
+    }
+    if ((acc.x | acc.y | acc.z | acc.w) == magic) sink[threadIdx.x] = 1.0f;
+}
+
+// The copy in the same order: tiles of 4 * BLOCK items per block step.
+__global__ __launch_bounds__(BLOCK) void k_copy_ranges(const f4* __restrict__ src, f4* __restrict__ dst, int64_t n4) {
+    int64_t tb, te;
+    block_range(n4 / (4 * BLOCK), tb, te);
+    for (int64_t t = tb; t < te; ++t) {
+        const int64_t i = t * 4 * BLOCK + threadIdx.x;
+        f4 x[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) x[u] = __builtin_nontemporal_load(src + i + u * BLOCK);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) __builtin_nontemporal_store(x[u], dst + i + u * BLOCK);
+    }
 }
 
 // n codes of IN bytes each in, n fp32 out; PER elements per thread per step.
@@ -306,6 +416,46 @@ extern "C" int probe_copy(const float* src, float* dst, int64_t n, int blocks_pe
     if (!src || !dst || n < 4 || (n & 3) || blocks_per_cu < 1) return -2;
     const int64_t n4 = n / 4;
     hipLaunchKernelGGL(k_copy, dim3((unsigned)grid_for((n4 + BLOCK - 1) / BLOCK, blocks_per_cu)), dim3(BLOCK), 0,
+                       (hipStream_t)stream, (const f4*)src, (f4*)dst, n4);
+    return probe_done();
+}
+
+// The wide row walk: chx chunks per block step (2 or 4), r rows per register
+// set (2 or 4), out 0 (read only), 1 (2-byte halves) or 2 (fp32 row); W a
+// multiple of 2r; whole steps of chx chunks are walked.
+extern "C" int probe_rows_wide(int chx, int r, int out_mode, const float* G, int32_t W, int64_t ld, int64_t n,
+                               float* out, void* half, int blocks_per_cu, void* stream) {
+    if (!G || !out || W < 1 || (W % (2 * r)) || n < chx * CH || ld < n || (ld & 3) || blocks_per_cu < 1) return -2;
+    if (out_mode == OUT_HALF && !half) return -2;
+    RowArgs a{G, out, nullptr, (uint16_t*)half, ld, n, W, 0x5A5A5A5Au};
+    const dim3 grid((unsigned)grid_for(n / (chx * CH), blocks_per_cu));
+    hipStream_t s = (hipStream_t)stream;
+#define PROBE_RW(X, RR, O)                                                                  \
+    if (chx == X && r == RR && out_mode == O) {                                             \
+        hipLaunchKernelGGL((k_rows_wide<X, RR, O>), grid, dim3(BLOCK), 0, s, a);            \
+        return probe_done();                                                                \
+    }
+    PROBE_RW(2, 2, OUT_NONE) PROBE_RW(2, 2, OUT_HALF) PROBE_RW(2, 2, OUT_F32)
+    PROBE_RW(2, 4, OUT_NONE) PROBE_RW(2, 4, OUT_HALF) PROBE_RW(2, 4, OUT_F32)
+    PROBE_RW(4, 2, OUT_NONE) PROBE_RW(4, 2, OUT_HALF) PROBE_RW(4, 2, OUT_F32)
+#undef PROBE_RW
+    return -5;
+}
+
+// A flat read of n floats (n a multiple of 4 * 4 * BLOCK); sink needs BLOCK floats.
+extern "C" int probe_read_flat(const float* src, int64_t n, float* sink, int blocks_per_cu, void* stream) {
+    if (!src || !sink || n < 16 * BLOCK || (n % (16 * BLOCK)) || blocks_per_cu < 1) return -2;
+    const int64_t n4 = n / 4;
+    hipLaunchKernelGGL(k_read_flat, dim3((unsigned)grid_for(n4 / (4 * BLOCK), blocks_per_cu)), dim3(BLOCK), 0,
+                       (hipStream_t)stream, (const f4*)src, n4, sink, 0x5A5A5A5Au);
+    return probe_done();
+}
+
+// The copy of n floats in block ranges (n a multiple of 4 * 4 * BLOCK).
+extern "C" int probe_copy_ranges(const float* src, float* dst, int64_t n, int blocks_per_cu, void* stream) {
+    if (!src || !dst || n < 16 * BLOCK || (n % (16 * BLOCK)) || blocks_per_cu < 1) return -2;
+    const int64_t n4 = n / 4;
+    hipLaunchKernelGGL(k_copy_ranges, dim3((unsigned)grid_for(n4 / (4 * BLOCK), blocks_per_cu)), dim3(BLOCK), 0,
                        (hipStream_t)stream, (const f4*)src, (f4*)dst, n4);
     return probe_done();
 }
