@@ -188,19 +188,24 @@ constexpr int DEQ_GROUP = 4;
 
 // Codes of up to 8 bits decode through a table in LDS, one per palette
 // entry (value of every code), filled once per block; 16-bit codes decode
-// arithmetically.
+// arithmetically.  A block walks its chunks in groups of DEQ_GROUP: the loads
+// of the next group are issued before the current one is decoded and
+// stored, and the first group's before the table is filled, so each wave
+// has a group's loads in flight while it works.
 template <int IN>
 __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal pal) {
     constexpr bool TABLE = IN == 1 || IN == 2;
     constexpr int NCODES = IN == 1 ? 16 : 256;
     __shared__ FmtK spal[APS_MAX_FORMATS];
     __shared__ float lut[TABLE ? APS_MAX_FORMATS : 1][TABLE ? NCODES : 1];
-    pal_to_lds(pal, spal);
-    if constexpr (TABLE) {
-        for (int t = threadIdx.x; t < ly.n_fmts * NCODES; t += BLOCK)
-            lut[t / NCODES][t % NCODES] = decode((uint32_t)(t % NCODES), spal[t / NCODES]);
-        __syncthreads();
-    }
+    auto setup = [&]() {
+        pal_to_lds(pal, spal);
+        if constexpr (TABLE) {
+            for (int t = threadIdx.x; t < ly.n_fmts * NCODES; t += BLOCK)
+                lut[t / NCODES][t % NCODES] = decode((uint32_t)(t % NCODES), spal[t / NCODES]);
+            __syncthreads();
+        }
+    };
     auto dec = [&](uint32_t code, int p, const FmtK& f) -> float {
         if constexpr (TABLE) return lut[p][code];
         else return decode(code, f);
@@ -208,7 +213,6 @@ __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal 
     const int64_t nchunks = (ly.n + CH - 1) / CH;
     int64_t cb, ce;
     block_range(nchunks, cb, ce);
-    int hint = 0;
     // the group's loads are unconditional (a branch around each would make
     // the compiler wait for it before the next): past the block's last chunk
     // a thread loads that chunk again, past the gradient's end its last whole
@@ -221,13 +225,17 @@ __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal 
         a.out[jj] = __builtin_amdgcn_ldexpf(v, -ft);
     };
     if (jlast < 0) {  // fewer than 4 elements: no whole group to load
+        setup();
         if (blockIdx.x == 0 && threadIdx.x < ly.n) one(threadIdx.x, find_layer(ly.offsets, ly.L, threadIdx.x, 0));
         return;
     }
-    for (int64_t c0 = cb; c0 < ce; c0 += DEQ_GROUP) {
-        // the chunks' layers first (scalar loads, wave-uniform), then the
-        // group's data loads, all in flight together
-        ChunkInfo cis[DEQ_GROUP];
+    if (cb >= ce) return;  // uniform per block
+    int hint = 0;
+    ChunkInfo cis[DEQ_GROUP];
+    DeqRaw raw[DEQ_GROUP];
+    // the chunks' layers first (scalar loads, wave-uniform), then the group's
+    // data loads, all in flight together
+    auto issue = [&](int64_t c0) {
         // usually the whole group lies in one layer: one lookup for all of it
         const int64_t gend = min(min(c0 + DEQ_GROUP, ce) * CH, ly.n);
         const ChunkInfo gi = chunk_layers(ly, c0 * CH, gend, hint);
@@ -243,19 +251,20 @@ __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal 
                 hint = __builtin_amdgcn_readfirstlane(cis[g].i0);
             }
         }
-        DeqRaw raw[DEQ_GROUP];
 #pragma unroll
         for (int g = 0; g < DEQ_GROUP; ++g) {
             const int64_t j = min(c0 + g, ce - 1) * CH + (int64_t)threadIdx.x * VEC;
             raw[g] = deq_load<IN>(a, min(j, jlast));
         }
+    };
+    auto process = [&](int64_t c0, const ChunkInfo* gci, const DeqRaw* graw) {
 #pragma unroll
         for (int g = 0; g < DEQ_GROUP; ++g) {
             const int64_t c = c0 + g;
             if (c >= ce) break;
             const int64_t start = c * CH;
             const int64_t end = min(start + CH, ly.n);
-            const ChunkInfo& ci = cis[g];
+            const ChunkInfo& ci = gci[g];
             const int64_t j = start + (int64_t)threadIdx.x * VEC;
             if (j >= end) continue;
             if (ci.i0 == ci.i1 && j + 4 <= end) {
@@ -264,7 +273,7 @@ __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal 
                 const int32_t ft = ly.scale_exp ? clamp_exp(cld(ly.scale_exp, ci.i0)) : 0;
                 float v[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] = IN == 0 ? u2f(raw[g].w[e]) : dec(raw[g].w[e], ci.pidx, f);
+                for (int e = 0; e < 4; ++e) v[e] = IN == 0 ? u2f(graw[g].w[e]) : dec(graw[g].w[e], ci.pidx, f);
                 const f4 o = {__builtin_amdgcn_ldexpf(v[0], -ft), __builtin_amdgcn_ldexpf(v[1], -ft),
                               __builtin_amdgcn_ldexpf(v[2], -ft), __builtin_amdgcn_ldexpf(v[3], -ft)};
                 __builtin_nontemporal_store(o, (f4*)(a.out + j));  // out may alias Q: same elements
@@ -279,7 +288,22 @@ __global__ __launch_bounds__(BLOCK) void k_dequantize(DeqArgs a, Layers ly, Pal 
                 one(jj, li);
             }
         }
+    };
+    issue(cb);
+    setup();
+    const int64_t ngroups = (ce - cb + DEQ_GROUP - 1) / DEQ_GROUP;
+    for (int64_t k = 0; k + 1 < ngroups; ++k) {
+        ChunkInfo cur_ci[DEQ_GROUP];
+        DeqRaw cur[DEQ_GROUP];
+#pragma unroll
+        for (int g = 0; g < DEQ_GROUP; ++g) {
+            cur_ci[g] = cis[g];
+            cur[g] = raw[g];
+        }
+        issue(cb + (k + 1) * DEQ_GROUP);
+        process(cb + k * DEQ_GROUP, cur_ci, cur);
     }
+    process(cb + (ngroups - 1) * DEQ_GROUP, cis, raw);
 }
 
 }  // namespace aps
@@ -343,8 +367,10 @@ extern "C" int aps_dequantize(const float* Q, const void* codes, int64_t n, cons
     Layers ly{offsets, fmt_idx, scale_exp, n, L, n_fmts};
     DeqArgs a{Q, (const uint8_t*)codes, out, ccls};
     const int64_t nchunks = (n + CH - 1) / CH;
-    // measured on MI355X (ResNet-50's 25.6 M byte codes): 16 blocks per CU
-    // with 4 chunks in flight beat 8 with 8, 32 with 1 or 2, and 4 with 16
+    // measured on MI355X (ResNet-50's 25.6 M byte codes, the next group's
+    // loads issued before the current group is stored): 16 blocks per CU with
+    // 4 chunks per group (30.7 us) beat 8 with 4 or 8, 16 with 2, 32 with 2
+    // and 4 with 8 (31.6 to 35.5 us)
     const dim3 grid((unsigned)grid_for(nchunks, 16));
     hipStream_t s = (hipStream_t)stream;
     const int in = Q ? 0 : 1 + ccls;

@@ -283,6 +283,23 @@ def test_quantize_mixed_palette_many_workers(dev):
         log(f"quantize W={W} mixed palette {mode}: values and codes match")
 
 
+@pytest.mark.parametrize("n_total", [1, 2, 3, 4, 5, 7, 9])
+def test_tiny_gradients(dev, n_total):
+    """Gradients of a few elements, fewer than one thread's 4 or just past
+    them: every call, in one layer and in two, in APS and RAW mode."""
+    seed = zlib.crc32(f"tiny/{n_total}".encode())
+    rng = np.random.default_rng(seed)
+    for sizes in ([n_total], [n_total // 2, n_total - n_total // 2]):
+        offs, n, ld = _layout(sizes)
+        for f in (F(5, 2), F(3, 0), F(5, 10)):
+            for W in (1, 3):
+                G = _values(rng, W, ld, offs, "normal")
+                tag = f"{f} sizes={sizes} W={W} seed={seed}"
+                log("case", tag)
+                run_case(dev, G, n, offs, [f], mode="aps", tag=tag + " aps")
+                run_case(dev, G, n, offs, [f], mode="raw", tag=tag + " raw")
+
+
 def test_empty_gradient(dev):
     offs = np.zeros(4, np.int64)
     G = np.zeros((3, 4), np.float32)
