@@ -163,6 +163,30 @@ def test_sync_mixed_palette(dev, seed):
             sync_case(dev, G, n, offs, pal, fmt_idx=fmt_idx, tag=tag + " guessed scales", route=A.APS_SYNC_GUESS)
 
 
+def test_many_tiny_layers(dev):
+    """70,000 layers of 0 to 5 elements: every chunk spans hundreds of layers,
+    and the grids over the layers pass 65,535 blocks.  The five calls and
+    aps_sync on every route, one format and a two-format palette."""
+    from tests.test_gpu_parity import run_case
+
+    seed = zlib.crc32(b"many-tiny-layers")
+    rng = np.random.default_rng(seed)
+    sizes = [int(v) for v in rng.integers(0, 6, 70000)]
+    offs, n, ld = _layout(sizes)
+    fmt_idx = rng.integers(0, 2, len(sizes)).astype(np.uint8)
+    for W in (4, 64, 128):
+        G = _values(rng, W, ld, offs, "normal")
+        tag = f"L={len(sizes)} n={n} W={W} seed={seed}"
+        log("case", tag)
+        if W == 4:
+            run_case(dev, G, n, offs, [F(5, 2)], mode="aps", tag=tag + " calls")
+            run_case(dev, G, n, offs, [F(5, 2), F(4, 3)], fmt_idx=fmt_idx, mode="aps", tag=tag + " calls mixed")
+        for route, name in ((A.APS_SYNC_ONE_PASS, "one pass"), (A.APS_SYNC_GUESS, "guessed scales"),
+                            (A.APS_SYNC_TWO_PASS, "two passes")):
+            sync_case(dev, G, n, offs, [F(5, 2)], tag=f"{tag} {name}", route=route)
+            sync_case(dev, G, n, offs, [F(5, 2), F(4, 3)], fmt_idx=fmt_idx, tag=f"{tag} {name} mixed", route=route)
+
+
 def test_sync_empty_gradient(dev):
     offs = np.zeros(4, np.int64)
     G = np.zeros((4, 4), np.float32)
