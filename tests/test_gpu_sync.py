@@ -187,6 +187,31 @@ def test_many_tiny_layers(dev):
             sync_case(dev, G, n, offs, [F(5, 2), F(4, 3)], fmt_idx=fmt_idx, tag=f"{tag} {name} mixed", route=route)
 
 
+def test_eight_format_palette(dev):
+    """A palette of the maximum 8 formats (4-, 8- and 16-bit codes, one GEN
+    format), layers assigned at random: the five calls and aps_sync on every
+    route; and the 8 byte-code formats alone, codes included."""
+    from tests.test_gpu_parity import run_case
+
+    seed = zlib.crc32(b"eight-formats")
+    rng = np.random.default_rng(seed)
+    mixed = [F(5, 2), F(4, 3), F(3, 0), F(2, 1), F(6, 1), F(5, 10), F(8, 7), F(5, 10, 120)]
+    bytes8 = [F(5, 2), F(4, 3), F(6, 1), F(3, 4), F(2, 5), F(4, 3, 5), F(5, 2, 20), F(7, 0)]
+    assert len(mixed) == len(bytes8) == A.APS_MAX_FORMATS
+    sizes = [int(v) for v in rng.choice([0, 1, 3, 17, 255, 1000, 1024, 1500, 4096], 60)]
+    offs, n, ld = _layout(sizes)
+    for pal, name in ((mixed, "mixed classes"), (bytes8, "byte codes")):
+        fmt_idx = rng.integers(0, len(pal), len(sizes)).astype(np.uint8)
+        for W in (3, 8, 128):
+            G = _values(rng, W, ld, offs, "normal")
+            tag = f"8 formats ({name}) W={W} seed={seed}"
+            log("case", tag)
+            run_case(dev, G, n, offs, pal, fmt_idx=fmt_idx, mode="aps", tag=tag + " calls")
+            run_case(dev, G, n, offs, pal, fmt_idx=fmt_idx, mode="raw", tag=tag + " calls raw")
+            for route in (A.APS_SYNC_ONE_PASS, A.APS_SYNC_GUESS, A.APS_SYNC_TWO_PASS, 0):
+                sync_case(dev, G, n, offs, pal, fmt_idx=fmt_idx, tag=f"{tag} route {route}", route=route)
+
+
 def test_sync_empty_gradient(dev):
     offs = np.zeros(4, np.int64)
     G = np.zeros((4, 4), np.float32)
