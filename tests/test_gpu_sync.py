@@ -212,6 +212,58 @@ def test_eight_format_palette(dev):
                 sync_case(dev, G, n, offs, pal, fmt_idx=fmt_idx, tag=f"{tag} route {route}", route=route)
 
 
+def test_calls_from_several_threads_and_streams(dev):
+    """The header's thread-safety: four host threads, each on a stream of its
+    own with its own buffers, call aps_sync (one-pass and guessed-scale
+    routes) and the two-pass calls on different sets at the same time; every
+    result equals the oracle's."""
+    import threading
+
+    seed = zlib.crc32(b"threads")
+    rng = np.random.default_rng(seed)
+    offs, n, ld = _layout(SIZES)
+    jobs = []
+    for k in range(4):
+        W = (8, 256, 64, 3)[k]
+        G = _values(rng, W, ld, offs, "normal")
+        o_mab = O.layer_maxabs(G, n, offs)
+        o_se = O.layer_scales(o_mab, W, [ofmt(F(5, 2))])
+        jobs.append((G, O.sim_reduce(G, n, offs, o_se, [ofmt(F(5, 2))]), o_se))
+    results, errors = {}, []
+    offs_t = torch.from_numpy(offs).to(dev)
+
+    def work(k):
+        try:
+            G, _, _ = jobs[k]
+            stream = torch.cuda.Stream(device=dev)
+            with torch.cuda.stream(stream):
+                G_t = torch.from_numpy(G).to(dev, non_blocking=False)
+                outs = []
+                for it in range(6):
+                    route = (A.APS_SYNC_ONE_PASS, A.APS_SYNC_GUESS, A.APS_SYNC_TWO_PASS)[it % 3]
+                    o, se, _, _ = A.aps_sync(G_t, n, offs_t, [F(5, 2)], None,
+                                             A.APS_SYNC_PASS1 | A.APS_SYNC_PASS2 | route)
+                    outs.append((o, se))
+                stream.synchronize()
+                results[k] = [(o.cpu().numpy(), se.cpu().numpy()) for o, se in outs]
+        except Exception as e:  # reported in the main thread
+            errors.append(f"thread {k}: {e!r}")
+
+    threads = [threading.Thread(target=work, args=(k,)) for k in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for k, (G, o_out, o_se) in enumerate(jobs):
+        for it, (g, se) in enumerate(results[k]):
+            tag = f"thread {k} W={G.shape[0]} call {it} seed={seed}"
+            assert np.array_equal(se, o_se), f"{tag} scales"
+            assert same_f32(g[:n], o_out), f"{tag} sum {first_diff(g[:n], o_out)}"
+    log(f"4 threads x 6 calls on their own streams: all equal the oracle's (seed={seed})")
+
+
 def test_sync_empty_gradient(dev):
     offs = np.zeros(4, np.int64)
     G = np.zeros((4, 4), np.float32)
