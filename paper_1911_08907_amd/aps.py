@@ -166,10 +166,82 @@ def _check(fn: str, st: int):
         raise ApsError(fn, st)
 
 
-def _rows(G):
+def _dtypes(*names):
+    import torch
+    return tuple(getattr(torch, nm) for nm in names if hasattr(torch, nm))
+
+
+def _dev_of(*ts):
+    """The device of the first tensor among ts (raw int addresses and None
+    are skipped), or None."""
+    for t in ts:
+        if t is not None and not isinstance(t, int):
+            return t.device
+    return None
+
+
+def _need(t, name: str, dtypes, numel: int = 0, dev=None, optional: bool = False) -> None:
+    """The library reads and writes device memory through raw pointers:
+    refuse, before anything reaches it, a tensor that is not on the GPU, not
+    of one of ``dtypes``, not contiguous, on another device than ``dev`` or
+    smaller than ``numel`` elements.  A raw int address is the caller's
+    responsibility."""
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if isinstance(t, int):
+        return
+    if not getattr(t, "is_cuda", False):
+        raise ValueError(f"{name} must be a GPU tensor, got one on {t.device}")
+    if dev is not None and t.device != dev:
+        raise ValueError(f"{name} is on {t.device}, the other arrays on {dev}")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} must be of dtype {' or '.join(str(d) for d in dtypes)}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() < numel:
+        raise ValueError(f"{name} has {t.numel()} elements, needs at least {numel}")
+
+
+def _rows(G, n: int | None = None, name: str = "G"):
+    """W and the row stride ld of a [W][ld] fp32 GPU tensor with unit column
+    stride and at least n columns."""
+    if not isinstance(G, int) and (G is None or not getattr(G, "is_cuda", False)):
+        raise ValueError(f"{name} must be a GPU tensor" + ("" if G is None else f", got one on {G.device}"))
     if G.dim() != 2:
-        raise ValueError("expected a [W][ld] tensor")
+        raise ValueError(f"{name}: expected a [W][ld] tensor")
+    if G.dtype not in _dtypes("float32"):
+        raise ValueError(f"{name} must be float32, got {G.dtype}")
+    if G.shape[1] > 1 and G.stride(1) != 1:
+        raise ValueError(f"{name} needs unit column stride")
+    if n is not None and G.shape[1] < n:
+        raise ValueError(f"{name} has {G.shape[1]} columns, fewer than n = {n}")
     return G.shape[0], G.stride(0)
+
+
+def _layers(offsets, dev) -> int:
+    _need(offsets, "offsets", _dtypes("int64"), 1, dev)
+    return offsets.numel() - 1
+
+
+def _code_bytes_of(fmts, count: int) -> int:
+    """Bytes of count packed codes of the palette's widest format."""
+    bits = max(f.bits for f in ([fmts] if isinstance(fmts, Format) else fmts))
+    return code_bytes(count, bits)
+
+
+_F32 = ("float32",)
+_I32 = ("int32",)
+_U8 = ("uint8",)
+_BITS = ("int32", "uint32")
+
+
+def _reduce_arrays(dev, L: int, n: int, fmts, scale_exp, fmt_idx, out, codes_out) -> None:
+    _need(scale_exp, "scale_exp", _dtypes(*_I32), L, dev, optional=True)
+    _need(fmt_idx, "fmt_idx", _dtypes(*_U8), L, dev, optional=True)
+    _need(out, "out", _dtypes(*_F32), n, dev, optional=True)
+    _need(codes_out, "codes_out", _dtypes(*_U8), _code_bytes_of(fmts, n), dev, optional=True)
 
 
 # ------------------------------------------------------------ entry points
@@ -177,31 +249,48 @@ def _rows(G):
 # length and ``offsets`` an int64 tensor of L+1 layer boundaries.
 
 def aps_layer_maxabs(G, n: int, offsets, maxabs_bits, stream=None) -> None:
-    W, ld = _rows(G)
-    L = offsets.numel() - 1
+    W, ld = _rows(G, n)
+    dev = G.device
+    L = _layers(offsets, dev)
+    _need(maxabs_bits, "maxabs_bits", _dtypes(*_BITS), L, dev)
     _check("aps_layer_maxabs", lib().aps_layer_maxabs(_ptr(G), W, ld, n, _ptr(offsets), L,
                                                       _ptr(maxabs_bits), _stream(stream)))
 
 
 def aps_layer_scales(maxabs_bits, N: int, fmts, fmt_idx, scale_exp, stream=None) -> None:
+    dev = _dev_of(maxabs_bits)
+    _need(maxabs_bits, "maxabs_bits", _dtypes(*_BITS), 1, dev)
+    L = maxabs_bits.numel()
+    _need(fmt_idx, "fmt_idx", _dtypes(*_U8), L, dev, optional=True)
+    _need(scale_exp, "scale_exp", _dtypes(*_I32), L, dev)
     pal, nf = _palette(fmts)
     _check("aps_layer_scales", lib().aps_layer_scales(_ptr(maxabs_bits), maxabs_bits.numel(), int(N), pal,
                                                       nf, _ptr(fmt_idx), _ptr(scale_exp), _stream(stream)))
 
 
 def aps_quantize(X, n: int, offsets, scale_exp, fmts, fmt_idx, Q=None, codes=None, stream=None) -> None:
-    W, ld = _rows(X)
+    W, ld = _rows(X, n, "X")
+    dev = X.device
+    L = _layers(offsets, dev)
+    _need(scale_exp, "scale_exp", _dtypes(*_I32), L, dev, optional=True)
+    _need(fmt_idx, "fmt_idx", _dtypes(*_U8), L, dev, optional=True)
+    if Q is not None and not isinstance(Q, int):
+        _rows(Q, n, "Q")
+        if Q.device != dev or Q.shape[0] < W or Q.stride(0) != ld:
+            raise ValueError("Q must have X's row stride, at least X's rows and X's device")
+    _need(codes, "codes", _dtypes(*_U8), W * _code_bytes_of(fmts, ld), dev, optional=True)
     pal, nf = _palette(fmts)
-    L = offsets.numel() - 1
     _check("aps_quantize", lib().aps_quantize(_ptr(X), W, ld, n, _ptr(offsets), L, _ptr(scale_exp), pal, nf,
                                               _ptr(fmt_idx), _ptr(Q), _ptr(codes), _stream(stream)))
 
 
 def aps_sim_reduce(G, n: int, offsets, scale_exp, fmts, fmt_idx, flags: int = 0, out=None,
                    codes_out=None, stream=None) -> None:
-    W, ld = _rows(G)
+    W, ld = _rows(G, n)
+    dev = G.device
+    L = _layers(offsets, dev)
+    _reduce_arrays(dev, L, n, fmts, scale_exp, fmt_idx, out, codes_out)
     pal, nf = _palette(fmts)
-    L = offsets.numel() - 1
     _check("aps_sim_reduce", lib().aps_sim_reduce(_ptr(G), W, ld, n, _ptr(offsets), L, _ptr(scale_exp), pal,
                                                   nf, _ptr(fmt_idx), int(flags), _ptr(out), _ptr(codes_out),
                                                   _stream(stream)))
@@ -211,9 +300,11 @@ def aps_sim_reduce_ex(G, n: int, offsets, scale_exp, fmts, fmt_idx, flags: int =
                       accumulator: int = APS_ACC_SEQUENTIAL, out=None, codes_out=None, stream=None) -> None:
     """aps_sim_reduce with the hierarchical-all-reduce order (group size k)
     and a plain or Kahan low-precision accumulator."""
-    W, ld = _rows(G)
+    W, ld = _rows(G, n)
+    dev = G.device
+    L = _layers(offsets, dev)
+    _reduce_arrays(dev, L, n, fmts, scale_exp, fmt_idx, out, codes_out)
     pal, nf = _palette(fmts)
-    L = offsets.numel() - 1
     opts = aps_reduce_opts(W if group is None else int(group), int(accumulator))
     _check("aps_sim_reduce_ex", lib().aps_sim_reduce_ex(_ptr(G), W, ld, n, _ptr(offsets), L, _ptr(scale_exp), pal,
                                                         nf, _ptr(fmt_idx), int(flags), ctypes.byref(opts),
@@ -224,16 +315,27 @@ def aps_sim_reduce_codes(codes, W: int, ld: int, n: int, offsets, scale_exp, fmt
                          out=None, codes_out=None, stream=None) -> None:
     """codes: a uint8 tensor holding W rows of packed codes (row stride: the
     code bytes of ld elements)."""
+    dev = _dev_of(codes)
+    _need(codes, "codes", _dtypes(*_U8), int(W) * _code_bytes_of(fmts, int(ld)), dev)
+    if int(ld) < n:
+        raise ValueError(f"ld = {ld} is below n = {n}")
+    L = _layers(offsets, dev)
+    _reduce_arrays(dev, L, n, fmts, scale_exp, fmt_idx, out, codes_out)
     pal, nf = _palette(fmts)
-    L = offsets.numel() - 1
     _check("aps_sim_reduce_codes", lib().aps_sim_reduce_codes(_ptr(codes), int(W), int(ld), n, _ptr(offsets), L,
                                                               _ptr(scale_exp), pal, nf, _ptr(fmt_idx), int(flags),
                                                               _ptr(out), _ptr(codes_out), _stream(stream)))
 
 
 def aps_dequantize(Q, codes, n: int, offsets, scale_exp, fmts, fmt_idx, out, stream=None) -> None:
+    dev = _dev_of(Q, codes, out)
+    _need(Q, "Q", _dtypes(*_F32), n, dev, optional=True)
+    _need(codes, "codes", _dtypes(*_U8), _code_bytes_of(fmts, n), dev, optional=True)
+    _need(out, "out", _dtypes(*_F32), n, dev)
+    L = _layers(offsets, dev)
+    _need(scale_exp, "scale_exp", _dtypes(*_I32), L, dev, optional=True)
+    _need(fmt_idx, "fmt_idx", _dtypes(*_U8), L, dev, optional=True)
     pal, nf = _palette(fmts)
-    L = offsets.numel() - 1
     _check("aps_dequantize", lib().aps_dequantize(_ptr(Q), _ptr(codes), n, _ptr(offsets), L, _ptr(scale_exp),
                                                   pal, nf, _ptr(fmt_idx), _ptr(out), _stream(stream)))
 
@@ -245,10 +347,21 @@ def aps_lp_gemm(A, B, fin: Format, facc: Format, accumulator: int = APS_ACC_SEQU
     inputs cast to ``fin``, products and partial sums rounded to ``facc``."""
     import torch
 
+    for name, t in (("A", A), ("B", B), ("C", C)):
+        if t is None and name == "C":
+            continue
+        if not getattr(t, "is_cuda", False):
+            raise ValueError(f"{name} must be a GPU tensor")
+        if t.dtype != torch.float32 or t.dim() != 2:
+            raise ValueError(f"{name} must be a 2-D float32 tensor")
+        if t.device != A.device:
+            raise ValueError(f"{name} is on {t.device}, A on {A.device}")
     M, K = A.shape
     K2, N = B.shape
     if K != K2:
         raise ValueError(f"inner dimensions differ: {K} vs {K2}")
+    if C is not None and tuple(C.shape) != (M, N):
+        raise ValueError(f"C has shape {tuple(C.shape)}, the product {(M, N)}")
     def ld(t, rows, cols):  # row stride; an empty or one-row tensor may report anything
         if rows <= 1 or cols == 0:
             return max(cols, 1)
@@ -286,9 +399,10 @@ def aps_sync(G, n: int, offsets, fmts, fmt_idx=None, flags: int = APS_SYNC_PASS1
     workspace tensors are allocated here.  Returns
     (out, scale_exp, maxabs_bits, workspace)."""
     import torch
-    W, ld = _rows(G)
-    L = offsets.numel() - 1
+    W, ld = _rows(G, n)
     dev = G.device
+    L = _layers(offsets, dev)
+    _need(fmt_idx, "fmt_idx", _dtypes(*_U8), L, dev, optional=True)
     if maxabs_bits is None:
         maxabs_bits = torch.empty(L, dtype=torch.int32, device=dev)
     if scale_exp is None:
@@ -298,6 +412,10 @@ def aps_sync(G, n: int, offsets, fmts, fmt_idx=None, flags: int = APS_SYNC_PASS1
     need = aps_sync_workspace_bytes(n, L)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    _need(maxabs_bits, "maxabs_bits", _dtypes(*_BITS), L, dev)
+    _need(scale_exp, "scale_exp", _dtypes(*_I32), L, dev)
+    _need(out, "out", _dtypes(*_F32), n, dev)
+    _need(workspace, "workspace", _dtypes(*_U8), 0, dev)
     pal, nf = _palette(fmts)
     _check("aps_sync", lib().aps_sync(_ptr(G), W, ld, n, _ptr(offsets), L, pal, nf, _ptr(fmt_idx), int(flags),
                                       _ptr(maxabs_bits), _ptr(scale_exp), _ptr(out), _ptr(workspace),
@@ -310,8 +428,13 @@ def aps_sync_noalloc(G, n: int, offsets, fmts, fmt_idx, maxabs_bits, scale_exp, 
     """aps_sync with the library's static per-GPU workspace instead of a
     caller's (nothing is allocated, here or in the library): every output
     tensor is the caller's."""
-    W, ld = _rows(G)
-    L = offsets.numel() - 1
+    W, ld = _rows(G, n)
+    dev = G.device
+    L = _layers(offsets, dev)
+    _need(fmt_idx, "fmt_idx", _dtypes(*_U8), L, dev, optional=True)
+    _need(maxabs_bits, "maxabs_bits", _dtypes(*_BITS), L, dev)
+    _need(scale_exp, "scale_exp", _dtypes(*_I32), L, dev)
+    _need(out, "out", _dtypes(*_F32), n, dev)
     pal, nf = _palette(fmts)
     _check("aps_sync_noalloc", lib().aps_sync_noalloc(_ptr(G), W, ld, n, _ptr(offsets), L, pal, nf, _ptr(fmt_idx),
                                                       int(flags), _ptr(maxabs_bits), _ptr(scale_exp), _ptr(out),
@@ -334,9 +457,9 @@ def aps_step(G, n: int, offsets, fmts, fmt_idx=None, N: int | None = None, flags
     max-abs, scales, fused scale/cast/rounded-sum/unscale.  Returns
     (out, scale_exp, maxabs_bits) as new device tensors."""
     import torch
-    W, _ = _rows(G)
-    L = offsets.numel() - 1
+    W, _ = _rows(G, n)
     dev = G.device
+    L = _layers(offsets, dev)
     maxabs = torch.empty(L, dtype=torch.int32, device=dev)
     scale = torch.empty(L, dtype=torch.int32, device=dev)
     out = torch.empty(max(n, 1), dtype=torch.float32, device=dev)[:n]
