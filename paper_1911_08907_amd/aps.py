@@ -142,9 +142,18 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
-def _stream(stream):
+def _stream(stream, dev=None):
+    """The hipStream_t to launch on: the given stream, or torch's current
+    stream.  The library launches on the current device, so the arrays'
+    device must be the current one (and a torch stream's device)."""
+    import torch
+    if dev is not None and dev.type == "cuda":
+        cur = torch.cuda.current_device()
+        if (dev.index if dev.index is not None else cur) != cur:
+            raise ValueError(f"the arrays are on {dev}, the current device is cuda:{cur}")
+        if stream is not None and not isinstance(stream, int) and stream.device != torch.device("cuda", cur):
+            raise ValueError(f"the stream is on {stream.device}, the arrays on {dev}")
     if stream is None:
-        import torch
         return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     if isinstance(stream, int):
         return ctypes.c_void_p(stream)
@@ -254,7 +263,7 @@ def aps_layer_maxabs(G, n: int, offsets, maxabs_bits, stream=None) -> None:
     L = _layers(offsets, dev)
     _need(maxabs_bits, "maxabs_bits", _dtypes(*_BITS), L, dev)
     _check("aps_layer_maxabs", lib().aps_layer_maxabs(_ptr(G), W, ld, n, _ptr(offsets), L,
-                                                      _ptr(maxabs_bits), _stream(stream)))
+                                                      _ptr(maxabs_bits), _stream(stream, dev)))
 
 
 def aps_layer_scales(maxabs_bits, N: int, fmts, fmt_idx, scale_exp, stream=None) -> None:
@@ -265,7 +274,7 @@ def aps_layer_scales(maxabs_bits, N: int, fmts, fmt_idx, scale_exp, stream=None)
     _need(scale_exp, "scale_exp", _dtypes(*_I32), L, dev)
     pal, nf = _palette(fmts)
     _check("aps_layer_scales", lib().aps_layer_scales(_ptr(maxabs_bits), maxabs_bits.numel(), int(N), pal,
-                                                      nf, _ptr(fmt_idx), _ptr(scale_exp), _stream(stream)))
+                                                      nf, _ptr(fmt_idx), _ptr(scale_exp), _stream(stream, dev)))
 
 
 def aps_quantize(X, n: int, offsets, scale_exp, fmts, fmt_idx, Q=None, codes=None, stream=None) -> None:
@@ -281,7 +290,7 @@ def aps_quantize(X, n: int, offsets, scale_exp, fmts, fmt_idx, Q=None, codes=Non
     _need(codes, "codes", _dtypes(*_U8), W * _code_bytes_of(fmts, ld), dev, optional=True)
     pal, nf = _palette(fmts)
     _check("aps_quantize", lib().aps_quantize(_ptr(X), W, ld, n, _ptr(offsets), L, _ptr(scale_exp), pal, nf,
-                                              _ptr(fmt_idx), _ptr(Q), _ptr(codes), _stream(stream)))
+                                              _ptr(fmt_idx), _ptr(Q), _ptr(codes), _stream(stream, dev)))
 
 
 def aps_sim_reduce(G, n: int, offsets, scale_exp, fmts, fmt_idx, flags: int = 0, out=None,
@@ -293,7 +302,7 @@ def aps_sim_reduce(G, n: int, offsets, scale_exp, fmts, fmt_idx, flags: int = 0,
     pal, nf = _palette(fmts)
     _check("aps_sim_reduce", lib().aps_sim_reduce(_ptr(G), W, ld, n, _ptr(offsets), L, _ptr(scale_exp), pal,
                                                   nf, _ptr(fmt_idx), int(flags), _ptr(out), _ptr(codes_out),
-                                                  _stream(stream)))
+                                                  _stream(stream, dev)))
 
 
 def aps_sim_reduce_ex(G, n: int, offsets, scale_exp, fmts, fmt_idx, flags: int = 0, group: int | None = None,
@@ -308,7 +317,7 @@ def aps_sim_reduce_ex(G, n: int, offsets, scale_exp, fmts, fmt_idx, flags: int =
     opts = aps_reduce_opts(W if group is None else int(group), int(accumulator))
     _check("aps_sim_reduce_ex", lib().aps_sim_reduce_ex(_ptr(G), W, ld, n, _ptr(offsets), L, _ptr(scale_exp), pal,
                                                         nf, _ptr(fmt_idx), int(flags), ctypes.byref(opts),
-                                                        _ptr(out), _ptr(codes_out), _stream(stream)))
+                                                        _ptr(out), _ptr(codes_out), _stream(stream, dev)))
 
 
 def aps_sim_reduce_codes(codes, W: int, ld: int, n: int, offsets, scale_exp, fmts, fmt_idx, flags: int = 0,
@@ -324,7 +333,7 @@ def aps_sim_reduce_codes(codes, W: int, ld: int, n: int, offsets, scale_exp, fmt
     pal, nf = _palette(fmts)
     _check("aps_sim_reduce_codes", lib().aps_sim_reduce_codes(_ptr(codes), int(W), int(ld), n, _ptr(offsets), L,
                                                               _ptr(scale_exp), pal, nf, _ptr(fmt_idx), int(flags),
-                                                              _ptr(out), _ptr(codes_out), _stream(stream)))
+                                                              _ptr(out), _ptr(codes_out), _stream(stream, dev)))
 
 
 def aps_dequantize(Q, codes, n: int, offsets, scale_exp, fmts, fmt_idx, out, stream=None) -> None:
@@ -337,7 +346,7 @@ def aps_dequantize(Q, codes, n: int, offsets, scale_exp, fmts, fmt_idx, out, str
     _need(fmt_idx, "fmt_idx", _dtypes(*_U8), L, dev, optional=True)
     pal, nf = _palette(fmts)
     _check("aps_dequantize", lib().aps_dequantize(_ptr(Q), _ptr(codes), n, _ptr(offsets), L, _ptr(scale_exp),
-                                                  pal, nf, _ptr(fmt_idx), _ptr(out), _stream(stream)))
+                                                  pal, nf, _ptr(fmt_idx), _ptr(out), _stream(stream, dev)))
 
 
 def aps_lp_gemm(A, B, fin: Format, facc: Format, accumulator: int = APS_ACC_SEQUENTIAL, C=None,
@@ -373,7 +382,7 @@ def aps_lp_gemm(A, B, fin: Format, facc: Format, accumulator: int = APS_ACC_SEQU
         C = torch.empty((M, N), dtype=torch.float32, device=A.device)
     lda, ldb, ldc = ld(A, M, K), ld(B, K, N), ld(C, M, N)
     _check("aps_lp_gemm", lib().aps_lp_gemm(_ptr(A), lda, _ptr(B), ldb, _ptr(C), ldc, M, N, K, fin.c(),
-                                            facc.c(), int(accumulator), _stream(stream)))
+                                            facc.c(), int(accumulator), _stream(stream, A.device)))
     return C
 
 
@@ -419,7 +428,7 @@ def aps_sync(G, n: int, offsets, fmts, fmt_idx=None, flags: int = APS_SYNC_PASS1
     pal, nf = _palette(fmts)
     _check("aps_sync", lib().aps_sync(_ptr(G), W, ld, n, _ptr(offsets), L, pal, nf, _ptr(fmt_idx), int(flags),
                                       _ptr(maxabs_bits), _ptr(scale_exp), _ptr(out), _ptr(workspace),
-                                      workspace.numel() * workspace.element_size(), _stream(stream)))
+                                      workspace.numel() * workspace.element_size(), _stream(stream, dev)))
     return out, scale_exp, maxabs_bits, workspace
 
 
@@ -438,7 +447,7 @@ def aps_sync_noalloc(G, n: int, offsets, fmts, fmt_idx, maxabs_bits, scale_exp, 
     pal, nf = _palette(fmts)
     _check("aps_sync_noalloc", lib().aps_sync_noalloc(_ptr(G), W, ld, n, _ptr(offsets), L, pal, nf, _ptr(fmt_idx),
                                                       int(flags), _ptr(maxabs_bits), _ptr(scale_exp), _ptr(out),
-                                                      _stream(stream)))
+                                                      _stream(stream, dev)))
 
 
 def code_bytes(count: int, bits: int) -> int:
