@@ -8,6 +8,7 @@ and must fail.  CPU only; the real oracle is untouched."""
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 import pytest
 
@@ -53,19 +54,53 @@ MUTANTS = {
                              "const double a = (double)A[(int64_t)i * lda + k];"),
     "gemm_accumulates_in_input_format": ("chain_add(&s, &c, p, acc, accumulator);",
                                          "chain_add(&s, &c, p, in, accumulator);"),
+    "decode_subnormal_exponent": ("a = ldexp((double)mant, oracle_emin(f) - f.m);",
+                                  "a = ldexp((double)mant, oracle_emin(f) - f.m - 1);"),
+    "encode_bias_off_by_one": ("ef = (uint32_t)(E + f.bias);", "ef = (uint32_t)(E + f.bias + 1);"),
+    "encode_nan_low_mantissa_bit": ("mant = f.m > 0 ? (1u << (f.m - 1)) : 0u;", "mant = f.m > 0 ? 1u : 0u;"),
+    "nibble_order_swapped": ("(int)(j & 1) * 4", "(int)(~j & 1) * 4"),
+    "uint16_codes_big_endian": ("b[2 * j] = (uint8_t)(c & 0xFF);\n        b[2 * j + 1] = (uint8_t)(c >> 8);",
+                                "b[2 * j] = (uint8_t)(c >> 8);\n        b[2 * j + 1] = (uint8_t)(c & 0xFF);"),
+    "group_members_reversed": ("const float x = G[(int64_t)(g * k + m) * ld + j];",
+                               "const float x = G[(int64_t)(g * k + (k - 1 - m)) * ld + j];"),
+    "ring_not_rotated": ("const int64_t seg = j * ng / n;", "const int64_t seg = 0;"),
+    "round_off_counts_zero_grad_h": ("if (grad_h[j] == 0.0f) continue;", "if (0) continue;"),
+    "round_off_signed": ("sum += fabs(((double)grad_h[j] - (double)grad_l[j]) / (double)grad_h[j]);",
+                         "sum += ((double)grad_h[j] - (double)grad_l[j]) / (double)grad_h[j];"),
+    "dequantize_scale_not_undone": ("out[j] = (float)ldexp(v, -ft);", "out[j] = (float)v;"),
+    "codes_reduce_unrounded": ("s = (w == 0) ? q : oracle_round(s + q, f); /* low-precision accumulator */",
+                               "s = (w == 0) ? q : s + q; /* low-precision accumulator */"),
+    "nibble_row_stride": ("return bits <= 4 ? ld / 2 : (bits <= 8 ? ld : 2 * ld);",
+                          "return bits <= 4 ? ld : (bits <= 8 ? ld : 2 * ld);"),
 }
 
 
-@pytest.mark.parametrize("name", sorted(MUTANTS))
-def test_pins_catch_mutant(tmp_path, name):
+def _run_mutant(src: str, tmp, name: str):
+    """Build the oracle with one mutation and run the pins against it in a
+    process of its own; returns (name, pytest's exit status or None when the
+    mutation site is missing, the tail of its output)."""
     old, new = MUTANTS[name]
-    src = open(SRC).read()
-    assert src.count(old) >= 1, f"mutation site for {name} not found"
-    mutated = tmp_path / "oracle_mut.c"
+    if src.count(old) < 1:
+        return name, None, "mutation site not found"
+    d = tmp / name
+    d.mkdir()
+    mutated = d / "oracle_mut.c"
     mutated.write_text(src.replace(old, new))
-    lib = O.build(force=True, src=str(mutated), out=str(tmp_path / "liboracle_mut.so"))
-    env = dict(os.environ, APS_ORACLE_LIB=lib)
+    lib = O.build(force=True, src=str(mutated), out=str(d / "liboracle_mut.so"))
+    env = dict(os.environ, APS_ORACLE_LIB=lib, OMP_NUM_THREADS="1")
     res = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                           os.path.join(ROOT, "tests", "test_oracle_pins.py")],
-                         cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
-    assert res.returncode != 0, f"mutant {name} survived the pins:\n{res.stdout[-2000:]}"
+                         cwd=ROOT, env=env, capture_output=True, text=True, timeout=900)
+    return name, res.returncode, res.stdout[-2000:]
+
+
+def test_pins_catch_every_mutant(tmp_path):
+    """Every mutant, each in a pin run of its own, several at a time."""
+    src = open(SRC).read()
+    workers = max(1, min(8, os.cpu_count() or 1))
+    with ThreadPoolExecutor(workers) as ex:
+        results = list(ex.map(lambda nm: _run_mutant(src, tmp_path, nm), sorted(MUTANTS)))
+    missing = [nm for nm, rc, _ in results if rc is None]
+    survivors = [(nm, out) for nm, rc, out in results if rc == 0]
+    assert not missing, f"mutation sites not found: {missing}"
+    assert not survivors, "mutants that survived the pins:\n" + "\n".join(f"{nm}:\n{out}" for nm, out in survivors)

@@ -434,6 +434,55 @@ def test_w1_reduce_is_quantize_dequantize_and_composition():
         assert np.array_equal(full, comp2)
 
 
+def test_code_layout_against_library_bit_patterns():
+    """The packed code layout of the header (code = sign, exponent field,
+    mantissa; 9..16-bit codes as little-endian uint16, 5..8-bit codes one
+    byte each, 2..4-bit codes two per byte with element 2i in the low
+    nibble), pinned to bit patterns the oracle does not produce: numpy's
+    IEEE half for 1-5-10, torch's float8_e5m2 for 1-5-2, and, for 4-bit
+    codes, values built from each code by the format's definition."""
+    rng = np.random.default_rng(515)
+    # 1-5-10 is IEEE half precision: its codes are float16 bit patterns
+    h = (rng.standard_normal(2000) * 2.0 ** rng.integers(-26, 16, 2000)).astype(np.float16)
+    h[:6] = [0.0, -0.0, np.inf, -np.inf, 6.1035e-05, -5.96e-08]  # 2^-14, -2^-24
+    v = h.astype(np.float32)
+    assert np.array_equal(v.astype(np.float16).view(np.uint16), h.view(np.uint16))
+    offs = np.array([0, v.size], np.int64)
+    assert O.pack_codes(v, offs, F(5, 10)).tobytes() == h.astype("<f2").tobytes()
+    # 1-5-2 is float8_e5m2: one byte per code (NaN is not compared: torch writes another pattern)
+    x = torch.from_numpy(rng.standard_normal(2000).astype(np.float32) * 2.0 ** 8)
+    x[:4] = torch.tensor([0.0, -0.0, float("inf"), -float("inf")])
+    e5 = x.to(torch.float8_e5m2)
+    v8 = e5.to(torch.float32).numpy()
+    offs = np.array([0, v8.size], np.int64)
+    assert np.array_equal(O.pack_codes(v8, offs, F(5, 2)), e5.view(torch.uint8).numpy())
+    # 4-bit codes of 1-3-0 (bias 3) and 1-2-1 (bias 1): every code's value from the definition
+    for f, bias in ((F(3, 0), 3), (F(2, 1), 1)):
+        emask = (1 << f.e) - 1
+        codes = rng.integers(0, 16, 601)
+        vals = []
+        for c in codes:
+            sign = -1.0 if c >> (f.e + f.m) else 1.0
+            ef, mant = (c >> f.m) & emask, c & ((1 << f.m) - 1)
+            if ef == emask:
+                codes[len(vals)] = c = c & ~((1 << f.m) - 1)  # INF only: NaN's mantissa is checked below
+                vals.append(sign * np.inf)
+            elif ef == 0:
+                vals.append(sign * mant * 2.0 ** (1 - bias - f.m))
+            else:
+                vals.append(sign * (1 + mant / 2 ** f.m) * 2.0 ** (ef - bias))
+        vals = np.array(vals, np.float32)
+        offs = np.array([0, vals.size], np.int64)
+        packed = O.pack_codes(vals, offs, f)
+        c = np.append(codes, 0).astype(np.uint8)
+        assert np.array_equal(packed, c[0::2] | (c[1::2] << 4)), f
+    # NaN: the all-ones exponent with the top mantissa bit (the INF code when m = 0)
+    assert O.encode(float("nan"), F(5, 10)) & 0x7FFF == 0x7E00
+    assert O.encode(float("nan"), F(5, 2)) & 0x7F == 0x7E
+    assert O.encode(float("nan"), F(4, 3)) & 0x7F == 0x7C
+    assert O.encode(float("nan"), F(3, 0)) & 0x7 == 0x7
+
+
 def test_raw_mode_overflow_and_nan():
     f = F(5, 2)
     offs = np.array([0, 4], np.int64)
