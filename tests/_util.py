@@ -1,7 +1,6 @@
 """Helpers shared by the tests (no APS arithmetic here)."""
 from __future__ import annotations
 
-import os
 import sys
 
 import numpy as np
@@ -45,11 +44,3 @@ def same_maxabs(a, b) -> bool:
     b = np.asarray(b).view(np.uint32)
     an, bn = a > 0x7F800000, b > 0x7F800000
     return np.array_equal(an, bn) and np.array_equal(a[~an], b[~bn])
-
-
-def gpu_available() -> bool:
-    try:
-        import torch
-        return torch.cuda.is_available()
-    except Exception:
-        return False
