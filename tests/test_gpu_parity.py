@@ -300,6 +300,35 @@ def test_tiny_gradients(dev, n_total):
                 run_case(dev, G, n, offs, [f], mode="raw", tag=tag + " raw")
 
 
+@pytest.mark.parametrize("f", [F(5, 2), F(3, 0), F(5, 10), F(8, 7, 130)], ids=str)
+def test_quantize_in_place_and_dequantize_in_place(dev, f):
+    """The header lets Q alias X (aps_quantize) and out alias Q
+    (aps_dequantize): both in place, on the edge layout with specials, equal
+    the oracle's out-of-place results."""
+    seed = zlib.crc32(f"in-place/{f}".encode())
+    rng = np.random.default_rng(seed)
+    offs, n, ld = _layout(SIZES)
+    opal = [ofmt(f)]
+    for W in (1, 3):
+        G = _values(rng, W, ld, offs, "special")
+        se = rng.integers(-40, 40, offs.size - 1).astype(np.int32)
+        X_t = torch.from_numpy(G).to(dev)
+        offs_t = torch.from_numpy(offs).to(dev)
+        se_t = torch.from_numpy(se).to(dev)
+        A.aps_quantize(X_t, n, offs_t, se_t, [f], None, Q=X_t)
+        torch.cuda.synchronize()
+        o_Q = O.quantize(G, n, offs, se, opal)
+        got = X_t.cpu().numpy()
+        assert same_f32(got[:, :n], o_Q[:, :n]), f"{f} W={W} seed={seed} quantize in place"
+        # the padding past n is left as it was
+        assert same_f32(got[:, n:], G[:, n:]), f"{f} W={W} padding"
+        row = X_t[0, :].contiguous()
+        A.aps_dequantize(row, None, n, offs_t, se_t, [f], None, row)
+        torch.cuda.synchronize()
+        o_d = O.dequantize(o_Q[0, :n], None, n, offs, se, opal)
+        assert same_f32(row.cpu().numpy()[:n], o_d), f"{f} W={W} seed={seed} dequantize in place"
+
+
 def test_empty_gradient(dev):
     offs = np.zeros(4, np.int64)
     G = np.zeros((3, 4), np.float32)
