@@ -632,15 +632,18 @@ def lp_gemm_calls(A, dev, reps: int = 5):
     return res
 
 
-def measure_step(A, gs, pal, idx_t, offs_t, mode: str, steps: int, warmup: int, graph: bool = False) -> dict:
+def measure_step(A, gs, pal, idx_t, offs_t, mode: str, steps: int, warmup: int, graph: bool = False,
+                 loops: int = 1) -> dict:
     """Time `steps` APS synchronisations of a gradient set after `warmup`
     untimed ones: aps_sync's pass 1 and pass 2 as two calls (APS mode), or
     the reduce with every exponent 0 (RAW mode, casting without APS).  The
     step time is wall-clock over steps run back to back; the pass spans come
     from as many further steps with HIP events around each pass on the
-    launch stream.  Returns the step time, the pass times, the route and the
-    dominant kernel's roofline figures, plus the device arrays the step
-    wrote."""
+    launch stream.  With loops > 1 the back-to-back run is repeated and the
+    median of its per-step times is kept (a host hiccup of a few ms in one
+    short run would otherwise weigh on the figure).  Returns the step time,
+    the pass times, the route and the dominant kernel's roofline figures,
+    plus the device arrays the step wrote."""
     import torch
 
     dev = gs.G.device
@@ -675,12 +678,16 @@ def measure_step(A, gs, pal, idx_t, offs_t, mode: str, steps: int, warmup: int, 
         step(False)
     torch.cuda.synchronize()
     # the step time: `steps` steps back to back with nothing between them
-    t0 = time.perf_counter()
-    for _ in range(steps):
-        step(False)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / steps
+    runs = []
+    for _ in range(loops):
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step(False)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        runs.append((t1 - t0) * 1e3 / steps)
+    ms_per_step = sorted(runs)[len(runs) // 2]
+    ms_runs = runs if loops > 1 else None
     # the pass spans: as many steps again, with events around each pass
     for _ in range(steps):
         step(True)
@@ -751,7 +758,7 @@ def measure_step(A, gs, pal, idx_t, offs_t, mode: str, steps: int, warmup: int, 
     return {"ms_per_step": ms_per_step, "pass1_ms": p1, "pass2_ms": p2, "aps": aps, "one": one, "guess": guess,
             "route": ("one pass" if one else ("guessed scales" if guess else "two passes")) if aps else "raw reduce",
             "kernel": kernel, "kernel_ms": k_ms, "alg_bytes": alg_bytes, "achieved": achieved, "note": note,
-            "rerun": rerun, "graph_ms_per_step": graph_ms, "arrays": (mab, se, out, ws)}
+            "rerun": rerun, "graph_ms_per_step": graph_ms, "ms_per_step_runs": ms_runs, "arrays": (mab, se, out, ws)}
 
 
 # The other workloads timed after the headline step (each also in RAW mode,
@@ -784,11 +791,12 @@ def other_configs(A, WL, dev, cfg0: str, pal0: str, held: dict, steps: int, warm
         pal = [A.Format(p.e, p.m, p.bias) for p in WL.CONFIGS[cfg].palettes[palette]]
         offs_t = torch.from_numpy(gs.offsets).to(dev)
         idx_t = None if gs.fmt_idx is None else torch.from_numpy(gs.fmt_idx).to(dev)
-        m = measure_step(A, gs, pal, idx_t, offs_t, mode, steps, warmup, graph=True)
+        m = measure_step(A, gs, pal, idx_t, offs_t, mode, steps, warmup, graph=True, loops=3)
         del m["arrays"]
         W, n = gs.W, gs.n
         res[f"{cfg} {palette} {mode}"] = {
-            "W": W, "n": n, "ms_per_step": m["ms_per_step"], "elements_per_s": W * n / (m["ms_per_step"] * 1e-3),
+            "W": W, "n": n, "ms_per_step": m["ms_per_step"], "ms_per_step_runs": m["ms_per_step_runs"],
+            "elements_per_s": W * n / (m["ms_per_step"] * 1e-3),
             "route": m["route"], "kernel": m["kernel"], "kernel_ms": m["kernel_ms"],
             "algorithmic_bytes_per_launch": m["alg_bytes"], "achieved_GBps": m["achieved"],
             "frac": m["achieved"] / HBM_PEAK_GBPS, "pass1_ms": m["pass1_ms"], "pass2_ms": m["pass2_ms"],
