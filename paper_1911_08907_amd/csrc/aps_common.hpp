@@ -4,7 +4,8 @@
 //
 // Work decomposition.  The flat n-element gradient is cut into chunks of
 // CH = 1024 elements; each thread owns 4 consecutive elements (one 16-byte
-// load per worker row).  A launch has about 8 blocks per CU and each block
+// load per worker row).  A launch has a measured number of blocks per CU
+// (BLOCKS_PER_CU, or a kernel's own; stream_grid below) and each block
 // walks a contiguous range of chunks, so the layer of a chunk is found by a
 // forward scan from the previous one (scalar loads of the offsets table).
 // A chunk may cover several layers; as long as they share one palette entry
