@@ -860,7 +860,7 @@ def main():
     idx_t = None if gs.fmt_idx is None else torch.from_numpy(gs.fmt_idx).to(dev)
     G = gs.G
     aps = args.mode == "aps"
-    m = measure_step(A, gs, pal, idx_t, offs_t, args.mode, args.steps, args.warmup)
+    m = measure_step(A, gs, pal, idx_t, offs_t, args.mode, args.steps, args.warmup, graph=True)
     mab, se, out, _ = m.pop("arrays")
     ms_per_step = m["ms_per_step"]
 
@@ -904,6 +904,9 @@ def main():
             "traffic_source": traffic_src,
         },
         "passes_ms": {"pass1": m["pass1_ms"], "pass2": m["pass2_ms"]},
+        # the same step captured once in a HIP graph and replayed `steps` times
+        # (timed after the eager steps; the replays equal the eager result)
+        "graph_ms_per_step": m["graph_ms_per_step"],
         **({"guess_reruns": m["rerun"]} if m["rerun"] else {}),
         "other_calls": other,
         "kernel_source": source_digest(),
