@@ -39,6 +39,7 @@ def test_bench_json_line():
     assert res["unit"] == "elements/s" and res["value"] > 0
     assert res["n_gpus"] == 1 and res["steps"] == 3 and res["warmup"] == 1
     assert res["ms_per_step"] > 0 and res["higher_is_better"] is True
+    assert res["graph_ms_per_step"] > 0  # the same step replayed as a captured HIP graph
     assert res["scaling"] == "weak" and res["vs_baseline"] is None
     assert res["dtype"] == "f32" and res["data"] == "synthetic"
     assert res["config"]["workload"] == "mlp"
