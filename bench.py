@@ -377,6 +377,23 @@ def other_calls(A, G, gs, pal, idx_t, offs_t, se, out, reps: int = 5):
         t = timed(lambda: A.aps_sim_reduce_codes(codes, W, ld, n, offs_t, se, pal, idx_t, 0, out=out))
         res["sim_reduce_codes"] = {"ms": t, "GBps": (A.code_bytes(n, bits) * W + 4.0 * n) / (t * 1e-3) / 1e9,
                                    "elements_per_s": W * n / (t * 1e-3)}
+        if W >= 8:
+            # one owner's share on an 8-GPU node: the 8 workers' code rows of
+            # its n/8 elements (here rows 0..7 and elements [0, n/8), the
+            # layer table cut there), reduced in worker order
+            import numpy as np
+            n8 = n // 8
+            offs = offs_t.cpu().numpy()
+            L8 = int(np.searchsorted(offs, n8, side="left"))
+            offs8 = torch.from_numpy(np.append(offs[:L8], n8).astype(np.int64)).to(G.device)
+            se8 = None if se is None else se[:L8].contiguous()
+            idx8 = None if idx_t is None else idx_t[:L8].contiguous()
+            out8 = out[:n8]
+            t = timed(lambda: A.aps_sim_reduce_codes(codes[:8 * row_bytes], 8, ld, n8, offs8, se8, pal, idx8, 0,
+                                                     out=out8))
+            res["owner_reduce_codes_8gpu"] = {
+                "shape": f"8 code rows x {n8} elements (one owner's n/8 slice on an 8-GPU node)",
+                "ms": t, "GBps": (A.code_bytes(n8, bits) * 8 + 4.0 * n8) / (t * 1e-3) / 1e9}
     # summation orders of the hierarchical all-reduce and the Kahan accumulator (fp32 input)
     for name, k, acc in (("sim_reduce_ex_group16", 16, A.APS_ACC_SEQUENTIAL), ("sim_reduce_ex_ring", 1, A.APS_ACC_SEQUENTIAL),
                          ("sim_reduce_ex_kahan", None, A.APS_ACC_KAHAN)):
