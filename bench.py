@@ -123,7 +123,7 @@ ROW_MODES = {"read": 0, "sum_f32": 1, "sum_half": 2, "sum_bytes": 3, "row_bytes"
 VALU_OPS = {"v_add_f32_e32": (0, 1), "v_mul_f32_e32": (1, 1), "v_and_b32_e32": (2, 1), "v_fma_f32": (3, 1),
             "v_add3_u32": (4, 1), "v_bfe_u32": (5, 1), "v_ldexp_f32": (6, 1), "v_and_or_b32": (7, 1),
             "v_subrev_f32_e32": (8, 1), "v_cmp_nle_f32_e32+v_cndmask_b32_e32 (VCC)": (9, 2),
-            "v_cmp_nle_f32_e64+v_cndmask_b32_e64 (SGPR mask)": (10, 2)}
+            "v_cmp_nle_f32_e64+v_cndmask_b32_e64 (SGPR mask)": (10, 2), "v_rndne_f32_e32": (11, 1)}
 
 
 def ceilings(only: str | None = None, reps: int = 5) -> dict:

@@ -15,6 +15,7 @@ struct GemmArgs {
     int32_t ka, kb;  // staged A and B carry 2^ka, 2^kb (ka + kb = k of the accumulator, or both 0)
     int64_t tiles;   // output tiles, ntn of them per row of tiles (n fastest)
     int32_t ntn;
+    float qs;        // GP_GRID: 2^Q, the accumulator's subnormal step in its working domain
 };
 
 // How a product reaches the accumulator's working domain and is rounded:
@@ -22,7 +23,21 @@ enum GemmProduct {
     GP_LDEXP = 0,   // operands native: fl32(a * b) then 2^k, rounded (quant)
     GP_SCALED = 1,  // operands pre-scaled at staging: a_w * b_w rounded (quant_w)
     GP_FIT = 2,     // pre-scaled, and every product fits the significand (quant_fit)
+    GP_GRID = 3,    // as GP_FIT, staged so that the subnormal step is 1: rint, then 2^Q
 };
+
+// GP_GRID.  A product of two input values that fits the accumulator's
+// significand is, from 2^emin up, already a multiple of the accumulator's
+// subnormal step 2^(emin - m); below 2^emin the format rounds it to the
+// nearest such multiple, ties to even.  So on a scale where that step is 1
+// its rounding is one round-to-nearest-even to an integer at every
+// magnitude, with no compare and select between the normal and subnormal
+// cases.  The operands are staged with 2^(m - emin) between them, the
+// product is rounded by rint, and 2^Q (Q = the step's exponent in the
+// working domain, >= 0) carries it into the working domain: exactly, or to
+// INF where the product overflows the format, as the format's own
+// overflow threshold sits at fp32's there.  A staged product below 2^-126
+// is below 1/2 and rounds to a signed zero whatever fp32 made of it.
 
 constexpr int GT = 64;  // output tile GT x GT per block, 4 x 4 per thread
 constexpr int GK = 16;  // k-tile staged in LDS
@@ -79,8 +94,10 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
                         p = quant<V>(a[i] * b[j], fa.k, fa, bad[i][j]);
                     else if constexpr (PM == GP_SCALED)
                         p = quant_w<V>(a[i] * b[j], fa, bad[i][j]);
-                    else
+                    else if constexpr (PM == GP_FIT)
                         p = quant_fit<V>(a[i] * b[j], fa);
+                    else
+                        p = __builtin_rintf(a[i] * b[j]) * g.qs;
                     if (first)
                         s[i][j] = p;
                     else
@@ -150,6 +167,12 @@ static void launch_lp_gemm_v(bool kahan, int pm, dim3 grid, hipStream_t s, const
     constexpr bool can_fit = (VT<V>::cls == CLS_TOP || VT<V>::cls == CLS_LOW) && !VT<V>::m0;
     constexpr bool can_ldexp = VT<V>::cls == CLS_TOP || VT<V>::cls == CLS_LOW;
 #define APS_G(K, P) hipLaunchKernelGGL((k_lp_gemm<V, K, P>), grid, dim3(BLOCK), 0, s, g, fi, fa)
+    if (pm == GP_GRID) {
+        if constexpr (can_fit) {
+            if (kahan) APS_G(true, GP_GRID); else APS_G(false, GP_GRID);
+            return;
+        }
+    }
     if (pm == GP_FIT) {
         if constexpr (can_fit) {
             if (kahan) APS_G(true, GP_FIT); else APS_G(false, GP_FIT);
@@ -196,7 +219,7 @@ extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t 
     if (!has_out) return APS_OK;
     const FmtK fi = make_fmtk(in_fmt), fa = make_fmtk(acc_fmt);
     const int64_t mt = (M + GT - 1) / GT, nt = (N + GT - 1) / GT;
-    GemmArgs g{A, B, C, lda, ldb, ldc, M, N, K, 0, 0, mt * nt, (int32_t)nt};
+    GemmArgs g{A, B, C, lda, ldb, ldc, M, N, K, 0, 0, mt * nt, (int32_t)nt, 1.0f};
     // Pre-scale the staged operands by 2^ka and 2^kb (ka + kb = k) when both
     // stay below 2^128: a value below 2^(emax_in+1) times 2^(127-emax_in) does.
     const int room = 127 - fi.emax;
@@ -208,6 +231,23 @@ extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t 
         // every product has at most 2(m_in+1) significant bits
         const int cls = fa.variant <= V_INT_M0 ? CLS_INT : (fa.variant <= V_TOP_M0 ? CLS_TOP : CLS_LOW);
         if (cls != CLS_INT && acc_fmt.m > 0 && 2 * (in_fmt.m + 1) <= acc_fmt.m + 1) pm = GP_FIT;
+    }
+    if (pm == GP_FIT) {
+        // GP_GRID where the step's exponent Q is >= 0 (the format spans at
+        // most 128 binades with its subnormals, so a staged product overflows
+        // fp32 only where the format does) and the operands can carry
+        // 2^(m - emin) between them as fp32 normals: staged values from the
+        // input's smallest subnormal to below 2^128
+        const int q = fa.emin + fa.k - acc_fmt.m;
+        const int kq = acc_fmt.m - fa.emin;
+        const int lo = -126 - (fi.emin - in_fmt.m), hi = 127 - fi.emax;
+        const int ka = std::min(std::max(kq / 2, lo), hi), kb = kq - ka;
+        if (q >= 0 && q <= 127 && kb >= lo && kb <= hi) {
+            g.ka = ka;
+            g.kb = kb;
+            g.qs = pow2f_host(q);
+            pm = GP_GRID;
+        }
     }
     const dim3 grid((unsigned)std::min<int64_t>(g.tiles, INT32_MAX));
     launch_lp_gemm(fa.variant, accumulator == APS_ACC_KAHAN, pm, grid, (hipStream_t)stream, g, fi, fa);

@@ -308,7 +308,7 @@ __global__ __launch_bounds__(BLOCK) void k_widen(const uint8_t* __restrict__ in,
 }
 
 enum ValuOp { V_ADD = 0, V_MUL = 1, V_AND = 2, V_FMA = 3, V_ADD3 = 4, V_BFE = 5, V_LDEXP = 6, V_AND_OR = 7,
-              V_SUBREV = 8, V_CMP_CNDMASK = 9, V_CMP_CNDMASK_SGPR = 10 };
+              V_SUBREV = 8, V_CMP_CNDMASK = 9, V_CMP_CNDMASK_SGPR = 10, V_RNDNE = 11 };
 
 template <int OP>
 __device__ __forceinline__ void valu_step(float& x, float y, float z, int s) {
@@ -321,6 +321,7 @@ __device__ __forceinline__ void valu_step(float& x, float y, float z, int s) {
     if constexpr (OP == V_LDEXP) asm volatile("v_ldexp_f32 %0, %0, %1" : "+v"(x) : "v"(s));
     if constexpr (OP == V_AND_OR) asm volatile("v_and_or_b32 %0, %0, %1, %2" : "+v"(x) : "v"(y), "v"(z));
     if constexpr (OP == V_SUBREV) asm volatile("v_subrev_f32_e32 %0, %1, %0" : "+v"(x) : "v"(y));
+    if constexpr (OP == V_RNDNE) asm volatile("v_rndne_f32_e32 %0, %0" : "+v"(x));
     // a compare into VCC and a select by it, as the compiler emits a rounding's
     // branch-free choice (one pair counted as two instructions)
     if constexpr (OP == V_CMP_CNDMASK)
@@ -486,7 +487,7 @@ extern "C" int probe_valu(int op, float* out, int blocks_per_cu, int32_t iters, 
     case o: hipLaunchKernelGGL(k_valu<o>, grid, dim3(BLOCK), 0, s, out, iters, magic); break;
     switch (op) {
         PROBE_V(V_ADD) PROBE_V(V_MUL) PROBE_V(V_AND) PROBE_V(V_FMA) PROBE_V(V_ADD3) PROBE_V(V_BFE) PROBE_V(V_LDEXP)
-        PROBE_V(V_AND_OR) PROBE_V(V_SUBREV) PROBE_V(V_CMP_CNDMASK) PROBE_V(V_CMP_CNDMASK_SGPR)
+        PROBE_V(V_AND_OR) PROBE_V(V_SUBREV) PROBE_V(V_CMP_CNDMASK) PROBE_V(V_CMP_CNDMASK_SGPR) PROBE_V(V_RNDNE)
         default: return -5;
     }
 #undef PROBE_V

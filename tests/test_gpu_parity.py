@@ -615,8 +615,9 @@ GEMM_PAIRS = [
     (F(4, 3), F(5, 0)),     # m = 0, TOP class
     (F(2, 1), F(2, 0)),     # m = 0, LOW class: the 3-bit accumulator
     (F(8, 3), F(8, 0)),     # m = 0, INT class
-    (F(5, 2), F(5, 10)),    # products fit the accumulator's significand: TOP class
-    (F(2, 1), F(4, 6)),     # products fit: LOW class
+    (F(5, 2), F(5, 10)),    # products fit the accumulator's significand: TOP class (rounded on its grid)
+    (F(2, 1), F(4, 6)),     # products fit: LOW class (rounded on its grid)
+    (F(7, 1), F(7, 3)),     # products fit, but the accumulator spans 129 binades: the compare-and-select rounding
     (F(8, 3), F(5, 10)),    # bf16-range inputs cannot be pre-scaled: one ldexp per product, TOP
     (F(8, 2), F(4, 3)),     # the same, LOW class
 ]
@@ -648,6 +649,65 @@ def test_lp_gemm_parity(dev, fin, facc, acc):
             ref = O.lp_gemm(Am, Bm, ofmt(fin), ofmt(facc), acc)
             g = got.cpu().numpy()
             assert same_f32(g, ref), (fin, facc, acc, M, N, K, specials, first_diff(g, ref))
+
+
+def _grid_edge_inputs(rng, M, K, N):
+    # 1-5-2 values whose products land at the edges of 1-5-10: its subnormal
+    # range (step 2^-24, products on and between the steps, halfway ties
+    # included), its smallest normal 2^-14, and its overflow at 2^16
+    sig = np.array([1.0, 1.25, 1.5, 1.75])
+
+    def vals(shape, lo, hi):
+        e = rng.integers(lo, hi + 1, shape)
+        return (rng.choice([-1.0, 1.0], shape) * rng.choice(sig, shape) * np.exp2(e)).astype(np.float32)
+
+    Am = vals((M, K), -14, 8)
+    Bm = vals((K, N), -14, 8)
+    # rows of A small and columns of B small: products around 2^-28 .. 2^-10;
+    # the other rows and columns large: products around 2^12 .. 2^17
+    Am[: M // 2] = vals((M // 2, K), -14, -5)
+    Bm[:, : N // 2] = vals((K, N // 2), -14, -5)
+    Am[M // 2:] = vals((M - M // 2, K), 5, 8)
+    Bm[:, N // 2:] = vals((K, N - N // 2), 5, 8)
+    return Am, Bm
+
+
+@pytest.mark.parametrize("acc", [A.APS_ACC_SEQUENTIAL, A.APS_ACC_KAHAN])
+def test_lp_gemm_product_grid_edges(dev, acc):
+    """1-5-2 inputs, a 1-5-10 accumulator: products rounded on the
+    accumulator's subnormal grid (ties to even), at its smallest normal, and
+    at its overflow with a partial sum of the other sign already there."""
+    fin, facc = F(5, 2), F(5, 10)
+    # hand-made chains of two products (row i of A with column i of B)
+    cases = [
+        ((1.75 * 2 ** 7, 2.0 ** 8), (-(2.0 ** 8), 2.0 ** 8)),         # -57344, then 2^16 overflows: INF
+        ((1.75 * 2 ** 7, 1.75 * 2 ** 7), (-(2.0 ** 8), 2.0 ** 8)),    # -57344 + 57344 = 0
+        ((1.25 * 2 ** -12, 1.5 * 2 ** -12), (2.0 ** -11, 2.0 ** -12)),  # 2.5 and 1.5 steps: ties to 2 and 2
+        ((2.0 ** -12, 1.5 * 2 ** -13), (2.0 ** -13, 2.0 ** -12)),     # 0.5 step (to 0), 0.75 step (to 1)
+        ((1.75 * 2 ** -8, 2.0 ** -7), (1.75 * 2 ** -8, 2.0 ** -7)),   # 784 steps, then 2^-14 itself
+        ((-1.25 * 2 ** -12, 2.0 ** -12), (2.0 ** -11, -(2.0 ** -13))),  # -2.5 steps (to -2), -0.5 (to -0)
+        ((2.0 ** 8, 1.5 * 2 ** -12), (-(2.0 ** 8), 2.0 ** -12)),      # overflow to -INF first, then a tiny one
+    ]
+    n = len(cases)
+    Am = np.zeros((n, 2), np.float32)
+    Bm = np.zeros((2, n), np.float32)
+    for i, (a, b) in enumerate(cases):
+        Am[i] = a
+        Bm[:, i] = b
+    rng = np.random.default_rng(1210 + acc)
+    for tag, (Ax, Bx) in (("hand-made", (Am, Bm)), ("random K=64", _grid_edge_inputs(rng, 96, 64, 80)),
+                          ("random K=300", _grid_edge_inputs(rng, 70, 300, 70))):
+        log(f"lp_gemm grid edges {tag} acc={acc}")
+        got = A.aps_lp_gemm(torch.from_numpy(Ax).to(dev), torch.from_numpy(Bx).to(dev), fin, facc, acc)
+        torch.cuda.synchronize()
+        ref = O.lp_gemm(Ax, Bx, ofmt(fin), ofmt(facc), acc)
+        g = got.cpu().numpy()
+        assert same_f32(g, ref), (tag, first_diff(g, ref))
+        if tag == "hand-made":
+            d = np.diag(ref)
+            assert d[0] == np.inf and d[1] == 0.0 and d[6] == -np.inf
+            assert d[2] == 4 * 2.0 ** -24 and d[3] == 2.0 ** -24 and d[4] == 784 * 2.0 ** -24 + 2.0 ** -14
+            assert d[5] == -2 * 2.0 ** -24
 
 
 @pytest.mark.parametrize("M,N", [(1 << 22, 3), (2, 1 << 22)])
