@@ -123,7 +123,8 @@ ROW_MODES = {"read": 0, "sum_f32": 1, "sum_half": 2, "sum_bytes": 3, "row_bytes"
 VALU_OPS = {"v_add_f32_e32": (0, 1), "v_mul_f32_e32": (1, 1), "v_and_b32_e32": (2, 1), "v_fma_f32": (3, 1),
             "v_add3_u32": (4, 1), "v_bfe_u32": (5, 1), "v_ldexp_f32": (6, 1), "v_and_or_b32": (7, 1),
             "v_subrev_f32_e32": (8, 1), "v_cmp_nle_f32_e32+v_cndmask_b32_e32 (VCC)": (9, 2),
-            "v_cmp_nle_f32_e64+v_cndmask_b32_e64 (SGPR mask)": (10, 2), "v_rndne_f32_e32": (11, 1)}
+            "v_cmp_nle_f32_e64+v_cndmask_b32_e64 (SGPR mask)": (10, 2), "v_rndne_f32_e32": (11, 1),
+            "v_pk_add_f16": (12, 1), "v_pk_mul_f16": (13, 1)}
 
 
 def ceilings(only: str | None = None, reps: int = 5) -> dict:
@@ -587,31 +588,40 @@ def cpu_baseline(G_t, gs, pal, budget_s: float, slice_cols: int = 65536, single_
 # the published 157.3 TFLOP/s fp32 vector rate counted one lane-instruction
 # per FMA.
 VALU_PEAK_T = 256 * 128 * 2.4e9 / 1e12
-# Issue rates of the instructions of k_lp_gemm's k-loop, lanes per clock per
-# CU at 2.4 GHz, measured by bench.py --ceilings (chains of one instruction,
-# profiles/ceilings_patterns_and_valu.txt): two-operand adds, multiplies and
-# ands issue at about 112-120, v_bfe_u32 / v_add3_u32 / v_and_or_b32 at about
-# 62, and a compare into VCC followed by the select that reads it at about
-# 81 per instruction (the hazard wait between them included).
-VALU_RATES = {"v_and_b32": 119.9, "v_add_f32": 112.0, "v_sub_f32": 117.5, "v_mul_f32": 116.9,
-              "v_bfe_u32": 62.3, "v_add3_u32": 62.4, "v_and_or_b32": 62.0, "v_cmp+v_cndmask": 80.8}
-# k_lp_gemm's k-loop for 1-5-2 inputs and a 1-5-10 accumulator (products fit
-# the accumulator's significand), VALU instructions per multiply-accumulate,
-# counted in the kernel's ISA (256 multiply-accumulates per loop iteration;
-# the loop also issues 32 ds_read_b128, the operands from LDS).
+# Issue rates of the instructions of the GEMM kernels' k-loops, lanes per
+# clock per CU at 2.4 GHz, measured by bench.py --ceilings (chains of one
+# instruction, profiles/ceilings_patterns_and_valu.txt): two-operand adds,
+# multiplies and ands issue at about 112-120; v_bfe_u32, v_add3_u32,
+# v_rndne_f32 and the packed half-precision v_pk_add_f16 / v_pk_mul_f16
+# (two lanes of work each) at about 62.
+VALU_RATES = {"v_and_b32": 119.7, "v_add_f32": 111.0, "v_sub_f32": 118.2, "v_mul_f32": 117.3,
+              "v_bfe_u32": 62.2, "v_add3_u32": 62.1, "v_rndne_f32": 62.7,
+              "v_pk_add_f16": 62.5, "v_pk_mul_f16": 62.2}
+# VALU instructions per multiply-accumulate of each k-loop, counted in the
+# kernels' ISA (one loop iteration: 16 k-steps of the thread's 4 x 4 outputs).
+#   k_lp_gemm_h (the accumulator is IEEE half): a packed multiply and a packed
+#     add per two outputs; Kahan four packed adds.  The loop also issues 16
+#     ds_read2_b64 (the operands from LDS).
+#   k_lp_gemm, products on the accumulator's subnormal grid (1-5-2 inputs into
+#     1-5-7): the product, its rint, the multiply into the working domain, the
+#     add and its rounding (v_bfe_u32, v_add3_u32, v_and_b32); Kahan rounds four
+#     adds.  The loop also issues 32 ds_read_b128.
 GEMM_LOOP_MIX = {
-    "sequential": {"v_and_b32": 2, "v_add_f32": 2, "v_mul_f32": 1, "v_sub_f32": 1, "v_and_or_b32": 1,
-                   "v_bfe_u32": 1, "v_add3_u32": 1, "v_cmp+v_cndmask": 2},
-    "kahan": {"v_and_b32": 5, "v_bfe_u32": 4, "v_add3_u32": 4, "v_sub_f32": 4, "v_add_f32": 2, "v_mul_f32": 1,
-              "v_and_or_b32": 1, "v_cmp+v_cndmask": 2},
+    "sequential": {"v_pk_mul_f16": 0.5, "v_pk_add_f16": 0.5},
+    "kahan": {"v_pk_mul_f16": 0.5, "v_pk_add_f16": 2.0},
+    "sequential_emulated": {"v_mul_f32": 2, "v_rndne_f32": 1, "v_add_f32": 1, "v_and_b32": 1, "v_bfe_u32": 1,
+                            "v_add3_u32": 1},
+    "kahan_emulated": {"v_mul_f32": 2, "v_rndne_f32": 1, "v_add_f32": 1, "v_sub_f32": 3, "v_and_b32": 4,
+                       "v_bfe_u32": 4, "v_add3_u32": 4},
 }
 GEMM_SHAPE = (4096, 1024, 4096)  # BERT-large FFN up-projection at 8 x 512 tokens: M, K, N
 
 
 def lp_gemm_calls(A, dev, reps: int = 5):
-    """Event-timed aps_lp_gemm on the BERT-large FFN shape, 1-5-2 inputs and
-    a 1-5-10 accumulator, plain and Kahan; an ALU roofline from the VALU
-    instructions the kernel issues per multiply-accumulate."""
+    """Event-timed aps_lp_gemm on the BERT-large FFN shape with 1-5-2 inputs:
+    a 1-5-10 accumulator (IEEE half: k_lp_gemm_h) and a 1-5-7 one (emulated
+    in fp32: k_lp_gemm), plain and Kahan; an ALU roofline from the VALU
+    instructions each kernel issues per multiply-accumulate."""
     import torch
 
     M, K, N = GEMM_SHAPE
@@ -619,9 +629,13 @@ def lp_gemm_calls(A, dev, reps: int = 5):
     Am = torch.randn((M, K), generator=g, device=dev)
     Bm = torch.randn((K, N), generator=g, device=dev) * 0.02
     C = torch.empty((M, N), device=dev)
-    fin, facc = A.Format(5, 2), A.Format(5, 10)
-    res = {"workload": f"bert_large_ffn M={M} K={K} N={N}", "in": str(fin), "acc": str(facc)}
-    for name, acc in (("sequential", A.APS_ACC_SEQUENTIAL), ("kahan", A.APS_ACC_KAHAN)):
+    fin = A.Format(5, 2)
+    res = {"workload": f"bert_large_ffn M={M} K={K} N={N}", "in": str(fin)}
+    cases = (("sequential", A.APS_ACC_SEQUENTIAL, A.Format(5, 10), "k_lp_gemm_h"),
+             ("kahan", A.APS_ACC_KAHAN, A.Format(5, 10), "k_lp_gemm_h"),
+             ("sequential_emulated", A.APS_ACC_SEQUENTIAL, A.Format(5, 7), "k_lp_gemm"),
+             ("kahan_emulated", A.APS_ACC_KAHAN, A.Format(5, 7), "k_lp_gemm"))
+    for name, acc, facc, kernel in cases:
         A.aps_lp_gemm(Am, Bm, fin, facc, acc, C=C)
         torch.cuda.synchronize()
         ts = []
@@ -641,7 +655,7 @@ def lp_gemm_calls(A, dev, reps: int = 5):
         # their measured rates, back to back
         clk_per_lane_mac = sum(k / VALU_RATES[op] for op, k in mix.items())
         ceiling = 256 * 2.4e9 / clk_per_lane_mac
-        res[name] = {"ms": t, "MAC_per_s": macs / (t * 1e-3),
+        res[name] = {"acc": str(facc), "kernel": kernel, "ms": t, "MAC_per_s": macs / (t * 1e-3),
                      "roofline": {"bound": "alu", "achieved": achieved, "peak": VALU_PEAK_T,
                                   "unit": "T VALU lane-instructions/s", "frac": achieved / VALU_PEAK_T,
                                   "valu_per_mac": instr, "mix_ceiling_MAC_per_s": ceiling,

@@ -157,6 +157,147 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
     }
 }
 
+// ===================================== K6h: the accumulator is IEEE half
+//
+// When the accumulator is the half-precision format (e = 5, m = 10, bias
+// 15) and every input value is a half, the hardware's half-precision
+// multiply and add are the emulated unit: each rounds its exact result to
+// nearest even, with subnormals and overflow to INF, as the format does.
+// So the products and the chain run in packed halves, one multiply and one
+// add (Kahan: one multiply, four adds) per two outputs, with no bit
+// manipulation.  Nothing may fuse a multiply with the add that follows it.
+
+using h2 = _Float16 __attribute__((ext_vector_type(2)));
+
+constexpr int HT = 4;         // outputs per thread along each side: HT x HT
+constexpr int HGT = 16 * HT;  // output tile HGT x HGT per block (16 x 16 threads)
+constexpr int HGK = 16;       // k-tile staged in LDS
+constexpr int HST = HGT * HGK / BLOCK;  // staged values of A (and of B) per thread and k-tile
+
+template <int N>
+struct HVec {
+    using T = _Float16 __attribute__((ext_vector_type(N)));
+};
+
+template <bool KAHAN, int VI>
+__global__ __launch_bounds__(BLOCK) void k_lp_gemm_h(GemmArgs g, FmtK fi) {
+#pragma clang fp contract(off)
+    using hv = typename HVec<HT>::T;
+    __shared__ __align__(16) _Float16 As[HGK][HGT + 8];  // As[k][m]; the pad spreads the staging writes over banks
+    __shared__ __align__(16) _Float16 Bs[HGK][HGT + 8];  // Bs[k][n]
+    const int t = threadIdx.x;
+    const int tx = t & 15, ty = t >> 4;
+    for (int64_t tile = blockIdx.x; tile < g.tiles; tile += gridDim.x) {
+        const int64_t m0 = tile / g.ntn * HGT, n0 = tile % g.ntn * HGT;
+        // output (ty*HT + i, tx*HT + 2*h + e) is element e of s[i][h]
+        h2 s[HT][HT / 2], c[HT][HT / 2];
+#pragma unroll
+        for (int i = 0; i < HT; ++i)
+#pragma unroll
+            for (int h = 0; h < HT / 2; ++h) {
+                s[i][h] = h2{0, 0};
+                c[i][h] = h2{0, 0};
+            }
+        _Float16 ra[HST], rb[HST];
+        // global -> registers, cast to the input format (a half, exactly); outside A and B: 0.
+        // Every load reads an address inside the matrix, so no lane branches.
+        auto fetch = [&](int64_t k0) {
+#pragma unroll
+            for (int r = 0; r < HST; ++r) {
+                const int idx = t + BLOCK * r;
+                const int64_t am = m0 + idx / HGK, ak = k0 + idx % HGK;
+                const bool oka = am < g.M && ak < g.K;
+                const _Float16 qa = (_Float16)quant_native<VI>(g.A[oka ? am * g.lda + ak : 0], fi.k, fi);
+                ra[r] = oka ? qa : (_Float16)0.0f;
+                const int64_t bk = k0 + idx / HGT, bn = n0 + idx % HGT;
+                const bool okb = bk < g.K && bn < g.N;
+                const _Float16 qb = (_Float16)quant_native<VI>(g.B[okb ? bk * g.ldb + bn : 0], fi.k, fi);
+                rb[r] = okb ? qb : (_Float16)0.0f;
+            }
+        };
+        auto step_v = [&](const hv& av, const hv& bv, bool first) {
+#pragma unroll
+            for (int i = 0; i < HT; ++i) {
+                const h2 a = h2{av[i], av[i]};
+                h2 p[HT / 2];
+#pragma unroll
+                for (int h = 0; h < HT / 2; ++h) p[h] = a * h2{bv[2 * h], bv[2 * h + 1]};  // rounded to half
+                if (first) {
+#pragma unroll
+                    for (int h = 0; h < HT / 2; ++h) s[i][h] = p[h];  // a chain starts with its first product
+                } else if constexpr (KAHAN) {
+                    // each phase over the row's chains in turn, so that no add waits on the one before it
+                    h2 y[HT / 2], tt[HT / 2];
+#pragma unroll
+                    for (int h = 0; h < HT / 2; ++h) y[h] = p[h] - c[i][h];
+#pragma unroll
+                    for (int h = 0; h < HT / 2; ++h) tt[h] = s[i][h] + y[h];
+#pragma unroll
+                    for (int h = 0; h < HT / 2; ++h) c[i][h] = tt[h] - s[i][h];
+#pragma unroll
+                    for (int h = 0; h < HT / 2; ++h) {
+                        c[i][h] = c[i][h] - y[h];
+                        s[i][h] = tt[h];
+                    }
+                } else {
+#pragma unroll
+                    for (int h = 0; h < HT / 2; ++h) s[i][h] = s[i][h] + p[h];
+                }
+            }
+        };
+        auto step = [&](int kk, bool first) {
+            step_v(*(const hv*)&As[kk][ty * HT], *(const hv*)&Bs[kk][tx * HT], first);
+        };
+        if (g.K > 0) fetch(0);
+        for (int64_t k0 = 0; k0 < g.K; k0 += HGK) {
+            __syncthreads();  // the previous k-tile is consumed
+#pragma unroll
+            for (int r = 0; r < HST; ++r) {
+                const int idx = t + BLOCK * r;
+                As[idx % HGK][idx / HGK] = ra[r];
+                Bs[idx / HGT][idx % HGT] = rb[r];
+            }
+            __syncthreads();
+            if (k0 + HGK < g.K) fetch(k0 + HGK);  // the next k-tile's loads overlap this tile's math
+            const int kend = (int)min((int64_t)HGK, g.K - k0);
+            if (k0 > 0 && kend == HGK) {
+                // software-pipelined: step kk+1's LDS reads are issued before step kk's math
+                hv av = *(const hv*)&As[0][ty * HT], bv = *(const hv*)&Bs[0][tx * HT];
+#pragma unroll
+                for (int kk = 0; kk < HGK; ++kk) {
+                    hv an = av, bn = bv;
+                    if (kk + 1 < HGK) {
+                        an = *(const hv*)&As[kk + 1][ty * HT];
+                        bn = *(const hv*)&Bs[kk + 1][tx * HT];
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                    step_v(av, bv, false);
+                    av = an;
+                    bv = bn;
+                }
+            } else {
+                int kk = 0;
+                if (k0 == 0) {
+                    step(0, true);
+                    kk = 1;
+                }
+#pragma unroll 1
+                for (; kk < kend; ++kk) step(kk, false);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < HT; ++i) {
+            const int64_t m = m0 + ty * HT + i;
+            if (m >= g.M) continue;
+#pragma unroll
+            for (int j = 0; j < HT; ++j) {
+                const int64_t n = n0 + tx * HT + j;
+                if (n < g.N) g.C[m * g.ldc + n] = (float)s[i][j >> 1][j & 1];
+            }
+        }
+    }
+}
+
 }  // namespace aps
 
 using namespace aps;
@@ -250,6 +391,30 @@ extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t 
         }
     }
     const dim3 grid((unsigned)std::min<int64_t>(g.tiles, INT32_MAX));
+    // the accumulator is IEEE half and every input value a half (at most 10
+    // mantissa bits, at most 2^15 and no finer than half's step 2^-24); such
+    // an input format is of class TOP or LOW
+    const bool half_acc = acc_fmt.e == 5 && acc_fmt.m == 10 && acc_fmt.bias == 15;
+    if (half_acc && in_fmt.m <= 10 && fi.emax <= 15 && fi.emin - in_fmt.m >= -24) {
+        const int64_t hmt = (M + HGT - 1) / HGT, hnt = (N + HGT - 1) / HGT;
+        g.tiles = hmt * hnt;
+        g.ntn = (int32_t)hnt;
+        const dim3 hgrid((unsigned)std::min<int64_t>(g.tiles, INT32_MAX));
+        const hipStream_t hs = (hipStream_t)stream;
+        const bool kh = accumulator == APS_ACC_KAHAN;
+#define APS_HK(VI)                                                                          \
+    if (fi.variant == (VI)) {                                                              \
+        if (kh)                                                                            \
+            hipLaunchKernelGGL((k_lp_gemm_h<true, VI>), hgrid, dim3(BLOCK), 0, hs, g, fi);  \
+        else                                                                               \
+            hipLaunchKernelGGL((k_lp_gemm_h<false, VI>), hgrid, dim3(BLOCK), 0, hs, g, fi); \
+        return launched();                                                                 \
+    }
+        APS_HK(V_TOP_F32) APS_HK(V_TOP_M0) APS_HK(V_LOW_F32) APS_HK(V_LOW_M0)
+#undef APS_HK
+        g.tiles = mt * nt;  // another input class: the emulated kernel
+        g.ntn = (int32_t)nt;
+    }
     launch_lp_gemm(fa.variant, accumulator == APS_ACC_KAHAN, pm, grid, (hipStream_t)stream, g, fi, fa);
     return launched();
 }

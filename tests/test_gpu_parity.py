@@ -615,8 +615,10 @@ GEMM_PAIRS = [
     (F(4, 3), F(5, 0)),     # m = 0, TOP class
     (F(2, 1), F(2, 0)),     # m = 0, LOW class: the 3-bit accumulator
     (F(8, 3), F(8, 0)),     # m = 0, INT class
-    (F(5, 2), F(5, 10)),    # products fit the accumulator's significand: TOP class (rounded on its grid)
+    (F(5, 2), F(5, 10)),    # the accumulator is IEEE half: the hardware's half-precision arithmetic
+    (F(4, 2), F(5, 9)),     # products fit the accumulator's significand: TOP class (rounded on its grid)
     (F(2, 1), F(4, 6)),     # products fit: LOW class (rounded on its grid)
+    (F(5, 2, 14), F(5, 10, 13)),  # 1-5-10 with another bias: not half, rounded on its grid
     (F(7, 1), F(7, 3)),     # products fit, but the accumulator spans 129 binades: the compare-and-select rounding
     (F(8, 3), F(5, 10)),    # bf16-range inputs cannot be pre-scaled: one ldexp per product, TOP
     (F(8, 2), F(4, 3)),     # the same, LOW class
@@ -672,12 +674,16 @@ def _grid_edge_inputs(rng, M, K, N):
     return Am, Bm
 
 
+@pytest.mark.parametrize("shift", [0, 1], ids=["half", "bias-shifted"])
 @pytest.mark.parametrize("acc", [A.APS_ACC_SEQUENTIAL, A.APS_ACC_KAHAN])
-def test_lp_gemm_product_grid_edges(dev, acc):
+def test_lp_gemm_product_grid_edges(dev, acc, shift):
     """1-5-2 inputs, a 1-5-10 accumulator: products rounded on the
     accumulator's subnormal grid (ties to even), at its smallest normal, and
-    at its overflow with a partial sum of the other sign already there."""
-    fin, facc = F(5, 2), F(5, 10)
+    at its overflow with a partial sum of the other sign already there.  With
+    shift 1 every input is doubled and both biases lowered by one and two:
+    the same chains at 4 times the scale, in formats that are not IEEE half
+    (the kernel rounds them on the grid instead of in half precision)."""
+    fin, facc = F(5, 2, 15 - shift), F(5, 10, 15 - 2 * shift)
     # hand-made chains of two products (row i of A with column i of B)
     cases = [
         ((1.75 * 2 ** 7, 2.0 ** 8), (-(2.0 ** 8), 2.0 ** 8)),         # -57344, then 2^16 overflows: INF
@@ -698,23 +704,25 @@ def test_lp_gemm_product_grid_edges(dev, acc):
     for tag, (Ax, Bx) in (("hand-made", (Am, Bm)), ("random K=64", _grid_edge_inputs(rng, 96, 64, 80)),
                           ("random K=300", _grid_edge_inputs(rng, 70, 300, 70))):
         log(f"lp_gemm grid edges {tag} acc={acc}")
+        Ax, Bx = Ax * np.float32(2 ** shift), Bx * np.float32(2 ** shift)
         got = A.aps_lp_gemm(torch.from_numpy(Ax).to(dev), torch.from_numpy(Bx).to(dev), fin, facc, acc)
         torch.cuda.synchronize()
         ref = O.lp_gemm(Ax, Bx, ofmt(fin), ofmt(facc), acc)
         g = got.cpu().numpy()
         assert same_f32(g, ref), (tag, first_diff(g, ref))
         if tag == "hand-made":
-            d = np.diag(ref)
+            d = np.diag(ref) / 4.0 ** shift
             assert d[0] == np.inf and d[1] == 0.0 and d[6] == -np.inf
             assert d[2] == 4 * 2.0 ** -24 and d[3] == 2.0 ** -24 and d[4] == 784 * 2.0 ** -24 + 2.0 ** -14
             assert d[5] == -2 * 2.0 ** -24
 
 
+@pytest.mark.parametrize("fin,facc", [(F(5, 2), F(5, 10)), (F(4, 3), F(5, 2))], ids=["half", "emulated"])
 @pytest.mark.parametrize("M,N", [(1 << 22, 3), (2, 1 << 22)])
-def test_lp_gemm_largest_dimensions(dev, M, N):
-    """M or N at APS_MAX_GEMM_DIM = 2^22: 65536 tiles along one dimension."""
+def test_lp_gemm_largest_dimensions(dev, M, N, fin, facc):
+    """M or N at APS_MAX_GEMM_DIM = 2^22: 65536 tiles along one dimension,
+    in both GEMM kernels (half-precision accumulator, and the emulated one)."""
     rng = np.random.default_rng(977 + M % 7)
-    fin, facc = F(5, 2), F(5, 10)
     Am, Bm = _gemm_inputs(rng, M, N, 2, fin)
     got = A.aps_lp_gemm(torch.from_numpy(Am).to(dev), torch.from_numpy(Bm).to(dev), fin, facc)
     torch.cuda.synchronize()
@@ -723,10 +731,10 @@ def test_lp_gemm_largest_dimensions(dev, M, N):
     assert same_f32(g, ref), first_diff(g, ref)
 
 
-def test_lp_gemm_strided_views(dev):
+@pytest.mark.parametrize("fin,facc", [(F(5, 2), F(5, 10)), (F(4, 3), F(5, 2))], ids=["half", "emulated"])
+def test_lp_gemm_strided_views(dev, fin, facc):
     # row strides from the tensors (leading dimensions larger than the width)
     rng = np.random.default_rng(950)
-    fin, facc = F(4, 3), F(5, 2)
     Abig = rng.standard_normal((40, 100)).astype(np.float32)
     Bbig = rng.standard_normal((77, 90)).astype(np.float32)
     At = torch.from_numpy(Abig).to(dev)[:, 3:80]
@@ -762,7 +770,7 @@ def test_lp_gemm_bert_ffn_sampled(dev, acc):
     assert same_f32(g[:, cols], ref_c), first_diff(g[:, cols], ref_c)
 
 
-@pytest.mark.parametrize("f", [F(3, 0), F(5, 0), F(8, 0), F(5, 2)], ids=str)
+@pytest.mark.parametrize("f", [F(3, 0), F(5, 0), F(8, 0), F(5, 2), F(5, 10)], ids=str)
 def test_kahan_compensation_nan_does_not_reach_the_sum(dev, f):
     # s = INF, then x = 1: t = INF, but the compensation R(R(t - s) - y) is
     # NaN; the sum itself stays INF (m = 0 formats included)
