@@ -594,9 +594,9 @@ VALU_PEAK_T = 256 * 128 * 2.4e9 / 1e12
 # multiplies and ands issue at about 112-120; v_bfe_u32, v_add3_u32,
 # v_rndne_f32 and the packed half-precision v_pk_add_f16 / v_pk_mul_f16
 # (two lanes of work each) at about 62.
-VALU_RATES = {"v_and_b32": 119.7, "v_add_f32": 111.0, "v_sub_f32": 118.2, "v_mul_f32": 117.3,
-              "v_bfe_u32": 62.2, "v_add3_u32": 62.1, "v_rndne_f32": 62.7,
-              "v_pk_add_f16": 62.5, "v_pk_mul_f16": 62.2}
+VALU_RATES = {"v_and_b32": 119.3, "v_add_f32": 112.7, "v_sub_f32": 118.5, "v_mul_f32": 116.6,
+              "v_bfe_u32": 62.1, "v_add3_u32": 62.2, "v_rndne_f32": 62.7,
+              "v_pk_add_f16": 62.2, "v_pk_mul_f16": 62.0}
 # VALU instructions per multiply-accumulate of each k-loop, counted in the
 # kernels' ISA (one loop iteration: 16 k-steps of the thread's 4 x 4 outputs).
 #   k_lp_gemm_h (the accumulator is IEEE half): a packed multiply and a packed
