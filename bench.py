@@ -41,11 +41,12 @@ KERNEL_SOURCES = sorted(glob.glob(os.path.join(ROOT, "paper_1911_08907_amd", "cs
                         + glob.glob(os.path.join(ROOT, "paper_1911_08907_amd", "csrc", "*.hpp")))
 
 
-def source_digest() -> str:
-    """Digest of the kernel sources' code: comments and whitespace are
-    dropped, so a change to a comment does not count as a kernel change."""
+def source_digest(paths=None) -> str:
+    """Digest of the kernel sources' code (all of them, or the given files,
+    relative to the repository): comments and whitespace are dropped, so a
+    change to a comment does not count as a kernel change."""
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in (KERNEL_SOURCES if paths is None else [os.path.join(ROOT, q) for q in paths]):
         with open(p) as fh:
             txt = fh.read()
         txt = re.sub(r"/\*.*?\*/", " ", txt, flags=re.S)
@@ -303,7 +304,8 @@ def traffic_from_profile(kernel: str, config: str, palette: str):
         return None, "no counter summary"
     with open(path) as fh:
         c = json.load(fh)
-    if c.get("source_digest") != source_digest():
+    # the digest covers the files the kernel is compiled from, as the summary lists them
+    if c.get("source_digest") != source_digest(c.get("sources")):
         return None, "kernel changed since the counters were taken"
     fetch = c["fetch_kib_per_dispatch"] * 1024 * c["fetch_scale"]
     write = c["write_kib_per_dispatch"] * 1024 * c["write_scale"]

@@ -54,3 +54,29 @@ def test_bench_json_line():
     assert cb["kind"] == "oracle" and cb["unit"] == "elements/s"
     assert cb["value"] > 0 and cb["cores"] >= 1 and cb["sample"]
     assert cb["cpu_model"] and "physical_cores" in cb and "logical_cpus" in cb
+
+
+def test_counter_summary_is_tied_to_its_kernel_sources(tmp_path, monkeypatch):
+    # the HBM bytes of a counter summary count only while the files it names
+    # are unchanged (comments aside)
+    import json as _json
+
+    sys.path.insert(0, ROOT)
+    import bench
+
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    src = ["paper_1911_08907_amd/csrc/aps_sync.hip", "include/aps.h"]
+    summary = {"fetch_kib_per_dispatch": 3.0, "write_kib_per_dispatch": 5.0, "fetch_scale": 2.0,
+               "write_scale": 1.0, "sources": src, "source_digest": bench.source_digest(src)}
+    path = tmp_path / "sync_spec_demo_1-5-2_counters.json"
+    path.write_text(_json.dumps(summary))
+    got, where = bench.traffic_from_profile("sync_spec", "demo", "1-5-2")
+    assert got == (3.0 * 2.0 + 5.0) * 1024 and where.endswith("_counters.json")
+    summary["source_digest"] = "0" * 16
+    path.write_text(_json.dumps(summary))
+    assert bench.traffic_from_profile("sync_spec", "demo", "1-5-2") == (None, "kernel changed since the counters were taken")
+    assert bench.traffic_from_profile("sync_spec", "other", "1-5-2") == (None, "no counter summary")
+    # the committed summary of the dominant kernel names the files it was taken on
+    with open(os.path.join(ROOT, "profiles", "sync_spec_resnet50_w256_1-5-2_counters.json")) as fh:
+        committed = _json.load(fh)
+    assert "paper_1911_08907_amd/csrc/aps_sync.hip" in committed["sources"]
