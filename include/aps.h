@@ -394,6 +394,9 @@ int aps_dequantize(const float* Q, const void* codes, int64_t n,
  * rounded in fp64 (see aps_format_supported), return APS_ERR_UNSUPPORTED.
  * M, N, K in [0, 2^22]; lda >= K, ldb >= N,
  * ldc >= N; A and B may be NULL when K = 0 or M * N = 0.
+ * When acc_fmt is IEEE half (e = 5, m = 10, bias 15) and every in_fmt value
+ * is a half, the products and adds run on the GPU's half-precision
+ * arithmetic, which rounds exactly as above: the results are the same.
  */
 #define APS_MAX_GEMM_DIM (1 << 22)
 int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t ldb, float* C, int64_t ldc,
