@@ -199,9 +199,22 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm_h(GemmArgs g, FmtK fi) {
                 c[i][h] = h2{0, 0};
             }
         _Float16 ra[HST], rb[HST];
+        // Staged value r of this thread: A[m0 + t/HGK + r*BLOCK/HGK][k0 + t%HGK] and
+        // B[k0 + t/HGT + r*BLOCK/HGT][n0 + t%HGT].
+        const bool inner = m0 + HGT <= g.M && n0 + HGT <= g.N;  // the tile lies inside C
+        const float* __restrict__ pa = g.A + (m0 + t / HGK) * g.lda + t % HGK;
+        const float* __restrict__ pb = g.B + (int64_t)(t / HGT) * g.ldb + n0 + t % HGT;
         // global -> registers, cast to the input format (a half, exactly); outside A and B: 0.
         // Every load reads an address inside the matrix, so no lane branches.
         auto fetch = [&](int64_t k0) {
+            if (inner && k0 + HGK <= g.K) {  // the whole k-tile inside A and B: no checks
+#pragma unroll
+                for (int r = 0; r < HST; ++r) {
+                    ra[r] = (_Float16)quant_native<VI>(pa[r * (BLOCK / HGK) * g.lda + k0], fi.k, fi);
+                    rb[r] = (_Float16)quant_native<VI>(pb[(k0 + r * (BLOCK / HGT)) * g.ldb], fi.k, fi);
+                }
+                return;
+            }
 #pragma unroll
             for (int r = 0; r < HST; ++r) {
                 const int idx = t + BLOCK * r;
