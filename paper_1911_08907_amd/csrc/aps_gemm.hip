@@ -68,8 +68,20 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
                 bad[i][j] = false;
             }
         float ra[4], rb[4];
+        // Staged value r of this thread: A[m0 + t/16 + 16r][k0 + t%16] and B[k0 + t/64 + 4r][n0 + t%64].
+        const bool inner = m0 + GT <= g.M && n0 + GT <= g.N;  // the tile lies inside C
+        const float* __restrict__ pa = g.A + (m0 + (t >> 4)) * g.lda + (t & 15);
+        const float* __restrict__ pb = g.B + (int64_t)(t >> 6) * g.ldb + n0 + (t & 63);
         // global -> registers, cast to the input format; outside A and B: 0
         auto fetch = [&](int64_t k0) {
+            if (inner && k0 + GK <= g.K) {  // the whole k-tile inside A and B: no checks
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    ra[r] = __builtin_amdgcn_ldexpf(quant_any(pa[r * 16 * g.lda + k0], fi.k, fi), g.ka);
+                    rb[r] = __builtin_amdgcn_ldexpf(quant_any(pb[(k0 + 4 * r) * g.ldb], fi.k, fi), g.kb);
+                }
+                return;
+            }
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int idx = t + BLOCK * r;
