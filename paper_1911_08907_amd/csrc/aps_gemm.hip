@@ -70,15 +70,15 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
         float ra[4], rb[4];
         // Staged value r of this thread: A[m0 + t/16 + 16r][k0 + t%16] and B[k0 + t/64 + 4r][n0 + t%64].
         const bool inner = m0 + GT <= g.M && n0 + GT <= g.N;  // the tile lies inside C
-        const float* __restrict__ pa = g.A + (m0 + (t >> 4)) * g.lda + (t & 15);
-        const float* __restrict__ pb = g.B + (int64_t)(t >> 6) * g.ldb + n0 + (t & 63);
+        const int64_t oa = (m0 + (t >> 4)) * g.lda + (t & 15);  // offsets of value 0 in A and B
+        const int64_t ob = (int64_t)(t >> 6) * g.ldb + n0 + (t & 63);
         // global -> registers, cast to the input format; outside A and B: 0
         auto fetch = [&](int64_t k0) {
             if (inner && k0 + GK <= g.K) {  // the whole k-tile inside A and B: no checks
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    ra[r] = __builtin_amdgcn_ldexpf(quant_any(pa[r * 16 * g.lda + k0], fi.k, fi), g.ka);
-                    rb[r] = __builtin_amdgcn_ldexpf(quant_any(pb[(k0 + 4 * r) * g.ldb], fi.k, fi), g.kb);
+                    ra[r] = __builtin_amdgcn_ldexpf(quant_any(g.A[oa + r * 16 * g.lda + k0], fi.k, fi), g.ka);
+                    rb[r] = __builtin_amdgcn_ldexpf(quant_any(g.B[ob + (k0 + 4 * r) * g.ldb], fi.k, fi), g.kb);
                 }
                 return;
             }
@@ -214,16 +214,16 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm_h(GemmArgs g, FmtK fi) {
         // Staged value r of this thread: A[m0 + t/HGK + r*BLOCK/HGK][k0 + t%HGK] and
         // B[k0 + t/HGT + r*BLOCK/HGT][n0 + t%HGT].
         const bool inner = m0 + HGT <= g.M && n0 + HGT <= g.N;  // the tile lies inside C
-        const float* __restrict__ pa = g.A + (m0 + t / HGK) * g.lda + t % HGK;
-        const float* __restrict__ pb = g.B + (int64_t)(t / HGT) * g.ldb + n0 + t % HGT;
+        const int64_t oa = (m0 + t / HGK) * g.lda + t % HGK;  // offsets of value 0 in A and B
+        const int64_t ob = (int64_t)(t / HGT) * g.ldb + n0 + t % HGT;
         // global -> registers, cast to the input format (a half, exactly); outside A and B: 0.
         // Every load reads an address inside the matrix, so no lane branches.
         auto fetch = [&](int64_t k0) {
             if (inner && k0 + HGK <= g.K) {  // the whole k-tile inside A and B: no checks
 #pragma unroll
                 for (int r = 0; r < HST; ++r) {
-                    ra[r] = (_Float16)quant_native<VI>(pa[r * (BLOCK / HGK) * g.lda + k0], fi.k, fi);
-                    rb[r] = (_Float16)quant_native<VI>(pb[(k0 + r * (BLOCK / HGT)) * g.ldb], fi.k, fi);
+                    ra[r] = (_Float16)quant_native<VI>(g.A[oa + r * (BLOCK / HGK) * g.lda + k0], fi.k, fi);
+                    rb[r] = (_Float16)quant_native<VI>(g.B[ob + (k0 + r * (BLOCK / HGT)) * g.ldb], fi.k, fi);
                 }
                 return;
             }
