@@ -608,6 +608,8 @@ VALU_RATES = {"v_and_b32": 119.3, "v_add_f32": 112.7, "v_sub_f32": 118.5, "v_mul
 #     1-5-7): the product, its rint, the multiply into the working domain, the
 #     add and its rounding (v_bfe_u32, v_add3_u32, v_and_b32); Kahan rounds four
 #     adds.  The loop also issues 32 ds_read_b128.
+#   k_lp_gemm, exact products (1-5-2 inputs into bfloat16, 1-8-7: every product
+#     fits and none is subnormal): the product, the add and its rounding.
 GEMM_LOOP_MIX = {
     "sequential": {"v_pk_mul_f16": 0.5, "v_pk_add_f16": 0.5},
     "kahan": {"v_pk_mul_f16": 0.5, "v_pk_add_f16": 2.0},
@@ -615,15 +617,19 @@ GEMM_LOOP_MIX = {
                             "v_add3_u32": 1},
     "kahan_emulated": {"v_mul_f32": 2, "v_rndne_f32": 1, "v_add_f32": 1, "v_sub_f32": 3, "v_and_b32": 4,
                        "v_bfe_u32": 4, "v_add3_u32": 4},
+    "sequential_bf16": {"v_mul_f32": 1, "v_add_f32": 1, "v_and_b32": 1, "v_bfe_u32": 1, "v_add3_u32": 1},
+    "kahan_bf16": {"v_mul_f32": 1, "v_add_f32": 1, "v_sub_f32": 3, "v_and_b32": 4, "v_bfe_u32": 4,
+                   "v_add3_u32": 4},
 }
 GEMM_SHAPE = (4096, 1024, 4096)  # BERT-large FFN up-projection at 8 x 512 tokens: M, K, N
 
 
 def lp_gemm_calls(A, dev, reps: int = 5):
     """Event-timed aps_lp_gemm on the BERT-large FFN shape with 1-5-2 inputs:
-    a 1-5-10 accumulator (IEEE half: k_lp_gemm_h) and a 1-5-7 one (emulated
-    in fp32: k_lp_gemm), plain and Kahan; an ALU roofline from the VALU
-    instructions each kernel issues per multiply-accumulate."""
+    a 1-5-10 accumulator (IEEE half: k_lp_gemm_h), a 1-5-7 one and a
+    bfloat16 one (emulated in fp32: k_lp_gemm), plain and Kahan; an ALU
+    roofline from the VALU instructions each kernel issues per
+    multiply-accumulate."""
     import torch
 
     M, K, N = GEMM_SHAPE
@@ -636,7 +642,9 @@ def lp_gemm_calls(A, dev, reps: int = 5):
     cases = (("sequential", A.APS_ACC_SEQUENTIAL, A.Format(5, 10), "k_lp_gemm_h"),
              ("kahan", A.APS_ACC_KAHAN, A.Format(5, 10), "k_lp_gemm_h"),
              ("sequential_emulated", A.APS_ACC_SEQUENTIAL, A.Format(5, 7), "k_lp_gemm"),
-             ("kahan_emulated", A.APS_ACC_KAHAN, A.Format(5, 7), "k_lp_gemm"))
+             ("kahan_emulated", A.APS_ACC_KAHAN, A.Format(5, 7), "k_lp_gemm"),
+             ("sequential_bf16", A.APS_ACC_SEQUENTIAL, A.Format(8, 7), "k_lp_gemm"),
+             ("kahan_bf16", A.APS_ACC_KAHAN, A.Format(8, 7), "k_lp_gemm"))
     for name, acc, facc, kernel in cases:
         A.aps_lp_gemm(Am, Bm, fin, facc, acc, C=C)
         torch.cuda.synchronize()

@@ -24,7 +24,14 @@ enum GemmProduct {
     GP_SCALED = 1,  // operands pre-scaled at staging: a_w * b_w rounded (quant_w)
     GP_FIT = 2,     // pre-scaled, and every product fits the significand (quant_fit)
     GP_GRID = 3,    // as GP_FIT, staged so that the subnormal step is 1: rint, then 2^Q
+    GP_EXACT = 4,   // pre-scaled, every product fits and none reaches the subnormal range: no rounding
 };
+
+// GP_EXACT.  When every product of two input values fits the accumulator's
+// significand and no nonzero product lies below 2^emin (the square of the
+// input's smallest subnormal is at least 2^emin), every product is already
+// a format value, or beyond the largest one, where the working domain makes
+// it INF as fp32 does: the exact fp32 product is its own rounding.
 
 // GP_GRID.  A product of two input values that fits the accumulator's
 // significand is, from 2^emin up, already a multiple of the accumulator's
@@ -108,8 +115,10 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
                         p = quant_w<V>(a[i] * b[j], fa, bad[i][j]);
                     else if constexpr (PM == GP_FIT)
                         p = quant_fit<V>(a[i] * b[j], fa);
-                    else
+                    else if constexpr (PM == GP_GRID)
                         p = __builtin_rintf(a[i] * b[j]) * g.qs;
+                    else
+                        p = a[i] * b[j];
                     if (first)
                         s[i][j] = p;
                     else
@@ -332,7 +341,14 @@ static void launch_lp_gemm_v(bool kahan, int pm, dim3 grid, hipStream_t s, const
                              const FmtK& fa) {
     constexpr bool can_fit = (VT<V>::cls == CLS_TOP || VT<V>::cls == CLS_LOW) && !VT<V>::m0;
     constexpr bool can_ldexp = VT<V>::cls == CLS_TOP || VT<V>::cls == CLS_LOW;
+    constexpr bool can_exact = VT<V>::cls != CLS_GEN && !VT<V>::m0;
 #define APS_G(K, P) hipLaunchKernelGGL((k_lp_gemm<V, K, P>), grid, dim3(BLOCK), 0, s, g, fi, fa)
+    if (pm == GP_EXACT) {
+        if constexpr (can_exact) {
+            if (kahan) APS_G(true, GP_EXACT); else APS_G(false, GP_EXACT);
+            return;
+        }
+    }
     if (pm == GP_GRID) {
         if constexpr (can_fit) {
             if (kahan) APS_G(true, GP_GRID); else APS_G(false, GP_GRID);
@@ -414,6 +430,16 @@ extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t 
             g.qs = pow2f_host(q);
             pm = GP_GRID;
         }
+    }
+    if (pm != GP_LDEXP && acc_fmt.m > 0 && 2 * (in_fmt.m + 1) <= acc_fmt.m + 1 &&
+        2 * (fi.emin - in_fmt.m) >= fa.emin) {
+        // products staged in the working domain (ka + kb = k, both >= 0, so
+        // every staged value stays exact), each one fits and none is
+        // subnormal in the accumulator: GP_EXACT
+        g.ka = fa.k < room ? fa.k : room;
+        g.kb = fa.k - g.ka;
+        g.qs = 1.0f;
+        pm = GP_EXACT;
     }
     const dim3 grid((unsigned)std::min<int64_t>(g.tiles, INT32_MAX));
     // the accumulator is IEEE half and every input value a half (at most 10

@@ -617,7 +617,10 @@ GEMM_PAIRS = [
     (F(8, 3), F(8, 0)),     # m = 0, INT class
     (F(5, 2), F(5, 10)),    # the accumulator is IEEE half: the hardware's half-precision arithmetic
     (F(4, 2), F(5, 9)),     # products fit the accumulator's significand: TOP class (rounded on its grid)
-    (F(2, 1), F(4, 6)),     # products fit: LOW class (rounded on its grid)
+    (F(4, 1), F(4, 6)),     # products fit: LOW class (rounded on its grid)
+    (F(2, 1), F(4, 6)),     # products fit and never reach the subnormal range: LOW class, no rounding
+    (F(3, 1), F(5, 7)),     # the same, TOP class
+    (F(5, 2), F(8, 7)),     # the same, INT class (a bfloat16 accumulator for 8-bit inputs)
     (F(5, 2, 14), F(5, 10, 13)),  # 1-5-10 with another bias: not half, rounded on its grid
     (F(7, 1), F(7, 3)),     # products fit, but the accumulator spans 129 binades: the compare-and-select rounding
     (F(8, 3), F(5, 10)),    # bf16-range inputs cannot be pre-scaled: one ldexp per product, TOP
