@@ -106,6 +106,7 @@ def _probe_lib():
     for name, args in {"probe_rows": [i32, P, i32, i64, i64, P, P, P, i32, P],
                        "probe_flat": [i32, P, i32, i64, i64, P, i32, P],
                        "probe_rowmajor": [i32, i32, P, i32, i64, i64, P, i32, P],
+                       "probe_flatrow_bytes": [i32, P, i32, i64, i64, P, i64, i32, P],
                        "probe_copy": [P, P, i64, i32, P],
                        "probe_rows_wide": [i32, i32, i32, P, i32, i64, i64, P, P, i32, P],
                        "probe_read_flat": [P, i64, P, i32, P],
@@ -178,6 +179,7 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
         if writes_rows:
             names += [f"{k}_{o}_{tag}" for k in ("flat", "rowmajor") for o in ("bytes", "f32")]
             names += [f"rowmajor_{o}_{g}inflight_{tag}" for o in ("bytes", "f32") for g in (1, 4, 8)]
+            names += [f"flatrow_bytes_{k}_{tag}" for k in ("4B", "16B")]
         if only and not any(nm.startswith(only) or only.startswith(nm) for nm in names):
             return
         G = torch.zeros((W, ld), dtype=torch.float32, device=dev)
@@ -224,6 +226,17 @@ def ceilings(only: str | None = None, reps: int = 5) -> dict:
                         timed(f"rowmajor_{kind}_{g}inflight_{tag}_{bpc}percu",
                               lambda: L.probe_rowmajor(outb, g, ptr(G), W, ld, n, ptr(dst), bpc, stream()),
                               (4.0 + outb) * W * n, W=W, n=n, chunks_in_flight=g, blocks_per_cu=bpc)
+                del dst
+                torch.cuda.empty_cache()
+            if group(f"flatrow_bytes_"):
+                # a coalesced flat walk: 4 chunks of one row per block step, code bytes stored 4 or 16 per lane
+                nf = n // 4096 * 4096
+                dst = torch.empty((W, ld), dtype=torch.uint8, device=dev)
+                for staged, kname in ((0, "4B"), (1, "16B")):
+                    for bpc in (8, 16, 32):
+                        timed(f"flatrow_bytes_{kname}_{tag}_{bpc}percu",
+                              lambda: L.probe_flatrow_bytes(staged, ptr(G), W, ld, nf, ptr(dst), ld, bpc, stream()),
+                              5.0 * W * nf, W=W, n=nf, blocks_per_cu=bpc)
                 del dst
                 torch.cuda.empty_cache()
         del G, out, byt, half

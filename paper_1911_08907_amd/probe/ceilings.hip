@@ -164,6 +164,48 @@ __global__ __launch_bounds__(BLOCK) void k_rowmajor(const float* __restrict__ X,
     }
 }
 
+// Flat order with coalesced loads: block b takes a contiguous range of tiles
+// of 4 chunks of one row (rows one after another); per tile each thread
+// loads its 16-byte slice of the 4 chunks and writes the 4 code bytes of
+// each (4 stores of 4 bytes, STAGED = 0), or passes them through LDS so
+// that it stores 16 consecutive code bytes at once (STAGED = 1).
+template <int STAGED>
+__global__ __launch_bounds__(BLOCK) void k_flatrow_bytes(const float* __restrict__ G, uint8_t* __restrict__ dst,
+                                                        int64_t ld, int64_t row_bytes, int64_t n, int32_t W) {
+    __shared__ uint32_t lds[4 * BLOCK];
+    constexpr int64_t TILE = 4 * CH;
+    const int64_t tpr = n / TILE;  // whole tiles per row
+    int64_t tb, te;
+    block_range(tpr * W, tb, te);
+    for (int64_t t = tb; t < te; ++t) {
+        const int64_t w = t / tpr;
+        const int64_t j0 = (t - w * tpr) * TILE;
+        const float* p = G + w * ld + j0 + (int64_t)threadIdx.x * VEC;
+        f4 x[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) x[k] = ld4(p + k * CH);
+        uint32_t c[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            c[k] = (f2u(x[k].x) >> 24) | ((f2u(x[k].y) >> 24) << 8) | ((f2u(x[k].z) >> 24) << 16) |
+                   (f2u(x[k].w) & 0xFF000000u);
+        uint8_t* d = dst + w * row_bytes + j0;
+        if constexpr (STAGED == 0) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                __builtin_nontemporal_store(c[k], (uint32_t*)(d + k * CH + (int64_t)threadIdx.x * VEC));
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) lds[k * BLOCK + threadIdx.x] = c[k];
+            __syncthreads();
+            const u4v v = {lds[4 * threadIdx.x], lds[4 * threadIdx.x + 1], lds[4 * threadIdx.x + 2],
+                           lds[4 * threadIdx.x + 3]};
+            __syncthreads();
+            __builtin_nontemporal_store(v, (u4v*)(d + 16 * (int64_t)threadIdx.x));
+        }
+    }
+}
+
 __global__ __launch_bounds__(BLOCK) void k_copy(const f4* __restrict__ src, f4* __restrict__ dst, int64_t n4) {
     const int64_t stride = (int64_t)gridDim.x * BLOCK;
     for (int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x; i < n4; i += stride)
@@ -462,6 +504,22 @@ extern "C" int probe_copy_ranges(const float* src, float* dst, int64_t n, int bl
     const int64_t n4 = n / 4;
     hipLaunchKernelGGL(k_copy_ranges, dim3((unsigned)grid_for(n4 / (4 * BLOCK), blocks_per_cu)), dim3(BLOCK), 0,
                        (hipStream_t)stream, (const f4*)src, (f4*)dst, n4);
+    return probe_done();
+}
+
+// Flat coalesced walk writing a byte per element (k_flatrow_bytes): staged 0
+// or 1; n a multiple of 4 chunks, ld >= n, row_bytes >= n.
+extern "C" int probe_flatrow_bytes(int staged, const float* G, int32_t W, int64_t ld, int64_t n, void* dst,
+                                   int64_t row_bytes, int blocks_per_cu, void* stream) {
+    if (!G || !dst || W < 1 || n < 4 * CH || (n % (4 * CH)) || ld < n || row_bytes < n || blocks_per_cu < 1) return -2;
+    const dim3 grid((unsigned)grid_for(n / (4 * CH) * W, blocks_per_cu));
+    hipStream_t s = (hipStream_t)stream;
+    if (staged == 0)
+        hipLaunchKernelGGL(k_flatrow_bytes<0>, grid, dim3(BLOCK), 0, s, G, (uint8_t*)dst, ld, row_bytes, n, W);
+    else if (staged == 1)
+        hipLaunchKernelGGL(k_flatrow_bytes<1>, grid, dim3(BLOCK), 0, s, G, (uint8_t*)dst, ld, row_bytes, n, W);
+    else
+        return -5;
     return probe_done();
 }
 
