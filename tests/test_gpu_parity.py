@@ -751,17 +751,19 @@ def test_lp_gemm_strided_views(dev, fin, facc):
     assert (c[:, 65:] == 7.0).all()  # nothing written past N
 
 
+@pytest.mark.parametrize("facc", [F(5, 10), F(5, 7), F(8, 7)], ids=["half", "grid", "exact-bf16"])
 @pytest.mark.parametrize("acc", [A.APS_ACC_SEQUENTIAL, A.APS_ACC_KAHAN])
-def test_lp_gemm_bert_ffn_sampled(dev, acc):
+def test_lp_gemm_bert_ffn_sampled(dev, acc, facc):
     # BERT-large's first FFN product at 8 sequences of 512 tokens:
-    # [4096 tokens x 1024] x [1024 x 4096], 1-5-2 inputs, 1-5-10 accumulator;
-    # sampled rows and columns against the oracle
+    # [4096 tokens x 1024] x [1024 x 4096], 1-5-2 inputs, the accumulators the
+    # benchmark times (IEEE half; 1-5-7, products rounded on its grid;
+    # bfloat16, exact products); sampled rows and columns against the oracle
     rng = np.random.default_rng(960 + acc)
     M, K, N = 4096, 1024, 4096
-    fin, facc = F(5, 2), F(5, 10)
+    fin = F(5, 2)
     Am = rng.standard_normal((M, K)).astype(np.float32)
     Bm = (rng.standard_normal((K, N)) * 0.02).astype(np.float32)
-    log(f"lp_gemm BERT FFN M={M} K={K} N={N} acc={acc}")
+    log(f"lp_gemm BERT FFN M={M} K={K} N={N} acc={acc} into {facc}")
     got = A.aps_lp_gemm(torch.from_numpy(Am).to(dev), torch.from_numpy(Bm).to(dev), fin, facc, acc)
     torch.cuda.synchronize()
     g = got.cpu().numpy()
