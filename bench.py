@@ -126,7 +126,7 @@ VALU_OPS = {"v_add_f32_e32": (0, 1), "v_mul_f32_e32": (1, 1), "v_and_b32_e32": (
             "v_add3_u32": (4, 1), "v_bfe_u32": (5, 1), "v_ldexp_f32": (6, 1), "v_and_or_b32": (7, 1),
             "v_subrev_f32_e32": (8, 1), "v_cmp_nle_f32_e32+v_cndmask_b32_e32 (VCC)": (9, 2),
             "v_cmp_nle_f32_e64+v_cndmask_b32_e64 (SGPR mask)": (10, 2), "v_rndne_f32_e32": (11, 1),
-            "v_pk_add_f16": (12, 1), "v_pk_mul_f16": (13, 1)}
+            "v_pk_add_f16": (12, 1), "v_pk_mul_f16": (13, 1), "v_cvt_pk_bf16_f32": (14, 1)}
 
 
 def ceilings(only: str | None = None, reps: int = 5) -> dict:
@@ -611,7 +611,8 @@ VALU_PEAK_T = 256 * 128 * 2.4e9 / 1e12
 # (two lanes of work each) at about 62.
 VALU_RATES = {"v_and_b32": 119.3, "v_add_f32": 112.7, "v_sub_f32": 118.5, "v_mul_f32": 116.6,
               "v_bfe_u32": 62.1, "v_add3_u32": 62.2, "v_rndne_f32": 62.7,
-              "v_pk_add_f16": 62.2, "v_pk_mul_f16": 62.0}
+              "v_pk_add_f16": 62.2, "v_pk_mul_f16": 62.0, "v_cvt_pk_bf16_f32": 62.2,
+              "v_lshlrev_b32": 115.0}  # the shift not probed: the two-operand forms' rate
 # VALU instructions per multiply-accumulate of each k-loop, counted in the
 # kernels' ISA (one loop iteration: 16 k-steps of the thread's 4 x 4 outputs).
 #   k_lp_gemm_h (the accumulator is IEEE half): a packed multiply and a packed
@@ -621,8 +622,11 @@ VALU_RATES = {"v_and_b32": 119.3, "v_add_f32": 112.7, "v_sub_f32": 118.5, "v_mul
 #     1-5-7): the product, its rint, the multiply into the working domain, the
 #     add and its rounding (v_bfe_u32, v_add3_u32, v_and_b32); Kahan rounds four
 #     adds.  The loop also issues 32 ds_read_b128.
-#   k_lp_gemm, exact products (1-5-2 inputs into bfloat16, 1-8-7: every product
-#     fits and none is subnormal): the product, the add and its rounding.
+#   k_lp_gemm, exact products into bfloat16 (1-5-2 inputs into 1-8-7: every
+#     product fits and none is subnormal): the product, the add, and its
+#     rounding by a packed conversion to bfloat16 for two chains
+#     (v_cvt_pk_bf16_f32) and the two halves taken back (v_lshlrev_b32,
+#     v_and_b32); Kahan rounds four adds so.
 GEMM_LOOP_MIX = {
     "sequential": {"v_pk_mul_f16": 0.5, "v_pk_add_f16": 0.5},
     "kahan": {"v_pk_mul_f16": 0.5, "v_pk_add_f16": 2.0},
@@ -630,9 +634,10 @@ GEMM_LOOP_MIX = {
                             "v_add3_u32": 1},
     "kahan_emulated": {"v_mul_f32": 2, "v_rndne_f32": 1, "v_add_f32": 1, "v_sub_f32": 3, "v_and_b32": 4,
                        "v_bfe_u32": 4, "v_add3_u32": 4},
-    "sequential_bf16": {"v_mul_f32": 1, "v_add_f32": 1, "v_and_b32": 1, "v_bfe_u32": 1, "v_add3_u32": 1},
-    "kahan_bf16": {"v_mul_f32": 1, "v_add_f32": 1, "v_sub_f32": 3, "v_and_b32": 4, "v_bfe_u32": 4,
-                   "v_add3_u32": 4},
+    "sequential_bf16": {"v_mul_f32": 1, "v_add_f32": 1, "v_cvt_pk_bf16_f32": 0.5, "v_lshlrev_b32": 0.5,
+                        "v_and_b32": 0.5},
+    "kahan_bf16": {"v_mul_f32": 1, "v_add_f32": 1, "v_sub_f32": 3, "v_cvt_pk_bf16_f32": 2, "v_lshlrev_b32": 2,
+                   "v_and_b32": 2},
 }
 GEMM_SHAPE = (4096, 1024, 4096)  # BERT-large FFN up-projection at 8 x 512 tokens: M, K, N
 

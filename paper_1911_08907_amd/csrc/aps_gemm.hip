@@ -25,7 +25,24 @@ enum GemmProduct {
     GP_FIT = 2,     // pre-scaled, and every product fits the significand (quant_fit)
     GP_GRID = 3,    // as GP_FIT, staged so that the subnormal step is 1: rint, then 2^Q
     GP_EXACT = 4,   // pre-scaled, every product fits and none reaches the subnormal range: no rounding
+    GP_BF16 = 5,    // GP_EXACT into bfloat16: each add rounded by the hardware's conversion to bfloat16
 };
+
+// GP_BF16.  The accumulator is bfloat16 (e = 8, m = 7, bias 127): its values
+// are the fp32 values whose low 16 bits are zero, and fp32's own
+// round-to-nearest-even conversion to bfloat16 (subnormals and overflow to
+// INF included) is the format's rounding.  The fp32 add of two bfloat16
+// values rounded once more to bfloat16 is the rounded exact sum (24 >=
+// 2 * 8 + 2), so each add is an fp32 add and a conversion, one packed
+// conversion for two chains.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ void round_bf16x2(float x0, float x1, float& r0, float& r1) {
+    const uint32_t u = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{x0, x1}, bf16x2));
+    r0 = u2f(u << 16);
+    r1 = u2f(u & 0xFFFF0000u);
+}
 
 // GP_EXACT.  When every product of two input values fits the accumulator's
 // significand and no nonzero product lies below 2^emin (the square of the
@@ -103,6 +120,29 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
         auto mac_v = [&](const f4& av, const f4& bv, bool first) {
             const float a[4] = {av.x, av.y, av.z, av.w};
             const float b[4] = {bv.x, bv.y, bv.z, bv.w};
+            if constexpr (PM == GP_BF16) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; j += 2) {
+                        const float p0 = a[i] * b[j], p1 = a[i] * b[j + 1];  // exact, bfloat16 values or beyond
+                        if (first) {
+                            s[i][j] = p0;
+                            s[i][j + 1] = p1;
+                        } else if constexpr (KAHAN) {
+                            float y0, y1, t0, t1, u0, u1;
+                            round_bf16x2(p0 - c[i][j], p1 - c[i][j + 1], y0, y1);
+                            round_bf16x2(s[i][j] + y0, s[i][j + 1] + y1, t0, t1);
+                            round_bf16x2(t0 - s[i][j], t1 - s[i][j + 1], u0, u1);
+                            round_bf16x2(u0 - y0, u1 - y1, c[i][j], c[i][j + 1]);
+                            s[i][j] = t0;
+                            s[i][j + 1] = t1;
+                        } else {
+                            round_bf16x2(s[i][j] + p0, s[i][j + 1] + p1, s[i][j], s[i][j + 1]);
+                        }
+                    }
+                return;
+            }
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -343,7 +383,13 @@ static void launch_lp_gemm_v(bool kahan, int pm, dim3 grid, hipStream_t s, const
     constexpr bool can_ldexp = VT<V>::cls == CLS_TOP || VT<V>::cls == CLS_LOW;
     constexpr bool can_exact = VT<V>::cls != CLS_GEN && !VT<V>::m0;
 #define APS_G(K, P) hipLaunchKernelGGL((k_lp_gemm<V, K, P>), grid, dim3(BLOCK), 0, s, g, fi, fa)
-    if (pm == GP_EXACT) {
+    if (pm == GP_BF16) {
+        if constexpr (V == V_INT_F32) {
+            if (kahan) APS_G(true, GP_BF16); else APS_G(false, GP_BF16);
+            return;
+        }
+    }
+    if (pm == GP_EXACT || pm == GP_BF16) {
         if constexpr (can_exact) {
             if (kahan) APS_G(true, GP_EXACT); else APS_G(false, GP_EXACT);
             return;
@@ -439,7 +485,7 @@ extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t 
         g.ka = fa.k < room ? fa.k : room;
         g.kb = fa.k - g.ka;
         g.qs = 1.0f;
-        pm = GP_EXACT;
+        pm = (acc_fmt.e == 8 && acc_fmt.m == 7 && acc_fmt.bias == 127) ? GP_BF16 : GP_EXACT;
     }
     const dim3 grid((unsigned)std::min<int64_t>(g.tiles, INT32_MAX));
     // the accumulator is IEEE half and every input value a half (at most 10

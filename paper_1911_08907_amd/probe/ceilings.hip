@@ -351,7 +351,7 @@ __global__ __launch_bounds__(BLOCK) void k_widen(const uint8_t* __restrict__ in,
 
 enum ValuOp { V_ADD = 0, V_MUL = 1, V_AND = 2, V_FMA = 3, V_ADD3 = 4, V_BFE = 5, V_LDEXP = 6, V_AND_OR = 7,
               V_SUBREV = 8, V_CMP_CNDMASK = 9, V_CMP_CNDMASK_SGPR = 10, V_RNDNE = 11,
-              V_PK_ADD_F16 = 12, V_PK_MUL_F16 = 13 };
+              V_PK_ADD_F16 = 12, V_PK_MUL_F16 = 13, V_CVT_PK_BF16 = 14 };
 
 template <int OP>
 __device__ __forceinline__ void valu_step(float& x, float y, float z, int s) {
@@ -368,6 +368,8 @@ __device__ __forceinline__ void valu_step(float& x, float y, float z, int s) {
     // packed half precision: two lanes of work per instruction (counted as one instruction)
     if constexpr (OP == V_PK_ADD_F16) asm volatile("v_pk_add_f16 %0, %1, %0" : "+v"(x) : "v"(y));
     if constexpr (OP == V_PK_MUL_F16) asm volatile("v_pk_mul_f16 %0, %1, %0" : "+v"(x) : "v"(y));
+    // two fp32 values to a pair of bfloat16 (counted as one instruction)
+    if constexpr (OP == V_CVT_PK_BF16) asm volatile("v_cvt_pk_bf16_f32 %0, %0, %1" : "+v"(x) : "v"(y));
     // a compare into VCC and a select by it, as the compiler emits a rounding's
     // branch-free choice (one pair counted as two instructions)
     if constexpr (OP == V_CMP_CNDMASK)
@@ -550,7 +552,7 @@ extern "C" int probe_valu(int op, float* out, int blocks_per_cu, int32_t iters, 
     switch (op) {
         PROBE_V(V_ADD) PROBE_V(V_MUL) PROBE_V(V_AND) PROBE_V(V_FMA) PROBE_V(V_ADD3) PROBE_V(V_BFE) PROBE_V(V_LDEXP)
         PROBE_V(V_AND_OR) PROBE_V(V_SUBREV) PROBE_V(V_CMP_CNDMASK) PROBE_V(V_CMP_CNDMASK_SGPR) PROBE_V(V_RNDNE)
-        PROBE_V(V_PK_ADD_F16) PROBE_V(V_PK_MUL_F16)
+        PROBE_V(V_PK_ADD_F16) PROBE_V(V_PK_MUL_F16) PROBE_V(V_CVT_PK_BF16)
         default: return -5;
     }
 #undef PROBE_V

@@ -620,7 +620,9 @@ GEMM_PAIRS = [
     (F(4, 1), F(4, 6)),     # products fit: LOW class (rounded on its grid)
     (F(2, 1), F(4, 6)),     # products fit and never reach the subnormal range: LOW class, no rounding
     (F(3, 1), F(5, 7)),     # the same, TOP class
-    (F(5, 2), F(8, 7)),     # the same, INT class (a bfloat16 accumulator for 8-bit inputs)
+    (F(5, 2), F(8, 7)),     # the same into bfloat16: the adds rounded by the hardware's conversion
+    (F(7, 1), F(8, 7)),     # bfloat16 again, with products overflowing and sums below 2^-126
+    (F(5, 2), F(8, 10)),    # exact products, INT class, not bfloat16
     (F(5, 2, 14), F(5, 10, 13)),  # 1-5-10 with another bias: not half, rounded on its grid
     (F(7, 1), F(7, 3)),     # products fit, but the accumulator spans 129 binades: the compare-and-select rounding
     (F(8, 3), F(5, 10)),    # bf16-range inputs cannot be pre-scaled: one ldexp per product, TOP
@@ -718,6 +720,44 @@ def test_lp_gemm_product_grid_edges(dev, acc, shift):
             assert d[0] == np.inf and d[1] == 0.0 and d[6] == -np.inf
             assert d[2] == 4 * 2.0 ** -24 and d[3] == 2.0 ** -24 and d[4] == 784 * 2.0 ** -24 + 2.0 ** -14
             assert d[5] == -2 * 2.0 ** -24
+
+
+@pytest.mark.parametrize("acc", [A.APS_ACC_SEQUENTIAL, A.APS_ACC_KAHAN])
+def test_lp_gemm_bfloat16_edges(dev, acc):
+    """1-7-1 inputs into a bfloat16 accumulator (every product exact, the
+    adds rounded by the hardware's conversion to bfloat16): halfway sums
+    (ties to even), overflow of a sum to INF, cancellation, and products from
+    the inputs' smallest subnormal to beyond bfloat16's range."""
+    fin, facc = F(7, 1), F(8, 7)
+    big = 1.5 * 2.0 ** 63
+    cases = [  # (row of A, column of B): K = 3
+        ((1.0, 2.0 ** -4, 0.0), (1.0, 2.0 ** -4, 0.0)),                  # 1 + 2^-8: a tie, to 1
+        ((1.0, 2.0 ** -4, 2.0 ** -4), (1.0, 2.0 ** -3, 2.0 ** -4)),      # 1 + 2^-7, then + 2^-8: a tie, to 1 + 2^-6
+        ((big, big, 0.0), (big, big, 0.0)),                              # 2.25 * 2^126 twice: INF (Kahan: NaN next)
+        ((big, big, 1.0), (big, -big, 1.0)),                             # cancels to 0, then 1
+        ((big, 2.0 ** 63, big), (2.0 ** 63, 2.0 ** 63, big)),            # 1.5 * 2^126 + 2^126 + 2.25 * 2^126: INF
+        ((2.0 ** -63, 1.0, -1.0), (2.0 ** -63, 2.0 ** -40, 2.0 ** -40)),  # 2^-126 swamped by 2^-40, then cancelled
+    ]
+    n = len(cases)
+    Am = np.zeros((n, 3), np.float32)
+    Bm = np.zeros((3, n), np.float32)
+    for i, (a, b) in enumerate(cases):
+        Am[i] = a
+        Bm[:, i] = b
+    rng = np.random.default_rng(1230 + acc)
+    for tag, (Ax, Bx) in (("hand-made", (Am, Bm)), ("random", _gemm_inputs(rng, 70, 80, 300, fin))):
+        log(f"lp_gemm bfloat16 edges {tag} acc={acc}")
+        got = A.aps_lp_gemm(torch.from_numpy(Ax).to(dev), torch.from_numpy(Bx).to(dev), fin, facc, acc)
+        torch.cuda.synchronize()
+        ref = O.lp_gemm(Ax, Bx, ofmt(fin), ofmt(facc), acc)
+        g = got.cpu().numpy()
+        assert same_f32(g, ref), (tag, first_diff(g, ref))
+        if tag == "hand-made":
+            d = np.diag(ref)
+            assert d[0] == 1.0 and d[1] == 1.0 + 2.0 ** -6 and d[3] == 1.0 and d[4] == np.inf and d[5] == 0.0
+            # an INF partial sum with zero added: plain stays INF; Kahan's compensation is INF by then,
+            # so the next add is INF - INF
+            assert d[2] == np.inf if acc == A.APS_ACC_SEQUENTIAL else np.isnan(d[2])
 
 
 @pytest.mark.parametrize("fin,facc", [(F(5, 2), F(5, 10)), (F(4, 3), F(5, 2))], ids=["half", "emulated"])
