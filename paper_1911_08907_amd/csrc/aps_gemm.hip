@@ -71,7 +71,17 @@ constexpr int GK = 16;  // k-tile staged in LDS
 // four rows are one 16-byte read); each thread then runs 16 independent
 // chains, one per output, adding its products in k order.  The work is the
 // VALU's: a product, its rounding and the rounded add per multiply-accumulate.
-template <int V, bool KAHAN, int PM>
+// An input value cast to the input format (native value): through the
+// switch over classes, or straight to the class VI when the launch knows it.
+template <int VI>
+__device__ __forceinline__ float cast_in(float x, const FmtK& fi) {
+    if constexpr (VI < 0)
+        return quant_any(x, fi.k, fi);
+    else
+        return quant_native<VI>(x, fi.k, fi);
+}
+
+template <int V, bool KAHAN, int PM, int VI = -1>
 __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa) {
     __shared__ __align__(16) float As[GK][GT + 4];  // As[k][m]; the pad spreads the staging writes over banks
     __shared__ __align__(16) float Bs[GK][GT + 4];  // Bs[k][n]
@@ -101,8 +111,8 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
             if (inner && k0 + GK <= g.K) {  // the whole k-tile inside A and B: no checks
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    ra[r] = __builtin_amdgcn_ldexpf(quant_any(g.A[oa + r * 16 * g.lda + k0], fi.k, fi), g.ka);
-                    rb[r] = __builtin_amdgcn_ldexpf(quant_any(g.B[ob + (k0 + 4 * r) * g.ldb], fi.k, fi), g.kb);
+                    ra[r] = __builtin_amdgcn_ldexpf(cast_in<VI>(g.A[oa + r * 16 * g.lda + k0], fi), g.ka);
+                    rb[r] = __builtin_amdgcn_ldexpf(cast_in<VI>(g.B[ob + (k0 + 4 * r) * g.ldb], fi), g.kb);
                 }
                 return;
             }
@@ -110,10 +120,10 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa)
             for (int r = 0; r < 4; ++r) {
                 const int idx = t + BLOCK * r;
                 const int64_t am = m0 + (idx >> 4), ak = k0 + (idx & 15);
-                ra[r] = (am < g.M && ak < g.K) ? __builtin_amdgcn_ldexpf(quant_any(g.A[am * g.lda + ak], fi.k, fi), g.ka)
+                ra[r] = (am < g.M && ak < g.K) ? __builtin_amdgcn_ldexpf(cast_in<VI>(g.A[am * g.lda + ak], fi), g.ka)
                                                : 0.0f;
                 const int64_t bk = k0 + (idx >> 6), bn = n0 + (idx & 63);
-                rb[r] = (bk < g.K && bn < g.N) ? __builtin_amdgcn_ldexpf(quant_any(g.B[bk * g.ldb + bn], fi.k, fi), g.kb)
+                rb[r] = (bk < g.K && bn < g.N) ? __builtin_amdgcn_ldexpf(cast_in<VI>(g.B[bk * g.ldb + bn], fi), g.kb)
                                                : 0.0f;
             }
         };
@@ -385,6 +395,17 @@ static void launch_lp_gemm_v(bool kahan, int pm, dim3 grid, hipStream_t s, const
 #define APS_G(K, P) hipLaunchKernelGGL((k_lp_gemm<V, K, P>), grid, dim3(BLOCK), 0, s, g, fi, fa)
     if (pm == GP_BF16) {
         if constexpr (V == V_INT_F32) {
+            // one instantiation per input class (such inputs are TOP or LOW)
+#define APS_GB(VI)                                                                                           \
+    if (fi.variant == (VI)) {                                                                                \
+        if (kahan)                                                                                           \
+            hipLaunchKernelGGL((k_lp_gemm<V, true, GP_BF16, VI>), grid, dim3(BLOCK), 0, s, g, fi, fa);  \
+        else                                                                                                 \
+            hipLaunchKernelGGL((k_lp_gemm<V, false, GP_BF16, VI>), grid, dim3(BLOCK), 0, s, g, fi, fa); \
+        return;                                                                                              \
+    }
+            APS_GB(V_TOP_F32) APS_GB(V_TOP_M0) APS_GB(V_LOW_F32) APS_GB(V_LOW_M0)
+#undef APS_GB
             if (kahan) APS_G(true, GP_BF16); else APS_G(false, GP_BF16);
             return;
         }

@@ -622,6 +622,8 @@ GEMM_PAIRS = [
     (F(3, 1), F(5, 7)),     # the same, TOP class
     (F(5, 2), F(8, 7)),     # the same into bfloat16: the adds rounded by the hardware's conversion
     (F(7, 1), F(8, 7)),     # bfloat16 again, with products overflowing and sums below 2^-126
+    (F(4, 3), F(8, 7)),     # bfloat16 from LOW-class inputs
+    (F(5, 0), F(8, 7)),     # bfloat16 from inputs with no mantissa bits
     (F(5, 2), F(8, 10)),    # exact products, INT class, not bfloat16
     (F(5, 2, 14), F(5, 10, 13)),  # 1-5-10 with another bias: not half, rounded on its grid
     (F(7, 1), F(7, 3)),     # products fit, but the accumulator spans 129 binades: the compare-and-select rounding
