@@ -66,11 +66,6 @@ __device__ __forceinline__ void round_bf16x2(float x0, float x1, float& r0, floa
 constexpr int GT = 64;  // output tile GT x GT per block, 4 x 4 per thread
 constexpr int GK = 16;  // k-tile staged in LDS
 
-// One block computes a GT x GT tile of C.  Each k-tile of A and B is cast to
-// the input format while it is staged into LDS (A transposed, so a thread's
-// four rows are one 16-byte read); each thread then runs 16 independent
-// chains, one per output, adding its products in k order.  The work is the
-// VALU's: a product, its rounding and the rounded add per multiply-accumulate.
 // An input value cast to the input format (native value): through the
 // switch over classes, or straight to the class VI when the launch knows it.
 template <int VI>
@@ -81,6 +76,11 @@ __device__ __forceinline__ float cast_in(float x, const FmtK& fi) {
         return quant_native<VI>(x, fi.k, fi);
 }
 
+// One block computes a GT x GT tile of C.  Each k-tile of A and B is cast to
+// the input format while it is staged into LDS (A transposed, so a thread's
+// four rows are one 16-byte read); each thread then runs 16 independent
+// chains, one per output, adding its products in k order.  The work is the
+// VALU's: a product, its rounding and the rounded add per multiply-accumulate.
 template <int V, bool KAHAN, int PM, int VI = -1>
 __global__ __launch_bounds__(BLOCK) void k_lp_gemm(GemmArgs g, FmtK fi, FmtK fa) {
     __shared__ __align__(16) float As[GK][GT + 4];  // As[k][m]; the pad spreads the staging writes over banks
