@@ -148,11 +148,17 @@ __device__ __forceinline__ float quant_w(float y, const FmtK& f, bool& bad) {
             rn = b + f.half;
         else
             rn = b + f.half + __builtin_amdgcn_ubfe(b, f.sh, T::acc == ACC_F32 ? 1u : f.lsbw);
-        float ys = y;
-        if constexpr (T::cls == CLS_LOW) ys = __builtin_amdgcn_ldexpf(y, -f.j);
-        float rs = (__builtin_fabsf(ys) + f.c0) - f.c0;
-        if constexpr (T::cls == CLS_LOW) rs = __builtin_amdgcn_ldexpf(rs, f.j);
-        const uint32_t rsb = (b & 0x80000000u) | f2u(rs);
+        uint32_t rsb;
+        if constexpr (T::cls == CLS_LOW && !T::m0) {
+            // on the scale where the subnormal step is 1: an integer, ties to even, sign kept
+            rsb = f2u(__builtin_rintf(y * f.qi) * f.qs);
+        } else {
+            float ys = y;
+            if constexpr (T::cls == CLS_LOW) ys = __builtin_amdgcn_ldexpf(y, -f.j);
+            float rs = (__builtin_fabsf(ys) + f.c0) - f.c0;
+            if constexpr (T::cls == CLS_LOW) rs = __builtin_amdgcn_ldexpf(rs, f.j);
+            rsb = (b & 0x80000000u) | f2u(rs);
+        }
         // NaN fails the compare and takes the subnormal path, which keeps it NaN
         const uint32_t r = (__builtin_fabsf(y) >= f.thr) ? rn : rsb;
         return u2f(r & f.mask);

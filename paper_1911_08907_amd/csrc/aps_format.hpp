@@ -23,8 +23,12 @@
 //   * a value below 2^emin (format subnormal range) is rounded onto the fixed
 //     subnormal grid with one fp32 add/subtract of c0 = 2^(emin - m + 23)
 //     ("magic" constant): fp32's own round-to-nearest-even does the work.
-//     When c0 would not be an fp32 value (small e), the subtraction happens
-//     in a domain shifted down by j more bits (class LOW);
+//     When c0 would not be an fp32 value (small e, class LOW), the value is
+//     instead scaled so that the grid's step is 1 and rounded to an integer
+//     (rint, ties to even), then scaled back: the step 2^(emin - m) lies
+//     between 2^105 and 2^126 there, so both scalings are exact wherever the
+//     result is not zero (m = 0 formats keep the add/subtract in a domain
+//     shifted down by j more bits);
 //   * for e = 8 with bias 127 the format's subnormal grid is a coarsening of
 //     fp32's, so the bit-pattern rounding covers every magnitude (class INT);
 //   * class GEN keeps values native (k = 0; every format value is an fp32
@@ -77,6 +81,7 @@ struct FmtK {
     uint32_t mask;    // clears the dropped bits
     float thr;        // 2^emin in the working domain
     float c0;         // magic constant of the subnormal path (shifted by -j)
+    float qs, qi;     // LOW: 2^Q and 2^-Q, Q = emin - m in the working domain (the subnormal step)
     uint32_t sh64;    // 52 - m  (fp64 accumulator)
     int32_t esh;      // max(0, -126 - emin): codes scale by 2^esh so that 2^emin is an fp32 normal
     uint64_t half64;  // 2^(sh64-1) - 1 (GEN with m = 0: 2^51, ties up)
@@ -149,6 +154,8 @@ inline FmtK make_fmtk(const aps_format& f) {
         cls = CLS_LOW;
         o.j = emin_w - f.m + 23 - 127;
         o.c0 = pow2f_host(127);
+        o.qs = pow2f_host(emin_w - f.m);
+        o.qi = pow2f_host(f.m - emin_w);
     }
     int acc;
     if (is_int && f.m == 23)
