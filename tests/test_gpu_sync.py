@@ -123,7 +123,7 @@ def sync_case(dev, G, n, offs, pal, fmt_idx=None, tag="", split=False, garbage=T
 # ----------------------------------------------------------- edge layouts
 
 FORMATS = [F(5, 2), F(4, 3), F(3, 0), F(2, 0), F(2, 1), F(3, 2), F(5, 10), F(8, 7), F(8, 0), F(6, 1),
-           F(4, 3, 5), F(5, 2, 20), F(7, 5), F(5, 12), F(8, 23),
+           F(4, 3, 5), F(5, 2, 20), F(7, 5), F(5, 12), F(8, 23), F(3, 12),
            F(8, 7, 130), F(5, 10, 120), F(3, 0, 145), F(2, 1, 147)]  # the last four round in fp64
 SIZES = [0, 1, 3, 5, 7, 1023, 1024, 1025, 2049, 0, 64, 13, 4095, 2, 3000]
 
