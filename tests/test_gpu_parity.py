@@ -617,6 +617,7 @@ GEMM_PAIRS = [
     (F(2, 1), F(2, 0)),     # m = 0, LOW class: the 3-bit accumulator
     (F(8, 3), F(8, 0)),     # m = 0, INT class
     (F(5, 2), F(5, 10)),    # the accumulator is IEEE half: the hardware's half-precision arithmetic
+    (F(5, 2, 16), F(5, 10)),  # the same from inputs of another bias
     (F(4, 2), F(5, 9)),     # products fit the accumulator's significand: TOP class (rounded on its grid)
     (F(4, 1), F(4, 6)),     # products fit: LOW class (rounded on its grid)
     (F(2, 1), F(4, 6)),     # products fit and never reach the subnormal range: LOW class, no rounding
