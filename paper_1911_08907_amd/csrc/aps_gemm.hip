@@ -66,14 +66,37 @@ __device__ __forceinline__ void round_bf16x2(float x0, float x1, float& r0, floa
 constexpr int GT = 64;  // output tile GT x GT per block, 4 x 4 per thread
 constexpr int GK = 16;  // k-tile staged in LDS
 
+// Input format 1-5-2 with bias 15 has the bit layout and value set of the
+// OCP E5M2 8-bit float.  The hardware's conversion of fp32 to it (round to
+// nearest even, no saturation: beyond the largest finite value the result is
+// INF, a NaN stays NaN, subnormals kept) and back to fp32 is this format's
+// cast exactly; the two agree on every fp32 bit pattern.  Two values per
+// conversion.
+constexpr int VI_E5M2 = 100;
+
+__device__ __forceinline__ void cast_e5m2x2(float x0, float x1, float& r0, float& r1) {
+    const int pk = __builtin_amdgcn_cvt_pk_bf8_f32(x0, x1, 0, false);  // bytes 0 and 1
+    const f32x2 v = __builtin_amdgcn_cvt_pk_f32_bf8(pk, false);
+    r0 = v[0];
+    r1 = v[1];
+}
+
+inline bool is_e5m2(const FmtK& f) { return f.e == 5 && f.m == 2 && f.bias == 15; }
+
 // An input value cast to the input format (native value): through the
-// switch over classes, or straight to the class VI when the launch knows it.
+// switch over classes, straight to the class VI when the launch knows it, or
+// by the hardware's E5M2 conversion.
 template <int VI>
 __device__ __forceinline__ float cast_in(float x, const FmtK& fi) {
-    if constexpr (VI < 0)
+    if constexpr (VI == VI_E5M2) {
+        float r, unused;
+        cast_e5m2x2(x, x, r, unused);
+        return r;
+    } else if constexpr (VI < 0) {
         return quant_any(x, fi.k, fi);
-    else
+    } else {
         return quant_native<VI>(x, fi.k, fi);
+    }
 }
 
 // One block computes a GT x GT tile of C.  Each k-tile of A and B is cast to
@@ -279,10 +302,25 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm_h(GemmArgs g, FmtK fi) {
         // Every load reads an address inside the matrix, so no lane branches.
         auto fetch = [&](int64_t k0) {
             if (inner && k0 + HGK <= g.K) {  // the whole k-tile inside A and B: no checks
+                if constexpr (VI == VI_E5M2) {  // two values per conversion
+#pragma unroll
+                    for (int r = 0; r < HST; r += 2) {
+                        float a0, a1, b0, b1;
+                        cast_e5m2x2(g.A[oa + r * (BLOCK / HGK) * g.lda + k0],
+                                    g.A[oa + (r + 1) * (BLOCK / HGK) * g.lda + k0], a0, a1);
+                        cast_e5m2x2(g.B[ob + (k0 + r * (BLOCK / HGT)) * g.ldb],
+                                    g.B[ob + (k0 + (r + 1) * (BLOCK / HGT)) * g.ldb], b0, b1);
+                        ra[r] = (_Float16)a0;
+                        ra[r + 1] = (_Float16)a1;
+                        rb[r] = (_Float16)b0;
+                        rb[r + 1] = (_Float16)b1;
+                    }
+                    return;
+                }
 #pragma unroll
                 for (int r = 0; r < HST; ++r) {
-                    ra[r] = (_Float16)quant_native<VI>(g.A[oa + r * (BLOCK / HGK) * g.lda + k0], fi.k, fi);
-                    rb[r] = (_Float16)quant_native<VI>(g.B[ob + (k0 + r * (BLOCK / HGT)) * g.ldb], fi.k, fi);
+                    ra[r] = (_Float16)cast_in<VI>(g.A[oa + r * (BLOCK / HGK) * g.lda + k0], fi);
+                    rb[r] = (_Float16)cast_in<VI>(g.B[ob + (k0 + r * (BLOCK / HGT)) * g.ldb], fi);
                 }
                 return;
             }
@@ -291,11 +329,11 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm_h(GemmArgs g, FmtK fi) {
                 const int idx = t + BLOCK * r;
                 const int64_t am = m0 + idx / HGK, ak = k0 + idx % HGK;
                 const bool oka = am < g.M && ak < g.K;
-                const _Float16 qa = (_Float16)quant_native<VI>(g.A[oka ? am * g.lda + ak : 0], fi.k, fi);
+                const _Float16 qa = (_Float16)cast_in<VI>(g.A[oka ? am * g.lda + ak : 0], fi);
                 ra[r] = oka ? qa : (_Float16)0.0f;
                 const int64_t bk = k0 + idx / HGT, bn = n0 + idx % HGT;
                 const bool okb = bk < g.K && bn < g.N;
-                const _Float16 qb = (_Float16)quant_native<VI>(g.B[okb ? bk * g.ldb + bn : 0], fi.k, fi);
+                const _Float16 qb = (_Float16)cast_in<VI>(g.B[okb ? bk * g.ldb + bn : 0], fi);
                 rb[r] = okb ? qb : (_Float16)0.0f;
             }
         };
@@ -397,14 +435,14 @@ static void launch_lp_gemm_v(bool kahan, int pm, dim3 grid, hipStream_t s, const
         if constexpr (V == V_INT_F32) {
             // one instantiation per input class (such inputs are TOP or LOW)
 #define APS_GB(VI)                                                                                           \
-    if (fi.variant == (VI)) {                                                                                \
+    if ((VI) == VI_E5M2 ? is_e5m2(fi) : fi.variant == (VI)) {                                                                                \
         if (kahan)                                                                                           \
             hipLaunchKernelGGL((k_lp_gemm<V, true, GP_BF16, VI>), grid, dim3(BLOCK), 0, s, g, fi, fa);  \
         else                                                                                                 \
             hipLaunchKernelGGL((k_lp_gemm<V, false, GP_BF16, VI>), grid, dim3(BLOCK), 0, s, g, fi, fa); \
         return;                                                                                              \
     }
-            APS_GB(V_TOP_F32) APS_GB(V_TOP_M0) APS_GB(V_LOW_F32) APS_GB(V_LOW_M0)
+            APS_GB(VI_E5M2) APS_GB(V_TOP_F32) APS_GB(V_TOP_M0) APS_GB(V_LOW_F32) APS_GB(V_LOW_M0)
 #undef APS_GB
             if (kahan) APS_G(true, GP_BF16); else APS_G(false, GP_BF16);
             return;
@@ -418,6 +456,13 @@ static void launch_lp_gemm_v(bool kahan, int pm, dim3 grid, hipStream_t s, const
     }
     if (pm == GP_GRID) {
         if constexpr (can_fit) {
+            if (is_e5m2(fi)) {
+                if (kahan)
+                    hipLaunchKernelGGL((k_lp_gemm<V, true, GP_GRID, VI_E5M2>), grid, dim3(BLOCK), 0, s, g, fi, fa);
+                else
+                    hipLaunchKernelGGL((k_lp_gemm<V, false, GP_GRID, VI_E5M2>), grid, dim3(BLOCK), 0, s, g, fi, fa);
+                return;
+            }
             if (kahan) APS_G(true, GP_GRID); else APS_G(false, GP_GRID);
             return;
         }
@@ -521,14 +566,14 @@ extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t 
         const hipStream_t hs = (hipStream_t)stream;
         const bool kh = accumulator == APS_ACC_KAHAN;
 #define APS_HK(VI)                                                                          \
-    if (fi.variant == (VI)) {                                                              \
+    if ((VI) == VI_E5M2 ? is_e5m2(fi) : fi.variant == (VI)) {                                                              \
         if (kh)                                                                            \
             hipLaunchKernelGGL((k_lp_gemm_h<true, VI>), hgrid, dim3(BLOCK), 0, hs, g, fi);  \
         else                                                                               \
             hipLaunchKernelGGL((k_lp_gemm_h<false, VI>), hgrid, dim3(BLOCK), 0, hs, g, fi); \
         return launched();                                                                 \
     }
-        APS_HK(V_TOP_F32) APS_HK(V_TOP_M0) APS_HK(V_LOW_F32) APS_HK(V_LOW_M0)
+        APS_HK(VI_E5M2) APS_HK(V_TOP_F32) APS_HK(V_TOP_M0) APS_HK(V_LOW_F32) APS_HK(V_LOW_M0)
 #undef APS_HK
         g.tiles = mt * nt;  // another input class: the emulated kernel
         g.ntn = (int32_t)nt;

@@ -764,6 +764,38 @@ def test_lp_gemm_bfloat16_edges(dev, acc):
             assert d[2] == np.inf if acc == A.APS_ACC_SEQUENTIAL else np.isnan(d[2])
 
 
+def _cast_boundary_values():
+    # fp32 values at every rounding position of 1-5-2: both signs, every
+    # exponent field (zeros, subnormals, INF and NaN among them), the top six
+    # mantissa bits in all combinations (round bit and the bits above it for
+    # the normal and subnormal grids alike) and four patterns of the bits
+    # below (none set, the lowest, the highest, all)
+    sign = np.arange(2, dtype=np.uint32)[:, None, None, None] << 31
+    expo = np.arange(256, dtype=np.uint32)[None, :, None, None] << 23
+    top = np.arange(64, dtype=np.uint32)[None, None, :, None] << 17
+    low = np.array([0, 1, 0x10000, 0x1FFFF], dtype=np.uint32)[None, None, None, :]
+    return (sign | expo | top | low).reshape(-1).view(np.float32)
+
+
+@pytest.mark.parametrize("facc", [F(5, 10), F(5, 7), F(8, 7)], ids=["half", "grid", "exact-bf16"])
+def test_lp_gemm_input_cast_rounding_cases(dev, facc):
+    """1-5-2 inputs at every rounding case of their cast (ties, sticky bits,
+    the subnormal grid, overflow to INF, NaN, signed zeros), each times 1.0
+    with zeros in the other k slots, in whole tiles so that the half kernel
+    casts its staged values two at a time."""
+    x = _cast_boundary_values()
+    M, K, N = x.size, 16, 64
+    Am = np.zeros((M, K), np.float32)
+    Am[:, 0] = x
+    Bm = np.zeros((K, N), np.float32)
+    Bm[0, :] = 1.0
+    log(f"lp_gemm input cast cases 1-5-2->{facc} M={M}")
+    got = A.aps_lp_gemm(torch.from_numpy(Am).to(dev), torch.from_numpy(Bm).to(dev), F(5, 2), facc).cpu().numpy()
+    ref = O.lp_gemm(Am, np.ascontiguousarray(Bm[:, :1]), ofmt(F(5, 2)), ofmt(facc))
+    assert same_f32(got[:, :1], ref), first_diff(got[:, :1], ref)
+    assert same_f32(got, np.repeat(got[:, :1], N, axis=1))
+
+
 @pytest.mark.parametrize("fin,facc", [(F(5, 2), F(5, 10)), (F(4, 3), F(5, 2))], ids=["half", "emulated"])
 @pytest.mark.parametrize("M,N", [(1 << 22, 3), (2, 1 << 22)])
 def test_lp_gemm_largest_dimensions(dev, M, N, fin, facc):
