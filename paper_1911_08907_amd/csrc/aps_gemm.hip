@@ -81,16 +81,44 @@ __device__ __forceinline__ void cast_e5m2x2(float x0, float x1, float& r0, float
     r1 = v[1];
 }
 
-inline bool is_e5m2(const FmtK& f) { return f.e == 5 && f.m == 2 && f.bias == 15; }
+// Input format 1-4-3 with bias 7 shares its layout, subnormals and rounding
+// with the OCP E4M3 8-bit float below 248; E4M3 has no INF and goes on to
+// 448, so from 248 up (the tie at 248 rounds to 256) the cast is INF with the
+// input's sign, which also covers an INF input.  With that one select the
+// round trip is this format's cast on every fp32 bit pattern.
+constexpr int VI_E4M3 = 101;
+
+__device__ __forceinline__ void cast_e4m3x2(float x0, float x1, float& r0, float& r1) {
+    const int pk = __builtin_amdgcn_cvt_pk_fp8_f32(x0, x1, 0, false);  // bytes 0 and 1
+    const f32x2 v = __builtin_amdgcn_cvt_pk_f32_fp8(pk, false);
+    r0 = __builtin_fabsf(x0) >= 248.0f ? __builtin_copysignf(__builtin_inff(), x0) : v[0];
+    r1 = __builtin_fabsf(x1) >= 248.0f ? __builtin_copysignf(__builtin_inff(), x1) : v[1];
+}
+
+// Two input values cast by the hardware conversion of the launch's mode.
+template <int VI>
+__device__ __forceinline__ void cast_hw_x2(float x0, float x1, float& r0, float& r1) {
+    if constexpr (VI == VI_E5M2)
+        cast_e5m2x2(x0, x1, r0, r1);
+    else
+        cast_e4m3x2(x0, x1, r0, r1);
+}
+
+// The launch's input mode: a hardware conversion, or the format's class.
+inline bool input_mode_is(int vi, const FmtK& f) {
+    if (vi == VI_E5M2) return f.e == 5 && f.m == 2 && f.bias == 15;
+    if (vi == VI_E4M3) return f.e == 4 && f.m == 3 && f.bias == 7;
+    return f.variant == vi;
+}
 
 // An input value cast to the input format (native value): through the
 // switch over classes, straight to the class VI when the launch knows it, or
-// by the hardware's E5M2 conversion.
+// by a hardware conversion (E5M2, E4M3).
 template <int VI>
 __device__ __forceinline__ float cast_in(float x, const FmtK& fi) {
-    if constexpr (VI == VI_E5M2) {
+    if constexpr (VI == VI_E5M2 || VI == VI_E4M3) {
         float r, unused;
-        cast_e5m2x2(x, x, r, unused);
+        cast_hw_x2<VI>(x, x, r, unused);
         return r;
     } else if constexpr (VI < 0) {
         return quant_any(x, fi.k, fi);
@@ -302,14 +330,14 @@ __global__ __launch_bounds__(BLOCK) void k_lp_gemm_h(GemmArgs g, FmtK fi) {
         // Every load reads an address inside the matrix, so no lane branches.
         auto fetch = [&](int64_t k0) {
             if (inner && k0 + HGK <= g.K) {  // the whole k-tile inside A and B: no checks
-                if constexpr (VI == VI_E5M2) {  // two values per conversion
+                if constexpr (VI == VI_E5M2 || VI == VI_E4M3) {  // two values per conversion
 #pragma unroll
                     for (int r = 0; r < HST; r += 2) {
                         float a0, a1, b0, b1;
-                        cast_e5m2x2(g.A[oa + r * (BLOCK / HGK) * g.lda + k0],
-                                    g.A[oa + (r + 1) * (BLOCK / HGK) * g.lda + k0], a0, a1);
-                        cast_e5m2x2(g.B[ob + (k0 + r * (BLOCK / HGT)) * g.ldb],
-                                    g.B[ob + (k0 + (r + 1) * (BLOCK / HGT)) * g.ldb], b0, b1);
+                        cast_hw_x2<VI>(g.A[oa + r * (BLOCK / HGK) * g.lda + k0],
+                                       g.A[oa + (r + 1) * (BLOCK / HGK) * g.lda + k0], a0, a1);
+                        cast_hw_x2<VI>(g.B[ob + (k0 + r * (BLOCK / HGT)) * g.ldb],
+                                       g.B[ob + (k0 + (r + 1) * (BLOCK / HGT)) * g.ldb], b0, b1);
                         ra[r] = (_Float16)a0;
                         ra[r + 1] = (_Float16)a1;
                         rb[r] = (_Float16)b0;
@@ -435,14 +463,14 @@ static void launch_lp_gemm_v(bool kahan, int pm, dim3 grid, hipStream_t s, const
         if constexpr (V == V_INT_F32) {
             // one instantiation per input class (such inputs are TOP or LOW)
 #define APS_GB(VI)                                                                                           \
-    if ((VI) == VI_E5M2 ? is_e5m2(fi) : fi.variant == (VI)) {                                                                                \
+    if (input_mode_is((VI), fi)) {                                                                                \
         if (kahan)                                                                                           \
             hipLaunchKernelGGL((k_lp_gemm<V, true, GP_BF16, VI>), grid, dim3(BLOCK), 0, s, g, fi, fa);  \
         else                                                                                                 \
             hipLaunchKernelGGL((k_lp_gemm<V, false, GP_BF16, VI>), grid, dim3(BLOCK), 0, s, g, fi, fa); \
         return;                                                                                              \
     }
-            APS_GB(VI_E5M2) APS_GB(V_TOP_F32) APS_GB(V_TOP_M0) APS_GB(V_LOW_F32) APS_GB(V_LOW_M0)
+            APS_GB(VI_E5M2) APS_GB(VI_E4M3) APS_GB(V_TOP_F32) APS_GB(V_TOP_M0) APS_GB(V_LOW_F32) APS_GB(V_LOW_M0)
 #undef APS_GB
             if (kahan) APS_G(true, GP_BF16); else APS_G(false, GP_BF16);
             return;
@@ -456,13 +484,16 @@ static void launch_lp_gemm_v(bool kahan, int pm, dim3 grid, hipStream_t s, const
     }
     if (pm == GP_GRID) {
         if constexpr (can_fit) {
-            if (is_e5m2(fi)) {
-                if (kahan)
-                    hipLaunchKernelGGL((k_lp_gemm<V, true, GP_GRID, VI_E5M2>), grid, dim3(BLOCK), 0, s, g, fi, fa);
-                else
-                    hipLaunchKernelGGL((k_lp_gemm<V, false, GP_GRID, VI_E5M2>), grid, dim3(BLOCK), 0, s, g, fi, fa);
-                return;
-            }
+#define APS_GG(VI)                                                                                           \
+    if (input_mode_is((VI), fi)) {                                                                           \
+        if (kahan)                                                                                           \
+            hipLaunchKernelGGL((k_lp_gemm<V, true, GP_GRID, VI>), grid, dim3(BLOCK), 0, s, g, fi, fa);  \
+        else                                                                                                 \
+            hipLaunchKernelGGL((k_lp_gemm<V, false, GP_GRID, VI>), grid, dim3(BLOCK), 0, s, g, fi, fa); \
+        return;                                                                                              \
+    }
+            APS_GG(VI_E5M2) APS_GG(VI_E4M3)
+#undef APS_GG
             if (kahan) APS_G(true, GP_GRID); else APS_G(false, GP_GRID);
             return;
         }
@@ -566,14 +597,14 @@ extern "C" int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t 
         const hipStream_t hs = (hipStream_t)stream;
         const bool kh = accumulator == APS_ACC_KAHAN;
 #define APS_HK(VI)                                                                          \
-    if ((VI) == VI_E5M2 ? is_e5m2(fi) : fi.variant == (VI)) {                                                              \
+    if (input_mode_is((VI), fi)) {                                                              \
         if (kh)                                                                            \
             hipLaunchKernelGGL((k_lp_gemm_h<true, VI>), hgrid, dim3(BLOCK), 0, hs, g, fi);  \
         else                                                                               \
             hipLaunchKernelGGL((k_lp_gemm_h<false, VI>), hgrid, dim3(BLOCK), 0, hs, g, fi); \
         return launched();                                                                 \
     }
-        APS_HK(VI_E5M2) APS_HK(V_TOP_F32) APS_HK(V_TOP_M0) APS_HK(V_LOW_F32) APS_HK(V_LOW_M0)
+        APS_HK(VI_E5M2) APS_HK(VI_E4M3) APS_HK(V_TOP_F32) APS_HK(V_TOP_M0) APS_HK(V_LOW_F32) APS_HK(V_LOW_M0)
 #undef APS_HK
         g.tiles = mt * nt;  // another input class: the emulated kernel
         g.ntn = (int32_t)nt;

@@ -778,20 +778,22 @@ def _cast_boundary_values():
 
 
 @pytest.mark.parametrize("facc", [F(5, 10), F(5, 7), F(8, 7)], ids=["half", "grid", "exact-bf16"])
-def test_lp_gemm_input_cast_rounding_cases(dev, facc):
-    """1-5-2 inputs at every rounding case of their cast (ties, sticky bits,
-    the subnormal grid, overflow to INF, NaN, signed zeros), each times 1.0
-    with zeros in the other k slots, in whole tiles so that the half kernel
-    casts its staged values two at a time."""
+@pytest.mark.parametrize("fin", [F(5, 2), F(4, 3)], ids=str)
+def test_lp_gemm_input_cast_rounding_cases(dev, fin, facc):
+    """1-5-2 and 1-4-3 inputs (the formats the GEMM casts by the hardware's
+    8-bit float conversions) at every rounding case of their cast (ties,
+    sticky bits, the subnormal grid, overflow to INF, NaN, signed zeros),
+    each times 1.0 with zeros in the other k slots, in whole tiles so that
+    the half kernel casts its staged values two at a time."""
     x = _cast_boundary_values()
     M, K, N = x.size, 16, 64
     Am = np.zeros((M, K), np.float32)
     Am[:, 0] = x
     Bm = np.zeros((K, N), np.float32)
     Bm[0, :] = 1.0
-    log(f"lp_gemm input cast cases 1-5-2->{facc} M={M}")
-    got = A.aps_lp_gemm(torch.from_numpy(Am).to(dev), torch.from_numpy(Bm).to(dev), F(5, 2), facc).cpu().numpy()
-    ref = O.lp_gemm(Am, np.ascontiguousarray(Bm[:, :1]), ofmt(F(5, 2)), ofmt(facc))
+    log(f"lp_gemm input cast cases {fin}->{facc} M={M}")
+    got = A.aps_lp_gemm(torch.from_numpy(Am).to(dev), torch.from_numpy(Bm).to(dev), fin, facc).cpu().numpy()
+    ref = O.lp_gemm(Am, np.ascontiguousarray(Bm[:, :1]), ofmt(fin), ofmt(facc))
     assert same_f32(got[:, :1], ref), first_diff(got[:, :1], ref)
     assert same_f32(got, np.repeat(got[:, :1], N, axis=1))
 
