@@ -397,6 +397,9 @@ int aps_dequantize(const float* Q, const void* codes, int64_t n,
  * When acc_fmt is IEEE half (e = 5, m = 10, bias 15) and every in_fmt value
  * is a half, the products and adds run on the GPU's half-precision
  * arithmetic, which rounds exactly as above: the results are the same.
+ * Likewise in_fmt 1-5-2 (bias 15) and 1-4-3 (bias 7) are cast by the GPU's
+ * conversions to the 8-bit floats E5M2 and E4M3 and back (for 1-4-3 with
+ * INF from 248 up), which give this cast on every fp32 input.
  */
 #define APS_MAX_GEMM_DIM (1 << 22)
 int aps_lp_gemm(const float* A, int64_t lda, const float* B, int64_t ldb, float* C, int64_t ldc,
